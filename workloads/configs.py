@@ -1,0 +1,261 @@
+"""Seeded synthetic workloads: programs, trip tables and input tensors.
+
+Every random draw comes from ``numpy.random.default_rng(SeedSequence([cfg_id,
+seed, wg]))`` (PCG64); "uniform [a, b]" on integers is inclusive.  Nothing in
+this module computes a threshold, a loop register or a counter: it only lays
+out the loop nest, the dependency graph, the per-execution trip counts and the
+data that both the CPU oracle and the GPU library read.
+
+Trip tables.  ``trips[loop][j]`` is the trip count of the j-th execution of the
+loop statement ``loop`` inside one workgroup (a loop statement executes once
+per iteration of its parent, so j runs over all parent iterations in order).
+The flat form is ``trips`` (int32, concatenated) plus ``trip_off`` (int64
+``[n_wg][n_loops]``) giving where each loop's list starts; the top-level loop
+has a single entry 1.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from .program import (OP_ADDC, OP_LOAD, OP_NOP, OP_SCALE_ACC, OP_STORE_ACC,
+                      OP_STORE_RING, Program, ProgramBuilder, tile_args)
+
+CFG_CHAIN, CFG_STREAM, CFG_GEMM, CFG_ATTN, CFG_MOE, CFG_RANDOM = 1, 2, 3, 4, 5, 99
+
+
+def rng_for(cfg_id: int, seed: int, wg: int = 0) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([cfg_id, seed, wg]))
+
+
+# ---------------------------------------------------------------------------
+# trip tables
+# ---------------------------------------------------------------------------
+@dataclass
+class TripTables:
+    per_wg: list          # per workgroup: list over loops of np.int32 arrays
+
+    @property
+    def n_wg(self) -> int:
+        return len(self.per_wg)
+
+    def flat(self):
+        n_loops = len(self.per_wg[0])
+        off = np.zeros((self.n_wg, n_loops), dtype=np.int64)
+        chunks, pos = [], 0
+        for w, loops in enumerate(self.per_wg):
+            for l, arr in enumerate(loops):
+                off[w, l] = pos
+                chunks.append(np.asarray(arr, dtype=np.int32))
+                pos += len(arr)
+        trips = np.concatenate(chunks) if chunks else np.zeros(0, np.int32)
+        return trips.astype(np.int32), off
+
+    def total_iters(self, wg: int, loop: int) -> int:
+        return int(np.sum(self.per_wg[wg][loop], dtype=np.int64))
+
+
+def draw_trips(prog: Program, draw) -> list:
+    """Trip lists for one workgroup.  ``draw(loop, n_exec)`` returns the trip
+    counts of the ``n_exec`` executions of ``loop``.  Loops are numbered so
+    that a parent precedes its children, so one pass suffices."""
+    trips = [np.array([1], dtype=np.int32)]
+    for l in range(1, prog.n_loops):
+        parent = prog.loop_parent[l]
+        n_exec = int(np.sum(trips[parent], dtype=np.int64))
+        t = np.asarray(draw(l, n_exec), dtype=np.int32)
+        assert t.shape == (n_exec,)
+        trips.append(t)
+    return trips
+
+
+def tile_bases(tt: TripTables, loop: int) -> np.ndarray:
+    """Exclusive prefix sum over workgroups of the iteration count of ``loop``:
+    workgroup w's tiles start at this index in the packed tile buffers."""
+    counts = np.array([tt.total_iters(w, loop) for w in range(tt.n_wg)], dtype=np.int64)
+    return np.concatenate([[0], np.cumsum(counts)[:-1]]).astype(np.int64), counts
+
+
+# ---------------------------------------------------------------------------
+# cfg1: 2-engine chain, one workgroup
+# ---------------------------------------------------------------------------
+def chain_program(ring_slots: int = 4, scale: float = 0.5) -> Program:
+    """E0 loads 256-element fp32 tiles into a ring, E1 accumulates 0.5 * tile.
+
+    A{ E0:ACQ; B{ E0:LOAD X[n] -> ring[(rhat_B-1) % 4]; E1:CONS acc += 0.5*ring }}
+    E1:STORE acc -> out
+
+    LOAD->CONS (k=0) is the read-after-write; CONS->LOAD (k=4) keeps a slot
+    from being refilled before it is read within one trip of B; CONS->ACQ
+    (k=1) orders the next trip's loads after the previous trip's reads."""
+    b = ProgramBuilder("interp", n_engines=2)
+    with b.loop("A") as A:
+        b.instr(0, OP_NOP, name="ACQ")
+        with b.loop("B") as B:
+            b.instr(0, OP_LOAD, tile_args(src=1, dst=0, pos_loop=B, per_gen=ring_slots, idx_loop=B),
+                    name="LOAD")
+            b.instr(1, OP_SCALE_ACC, tile_args(src=0, dst=0, pos_loop=B, per_gen=ring_slots, const=scale),
+                    name="CONS")
+    b.instr(1, OP_STORE_ACC, tile_args(src=0, dst=2), name="STORE")
+    b.dep("LOAD", "CONS", 0)
+    b.dep("CONS", "LOAD", ring_slots)
+    b.dep("CONS", "ACQ", 1)
+    p = b.build()
+    p.tile_elems = 256
+    p.ring_slots = [ring_slots]
+    p.n_accs = 1
+    return p
+
+
+@dataclass
+class ChainWorkload:
+    prog: Program
+    trips: TripTables
+    base: np.ndarray      # int64 [n_wg]: tile base per workgroup
+    x: np.ndarray         # fp32 [n_tiles, 256]
+    n_tiles: int
+
+
+def chain_workload(seed: int = 0, outer: int = 16, inner_max: int = 8, n_wg: int = 1) -> ChainWorkload:
+    prog = chain_program()
+    per = []
+    for w in range(n_wg):
+        rng = rng_for(CFG_CHAIN, seed, w)
+
+        def draw(l, n, rng=rng):
+            if l == 1:
+                return np.full(n, outer)
+            return rng.integers(1, inner_max + 1, size=n)
+        per.append(draw_trips(prog, draw))
+    tt = TripTables(per)
+    base, counts = tile_bases(tt, prog.loop_id("B"))
+    n_tiles = int(counts.sum())
+    xs = [rng_for(CFG_CHAIN, seed, 1000 + w).uniform(-1.0, 1.0, size=(int(counts[w]), 256)).astype(np.float32)
+          for w in range(n_wg)]
+    return ChainWorkload(prog, tt, base, np.concatenate(xs), n_tiles)
+
+
+# ---------------------------------------------------------------------------
+# cfg2: sync-bound 3-engine stream, 1024 workgroups
+# ---------------------------------------------------------------------------
+def stream_program(n_gen: int = 4, per_gen: int = 4) -> Program:
+    """Load / vector-add / store engines over a 3-level nest O{M{I{...}}}.
+
+    Ring slot = ((r_M - 1) % n_gen) * per_gen + (rhat_I - 1): each M iteration
+    owns one generation of per_gen slots (inner trips are at most per_gen).
+    Markers at the end of each M / O iteration let the acquire instructions of
+    a later iteration wait for the previous users of a generation:
+
+      O{ E0:ACQX_O E1:ACQY_O
+         M{ E0:ACQX_M E1:ACQY_M
+            I{ E0:LOAD X->rx[slot]  E1:ADD rx[slot]+1->ry[slot]  E2:STORE ry[slot]->Y }
+            E1:MARKX_M E2:MARKY_M }
+         E1:MARKX_O E2:MARKY_O }
+    """
+    b = ProgramBuilder("stream3", n_engines=3)
+    with b.loop("O"):
+        b.instr(0, OP_NOP, name="ACQX_O")
+        b.instr(1, OP_NOP, name="ACQY_O")
+        with b.loop("M") as M:
+            b.instr(0, OP_NOP, name="ACQX_M")
+            b.instr(1, OP_NOP, name="ACQY_M")
+            with b.loop("I") as I:
+                slot = dict(gen_loop=M, n_gen=n_gen, pos_loop=I, per_gen=per_gen)
+                b.instr(0, OP_LOAD, tile_args(src=1, dst=0, idx_loop=I, **slot), name="LOAD")
+                b.instr(1, OP_ADDC, tile_args(src=0, dst=1, const=1.0, **slot), name="ADD")
+                b.instr(2, OP_STORE_RING, tile_args(src=1, dst=2, idx_loop=I, **slot), name="STORE")
+            b.instr(1, OP_NOP, name="MARKX_M")
+            b.instr(2, OP_NOP, name="MARKY_M")
+        b.instr(1, OP_NOP, name="MARKX_O")
+        b.instr(2, OP_NOP, name="MARKY_O")
+    b.dep("LOAD", "ADD", 0)
+    b.dep("ADD", "STORE", 0)
+    b.dep("ADD", "LOAD", per_gen)        # slot reuse inside one trip of I
+    b.dep("STORE", "ADD", per_gen)
+    b.dep("MARKX_M", "ACQX_M", n_gen)    # generation reuse across M iterations
+    b.dep("MARKY_M", "ACQY_M", n_gen)
+    b.dep("MARKX_O", "ACQX_O", 1)        # across O iterations
+    b.dep("MARKY_O", "ACQY_O", 1)
+    p = b.build()
+    p.tile_elems = 64
+    p.ring_slots = [n_gen * per_gen, n_gen * per_gen]
+    return p
+
+
+@dataclass
+class StreamWorkload:
+    prog: Program
+    trips: TripTables
+    base: np.ndarray      # int64 [n_wg]
+    counts: np.ndarray    # int64 [n_wg]: inner iterations per workgroup
+    x: np.ndarray | None  # fp32 [n_tiles, 64]
+    n_tiles: int
+
+
+def stream_workload(seed: int = 0, n_wg: int = 1024, outer: int = 256, mid_max: int = 16,
+                    inner_max: int = 4, n_gen: int = 4, with_data: bool = True) -> StreamWorkload:
+    prog = stream_program(n_gen=n_gen, per_gen=inner_max)
+    per = []
+    for w in range(n_wg):
+        rng = rng_for(CFG_STREAM, seed, w)
+
+        def draw(l, n, rng=rng):
+            if l == 1:
+                return np.full(n, outer)
+            if l == 2:
+                return rng.integers(1, mid_max + 1, size=n)
+            return rng.integers(1, inner_max + 1, size=n)
+        per.append(draw_trips(prog, draw))
+    tt = TripTables(per)
+    base, counts = tile_bases(tt, prog.loop_id("I"))
+    n_tiles = int(counts.sum())
+    x = None
+    if with_data:
+        x = np.empty((n_tiles, 64), dtype=np.float32)
+        for w in range(n_wg):
+            g = rng_for(CFG_STREAM, seed, 100000 + w)
+            x[base[w]:base[w] + counts[w]] = g.uniform(-1.0, 1.0, size=(int(counts[w]), 64))
+    return StreamWorkload(prog, tt, base, counts, x, n_tiles)
+
+
+# ---------------------------------------------------------------------------
+# random tiny nests (property tests of thresholds)
+# ---------------------------------------------------------------------------
+def random_nest(seed: int, max_depth: int = 3, n_engines: int = 3, max_items: int = 3,
+                max_trip: int = 3, n_deps: int = 6, max_k: int = 3):
+    """A random structured program with random dependency triples.
+
+    Offsets are drawn uniformly from [0, max_k], so some triples fall outside
+    the allocatable subset; callers keep whichever the planner accepts.
+    Returns (program, trip tables for one workgroup)."""
+    rng = rng_for(CFG_RANDOM, seed)
+    b = ProgramBuilder("interp", n_engines=n_engines)
+
+    def fill(depth):
+        n_items = int(rng.integers(1, max_items + 1))
+        for _ in range(n_items):
+            if depth < max_depth and rng.random() < 0.45:
+                with b.loop(f"L{len(b.p.loop_parent)}", is_cond=bool(rng.random() < 0.2)):
+                    fill(depth + 1)
+            else:
+                for _ in range(int(rng.integers(1, 4))):
+                    b.instr(int(rng.integers(0, n_engines)), OP_NOP)
+                b.block_break() if rng.random() < 0.3 else None
+
+    fill(0)
+    if not b.p.instrs:
+        b.instr(0, OP_NOP)
+    n_ins = len(b.p.instrs)
+    for _ in range(n_deps):
+        pr, cn = (int(v) for v in rng.integers(0, n_ins, size=2))
+        if pr == cn:
+            continue
+        b.dep(pr, cn, int(rng.integers(0, max_k + 1)))
+    prog = b.build()
+
+    def draw(l, n):
+        hi = 1 if prog.loop_is_cond[l] else max_trip
+        return rng.integers(0, hi + 1, size=n)
+    tt = TripTables([draw_trips(prog, draw)])
+    return prog, tt
