@@ -1,0 +1,237 @@
+/*
+ * bfs.h -- barrier-free synchronization of loop-nested multi-engine kernels
+ * on one MI355X (gfx950) GPU.
+ *
+ * The library takes what the paper's allocation pass takes -- a structured
+ * program (a tree of loops over blocks of per-engine instructions) plus a
+ * dependency graph of (producer, consumer, offset) triples (Section 1 and
+ * Appendix A.1) -- and produces the synchronization that enforces it:
+ *
+ *   - barrier-free mode (Sections 5.1-5.5): every dependency becomes one wait
+ *     on a monotone counter owned by (producer's loop, producer's engine),
+ *     against the threshold
+ *         isGT(rhat_S, k) * max(N * expr - (N - K), 0)           (Eq. 2, Eq. 5)
+ *     with expr = r_P - k when the producer sits directly in the shared loop
+ *     S (case C1), and expr = r_P when it is nested deeper (C2: forward,
+ *     k = 0; C3: backward, k = 1) (Section 5.2).  r_l counts every entry
+ *     (iteration start) of loop l and is never reset; rhat_l counts the
+ *     entries in the current trip and is reset when l's loop statement is
+ *     reached (Section 5.1).
+ *   - barrier mode (Section 3.4): all engines synchronize before every
+ *     non-top loop statement and at the end of every iteration of a non-top
+ *     loop (drain, barrier, counter reset, barrier); inside a region a
+ *     consumer waits for the producer's static ordinal on its engine.
+ *
+ * On the GPU an engine is a group of wavefronts of one workgroup; a counter
+ * is a 32-bit LDS word per (counter slot, producer wave); the loop registers
+ * live in scalar registers.  The datapath is a hand-written HIP kernel
+ * family selected by bfs_program.kernel.
+ *
+ * Conventions for every entry point:
+ *   - Returns a bfs_status.  Out-parameters are written only on BFS_OK.
+ *     bfs_last_error() then describes the most recent failure of the calling
+ *     thread.
+ *   - Input descriptors are caller-owned and copied; the caller may free them
+ *     when the call returns.
+ *   - Device pointers are caller-owned and must stay valid until the work
+ *     enqueued on the stream has completed.
+ */
+#ifndef BFS_H
+#define BFS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+struct ihipStream_t;                      /* hipStream_t is struct ihipStream_t* */
+
+typedef struct bfs_plan bfs_plan;         /* opaque, library-owned */
+
+typedef enum {
+  BFS_OK = 0,
+  BFS_E_INVALID = 1,          /* malformed program, bad id, bad argument */
+  BFS_E_ORDER = 2,            /* producer not before consumer where offset 0 requires it */
+  BFS_E_NOT_ALLOCATABLE = 3,  /* dependency outside the cases of Section 5.2 */
+  BFS_E_RESOURCE = 4,         /* exceeds LDS / wave / counter limits */
+  BFS_E_DEVICE = 5,           /* HIP runtime error */
+  BFS_E_DEADLOCK = 6,         /* a device wait exceeded the watchdog */
+  BFS_E_UNSUPPORTED = 7       /* program does not match the kernel family */
+} bfs_status;
+
+typedef enum { BFS_MODE_BARRIER_FREE = 0, BFS_MODE_BARRIER = 1 } bfs_mode;
+
+/* Semaphore granularity (Section 5.4 per-instruction, Section 5.5 per-loop). */
+typedef enum { BFS_ALLOC_PER_LOOP = 0, BFS_ALLOC_PER_INSTR = 1 } bfs_alloc;
+
+/* Datapath kernel families. */
+typedef enum {
+  BFS_KERNEL_INTERP = 0,      /* generic tile-machine interpreter, one wave per engine */
+  BFS_KERNEL_STREAM3 = 1,     /* load / add / store stream over a 3-level nest */
+  BFS_KERNEL_GEMM = 2,        /* bf16 GEMM + bias + GELU, load / MFMA / epilogue engines */
+  BFS_KERNEL_ATTN = 3,        /* variable-length attention forward */
+  BFS_KERNEL_MOE = 4          /* MoE grouped GEMM with runtime per-expert trip counts */
+} bfs_kernel;
+
+/*
+ * The program (the statement tree of Section 7.1 with the block streams of
+ * Appendix A.1), as flat int32 arrays:
+ *
+ *   loops        loop 0 is the top level (parent -1, runs once).  Every other
+ *                loop l has loop_parent[l] and appears exactly once in its
+ *                parent's body.  loop_is_cond[l] marks a conditional (a loop
+ *                whose trip count is 0 or 1).
+ *   body         CSR: loop l's body is items body_off[l] .. body_off[l+1]-1,
+ *                in program order; item i is a block (body_kind 0) or a loop
+ *                (body_kind 1) with id body_id[i].
+ *   blocks       CSR: block b lists instruction ids block_instrs[block_off[b]
+ *                .. block_off[b+1]-1] in one sequential program order; each
+ *                engine's stream is the projection onto that engine.
+ *   instrs       instr_engine[i], instr_opcode[i] and instr_args[8*i .. 8*i+7]
+ *                (datapath opcode and operands; meaning set by the family).
+ *   deps         deps[3*d .. 3*d+2] = producer, consumer, offset k >= 0, with
+ *                k the distance on the innermost loop enclosing both.
+ *   tile machine tile_elems fp32 values per tile (multiple of 64, <= 256),
+ *                ring_slots[r] slots in LDS ring r (0 = unused), n_accs
+ *                accumulator tiles.
+ */
+typedef struct {
+  int32_t kernel;                  /* bfs_kernel */
+  int32_t n_engines;               /* 1..8 */
+  int32_t waves_per_engine[8];
+  int32_t n_loops;
+  const int32_t *loop_parent;
+  const int32_t *loop_is_cond;
+  const int32_t *body_off;
+  const int32_t *body_kind;
+  const int32_t *body_id;
+  int32_t n_blocks;
+  const int32_t *block_off;
+  const int32_t *block_instrs;
+  int32_t n_instrs;
+  const int32_t *instr_engine;
+  const int32_t *instr_opcode;
+  const int32_t *instr_args;
+  int32_t n_deps;
+  const int32_t *deps;
+  int32_t tile_elems;
+  int32_t ring_slots[4];
+  int32_t n_accs;
+} bfs_program;
+
+/* One dependency's barrier-free wait (Eq. 5). */
+typedef struct {
+  int32_t dep;
+  int32_t kase;          /* 1 = C1 (P == S), 2 = C2 (nested, forward), 3 = C3 (nested, backward) */
+  int32_t loop_S;        /* innermost loop enclosing producer and consumer */
+  int32_t loop_P;        /* producer's parent loop */
+  int32_t k;             /* offset on S */
+  int32_t expr_sub;      /* k for C1, 0 for C2 / C3 */
+  int32_t N, K;          /* decode of the shared counter: N instructions, producer is the K-th */
+  int32_t needs_mask;    /* k > 0: multiply by isGT(rhat_S, k) */
+  int32_t counter;       /* counter slot the consumer polls */
+  int32_t prd_engine;
+  int32_t cns_engine;
+  int32_t forward;       /* producer precedes consumer in S's body */
+} bfs_formula;
+
+/* One dependency's barrier-mode wait (Section 3.4). */
+typedef struct {
+  int32_t dep;
+  int32_t same_region;   /* 0: a barrier always separates them, no wait */
+  int32_t prd_engine;
+  int32_t ordinal;       /* producer's position on its engine since the last barrier */
+} bfs_static_wait;
+
+/* Resource figures (Table alloc-resources / Table alloc-sema-combined columns). */
+typedef struct {
+  int32_t n_counters;            /* semaphores used */
+  int32_t regs_per_engine;       /* loop registers r, rhat plus the wait register */
+  int32_t salu_ops_per_wait;     /* 5 per-loop, 3 per-instruction, 0 barrier */
+  int32_t n_waits;               /* waits emitted */
+  int32_t n_sync_points;         /* barrier mode: loop statements + iteration ends in the tree */
+} bfs_stats;
+
+/* Options of one launch; NULL selects the defaults. */
+typedef struct {
+  uint64_t watchdog_polls;       /* polls before a wait gives up (0 = default, about 1 s) */
+  int32_t fault_dep;             /* test knob: dependency whose threshold is raised (-1 = none) */
+  int32_t fault_delta;           /* amount added to that threshold */
+  uint64_t *dev_stats;           /* NULL, or n_wg * W * 8 uint64 per-wave counters (W = waves per
+                                    workgroup), in 100 MHz ticks: [0] wave run time, [1] time
+                                    blocked in waits, [2] blocked waits, [3] time in barriers,
+                                    [4] time waiting for own loads to land, [5] polls, [6-7] 0 */
+} bfs_run_opts;
+
+/*
+ * Plan the synchronization of prog (Sections 5.2-5.5, or Section 3.4 in
+ * barrier mode).  Validates the tree, classifies every dependency, assigns
+ * counter slots and computes N, K and the barrier ordinals.  Host only; needs
+ * no GPU.  flags must be 0.
+ * Errors: BFS_E_INVALID, BFS_E_ORDER (offset 0 with the producer not before
+ * the consumer, or a nested backward producer at offset 0),
+ * BFS_E_NOT_ALLOCATABLE (nested producer with another offset), BFS_E_RESOURCE.
+ */
+bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc alloc, uint32_t flags,
+                           bfs_plan **out);
+
+/* Formula table (one entry per dependency, in dependency order).  The array
+ * is owned by the plan and valid until bfs_plan_destroy. */
+bfs_status bfs_plan_formulas(const bfs_plan *plan, const bfs_formula **out, int32_t *n);
+
+/* Barrier-mode waits (one per dependency); owned by the plan. */
+bfs_status bfs_plan_static_waits(const bfs_plan *plan, const bfs_static_wait **out, int32_t *n);
+
+bfs_status bfs_plan_stats(const bfs_plan *plan, bfs_stats *out);
+
+/*
+ * Host evaluation of dependency dep's threshold for the consumer engine's
+ * registers r_P (entries of the producer's parent loop) and rhat_S (entries of
+ * the shared loop in its current trip): Eq. 5 in barrier-free mode, the static
+ * ordinal (or 0) in barrier mode.  This is the value the device computes.
+ */
+bfs_status bfs_eval_threshold(const bfs_plan *plan, int32_t dep, uint32_t r_P, uint32_t rhat_S,
+                              uint32_t *out);
+
+/* Frees the plan and its device images.  NULL-safe. */
+void bfs_plan_destroy(bfs_plan *plan);
+
+/*
+ * Enqueue one execution of the planned program on stream (asynchronous).
+ *
+ *   dev_buffers  family-specific device pointers, n_buffers of them
+ *                (interp / stream3: [0] int64 per-workgroup tile base,
+ *                [1] fp32 input tiles, [2] fp32 output; see the family notes
+ *                in the implementation files for gemm / attn / moe).
+ *   dev_trips    int32 trip counts; dev_trip_off int64 [n_wg][n_loops]: the
+ *                j-th execution of loop l in workgroup w runs
+ *                dev_trips[dev_trip_off[w*n_loops + l] + j] iterations.
+ *                (gemm / attn / moe derive trips on the device and accept NULL.)
+ *   n_wg         workgroups.
+ *   dev_debug_log  NULL, or a uint32 buffer of n_wg * W * (1 + 4 * debug_capacity)
+ *                words (W = waves per workgroup): per (workgroup, wave) the
+ *                number of waits released, then up to debug_capacity entries
+ *                {dependency, consumer instance, threshold, observed counter}.
+ *                Logging is for tests; timed runs pass NULL.
+ *   opts         NULL for defaults.
+ * The first launch of a plan on a device uploads its tables (one allocation
+ * per plan and device).  Device-side deadlock is reported by bfs_run_status.
+ */
+bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t n_buffers,
+                   const int32_t *dev_trips, const int64_t *dev_trip_off, int32_t n_wg,
+                   struct ihipStream_t *stream, uint32_t *dev_debug_log, int64_t debug_capacity,
+                   const bfs_run_opts *opts);
+
+/* Synchronizes stream, then reports (and clears) the plan's watchdog word:
+ * BFS_E_DEADLOCK if any wait gave up since the last call. */
+bfs_status bfs_run_status(const bfs_plan *plan, struct ihipStream_t *stream);
+
+const char *bfs_status_string(bfs_status s);
+const char *bfs_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BFS_H */

@@ -1,0 +1,491 @@
+// Sync-bound stream over a dynamically bounded 3-level nest O{ M{ I{ ... } } }
+// with three single-wave engines: E0 loads a 64-element fp32 tile from HBM
+// into an LDS ring slot, E1 adds a constant into a second ring, E2 stores the
+// result to HBM.  Acquire / marker instructions (no datapath) may sit in the
+// bodies of O and M before or after the nested loop.
+//
+// Waits come from the plan: every instruction evaluates the waits whose
+// consumer it is, with Eq. 5 on the engine's loop registers (barrier-free),
+// or the static ordinal (barrier mode, which also synchronizes before every
+// loop statement and at every iteration end).  The waits of each engine's
+// instructions travel in the launch arguments, so the loop body reads no
+// descriptor tables.  Each engine runs its own copy of the loop nest, and the
+// synchronization mode and the instrumentation are compile-time choices, so
+// the innermost loop holds only that engine's work.
+//
+// Retirement is in issue order:
+//   * the load engine keeps up to kInflight direct-to-LDS loads outstanding
+//     and retires the oldest with a counted vmcnt wait;
+//   * the add and store engines retire tile n once a later LDS read has
+//     returned (LDS operations of one wave complete in order), i.e. one
+//     round trip per tile instead of two;
+//   * markers retire at once, after everything before them.
+// Before blocking on a wait that is not met, an engine retires what it holds
+// (the load engine one load at a time), so a consumer never waits on a
+// retirement that the blocked producer is holding back.
+//
+// Counters only grow, so a counter value an engine has already observed stays
+// a valid lower bound: the waits of the innermost instruction remember their
+// last observation and poll LDS only when the new threshold exceeds it.
+//
+// Family contract (BFS_KERNEL_STREAM3): loops top -> O -> M -> I, three
+// engines of one wave, tile_elems 64; the I body holds exactly one load
+// (engine 0), one add-constant (engine 1) and one store-slot (engine 2), all
+// addressed with slot = ((r_M - 1) % n_gen) * per_gen + (rhat_I - 1) % per_gen
+// and tile index base[wg] + r_I - 1.  Buffers: [0] int64 tile base per
+// workgroup, [1] fp32 input tiles, [2] fp32 output tiles.
+#include <string>
+
+#include "bfs_internal.h"
+#include "device_sync.h"
+
+using namespace bfsdev;
+
+namespace {
+
+constexpr int kMaxNops = 4;
+constexpr int kMaxWaitsPerEngine = 16;
+constexpr int kMaxInnerWaits = 4;
+
+struct InstrSync {
+  int16_t first;     // index of its first wait in the engine's wait list
+  int16_t n;         // number of waits
+  int16_t update;    // counter slot incremented at retirement (-1: none)
+  int16_t pad;
+};
+
+struct EngineCode {
+  InstrSync o_pre[kMaxNops], m_pre[kMaxNops], m_post[kMaxNops], o_post[kMaxNops];
+  int32_t n_o_pre, n_m_pre, n_m_post, n_o_post;
+  InstrSync inner;
+  bfs::PackedWait waits[kMaxWaitsPerEngine];
+};
+
+struct Stream3Params {
+  EngineCode eng[3];
+  const int32_t *trips;
+  const int64_t *trip_off;
+  const int64_t *base;
+  const float *x;
+  float *y;
+  uint32_t *dbg;
+  int64_t dbg_cap;
+  uint32_t *err;
+  uint64_t *stats;
+  uint64_t watchdog;
+  int32_t fault_dep, fault_delta;
+  int32_t n_gen, per_gen, n_slots;
+  float addc;
+};
+
+__device__ __forceinline__ uint32_t sel4(uint32_t a, uint32_t b, uint32_t c, uint32_t d, uint32_t i) {
+  return i == 0 ? a : i == 1 ? b : i == 2 ? c : d;
+}
+
+enum { ROLE_LOAD = 0, ROLE_ADD = 1, ROLE_STORE = 2 };
+
+// One engine wave: loop registers, counters, waits and retirement.
+template <int kRole, int kMode, bool kInstr, int kInflight>
+struct Engine {
+  const Stream3Params &P;
+  const EngineCode &C;
+  uint32_t r1 = 0, r2 = 0, r3 = 0;        // r of O, M, I (r of the top level is 1)
+  uint32_t h1 = 0, h2 = 0, h3 = 0;        // rhat of O, M, I
+  uint32_t cnt_base;
+  int wave, wg;
+  bool aborted = false;
+  uint32_t *log = nullptr;
+  uint32_t nlog = 0;
+  int pending = 0;                        // issued, not yet retired (loads or LDS ops)
+  uint32_t own_counter = 0;               // LDS address of the inner instruction's counter
+  bool has_own_counter = false;
+  WaveStats st;
+
+  __device__ Engine(const Stream3Params &p, const EngineCode &c, uint32_t cb, int w, int g)
+      : P(p), C(c), cnt_base(cb), wave(w), wg(g) {}
+
+  __device__ __forceinline__ uint32_t counter_addr(uint32_t slot) const {
+    return cnt_base + 4u * slot * (uint32_t)bfs::kMaxWavesPerEngine;
+  }
+
+  __device__ __forceinline__ uint32_t threshold(const bfs::PackedWait &w) const {
+    uint32_t thr;
+    if (kMode == BFS_MODE_BARRIER) {
+      thr = ((w.w0 >> 25) & 1u) ? (w.w3 >> 16) : 0u;
+    } else {
+      const uint32_t lp = (w.w0 >> 8) & 0xffu, ls = (w.w0 >> 16) & 0xffu;
+      const uint32_t rP = sel4(1u, r1, r2, r3, lp), hS = sel4(1u, h1, h2, h3, ls);
+      thr = eq5(rP, hS, (int)(w.w2 & 0xffffu), (int)(w.w2 >> 16), (int)(w.w1 & 0xffffu), (int)(w.w1 >> 16),
+                (int)((w.w0 >> 24) & 1u));
+    }
+    if (kInstr && (int)(w.w3 & 0xffffu) == P.fault_dep) thr += (uint32_t)P.fault_delta;
+    return thr;
+  }
+
+  // --- retirement of the inner instruction --------------------------------
+  // Load engine: the oldest of kInflight outstanding loads.
+  __device__ __forceinline__ void retire_oldest_of_full() {
+    const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
+    wait_vm<kInflight - 1>();
+    if (kInstr && st.on) st.own_loads += now_ticks() - t0;
+    if (has_own_counter) lds_add(own_counter, 1u);
+    pending -= 1;
+  }
+  // Retire everything held.
+  __device__ __forceinline__ void retire_all() {
+    if (pending > 0) {
+      if (kRole == ROLE_LOAD) {
+        const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
+        wait_vm<0>();
+        if (kInstr && st.on) st.own_loads += now_ticks() - t0;
+      } else {
+        drain_lds();
+      }
+      if (has_own_counter) lds_add(own_counter, (uint32_t)pending);
+      pending = 0;
+    }
+  }
+  // While blocked: the load engine retires one load at a time, the others
+  // everything at once.
+  __device__ __forceinline__ void retire_some() {
+    if (kRole == ROLE_LOAD) {
+      wait_vm_dyn(pending - 1);
+      if (has_own_counter) lds_add(own_counter, 1u);
+      pending -= 1;
+    } else {
+      retire_all();
+    }
+  }
+
+  __device__ WaitResult block(uint32_t addr, uint32_t thr, uint32_t dep, uint32_t instance) {
+    const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
+    if (kInstr && st.on) st.n_blocked += 1;
+    while (pending > 0) {
+      const uint32_t v = uniform(lds_poll(addr));
+      if (v >= thr) {
+        if (kInstr && st.on) st.blocked += now_ticks() - t0;
+        return WaitResult{v, true};
+      }
+      retire_some();
+    }
+    WaitResult res = wait_geq(addr, 1, thr, P.watchdog);
+    if (kInstr && st.on) st.blocked += now_ticks() - t0;
+    if (!res.ok) {
+      report_deadlock(P.err, dep, (uint32_t)wg, instance, thr, res.observed, (uint32_t)wave);
+      aborted = true;
+    }
+    return res;
+  }
+
+  __device__ __forceinline__ void logit(uint32_t dep, uint32_t instance, uint32_t thr, uint32_t obs) {
+    if (kInstr && log) {
+      retire_all();   // log stores share vmcnt with the loads
+      log_wait(log, P.dbg_cap, nlog, dep, instance, thr, obs);
+    }
+  }
+
+  // One wait: returns the observed counter (0 when nothing was owed).
+  __device__ __forceinline__ uint32_t wait_one(const bfs::PackedWait &w, uint32_t thr, uint32_t known,
+                                               uint32_t instance) {
+    uint32_t obs = known;
+    if (!aborted && thr > 0 && (obs < thr || (kInstr && log))) {
+      const uint32_t a = counter_addr(w.w0 & 0xffu);
+      obs = uniform(lds_poll(a));
+      if (kInstr && st.on) st.polls += 1;
+      if (obs < thr) obs = block(a, thr, w.w3 & 0xffffu, instance).observed;
+    }
+    logit(w.w3 & 0xffffu, instance, thr, thr > 0 ? obs : 0u);
+    return obs;
+  }
+
+  // A marker / acquire instruction: its waits, then retirement in order.
+  __device__ void nop(const InstrSync &s, uint32_t instance) {
+    for (int j = 0; j < s.n; ++j) {
+      const bfs::PackedWait w = C.waits[s.first + j];
+      wait_one(w, threshold(w), 0u, instance);
+    }
+    if (s.update >= 0) {
+      retire_all();
+      drain_lds();
+      lds_add(counter_addr((uint32_t)s.update), 1u);
+    }
+  }
+
+  __device__ __forceinline__ void nops(const InstrSync *list, int n, uint32_t instance) {
+    for (int i = 0; i < n; ++i) nop(list[i], instance);
+  }
+
+  __device__ __forceinline__ void sync_point() {
+    if (kMode == BFS_MODE_BARRIER) {
+      retire_all();
+      const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
+      region_sync(counter_addr((uint32_t)wave), 1);
+      if (kInstr && st.on) st.barrier += now_ticks() - t0;
+    }
+  }
+};
+
+template <int kRole, int kMode, bool kInstr, int kInflight>
+__device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_base, float *ring_x, float *ring_y) {
+  const int wave = kRole;
+  const uint32_t lane = lane_id();
+  const int wg = blockIdx.x;
+  const EngineCode &C = P.eng[kRole];
+  Engine<kRole, kMode, kInstr, kInflight> E(P, C, cnt_base, wave, wg);
+  if (kInstr) {
+    if (P.dbg) E.log = P.dbg + (int64_t)gridDim.x * 3 + ((int64_t)wg * 3 + wave) * 4 * P.dbg_cap;
+    if (P.stats) {
+      E.st.on = true;
+      E.st.t_start = now_ticks();
+    }
+  }
+  // The innermost instruction's waits, held in registers for the whole run.
+  const int n_iw = C.inner.n;
+  bfs::PackedWait iw[kMaxInnerWaits];
+  uint32_t seen[kMaxInnerWaits];
+#pragma unroll
+  for (int j = 0; j < kMaxInnerWaits; ++j) {
+    iw[j] = j < n_iw ? C.waits[C.inner.first + j] : bfs::PackedWait{0, 0, 0, 0};
+    seen[j] = 0;
+  }
+  if (C.inner.update >= 0) {
+    E.own_counter = E.counter_addr((uint32_t)C.inner.update);
+    E.has_own_counter = true;
+  }
+  const int64_t *toff = P.trip_off + (int64_t)wg * 4;
+  const int64_t tbase = ldc(P.base + wg);
+  const uint32_t xs = lds_addr(ring_x), ys = lds_addr(ring_y);
+  const float addc = P.addc;
+  const uint32_t per_gen = (uint32_t)P.per_gen, n_gen = (uint32_t)P.n_gen;
+
+  E.sync_point();                                         // before loop O
+  const uint32_t trip_o = (uint32_t)ldc(P.trips + ldc(toff + 1));
+  const int64_t off_m = ldc(toff + 2), off_i = ldc(toff + 3);
+  for (uint32_t o = 0; o < trip_o; ++o) {
+    E.r1 += 1;
+    E.h1 = o + 1;
+    E.nops(C.o_pre, C.n_o_pre, E.r1 - 1);
+    E.sync_point();                                       // before loop M
+    const uint32_t trip_m = (uint32_t)ldc(P.trips + off_m + E.r1 - 1);
+    for (uint32_t m = 0; m < trip_m; ++m) {
+      E.r2 += 1;
+      E.h2 = m + 1;
+      E.nops(C.m_pre, C.n_m_pre, E.r2 - 1);
+      E.sync_point();                                     // before loop I
+      const uint32_t trip_i = (uint32_t)ldc(P.trips + off_i + E.r2 - 1);
+      const uint32_t gen = ((E.r2 - 1) % n_gen) * per_gen;
+      for (uint32_t i = 0; i < trip_i; ++i) {
+        E.r3 += 1;
+        E.h3 = i + 1;
+        const uint32_t instance = E.r3 - 1;
+#pragma unroll
+        for (int j = 0; j < kMaxInnerWaits; ++j)
+          if (j < n_iw) seen[j] = E.wait_one(iw[j], E.threshold(iw[j]), seen[j], instance);
+        const uint32_t slot = gen + (i % per_gen);
+        const int64_t tile = tbase + (int64_t)E.r3 - 1;
+        if (!E.aborted) {
+          if (kRole == ROLE_LOAD) {
+            __builtin_amdgcn_global_load_lds((const void *)(P.x + tile * 64 + lane),
+                                             (BFS_LDS void *)(ring_x + slot * 64), 4, 0, 0);
+            E.pending += 1;
+            if (E.pending == kInflight) E.retire_oldest_of_full();
+          } else if (kRole == ROLE_ADD) {
+            float v;
+            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+                         : "=v"(v) : "v"(xs + 4u * (slot * 64 + lane)) : "memory");
+            // the read returned, so every earlier LDS write of this wave is done
+            if (E.pending > 0 && E.has_own_counter) lds_add(E.own_counter, (uint32_t)E.pending);
+            v = v + addc;
+            asm volatile("ds_write_b32 %0, %1" ::"v"(ys + 4u * (slot * 64 + lane)), "v"(v) : "memory");
+            E.pending = 1;
+          } else {
+            float v;
+            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+                         : "=v"(v) : "v"(ys + 4u * (slot * 64 + lane)) : "memory");
+            __builtin_nontemporal_store(v, P.y + tile * 64 + lane);
+            // the slot has been read: the store retires now
+            if (E.has_own_counter) lds_add(E.own_counter, 1u);
+          }
+        } else if (E.has_own_counter) {
+          lds_add(E.own_counter, 1u);
+        }
+        E.sync_point();                                   // end of an iteration of I
+        if (kMode == BFS_MODE_BARRIER) {
+#pragma unroll
+          for (int j = 0; j < kMaxInnerWaits; ++j) seen[j] = 0;   // counters were reset
+        }
+      }
+      E.nops(C.m_post, C.n_m_post, E.r2 - 1);
+      E.sync_point();                                     // end of an iteration of M
+    }
+    E.nops(C.o_post, C.n_o_post, E.r1 - 1);
+    E.sync_point();                                       // end of an iteration of O
+  }
+  E.retire_all();
+  drain_all();
+  if (kInstr) {
+    if (P.dbg && lane == 0) P.dbg[(int64_t)wg * 3 + wave] = E.nlog;
+    if (E.st.on && lane == 0) {
+      uint64_t *o = P.stats + ((int64_t)wg * 3 + wave) * 8;
+      o[0] = now_ticks() - E.st.t_start;
+      o[1] = E.st.blocked;
+      o[2] = E.st.n_blocked;
+      o[3] = E.st.barrier;
+      o[4] = E.st.own_loads;
+      o[5] = E.st.polls;
+      o[6] = 0;
+      o[7] = 0;
+    }
+  }
+}
+
+template <int kMode, bool kInstr, int kInflight>
+__global__ void __launch_bounds__(192) stream3_kernel(Stream3Params P) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
+  float *ring_x = reinterpret_cast<float *>(lds + bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4);
+  float *ring_y = ring_x + P.n_slots * 64;
+  for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
+  __syncthreads();
+  const uint32_t cb = lds_addr(cnt);
+  const int wave = wave_id();
+  if (wave == ROLE_LOAD) run_engine<ROLE_LOAD, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
+  else if (wave == ROLE_ADD) run_engine<ROLE_ADD, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
+  else run_engine<ROLE_STORE, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
+}
+
+template <int kMode, bool kInstr>
+void launch_variant(const Stream3Params &P, int n_wg, size_t lds, hipStream_t s) {
+  if (P.n_slots >= 32) hipLaunchKernelGGL((stream3_kernel<kMode, kInstr, 12>), dim3(n_wg), dim3(192), lds, s, P);
+  else hipLaunchKernelGGL((stream3_kernel<kMode, kInstr, 4>), dim3(n_wg), dim3(192), lds, s, P);
+}
+
+// --- host: match the plan against the family's loop structure --------------
+struct HostEngine {
+  std::vector<int> o_pre, m_pre, m_post, o_post;
+  int inner = -1;
+};
+
+bool collect(const bfs_plan *p, int loop, int e, bool before_child, std::vector<int> &out) {
+  out.clear();
+  bool seen_loop = false;
+  for (int it = p->body_off[loop]; it < p->body_off[loop + 1]; ++it) {
+    if (p->body_kind[it] == 1) { seen_loop = true; continue; }
+    if (seen_loop == before_child) continue;
+    int b = p->body_id[it];
+    for (int j = p->block_off[b]; j < p->block_off[b + 1]; ++j) {
+      int ins = p->block_instrs[j];
+      if (p->instr_engine[ins] != e) continue;
+      if (p->instr_opcode[ins] != 0 || (int)out.size() == kMaxNops) return false;
+      out.push_back(ins);
+    }
+  }
+  return true;
+}
+
+}  // namespace
+
+namespace bfs {
+
+bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
+                          const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream,
+                          uint32_t *dbg, int64_t dbg_cap, const bfs_run_opts &o) {
+  if (p->n_loops != 4 || p->loop_parent[1] != 0 || p->loop_parent[2] != 1 || p->loop_parent[3] != 2)
+    return fail(BFS_E_UNSUPPORTED, "stream3: loops must be top -> O -> M -> I");
+  if (p->n_engines != 3 || p->waves_per_engine[0] != 1 || p->waves_per_engine[1] != 1 || p->waves_per_engine[2] != 1)
+    return fail(BFS_E_UNSUPPORTED, "stream3: three single-wave engines");
+  if (p->tile_elems != 64) return fail(BFS_E_UNSUPPORTED, "stream3: tile_elems must be 64");
+  if (!trips || !trip_off || nbufs < 3) return fail(BFS_E_INVALID, "stream3: needs trips and [base, x, y]");
+  for (int it = p->body_off[0]; it < p->body_off[1]; ++it)
+    if (p->body_kind[it] != 1) return fail(BFS_E_UNSUPPORTED, "stream3: top level must hold only loop O");
+  const std::vector<DevWait> dw = device_waits(p);
+  Stream3Params P{};
+  const int want_op[3] = {1, 4, 5};
+  int n_gen = -1, per_gen = -1;
+  float addc = 0.f;
+  for (int e = 0; e < 3; ++e) {
+    HostEngine H;
+    if (!collect(p, 1, e, true, H.o_pre) || !collect(p, 1, e, false, H.o_post) || !collect(p, 2, e, true, H.m_pre) ||
+        !collect(p, 2, e, false, H.m_post))
+      return fail(BFS_E_UNSUPPORTED, "stream3: O and M bodies may hold at most 4 no-op instructions per engine");
+    for (int it = p->body_off[3]; it < p->body_off[4]; ++it) {
+      if (p->body_kind[it] != 0) return fail(BFS_E_UNSUPPORTED, "stream3: I is innermost");
+      int b = p->body_id[it];
+      for (int j = p->block_off[b]; j < p->block_off[b + 1]; ++j) {
+        int ins = p->block_instrs[j];
+        if (p->instr_engine[ins] != e) continue;
+        if (H.inner != -1 || p->instr_opcode[ins] != want_op[e])
+          return fail(BFS_E_UNSUPPORTED, "stream3: I body must hold load (E0), add (E1), store (E2)");
+        H.inner = ins;
+        const int32_t *a = &p->instr_args[8 * ins];
+        if (a[2] != 2 || a[4] != 3 || (e != 1 && a[6] != 3))
+          return fail(BFS_E_UNSUPPORTED, "stream3: slots must be addressed by (r_M, rhat_I), tiles by r_I");
+        if (n_gen == -1) { n_gen = a[3]; per_gen = a[5]; }
+        if (a[3] != n_gen || a[5] != per_gen) return fail(BFS_E_UNSUPPORTED, "stream3: inconsistent ring geometry");
+        if (e == 1) addc = __builtin_bit_cast(float, a[7]);
+      }
+    }
+    if (H.inner == -1) return fail(BFS_E_UNSUPPORTED, "stream3: every engine needs its instruction in I");
+    // Resolve each instruction's waits into the launch arguments.
+    EngineCode &C = P.eng[e];
+    int nw = 0;
+    auto fill = [&](int ins, InstrSync &s) -> bool {
+      s.first = (int16_t)nw;
+      s.n = 0;
+      s.update = (int16_t)p->instr_update[ins];
+      for (int wi = p->instr_wait_off[ins]; wi < p->instr_wait_off[ins + 1]; ++wi) {
+        if (nw == kMaxWaitsPerEngine) return false;
+        if (!pack_wait(dw[p->instr_wait_list[wi]], C.waits[nw])) return false;
+        ++nw;
+        ++s.n;
+      }
+      return true;
+    };
+    bool ok = true;
+    for (size_t i = 0; i < H.o_pre.size(); ++i) ok &= fill(H.o_pre[i], C.o_pre[i]);
+    for (size_t i = 0; i < H.m_pre.size(); ++i) ok &= fill(H.m_pre[i], C.m_pre[i]);
+    for (size_t i = 0; i < H.m_post.size(); ++i) ok &= fill(H.m_post[i], C.m_post[i]);
+    for (size_t i = 0; i < H.o_post.size(); ++i) ok &= fill(H.o_post[i], C.o_post[i]);
+    C.n_o_pre = (int32_t)H.o_pre.size();
+    C.n_m_pre = (int32_t)H.m_pre.size();
+    C.n_m_post = (int32_t)H.m_post.size();
+    C.n_o_post = (int32_t)H.o_post.size();
+    ok &= fill(H.inner, C.inner);
+    if (!ok || C.inner.n > kMaxInnerWaits)
+      return fail(BFS_E_RESOURCE, "stream3: too many waits per engine (16) or per inner instruction (4)");
+  }
+  if (n_gen < 1 || per_gen < 1 || n_gen * per_gen > 64) return fail(BFS_E_RESOURCE, "stream3: at most 64 ring slots");
+  if (p->ring_slots[0] < n_gen * per_gen || p->ring_slots[1] < n_gen * per_gen)
+    return fail(BFS_E_INVALID, "stream3: ring_slots smaller than the addressed slots");
+  P.trips = trips;
+  P.trip_off = trip_off;
+  P.base = static_cast<const int64_t *>(bufs[0]);
+  P.x = static_cast<const float *>(bufs[1]);
+  P.y = static_cast<float *>(const_cast<void *>(bufs[2]));
+  P.dbg = dbg;
+  P.dbg_cap = dbg_cap;
+  P.err = img->err;
+  P.stats = o.dev_stats;
+  P.watchdog = o.watchdog_polls;
+  P.fault_dep = o.fault_dep;
+  P.fault_delta = o.fault_delta;
+  P.n_gen = n_gen;
+  P.per_gen = per_gen;
+  P.n_slots = n_gen * per_gen;
+  P.addc = addc;
+  const size_t lds_bytes = (size_t)kMaxSlots * kMaxWavesPerEngine * 4 + 2ull * P.n_slots * 64 * 4;
+  const bool instr = dbg || o.dev_stats || o.fault_dep >= 0;
+  hipStream_t s = (hipStream_t)stream;
+  if (p->mode == BFS_MODE_BARRIER) {
+    if (instr) launch_variant<BFS_MODE_BARRIER, true>(P, n_wg, lds_bytes, s);
+    else launch_variant<BFS_MODE_BARRIER, false>(P, n_wg, lds_bytes, s);
+  } else {
+    if (instr) launch_variant<BFS_MODE_BARRIER_FREE, true>(P, n_wg, lds_bytes, s);
+    else launch_variant<BFS_MODE_BARRIER_FREE, false>(P, n_wg, lds_bytes, s);
+  }
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(BFS_E_DEVICE, std::string("stream3 launch: ") + hipGetErrorString(err));
+  return BFS_OK;
+}
+
+}  // namespace bfs

@@ -1,0 +1,211 @@
+"""GPU parity of the synchronization path (interpreter and stream kernels).
+
+Thresholds, counters and indices must match the oracle bit-exactly; the
+tile-machine values must match within 1e-5 max-abs (fp32 stages) and the two
+synchronization modes must produce bit-identical outputs."""
+import copy
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import core  # noqa: E402
+from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
+from tests.gpu_util import compare_log_with_oracle, dev, log_records, trip_tensors  # noqa: E402
+from workloads import chain_workload, random_nest, stream_program, stream_workload  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+MODES = [("barrier_free", MODE_BARRIER_FREE), ("barrier", MODE_BARRIER)]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    bfs.lib()
+
+
+def _say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+def _run_tile_machine(w, plan, n_out, cap=0):
+    trips, toff = trip_tensors(w.trips)
+    base, x = dev(w.base), dev(w.x)
+    out = torch.zeros(n_out, dtype=torch.float32, device="cuda")
+    log = None
+    if cap:
+        log = torch.zeros(plan.debug_log_words(w.trips.n_wg, cap), dtype=torch.int32, device="cuda")
+    plan.run([base, x, out], trips, toff, w.trips.n_wg, debug_log=log, debug_capacity=cap)
+    plan.status()
+    return out.cpu().numpy(), (log.cpu().numpy().view(np.uint32) if cap else None)
+
+
+# ---------------------------------------------------------------------------
+# cfg1: two-engine chain on the interpreter
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_chain_interp_parity(seed):
+    _say(f"[chain] seed={seed}")
+    w = chain_workload(seed)
+    trips, off = w.trips.flat()
+    res = core.run(w.prog, trips, off[0], 0, w.base, w.x, 256)
+    outs = {}
+    for name, mode in MODES:
+        plan = Plan(w.prog, mode)
+        out, logw = _run_tile_machine(w, plan, 256, cap=512)
+        assert np.abs(out - res.out).max() <= 1e-5
+        logs = log_records(plan, logw, 1, 512)
+        n = compare_log_with_oracle(w.prog, plan, logs, {0: res.recs}, name)
+        assert n > 0
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# random tiny nests: every threshold the GPU computes equals the brute force
+# ---------------------------------------------------------------------------
+def _allocatable(prog):
+    ok = []
+    for d in prog.deps:
+        q = copy.deepcopy(prog)
+        q.deps = [d]
+        try:
+            Plan(q)
+            ok.append(d)
+        except BfsError:
+            pass
+    return ok
+
+
+def test_random_nests_interp_thresholds():
+    checked = expected = 0
+    for seed in range(150):
+        prog, tt = random_nest(seed, max_trip=4 if seed % 2 else 3)
+        prog.deps = _allocatable(prog)
+        if not prog.deps:
+            continue
+        trips, off = tt.flat()
+        res = core.run(prog, trips, off[0], 0)
+        for name, mode in MODES:
+            plan = Plan(prog, mode)
+            if mode == MODE_BARRIER_FREE:
+                expected += len(res.recs)
+            else:
+                same = [w["same_region"] for w in plan.static_waits()]
+                expected += sum(1 for r in res.recs if same[int(r["dep"])])
+            t_trips, t_off = trip_tensors(tt)
+            base = torch.zeros(1, dtype=torch.int64, device="cuda")
+            x = torch.zeros(64, dtype=torch.float32, device="cuda")
+            out = torch.zeros(64, dtype=torch.float32, device="cuda")
+            cap = 256
+            log = torch.zeros(plan.debug_log_words(1, cap), dtype=torch.int32, device="cuda")
+            plan.run([base, x, out], t_trips, t_off, 1, debug_log=log, debug_capacity=cap)
+            plan.status()
+            logs = log_records(plan, log.cpu().numpy().view(np.uint32), 1, cap)
+            checked += compare_log_with_oracle(prog, plan, logs, {0: res.recs}, name)
+    assert checked == expected and checked > 500
+
+
+# ---------------------------------------------------------------------------
+# cfg2: sync-bound stream kernel
+# ---------------------------------------------------------------------------
+def test_stream_small_parity_and_thresholds():
+    w = stream_workload(seed=0, n_wg=6, outer=12)
+    trips, off = w.trips.flat()
+    recs = {g: core.run(w.prog, trips, off[g], g).recs for g in range(w.trips.n_wg)}
+    ref = w.x.reshape(-1) + np.float32(1.0)          # the same sum rounded to fp32
+    ref64 = core.values(w.prog, trips, off, w.base, w.x, w.n_tiles * 64)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[stream-small] mode={name}")
+        plan = Plan(w.prog, mode)
+        out, logw = _run_tile_machine(w, plan, w.n_tiles * 64, cap=4096)
+        assert np.abs(out.astype(np.float64) - ref64).max() <= 1e-5
+        assert np.array_equal(out, ref)
+        logs = log_records(plan, logw, w.trips.n_wg, 4096)
+        assert compare_log_with_oracle(w.prog, plan, logs, recs, name) > 0
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"], outs["barrier"])
+
+
+def test_stream_interp_cross_check():
+    """The generic interpreter runs the same stream program to the same values."""
+    w = stream_workload(seed=3, n_wg=3, outer=5)
+    p = copy.deepcopy(w.prog)
+    p.kernel = "interp"
+    _say("[stream-interp]")
+    out, _ = _run_tile_machine(w, Plan(p), w.n_tiles * 64)
+    assert np.array_equal(out, w.x.reshape(-1) + np.float32(1.0))
+
+
+def test_stream_full_size_thresholds_sampled_workgroups():
+    """Full per-workgroup nest (outer 256) on a few workgroups with the log on."""
+    w = stream_workload(seed=1, n_wg=2, outer=256)
+    trips, off = w.trips.flat()
+    recs = {g: core.run(w.prog, trips, off[g], g).recs for g in range(2)}
+    for name, mode in MODES:
+        _say(f"[stream-full-log] mode={name}")
+        plan = Plan(w.prog, mode)
+        cap = 1 << 15
+        out, logw = _run_tile_machine(w, plan, w.n_tiles * 64, cap=cap)
+        assert np.array_equal(out, w.x.reshape(-1) + np.float32(1.0))
+        assert compare_log_with_oracle(w.prog, plan, log_records(plan, logw, 2, cap), recs, name) > 10000
+
+
+@pytest.mark.parametrize("seed", [0])
+def test_stream_full_size_values(seed):
+    """The benchmark configuration: 1024 workgroups, 3-level nest 256 x U[1,16] x U[1,4]."""
+    _say(f"[stream-full] seed={seed}: generating")
+    w = stream_workload(seed=seed)
+    trips, toff = trip_tensors(w.trips)
+    base, x = dev(w.base), dev(w.x)
+    ref = torch.from_numpy(w.x.reshape(-1)).cuda() + 1.0
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[stream-full] mode={name}")
+        plan = Plan(w.prog, mode)
+        y = torch.full((w.n_tiles * 64,), float("nan"), dtype=torch.float32, device="cuda")
+        plan.run([base, x, y], trips, toff, w.trips.n_wg)
+        plan.status()
+        assert torch.equal(y, ref)
+        outs[name] = y
+    assert torch.equal(outs["barrier_free"], outs["barrier"])
+
+
+# ---------------------------------------------------------------------------
+# failure handling: an unsatisfiable wait is reported, and the kernel ends
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("kernel", ["interp", "stream3"])
+def test_watchdog_reports_deadlock(kernel):
+    _say(f"[watchdog] {kernel}")
+    if kernel == "interp":
+        w = chain_workload(0)
+        n_out = 256
+    else:
+        w = stream_workload(seed=0, n_wg=2, outer=3)
+        n_out = w.n_tiles * 64
+    plan = Plan(w.prog)
+    trips, toff = trip_tensors(w.trips)
+    base, x = dev(w.base), dev(w.x)
+    out = torch.zeros(n_out, dtype=torch.float32, device="cuda")
+    plan.run([base, x, out], trips, toff, w.trips.n_wg, watchdog_polls=2000, fault_dep=0, fault_delta=1 << 20)
+    with pytest.raises(BfsError) as e:
+        plan.status()
+    assert e.value.status == bfs.E_DEADLOCK
+    # the plan is usable again afterwards
+    plan.run([base, x, out], trips, toff, w.trips.n_wg)
+    plan.status()
+
+
+def test_stream_program_shape_is_checked():
+    p = stream_program()
+    p.instrs[p.instr_id("ADD")].opcode = 2
+    plan = Plan(p)
+    t = torch.zeros(4, dtype=torch.int32, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t, t, t], t, t, 1)
+    assert e.value.status == bfs.E_UNSUPPORTED

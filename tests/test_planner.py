@@ -1,0 +1,210 @@
+"""Planner (bfs_plan_create and friends) against the CPU oracle; no GPU needed.
+
+Thresholds must equal the oracle's brute force of Eq. (1) bit-exactly, for
+every consumer instance, in both counter units (per-loop semaphore values,
+Section 5.5) and completion counts (per-instruction semaphores, Section 5.4),
+and the barrier-mode static ordinals (Section 3.4)."""
+import copy
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import core
+from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER, MODE_BARRIER_FREE,
+                                  BfsError, Plan, bfs)
+from tests import fixtures
+from workloads import (OP_NOP, ProgramBuilder, TripTables, chain_workload, draw_trips, random_nest,
+                       stream_workload)
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _accepted_deps(prog):
+    """Split deps into accepted / rejected by planning each one alone."""
+    ok, rejected = [], []
+    for d in prog.deps:
+        q = copy.deepcopy(prog)
+        q.deps = [d]
+        try:
+            Plan(q)
+            ok.append(d)
+        except BfsError as e:
+            rejected.append((d, e.status))
+    return ok, rejected
+
+
+def _paper_case(prog, d):
+    """The allocatable cases of Section 5.2, restated: returns 'C1', 'C2',
+    'C3', 'order' or 'not-allocatable' for dependency d."""
+    p, c, k = d
+    par = {}
+    for l, items in enumerate(prog.body):
+        for kind, bid in items:
+            if kind == 0:
+                for i in prog.blocks[bid]:
+                    par[i] = l
+
+    def path(l):
+        out = []
+        while l >= 0:
+            out.append(l)
+            l = prog.loop_parent[l]
+        return out[::-1]
+    pp, pc = path(par[p]), path(par[c])
+    S = [a for a, b in zip(pp, pc) if a == b][-1]
+
+    def pos(i):
+        l = par[i]
+        if l == S:
+            for j, (kind, bid) in enumerate(prog.body[S]):
+                if kind == 0 and i in prog.blocks[bid]:
+                    return (j, prog.blocks[bid].index(i))
+        child = l
+        while prog.loop_parent[child] != S:
+            child = prog.loop_parent[child]
+        return (prog.body[S].index((1, child)), -1)
+    fwd = pos(p) < pos(c)
+    if par[p] == S:
+        return "order" if (not fwd and k == 0) else "C1"
+    if fwd:
+        return "C2" if k == 0 else "not-allocatable"
+    if k == 0:
+        return "order"
+    return "C3" if k == 1 else "not-allocatable"
+
+
+def _check_against_oracle(prog, tt):
+    trips, off = tt.flat()
+    res = core.run(prog, trips, off[0], 0)
+    pl = Plan(prog, MODE_BARRIER_FREE, ALLOC_PER_LOOP)
+    pi = Plan(prog, MODE_BARRIER_FREE, ALLOC_PER_INSTR)
+    pb = Plan(prog, MODE_BARRIER, ALLOC_PER_LOOP)
+    for rec in res.recs:
+        d, rP, rh = int(rec["dep"]), int(rec["r_P"]), int(rec["rhat_S"])
+        assert pl.eval_threshold(d, rP, rh) == rec["sem_thr"], (d, rec)
+        assert pi.eval_threshold(d, rP, rh) == rec["count_thr"], (d, rec)
+        assert pb.eval_threshold(d, rP, rh) == rec["barrier_thr"], (d, rec)
+        assert rec["order_ok"]
+    return len(res.recs)
+
+
+def test_random_nests_bit_exact():
+    n_checked, cases = 0, set()
+    for seed in range(1200):
+        prog, tt = random_nest(seed, max_trip=4 if seed % 2 else 3)
+        ok, rejected = _accepted_deps(prog)
+        for d, st in rejected:
+            want = _paper_case(prog, d)
+            assert want in ("order", "not-allocatable"), (seed, d, want)
+            assert st == (bfs.E_ORDER if want == "order" else bfs.E_NOT_ALLOCATABLE)
+        for d in ok:
+            cases.add(_paper_case(prog, d))
+        if not ok:
+            continue
+        prog.deps = ok
+        n_checked += _check_against_oracle(prog, tt)
+    assert n_checked > 5000
+    assert cases == {"C1", "C2", "C3"}
+
+
+@pytest.mark.parametrize("name", fixtures.all_fixtures())
+def test_paper_figures_through_planner(name):
+    fx, prog, tt = fixtures.load(name)
+    _check_against_oracle(prog, tt)
+
+
+def test_per_scope_figure_formula():
+    """Fig. per-scope-example-alloc: w = isGT(rhat_A, 0) * (2 * r_A)."""
+    fx, prog, tt = fixtures.load("fig_per_scope.json")
+    f = Plan(prog).formulas()[0]
+    assert (f["kase"], f["N"], f["K"], f["k"], f["needs_mask"]) == (1, 2, 2, 0, 0)
+    p = Plan(prog)
+    assert [p.eval_threshold(0, a, a) for a in (1, 2, 3)] == [2, 4, 6]
+    fi = Plan(prog, alloc=ALLOC_PER_INSTR)
+    assert [fi.eval_threshold(0, a, a) for a in (1, 2, 3)] == [1, 2, 3]
+
+
+def test_dep_nested_cases():
+    fx, prog, tt = fixtures.load("fig_dep_nested.json")
+    f = Plan(prog).formulas()
+    assert f[0]["kase"] == 2 and f[1]["kase"] == 3
+    assert f[0]["loop_P"] == f[1]["loop_P"] == prog.loop_id("B")
+
+
+def test_workload_programs():
+    for prog, tt in [(chain_workload(0).prog, chain_workload(0).trips)]:
+        _check_against_oracle(prog, tt)
+    s = stream_workload(seed=0, n_wg=1, outer=5, with_data=False)
+    _check_against_oracle(s.prog, s.trips)
+
+
+def test_rejections():
+    b = ProgramBuilder("interp", 2)
+    with b.loop("A"):
+        b.instr(1, OP_NOP, name="c")
+        b.instr(0, OP_NOP, name="p")
+    b.dep("p", "c", 0)                       # same-region backward at offset 0
+    with pytest.raises(BfsError) as e:
+        Plan(b.build())
+    assert e.value.status == bfs.E_ORDER
+
+    b = ProgramBuilder("interp", 2)
+    with b.loop("A"):
+        with b.loop("B"):
+            b.instr(0, OP_NOP, name="p")
+        b.instr(1, OP_NOP, name="c")
+    b.dep("p", "c", 1)                       # nested forward with offset 1
+    with pytest.raises(BfsError) as e:
+        Plan(b.build())
+    assert e.value.status == bfs.E_NOT_ALLOCATABLE
+
+    b = ProgramBuilder("interp", 2)
+    with b.loop("A"):
+        b.instr(1, OP_NOP, name="c")
+        with b.loop("B"):
+            b.instr(0, OP_NOP, name="p")
+    b.dep("p", "c", 2)                       # nested backward with offset 2
+    with pytest.raises(BfsError) as e:
+        Plan(b.build())
+    assert e.value.status == bfs.E_NOT_ALLOCATABLE
+
+
+def test_malformed_programs():
+    w = chain_workload(0)
+    base = w.prog.flat()
+    bad = dict(base)
+    bad["instr_engine"] = [0, 5, 1, 1]       # engine out of range
+    with pytest.raises(BfsError) as e:
+        Plan(bad)
+    assert e.value.status == bfs.E_INVALID
+    bad = dict(base)
+    bad["deps"] = [(0, 0, 0)]                # self dependency
+    with pytest.raises(BfsError):
+        Plan(bad)
+    bad = dict(base)
+    bad["loop_parent"] = [-1, 0, 0]          # loop listed outside its parent
+    with pytest.raises(BfsError):
+        Plan(bad)
+
+
+def test_resource_stats():
+    s = stream_workload(seed=0, n_wg=1, outer=2, with_data=False)
+    pl, pi, pb = Plan(s.prog), Plan(s.prog, alloc=ALLOC_PER_INSTR), Plan(s.prog, MODE_BARRIER)
+    st_l, st_i, st_b = pl.stats(), pi.stats(), pb.stats()
+    assert st_l["salu_ops_per_wait"] == 5 and st_i["salu_ops_per_wait"] == 3
+    assert st_b["n_counters"] == 3 and st_b["regs_per_engine"] == 0
+    assert st_l["n_waits"] == len(s.prog.deps)
+    # one counter per (loop, engine) pair that some dependency reads
+    pairs = {(f["loop_P"], f["prd_engine"]) for f in pl.formulas()}
+    assert st_l["n_counters"] == len(pairs)
+
+
+def test_abi_exports_every_header_symbol():
+    hdr = open(os.path.join(ROOT, "include", "bfs.h")).read()
+    names = set(re.findall(r"^\s*(?:const\s+)?[a-z_]+\s*\*?\s*(bfs_[a-z_]+)\s*\(", hdr, re.M))
+    assert names == set(bfs.EXPORTED), names ^ set(bfs.EXPORTED)
+    L = bfs.lib()
+    for n in names:
+        assert hasattr(L, n), n

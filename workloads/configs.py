@@ -139,7 +139,7 @@ def chain_workload(seed: int = 0, outer: int = 16, inner_max: int = 8, n_wg: int
 # ---------------------------------------------------------------------------
 # cfg2: sync-bound 3-engine stream, 1024 workgroups
 # ---------------------------------------------------------------------------
-def stream_program(n_gen: int = 4, per_gen: int = 4) -> Program:
+def stream_program(n_gen: int = 8, per_gen: int = 4) -> Program:
     """Load / vector-add / store engines over a 3-level nest O{M{I{...}}}.
 
     Ring slot = ((r_M - 1) % n_gen) * per_gen + (rhat_I - 1): each M iteration
@@ -194,7 +194,7 @@ class StreamWorkload:
 
 
 def stream_workload(seed: int = 0, n_wg: int = 1024, outer: int = 256, mid_max: int = 16,
-                    inner_max: int = 4, n_gen: int = 4, with_data: bool = True) -> StreamWorkload:
+                    inner_max: int = 4, n_gen: int = 8, with_data: bool = True) -> StreamWorkload:
     prog = stream_program(n_gen=n_gen, per_gen=inner_max)
     per = []
     for w in range(n_wg):
