@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--n-gen", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--modes", default="barrier_free,barrier")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the timed region, run one plain device copy of this many MiB "
+                         "(reference dispatch for HBM traffic counters)")
     return ap.parse_args()
 
 
@@ -60,6 +63,29 @@ def time_mode(plan, bufs, trips, toff, n_wg, steps, warmup):
     per = [s.elapsed_time(e) for s, e in zip(starts, ends)]   # ms, per launch
     return {"ms_mean": sum(per) / len(per), "ms_min": min(per), "ms_median": sorted(per)[len(per) // 2],
             "wall_ms_per_step": 1e3 * wall / steps}
+
+
+def kernel_source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("kern_stream3.hip", "device_sync.h"):
+        with open(os.path.join(ROOT, "paper_2608_13757_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic():
+    """HBM bytes per launch of the stream kernel measured with rocprofv3
+    FETCH_SIZE / WRITE_SIZE (profiles/stream3_traffic.json), or None when the
+    kernel source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "stream3_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_digest") != kernel_source_digest():
+        return None
+    return rec.get("traffic_bytes_per_launch")
 
 
 def cpu_baseline(w, budget_s=20.0):
@@ -145,8 +171,17 @@ def main():
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
         out["barrier_ops_per_s"] = ops / (res["barrier"]["ms_mean"] * 1e-3)
+    tr = recorded_traffic()
+    if tr is not None:
+        out["roofline"]["traffic"] = tr
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
+    if a.copy_calibration_mib:
+        src = torch.empty(a.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
     print(json.dumps(out), flush=True)
 
 

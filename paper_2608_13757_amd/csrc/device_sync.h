@@ -62,9 +62,18 @@ __device__ __forceinline__ uint32_t lds_poll(uint32_t addr) {
   return v;
 }
 
-// Increment a counter word by n (one lane issues the add).
+// Increment a counter word by n: the add is issued with only lane 0 active
+// (the exec mask is saved and restored around it).
 __device__ __forceinline__ void lds_add(uint32_t addr, uint32_t n) {
-  if (lane_id() == 0) asm volatile("ds_add_u32 %0, %1" ::"v"(addr), "v"(n) : "memory");
+  uint64_t saved;
+  asm volatile(
+      "s_mov_b64 %0, exec\n\t"
+      "s_mov_b64 exec, 1\n\t"
+      "ds_add_u32 %1, %2\n\t"
+      "s_mov_b64 exec, %0"
+      : "=&s"(saved)
+      : "v"(addr), "v"(n)
+      : "memory");
 }
 
 __device__ __forceinline__ void lds_store(uint32_t addr, uint32_t v) {
@@ -155,6 +164,24 @@ __device__ __forceinline__ WaitResult wait_geq(uint32_t addr, int nw, uint32_t t
       return r;
     }
     __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Poll one counter word until it reaches thr, sleeping between polls.  The
+// loop body is a handful of scalar instructions, so a blocked wave takes few
+// issue slots from the working waves of its compute unit.  Returns the last
+// value seen; ok = false when max_polls polls did not suffice.
+__device__ __forceinline__ WaitResult spin_geq(uint32_t addr, uint32_t thr, uint64_t max_polls) {
+  uint64_t polls = 0;
+  while (true) {
+    const uint32_t v = uniform(lds_poll(addr));
+    if (v >= thr) return WaitResult{v, true};
+    if (++polls > max_polls) return WaitResult{v, false};
+    // back off: 64, 128, 256 then 512 clocks between polls
+    if (polls < 4) __builtin_amdgcn_s_sleep(1);
+    else if (polls < 16) __builtin_amdgcn_s_sleep(2);
+    else if (polls < 64) __builtin_amdgcn_s_sleep(4);
+    else __builtin_amdgcn_s_sleep(8);
   }
 }
 

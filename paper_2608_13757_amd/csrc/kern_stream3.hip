@@ -45,7 +45,7 @@ namespace {
 
 constexpr int kMaxNops = 4;
 constexpr int kMaxWaitsPerEngine = 16;
-constexpr int kMaxInnerWaits = 4;
+constexpr int kMaxInnerWaits = 2;
 
 struct InstrSync {
   int16_t first;     // index of its first wait in the engine's wait list
@@ -93,12 +93,12 @@ struct Engine {
   uint32_t h1 = 0, h2 = 0, h3 = 0;        // rhat of O, M, I
   uint32_t cnt_base;
   int wave, wg;
-  bool aborted = false;
+  uint32_t aborted = 0;                   // a wait gave up: finish without waiting
   uint32_t *log = nullptr;
   uint32_t nlog = 0;
   int pending = 0;                        // issued, not yet retired (loads or LDS ops)
   uint32_t own_counter = 0;               // LDS address of the inner instruction's counter
-  bool has_own_counter = false;
+  uint32_t has_own_counter = 0;
   WaveStats st;
 
   __device__ Engine(const Stream3Params &p, const EngineCode &c, uint32_t cb, int w, int g)
@@ -129,7 +129,7 @@ struct Engine {
     wait_vm<kInflight - 1>();
     if (kInstr && st.on) st.own_loads += now_ticks() - t0;
     if (has_own_counter) lds_add(own_counter, 1u);
-    pending -= 1;
+    pending = (int)uniform((uint32_t)pending - 1u);
   }
   // Retire everything held.
   __device__ __forceinline__ void retire_all() {
@@ -168,11 +168,11 @@ struct Engine {
       }
       retire_some();
     }
-    WaitResult res = wait_geq(addr, 1, thr, P.watchdog);
+    WaitResult res = spin_geq(addr, thr, P.watchdog);
     if (kInstr && st.on) st.blocked += now_ticks() - t0;
     if (!res.ok) {
       report_deadlock(P.err, dep, (uint32_t)wg, instance, thr, res.observed, (uint32_t)wave);
-      aborted = true;
+      aborted = 1u;
     }
     return res;
   }
@@ -225,6 +225,57 @@ struct Engine {
   }
 };
 
+// One wait of the innermost instruction in the form evaluated per iteration.
+// Within one trip of loop I the threshold of Eq. 5 is
+//     thr(i) = [rhat_I > kk] * max(run(i), 0),   run(i) = N * r_P - c,
+// where run grows by N per iteration when P is loop I and is constant
+// otherwise, and kk is k when the mask reads rhat_I, 0 when no mask applies,
+// and "never" when a mask on an outer loop is 0 for this trip.  Everything
+// except run and the comparison is computed once at the loop statement
+// (loop-invariant code motion of the wait value, Section 6.2); the values
+// are exactly those of Eq. 5.
+struct InnerWait {
+  uint32_t packed_w0, packed_w1, packed_w2, packed_w3;
+  uint32_t run;        // N * r_P - c for the current iteration (as int)
+  uint32_t step;       // N when P is loop I, else 0
+  uint32_t kk;         // threshold is 0 while rhat_I <= kk
+  uint32_t seen;       // last observed counter value
+};
+
+__device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait &w) {
+  InnerWait iw;
+  iw.packed_w0 = w.w0;
+  iw.packed_w1 = w.w1;
+  iw.packed_w2 = w.w2;
+  iw.packed_w3 = w.w3;
+  iw.run = 0;
+  iw.step = 0;
+  iw.kk = 0;
+  iw.seen = 0;
+  return iw;
+}
+
+// At the statement of loop I (before its first iteration): r_O, r_M, r_I and
+// rhat_O, rhat_M are the engine's registers; r_I has not been incremented yet.
+__device__ __forceinline__ void enter_inner(InnerWait &iw, uint32_t r1, uint32_t r2, uint32_t r3, uint32_t h1,
+                                            uint32_t h2) {
+  const uint32_t N = iw.packed_w1 & 0xffffu, K = iw.packed_w1 >> 16;
+  const uint32_t k = iw.packed_w2 & 0xffffu, sub = iw.packed_w2 >> 16;
+  const uint32_t lp = (iw.packed_w0 >> 8) & 0xffu, ls = (iw.packed_w0 >> 16) & 0xffu;
+  const uint32_t mask = (iw.packed_w0 >> 24) & 1u;
+  const uint32_t c = N * sub + (N - K);
+  // run before the first iteration; the loop adds step before each evaluation
+  const uint32_t rP = lp == 3u ? r3 : sel4(1u, r1, r2, r3, lp);
+  iw.step = lp == 3u ? N : 0u;
+  iw.run = uniform(N * rP - c);
+  uint32_t kk = 0;
+  if (mask) {
+    if (ls == 3u) kk = k;
+    else kk = (sel4(1u, h1, h2, 0u, ls) > k) ? 0u : 0xffffffffu;
+  }
+  iw.kk = uniform(kk);
+}
+
 template <int kRole, int kMode, bool kInstr, int kInflight>
 __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_base, float *ring_x, float *ring_y) {
   const int wave = kRole;
@@ -239,28 +290,29 @@ __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_
       E.st.t_start = now_ticks();
     }
   }
-  // The innermost instruction's waits, held in registers for the whole run.
   const int n_iw = C.inner.n;
-  bfs::PackedWait iw[kMaxInnerWaits];
-  uint32_t seen[kMaxInnerWaits];
+  InnerWait iw[kMaxInnerWaits];
 #pragma unroll
-  for (int j = 0; j < kMaxInnerWaits; ++j) {
-    iw[j] = j < n_iw ? C.waits[C.inner.first + j] : bfs::PackedWait{0, 0, 0, 0};
-    seen[j] = 0;
-  }
+  for (int j = 0; j < kMaxInnerWaits; ++j)
+    iw[j] = make_inner(j < n_iw ? C.waits[C.inner.first + j] : bfs::PackedWait{0, 0, 0, 0});
   if (C.inner.update >= 0) {
     E.own_counter = E.counter_addr((uint32_t)C.inner.update);
-    E.has_own_counter = true;
+    E.has_own_counter = 1u;
   }
   const int64_t *toff = P.trip_off + (int64_t)wg * 4;
   const int64_t tbase = ldc(P.base + wg);
-  const uint32_t xs = lds_addr(ring_x), ys = lds_addr(ring_y);
-  const float addc = P.addc;
+  // per-lane addresses of the rings and of this workgroup's tiles
+  const uint32_t xl = lds_addr(ring_x) + 4u * lane, yl = lds_addr(ring_y) + 4u * lane;
+  const float *xg = P.x + tbase * 64 + lane;
+  float *yg = P.y + tbase * 64 + lane;
+  float addc;   // held in a vector register for the whole run
+  asm volatile("v_mov_b32 %0, %1" : "=v"(addc) : "s"(P.addc));
   const uint32_t per_gen = (uint32_t)P.per_gen, n_gen = (uint32_t)P.n_gen;
 
   E.sync_point();                                         // before loop O
   const uint32_t trip_o = (uint32_t)ldc(P.trips + ldc(toff + 1));
   const int64_t off_m = ldc(toff + 2), off_i = ldc(toff + 3);
+  uint32_t gen = 0;                                       // (r_M - 1) % n_gen
   for (uint32_t o = 0; o < trip_o; ++o) {
     E.r1 += 1;
     E.h1 = o + 1;
@@ -273,48 +325,77 @@ __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_
       E.nops(C.m_pre, C.n_m_pre, E.r2 - 1);
       E.sync_point();                                     // before loop I
       const uint32_t trip_i = (uint32_t)ldc(P.trips + off_i + E.r2 - 1);
-      const uint32_t gen = ((E.r2 - 1) % n_gen) * per_gen;
+      // loop-invariant parts of the inner waits for this trip of I
+      if (kMode == BFS_MODE_BARRIER_FREE) {
+#pragma unroll
+        for (int j = 0; j < kMaxInnerWaits; ++j)
+          if (j < n_iw) enter_inner(iw[j], E.r1, E.r2, E.r3, E.h1, E.h2);
+      }
+      uint32_t slot = gen * per_gen, lo = 0;
       for (uint32_t i = 0; i < trip_i; ++i) {
         E.r3 += 1;
         E.h3 = i + 1;
         const uint32_t instance = E.r3 - 1;
 #pragma unroll
-        for (int j = 0; j < kMaxInnerWaits; ++j)
-          if (j < n_iw) seen[j] = E.wait_one(iw[j], E.threshold(iw[j]), seen[j], instance);
-        const uint32_t slot = gen + (i % per_gen);
-        const int64_t tile = tbase + (int64_t)E.r3 - 1;
+        for (int j = 0; j < kMaxInnerWaits; ++j) {
+          if (j < n_iw) {
+            uint32_t thr;
+            if (kMode == BFS_MODE_BARRIER) {
+              thr = ((iw[j].packed_w0 >> 25) & 1u) ? (iw[j].packed_w3 >> 16) : 0u;
+            } else {
+              iw[j].run = uniform(iw[j].run + iw[j].step);
+              thr = (E.h3 > iw[j].kk && (int)iw[j].run > 0) ? iw[j].run : 0u;
+            }
+            const uint32_t dep = iw[j].packed_w3 & 0xffffu;
+            if (kInstr && (int)dep == P.fault_dep) thr += (uint32_t)P.fault_delta;
+            if (thr > iw[j].seen || (kInstr && E.log)) {
+              uint32_t obs = 0;
+              if (!E.aborted && thr > 0) {
+                const uint32_t addr = E.counter_addr(iw[j].packed_w0 & 0xffu);
+                obs = uniform(lds_poll(addr));
+                if (kInstr && E.st.on) E.st.polls += 1;
+                if (obs < thr) obs = E.block(addr, thr, dep, instance).observed;
+                iw[j].seen = obs;
+              }
+              E.logit(dep, instance, thr, obs);
+            }
+          }
+        }
         if (!E.aborted) {
           if (kRole == ROLE_LOAD) {
-            __builtin_amdgcn_global_load_lds((const void *)(P.x + tile * 64 + lane),
-                                             (BFS_LDS void *)(ring_x + slot * 64), 4, 0, 0);
-            E.pending += 1;
+            __builtin_amdgcn_global_load_lds((const void *)(xg + (int64_t)instance * 64),
+                                             (BFS_LDS void *)(ring_x + (slot + lo) * 64), 4, 0, 0);
+            E.pending = (int)uniform((uint32_t)E.pending + 1u);
             if (E.pending == kInflight) E.retire_oldest_of_full();
           } else if (kRole == ROLE_ADD) {
             float v;
             asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-                         : "=v"(v) : "v"(xs + 4u * (slot * 64 + lane)) : "memory");
+                         : "=v"(v) : "v"(xl + 256u * (slot + lo)) : "memory");
             // the read returned, so every earlier LDS write of this wave is done
-            if (E.pending > 0 && E.has_own_counter) lds_add(E.own_counter, (uint32_t)E.pending);
+            if (E.pending > 0) lds_add(E.own_counter, 1u);
             v = v + addc;
-            asm volatile("ds_write_b32 %0, %1" ::"v"(ys + 4u * (slot * 64 + lane)), "v"(v) : "memory");
-            E.pending = 1;
+            asm volatile("ds_write_b32 %0, %1" ::"v"(yl + 256u * (slot + lo)), "v"(v) : "memory");
+            E.pending = (int)E.has_own_counter;
           } else {
             float v;
             asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-                         : "=v"(v) : "v"(ys + 4u * (slot * 64 + lane)) : "memory");
-            __builtin_nontemporal_store(v, P.y + tile * 64 + lane);
+                         : "=v"(v) : "v"(yl + 256u * (slot + lo)) : "memory");
+            __builtin_nontemporal_store(v, yg + (int64_t)instance * 64);
             // the slot has been read: the store retires now
             if (E.has_own_counter) lds_add(E.own_counter, 1u);
           }
-        } else if (E.has_own_counter) {
-          lds_add(E.own_counter, 1u);
+        } else {
+          E.retire_all();
+          if (E.has_own_counter) lds_add(E.own_counter, 1u);
         }
-        E.sync_point();                                   // end of an iteration of I
+        lo = (lo + 1 == per_gen) ? 0u : lo + 1;
         if (kMode == BFS_MODE_BARRIER) {
+          E.sync_point();                                 // end of an iteration of I
 #pragma unroll
-          for (int j = 0; j < kMaxInnerWaits; ++j) seen[j] = 0;   // counters were reset
+          for (int j = 0; j < kMaxInnerWaits; ++j) iw[j].seen = 0;   // counters were reset
         }
       }
+      gen = (gen + 1 == n_gen) ? 0u : gen + 1;
       E.nops(C.m_post, C.n_m_post, E.r2 - 1);
       E.sync_point();                                     // end of an iteration of M
     }
@@ -349,6 +430,9 @@ __global__ void __launch_bounds__(192) stream3_kernel(Stream3Params P) {
   __syncthreads();
   const uint32_t cb = lds_addr(cnt);
   const int wave = wave_id();
+  // The add engine has the most work per tile; it wins issue arbitration
+  // against the load and store waves, which mostly poll.
+  if (wave == ROLE_ADD) __builtin_amdgcn_s_setprio(2);
   if (wave == ROLE_LOAD) run_engine<ROLE_LOAD, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
   else if (wave == ROLE_ADD) run_engine<ROLE_ADD, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
   else run_engine<ROLE_STORE, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
@@ -452,7 +536,7 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
     C.n_o_post = (int32_t)H.o_post.size();
     ok &= fill(H.inner, C.inner);
     if (!ok || C.inner.n > kMaxInnerWaits)
-      return fail(BFS_E_RESOURCE, "stream3: too many waits per engine (16) or per inner instruction (4)");
+      return fail(BFS_E_RESOURCE, "stream3: too many waits per engine (16) or per inner instruction (2)");
   }
   if (n_gen < 1 || per_gen < 1 || n_gen * per_gen > 64) return fail(BFS_E_RESOURCE, "stream3: at most 64 ring slots");
   if (p->ring_slots[0] < n_gen * per_gen || p->ring_slots[1] < n_gen * per_gen)

@@ -113,8 +113,9 @@ def test_random_nests_interp_thresholds():
 # ---------------------------------------------------------------------------
 # cfg2: sync-bound stream kernel
 # ---------------------------------------------------------------------------
-def test_stream_small_parity_and_thresholds():
-    w = stream_workload(seed=0, n_wg=6, outer=12)
+@pytest.mark.parametrize("inner_war", [False, True])
+def test_stream_small_parity_and_thresholds(inner_war):
+    w = stream_workload(seed=0, n_wg=6, outer=12, inner_war=inner_war)
     trips, off = w.trips.flat()
     recs = {g: core.run(w.prog, trips, off[g], g).recs for g in range(w.trips.n_wg)}
     ref = w.x.reshape(-1) + np.float32(1.0)          # the same sum rounded to fp32

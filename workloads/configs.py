@@ -139,11 +139,13 @@ def chain_workload(seed: int = 0, outer: int = 16, inner_max: int = 8, n_wg: int
 # ---------------------------------------------------------------------------
 # cfg2: sync-bound 3-engine stream, 1024 workgroups
 # ---------------------------------------------------------------------------
-def stream_program(n_gen: int = 8, per_gen: int = 4) -> Program:
+def stream_program(n_gen: int = 8, per_gen: int = 4, inner_war: bool = False) -> Program:
     """Load / vector-add / store engines over a 3-level nest O{M{I{...}}}.
 
     Ring slot = ((r_M - 1) % n_gen) * per_gen + (rhat_I - 1): each M iteration
-    owns one generation of per_gen slots (inner trips are at most per_gen).
+    owns one generation of per_gen slots.  With inner trips of at most per_gen
+    a slot is never reused inside one trip of I; ``inner_war`` adds the two
+    offset-per_gen dependencies that would order such reuse.
     Markers at the end of each M / O iteration let the acquire instructions of
     a later iteration wait for the previous users of a generation:
 
@@ -171,8 +173,11 @@ def stream_program(n_gen: int = 8, per_gen: int = 4) -> Program:
         b.instr(2, OP_NOP, name="MARKY_O")
     b.dep("LOAD", "ADD", 0)
     b.dep("ADD", "STORE", 0)
-    b.dep("ADD", "LOAD", per_gen)        # slot reuse inside one trip of I
-    b.dep("STORE", "ADD", per_gen)
+    if inner_war:
+        # slot reuse inside one trip of I; never owed when inner trips are at
+        # most per_gen (the hazard check proves the program covered without it)
+        b.dep("ADD", "LOAD", per_gen)
+        b.dep("STORE", "ADD", per_gen)
     b.dep("MARKX_M", "ACQX_M", n_gen)    # generation reuse across M iterations
     b.dep("MARKY_M", "ACQY_M", n_gen)
     b.dep("MARKX_O", "ACQX_O", 1)        # across O iterations
@@ -194,8 +199,9 @@ class StreamWorkload:
 
 
 def stream_workload(seed: int = 0, n_wg: int = 1024, outer: int = 256, mid_max: int = 16,
-                    inner_max: int = 4, n_gen: int = 8, with_data: bool = True) -> StreamWorkload:
-    prog = stream_program(n_gen=n_gen, per_gen=inner_max)
+                    inner_max: int = 4, n_gen: int = 8, with_data: bool = True,
+                    inner_war: bool = False) -> StreamWorkload:
+    prog = stream_program(n_gen=n_gen, per_gen=inner_max, inner_war=inner_war)
     per = []
     for w in range(n_wg):
         rng = rng_for(CFG_STREAM, seed, w)
