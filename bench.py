@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--n-gen", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--modes", default="barrier_free,barrier")
+    ap.add_argument("--workload", default="stream", choices=["stream", "gemm"],
+                    help="stream: the sync-bound microbenchmark (headline); gemm: 4096^3 bf16 GEMM + bias + GELU")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference dispatch for HBM traffic counters)")
@@ -113,6 +115,72 @@ def cpu_baseline(w, budget_s=20.0):
             "sample": f"{done} of {n_wg} workgroups ({iters} innermost iterations, {t_used:.1f} s)"}
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def bench_gemm(a):
+    """4096^3 bf16 GEMM + bias + GELU, one 256 x 256 tile per workgroup,
+    load / MFMA / epilogue engines; both synchronization modes."""
+    import numpy as np
+    import torch
+    from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
+    from workloads import GEMM_BK, GEMM_RING, gemm_program, gemm_trips
+    from workloads.tensors import gemm_inputs
+
+    m = n = k = 4096
+    gi = gemm_inputs(seed=a.seed, m=m, n=n, k=k)
+    dev = lambda bits: torch.from_numpy(bits.view(np.int16)).cuda()
+    A, Bt = dev(gi.a), dev(gi.bt)
+    bias = torch.from_numpy(gi.bias).cuda()
+    C = torch.empty(m * n, dtype=torch.int16, device="cuda")
+    tt = gemm_trips(m, n, k)
+    t_np, o_np = tt.flat()
+    trips, toff = torch.from_numpy(t_np).cuda(), torch.from_numpy(o_np).cuda()
+    res = {}
+    for name in a.modes.split(","):
+        mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
+        plan = Plan(gemm_program(m, n, k), mode)
+        res[name] = time_mode(plan, [A, Bt, bias, C], trips, toff, tt.n_wg, a.steps, a.warmup)
+    flop = 2.0 * m * n * k
+    bf = res.get("barrier_free", next(iter(res.values())))
+    ms = bf["ms_mean"]
+    tflops = flop / (ms * 1e-3) / 1e12
+    # context: the vendor library's bf16 matmul at the same shape (no bias / GELU)
+    x = torch.from_numpy(bf16_bits_as_f32(gi.a)).cuda().to(torch.bfloat16).reshape(m, k)
+    w = torch.from_numpy(bf16_bits_as_f32(gi.bt)).cuda().to(torch.bfloat16).reshape(n, k)
+    wt = w.t().contiguous()
+    for _ in range(3):
+        torch.matmul(x, wt)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        torch.matmul(x, wt)
+    e1.record()
+    torch.cuda.synchronize()
+    lib_ms = e0.elapsed_time(e1) / 10
+    out = {
+        "metric": METRIC, "value": tflops, "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "GEMM + bias + GELU, A, B bf16 4096 x 4096 ~ N(0,1)/64, 256 x 256 tiles, "
+                               f"K steps of {GEMM_BK} through a {GEMM_RING}-slot LDS ring", "m": m, "n": n, "k": k,
+                   "parallelism": "single GPU"},
+        "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
+        "library_matmul_tflops": flop / (lib_ms * 1e-3) / 1e12,
+    }
+    if "barrier" in res and "barrier_free" in res:
+        out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
+    print(json.dumps(out), flush=True)
+
+
+def bf16_bits_as_f32(bits):
+    import numpy as np
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -125,6 +193,9 @@ def main():
     from workloads import stream_workload
 
     torch.cuda.set_device(0)
+    if a.workload == "gemm":
+        bench_gemm(a)
+        return
     w = stream_workload(seed=a.seed, n_wg=a.n_wg, outer=a.outer, n_gen=a.n_gen)
     trips_np, off_np = w.trips.flat()
     trips = torch.from_numpy(trips_np).cuda()

@@ -72,6 +72,9 @@ struct DevImage {
   uint32_t *err = nullptr;         // watchdog word: [code, dep, wg, instance, thr, observed, wave, pad]
 };
 
+bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
+                       const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream,
+                       uint32_t *dbg, int64_t dbg_cap, const bfs_run_opts &o);
 }  // namespace bfs
 
 struct bfs_plan {
@@ -122,4 +125,7 @@ bfs_status launch_interp(const bfs_plan *p, DevImage *img, const void *const *bu
 bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
                           const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream,
                           uint32_t *dbg, int64_t dbg_cap, const bfs_run_opts &o);
+bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
+                       const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream,
+                       uint32_t *dbg, int64_t dbg_cap, const bfs_run_opts &o);
 }  // namespace bfs

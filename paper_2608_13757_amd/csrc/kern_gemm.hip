@@ -1,0 +1,547 @@
+// bf16 GEMM + bias + GELU with three engines per workgroup, one 256 x 256
+// output tile per workgroup:
+//
+//   E0 (2 waves, load)      BIAS: stage the tile's 256 bias values in LDS;
+//                           LOAD: copy the A rows and B columns of one 32-wide
+//                           K step from HBM into a ring slot with
+//                           direct-to-LDS loads (A by wave 0, B by wave 1).
+//   E1 (8 waves, MFMA)      MMA: 2 x 8 v_mfma_f32_32x32x16_bf16 per K step on
+//                           a 128 x 64 sub-tile per wave, fp32 accumulators;
+//                           SPILL: bias + GELU of one 32 x 32 accumulator
+//                           block in registers, packed to bf16 into an
+//                           epilogue ring slot.
+//   E2 (2 waves, epilogue)  EPI: read a chunk from the epilogue ring and
+//                           store it to HBM with 16-byte row segments.
+//
+// Dependencies (from the plan, Eq. 5 on the engines' loop registers):
+// LOAD->MMA (k = 0) and MMA->LOAD (k = ring slots) on the K ring, SPILL->EPI
+// (k = 0) and EPI->SPILL (k = epilogue slots) on the epilogue ring,
+// BIAS->SPILL at the top level.  Every engine wave keeps its own counter word;
+// a wait requires all waves of the producer engine.  Barrier mode
+// synchronizes all waves before each loop statement and at every iteration
+// end, with static ordinals inside a region.
+//
+// LDS (bytes): counters 2048 | K ring slots of 32 KiB (A 256 x 32 bf16, then
+// B 256 x 32 bf16; each row 64 B in four 16-byte chunks stored at chunk
+// c ^ ((row / 4) % 4), which makes the MFMA fragment reads conflict-free) |
+// bias 1 KiB.  The epilogue slots (16 KiB each: 8 blocks of 32 x 32 bf16,
+// row-major) reuse the memory of the K ring once the K loop is over; the
+// program's MMA->SPILL dependency orders every spill after the last K step
+// of every MFMA wave.
+//
+// MFMA operand order: the first operand is the B^T fragment and the second
+// the A fragment, so lane l of a 32 x 32 block holds output row (l % 32) and
+// columns 8 * (i / 4) + 4 * (l / 32) + i % 4 for accumulator element i: four
+// runs of four consecutive columns, written as 8-byte bf16 quads.
+//
+// GELU uses the exact-erf definition x * Phi(x), with erf evaluated by
+// Abramowitz & Stegun formula 7.1.26 (absolute error below 1.5e-7).
+//
+// Family contract (BFS_KERNEL_GEMM): instructions BIAS (E0, top level),
+// LOAD (E0) and MMA (E1) in loop K, SPILL (E1) and EPI (E2) in loop C;
+// waves per engine 2, 8, 2.  LOAD's args hold M, N, K and the ring depth;
+// SPILL's args[0] the epilogue ring depth.  M and N multiples of 256, K a
+// multiple of 32.  Buffers: [0] A bf16 [M][K], [1] B^T bf16 [N][K],
+// [2] bias fp32 [N], [3] C bf16 [M][N].  Trip tables: loop K runs K / 32
+// steps, loop C 8 chunks.
+#include <string>
+
+#include "bfs_internal.h"
+#include "device_sync.h"
+
+using namespace bfsdev;
+
+namespace {
+
+constexpr int kTile = 256, kBK = 32;
+constexpr int kLoadW = 2, kMmaW = 8, kEpiW = 2, kWaves = 12;
+constexpr int kMaxWaits = 4;
+constexpr uint32_t kCntBytes = bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4;
+constexpr uint32_t kSlotBytes = 2 * kTile * kBK * 2;     // A + B of one K step
+constexpr uint32_t kESlotBytes = kMmaW * 32 * 32 * 2;     // 8 bf16 blocks
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+struct Wait {
+  bfs::PackedWait w;
+  int32_t n_prd_waves;
+  int32_t pad;
+};
+
+struct InstrWaits {
+  int32_t n;
+  int32_t update;          // counter slot, -1 none
+  Wait w[kMaxWaits];
+};
+
+struct GemmParams {
+  InstrWaits bias, load, mma, spill, epi;
+  const __bf16 *a;
+  const __bf16 *bt;
+  const float *bias_v;
+  __bf16 *c;
+  const int32_t *trips;
+  const int64_t *trip_off;
+  uint32_t *dbg;
+  int64_t dbg_cap;
+  uint32_t *err;
+  uint64_t *stats;
+  uint64_t watchdog;
+  int32_t fault_dep, fault_delta;
+  int32_t m, n, k;
+  int32_t ring, e_ring;
+  int32_t tiles_m, tiles_n;
+  int32_t xcd_map;          // 1: group tiles per XCD
+};
+
+__device__ __forceinline__ float gelu_erf(float x) {
+  const float z = x * 0.70710678118654752f;
+  const float a = __builtin_fabsf(z);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * a);
+  const float poly =
+      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  const float erf_a = 1.0f - poly * __expf(-a * a);
+  const float erf_z = __builtin_copysignf(erf_a, z);
+  return 0.5f * x * (1.0f + erf_z);
+}
+
+// Loop registers of the GEMM nest: top (0), K (1), C (2).
+struct Regs {
+  uint32_t r1 = 0, r2 = 0, h1 = 0, h2 = 0;
+  __device__ __forceinline__ uint32_t r(uint32_t l) const { return l == 0 ? 1u : l == 1 ? r1 : r2; }
+  __device__ __forceinline__ uint32_t h(uint32_t l) const { return l == 0 ? 1u : l == 1 ? h1 : h2; }
+};
+
+template <int kMode, bool kInstr>
+struct Sync {
+  const GemmParams &P;
+  uint32_t cnt_base;
+  int wave, wg;
+  uint32_t aborted = 0;
+  uint32_t *log = nullptr;
+  uint32_t nlog = 0;
+  WaveStats st;
+
+  __device__ Sync(const GemmParams &p, uint32_t cb, int w, int g) : P(p), cnt_base(cb), wave(w), wg(g) {}
+
+  __device__ __forceinline__ uint32_t word(uint32_t slot, uint32_t w) const {
+    return cnt_base + 4u * (slot * (uint32_t)bfs::kMaxWavesPerEngine + w);
+  }
+
+  __device__ __forceinline__ uint32_t threshold(const bfs::PackedWait &w, const Regs &g) const {
+    uint32_t thr;
+    if (kMode == BFS_MODE_BARRIER) {
+      thr = ((w.w0 >> 25) & 1u) ? (w.w3 >> 16) : 0u;
+    } else {
+      thr = eq5(g.r((w.w0 >> 8) & 0xffu), g.h((w.w0 >> 16) & 0xffu), (int)(w.w2 & 0xffffu), (int)(w.w2 >> 16),
+                (int)(w.w1 & 0xffffu), (int)(w.w1 >> 16), (int)((w.w0 >> 24) & 1u));
+    }
+    if (kInstr && (int)(w.w3 & 0xffffu) == P.fault_dep) thr += (uint32_t)P.fault_delta;
+    return thr;
+  }
+
+  // All waits of one instruction.  on_block() retires what this wave holds
+  // before it would block.  seen[] keeps, per wait of this instruction, the
+  // last counter value observed: counters only grow, so it stays a valid lower
+  // bound (barrier mode resets counters, so there every wait polls).
+  template <class OnBlock>
+  __device__ __forceinline__ void waits(const InstrWaits &iw, const Regs &g, uint32_t instance,
+                                        uint32_t (&seen)[kMaxWaits], OnBlock on_block) {
+    for (int j = 0; j < iw.n; ++j) {
+      const bfs::PackedWait w = iw.w[j].w;
+      const int nw = iw.w[j].n_prd_waves;
+      const uint32_t thr = threshold(w, g);
+      uint32_t obs = kMode == BFS_MODE_BARRIER ? 0u : seen[j];
+      if (!aborted && thr > 0 && (obs < thr || (kInstr && log))) {
+        const uint32_t a = word(w.w0 & 0xffu, 0);
+        WaitResult res = wait_geq(a, nw, thr, 0);   // one poll
+        if (!res.ok) {
+          on_block();
+          const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
+          res = wait_geq(a, nw, thr, P.watchdog);
+          if (kInstr && st.on) {
+            st.blocked += now_ticks() - t0;
+            st.n_blocked += 1;
+          }
+          if (!res.ok) {
+            report_deadlock(P.err, w.w3 & 0xffffu, (uint32_t)wg, instance, thr, res.observed, (uint32_t)wave);
+            aborted = 1u;
+          }
+        }
+        obs = res.observed;
+        seen[j] = obs;
+      }
+      if (kInstr && log) {
+        on_block();
+        log_wait(log, P.dbg_cap, nlog, w.w3 & 0xffffu, instance, thr, thr > 0 ? obs : 0u);
+      }
+    }
+  }
+
+  __device__ __forceinline__ void signal(int update, uint32_t ew) {
+    if (update >= 0) lds_add(word((uint32_t)update, ew), 1u);
+  }
+
+  __device__ __forceinline__ void sync_point(uint32_t own_word) {
+    if (kMode == BFS_MODE_BARRIER) {
+      const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
+      region_sync(own_word, 1);
+      if (kInstr && st.on) st.barrier += now_ticks() - t0;
+    }
+  }
+
+  __device__ void finish(uint32_t lane) {
+    if (!kInstr) return;
+    if (P.dbg && lane == 0) P.dbg[(int64_t)wg * kWaves + wave] = nlog;
+    if (st.on && lane == 0) {
+      uint64_t *o = P.stats + ((int64_t)wg * kWaves + wave) * 8;
+      o[0] = now_ticks() - st.t_start;
+      o[1] = st.blocked;
+      o[2] = st.n_blocked;
+      o[3] = st.barrier;
+      o[4] = st.own_loads;
+      o[5] = 0;
+      o[6] = st.polls;          // time at the end of the K loop
+      o[7] = 0;
+    }
+  }
+};
+
+__device__ __forceinline__ uint32_t swz(uint32_t row, uint32_t chunk) {
+  return row * 64u + ((chunk ^ ((row >> 2) & 3u)) << 4);
+}
+
+template <int kMode, bool kInstr>
+__global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
+  unsigned char *ring = lds + kCntBytes;
+  unsigned char *ering = ring;                       // reused after the K loop
+  float *bias_l = reinterpret_cast<float *>(ring + (size_t)P.ring * kSlotBytes);
+  for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
+  __syncthreads();
+
+  const int wave = wave_id();
+  const uint32_t lane = lane_id();
+  const int wg = blockIdx.x;
+  // tile of this workgroup
+  int tm, tn;
+  if (P.xcd_map) {
+    const int xcd = wg & 7, local = wg >> 3;
+    const int br = P.tiles_m / 4, bc = P.tiles_n / 2;
+    tm = (xcd >> 1) * br + local / bc;
+    tn = (xcd & 1) * bc + local % bc;
+  } else {
+    tm = wg / P.tiles_n;
+    tn = wg % P.tiles_n;
+  }
+  const int m0 = tm * kTile, n0 = tn * kTile;
+
+  Sync<kMode, kInstr> S(P, lds_addr(cnt), wave, wg);
+  if (kInstr) {
+    if (P.dbg) S.log = P.dbg + (int64_t)gridDim.x * kWaves + ((int64_t)wg * kWaves + wave) * 4 * P.dbg_cap;
+    if (P.stats) {
+      S.st.on = true;
+      S.st.t_start = now_ticks();
+    }
+  }
+  const int64_t *toff = P.trip_off + (int64_t)wg * 3;
+  uint32_t trip_k = (uint32_t)ldc(P.trips + ldc(toff + 1));
+  uint32_t trip_c = (uint32_t)ldc(P.trips + ldc(toff + 2));
+  if (trip_k > (uint32_t)(P.k / kBK) || trip_c > 8u) {
+    report_deadlock(P.err, 0xffffu, (uint32_t)wg, 0, trip_k, trip_c, (uint32_t)wave);
+    trip_k = min(trip_k, (uint32_t)(P.k / kBK));
+    trip_c = min(trip_c, 8u);
+  }
+  Regs g;
+  const uint32_t ring_base = lds_addr(ring), ering_base = lds_addr(ering);
+
+  if (wave < kLoadW) {
+    // ------------------------------------------------------------ load engine
+    const uint32_t ew = (uint32_t)wave;
+    int pending = 0;                         // outstanding LOAD groups (16 loads each)
+    auto retire_one = [&]() {                // the oldest group has landed
+      if (pending == 3) wait_vm<32>();
+      else if (pending == 2) wait_vm<16>();
+      else wait_vm<0>();
+      S.signal(P.load.update, ew);
+      pending -= 1;
+    };
+    auto retire_all = [&]() {
+      if (pending > 0) {
+        wait_vm<0>();
+        for (int i = 0; i < pending; ++i) S.signal(P.load.update, ew);
+        pending = 0;
+      }
+    };
+    uint32_t seen_bias[kMaxWaits] = {0, 0, 0, 0}, seen_load[kMaxWaits] = {0, 0, 0, 0};
+    // BIAS (top level)
+    S.waits(P.bias, g, 0, seen_bias, [] {});
+    if (wave == 0 && !S.aborted)
+      __builtin_amdgcn_global_load_lds((const void *)(P.bias_v + n0 + 4 * lane), (BFS_LDS void *)bias_l, 16, 0, 0);
+    wait_vm<0>();
+    S.signal(P.bias.update, ew);
+    S.sync_point(S.word(0, ew));                            // before loop K
+    // per-lane source rows: lane l covers row 16 j + l / 4, logical chunk
+    // (l % 4) ^ ((l / 16) % 4), so its 16 bytes land at the swizzled place.
+    const uint32_t r_in = lane >> 2, chunk = (lane & 3u) ^ ((lane >> 4) & 3u);
+    const __bf16 *src = (wave == 0 ? P.a + (size_t)(m0 + r_in) * P.k : P.bt + (size_t)(n0 + r_in) * P.k) + 8 * chunk;
+    const size_t row16 = (size_t)16 * P.k;
+    uint32_t slot = 0;
+    for (uint32_t it = 0; it < trip_k; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
+      g.r1 += 1;
+      g.h1 = it + 1;
+      S.waits(P.load, g, g.r1 - 1, seen_load, [&] { retire_all(); });
+      if (!S.aborted) {
+        unsigned char *dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kSlotBytes / 2);
+        const __bf16 *s0 = src + (size_t)it * kBK;
+#pragma unroll 4
+        for (int j = 0; j < 16; ++j)
+          __builtin_amdgcn_global_load_lds((const void *)(s0 + j * row16), (BFS_LDS void *)(dst + j * 1024), 16, 0, 0);
+        pending += 1;
+        if (pending == 3) retire_one();
+      } else {
+        S.signal(P.load.update, ew);
+      }
+      if (kMode == BFS_MODE_BARRIER) {
+        retire_all();
+        S.sync_point(S.word(0, ew));                        // end of a K iteration
+      }
+    }
+    retire_all();
+    if (kInstr && S.st.on) S.st.polls = now_ticks() - S.st.t_start;   // K loop done
+    S.sync_point(S.word(0, ew));                            // before loop C
+    for (uint32_t it = 0; it < trip_c; ++it) {
+      g.r2 += 1;
+      g.h2 = it + 1;
+      S.sync_point(S.word(0, ew));                          // end of a C iteration
+    }
+  } else if (wave < kLoadW + kMmaW) {
+    // ------------------------------------------------------------ MFMA engine
+    const uint32_t ew = (uint32_t)(wave - kLoadW);
+    const uint32_t wm = ew >> 2, wn = ew & 3u;
+    f32x16 acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = f32x16{};
+    uint32_t seen_mma[kMaxWaits] = {0, 0, 0, 0}, seen_spill[kMaxWaits] = {0, 0, 0, 0};
+    S.sync_point(S.word(1, ew));                            // before loop K
+    const uint32_t l32 = lane & 31u, lhi = lane >> 5;
+    uint32_t slot = 0;
+    for (uint32_t it = 0; it < trip_k; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
+      g.r1 += 1;
+      g.h1 = it + 1;
+      S.waits(P.mma, g, g.r1 - 1, seen_mma, [] {});
+      const uint32_t a_base = ring_base + slot * kSlotBytes, b_base = a_base + kSlotBytes / 2;
+      if (!S.aborted) {
+        // Fragments are read one block ahead of the MFMAs that use them, so
+        // each LDS read overlaps the previous block's MFMAs.
+        auto rd = [&](uint32_t base, uint32_t row, uint32_t c) {
+          return __builtin_bit_cast(bf16x8, *(const BFS_LDS u32x4 *)(uintptr_t)(base + swz(row, c)));
+        };
+        const uint32_t arow = wm * 128u + l32, brow = wn * 64u + l32;
+        bf16x8 b0 = rd(b_base, brow, lhi), b1 = rd(b_base, brow + 32u, lhi);
+        bf16x8 a_cur = rd(a_base, arow, lhi);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          const uint32_t c = 2u * s + lhi;
+          bf16x8 nb0 = b0, nb1 = b1;
+#pragma unroll
+          for (int bm = 0; bm < 4; ++bm) {
+            bf16x8 a_next = a_cur;
+            if (bm < 3) {
+              a_next = rd(a_base, arow + 32u * (bm + 1), c);
+            } else if (s == 0) {
+              nb0 = rd(b_base, brow, c + 2u);
+              nb1 = rd(b_base, brow + 32u, c + 2u);
+              a_next = rd(a_base, arow, c + 2u);
+            }
+            acc[bm * 2 + 0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a_cur, acc[bm * 2 + 0], 0, 0, 0);
+            acc[bm * 2 + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a_cur, acc[bm * 2 + 1], 0, 0, 0);
+            a_cur = a_next;
+          }
+          b0 = nb0;
+          b1 = nb1;
+        }
+      }
+      // the slot's LDS reads have completed (the MFMAs consumed them)
+      drain_lds();
+      S.signal(P.mma.update, ew);
+      S.sync_point(S.word(1, ew));                          // end of a K iteration (barrier mode)
+    }
+    if (kInstr && S.st.on) S.st.polls = now_ticks() - S.st.t_start;   // K loop done
+    S.sync_point(S.word(1, ew));                            // before loop C
+    // The chunk loop is unrolled so that each chunk names its accumulator
+    // block statically; trip_c <= 8 chunks run.
+#pragma unroll
+    for (uint32_t it = 0; it < 8; ++it) {
+      if (it >= trip_c) break;
+      g.r2 += 1;
+      g.h2 = it + 1;
+      S.waits(P.spill, g, g.r2 - 1, seen_spill, [] {});
+      if (!S.aborted) {
+        const uint32_t b = it, bm = b >> 1, bn = b & 1u;
+        const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
+        const uint32_t blk = ering_base + eslot * kESlotBytes + ew * 2048u;
+        const f32x16 v = acc[it];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t ncol = wn * 64u + bn * 32u + 8u * j + 4u * lhi;   // first of 4 columns
+          const f32x4 bb = *(const BFS_LDS f32x4 *)(uintptr_t)(lds_addr(bias_l) + 4u * ncol);
+          const float x0 = gelu_erf(v[4 * j + 0] + bb.x), x1 = gelu_erf(v[4 * j + 1] + bb.y);
+          const float x2 = gelu_erf(v[4 * j + 2] + bb.z), x3 = gelu_erf(v[4 * j + 3] + bb.w);
+          const bf16x2 p01 = __builtin_convertvector(f32x2{x0, x1}, bf16x2);
+          const bf16x2 p23 = __builtin_convertvector(f32x2{x2, x3}, bf16x2);
+          const u32x2 q = {__builtin_bit_cast(uint32_t, p01), __builtin_bit_cast(uint32_t, p23)};
+          *(BFS_LDS u32x2 *)(uintptr_t)(blk + l32 * 64u + (8u * j + 4u * lhi) * 2u) = q;
+        }
+        (void)bm;
+      }
+      drain_lds();
+      S.signal(P.spill.update, ew);
+      S.sync_point(S.word(1, ew));                          // end of a C iteration
+    }
+  } else {
+    // -------------------------------------------------------- epilogue engine
+    const uint32_t ew = (uint32_t)(wave - kLoadW - kMmaW);
+    uint32_t seen_epi[kMaxWaits] = {0, 0, 0, 0};
+    S.sync_point(S.word(2, ew));                            // before loop K
+    for (uint32_t it = 0; it < trip_k; ++it) {
+      g.r1 += 1;
+      g.h1 = it + 1;
+      S.sync_point(S.word(2, ew));                          // end of a K iteration
+    }
+    S.sync_point(S.word(2, ew));                            // before loop C
+    for (uint32_t it = 0; it < trip_c; ++it) {
+      g.r2 += 1;
+      g.h2 = it + 1;
+      S.waits(P.epi, g, g.r2 - 1, seen_epi, [] {});
+      if (!S.aborted) {
+        const uint32_t b = it, bm = b >> 1, bn = b & 1u;
+        const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t v = ew * 4u + q;              // MFMA wave whose block this is
+          const uint32_t vm = v >> 2, vn = v & 3u;
+          const uint32_t blk = ering_base + eslot * kESlotBytes + v * 2048u;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const uint32_t row = 16u * h + (lane >> 2), cc = lane & 3u;
+            const u32x4 d = *(const BFS_LDS u32x4 *)(uintptr_t)(blk + row * 64u + cc * 16u);
+            const size_t gm = (size_t)m0 + vm * 128u + bm * 32u + row;
+            const size_t gn = (size_t)n0 + vn * 64u + bn * 32u + 8u * cc;
+            __builtin_nontemporal_store(d, reinterpret_cast<u32x4 *>(P.c + gm * P.n + gn));
+          }
+        }
+      }
+      drain_lds();
+      S.signal(P.epi.update, ew);
+      S.sync_point(S.word(2, ew));                          // end of a C iteration
+    }
+  }
+  drain_all();
+  S.finish(lane);
+}
+
+bool fill_waits(const bfs_plan *p, const std::vector<bfs::DevWait> &dw, int ins, InstrWaits &out) {
+  out.n = 0;
+  out.update = p->instr_update[ins];
+  for (int wi = p->instr_wait_off[ins]; wi < p->instr_wait_off[ins + 1]; ++wi) {
+    if (out.n == kMaxWaits) return false;
+    const bfs::DevWait &d = dw[p->instr_wait_list[wi]];
+    if (!bfs::pack_wait(d, out.w[out.n].w)) return false;
+    out.w[out.n].n_prd_waves = p->waves_per_engine[d.prd_engine];
+    out.n += 1;
+  }
+  return true;
+}
+
+}  // namespace
+
+namespace bfs {
+
+bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
+                       const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream, uint32_t *dbg,
+                       int64_t dbg_cap, const bfs_run_opts &o) {
+  // structure: top{ BIAS(E0); K{ LOAD(E0) MMA(E1) }; C{ SPILL(E1) EPI(E2) } }
+  if (p->n_loops != 3 || p->loop_parent[1] != 0 || p->loop_parent[2] != 0)
+    return fail(BFS_E_UNSUPPORTED, "gemm: loops must be top -> K, top -> C");
+  if (p->n_engines != 3 || p->waves_per_engine[0] != kLoadW || p->waves_per_engine[1] != kMmaW ||
+      p->waves_per_engine[2] != kEpiW)
+    return fail(BFS_E_UNSUPPORTED, "gemm: engines of 2, 8 and 2 waves");
+  int ins_bias = -1, ins_load = -1, ins_mma = -1, ins_spill = -1, ins_epi = -1;
+  for (size_t i = 0; i < p->instr_engine.size(); ++i) {
+    const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];
+    if (op == 20 && e == 0 && par == 0 && ins_bias < 0) ins_bias = (int)i;
+    else if (op == 16 && e == 0 && par == 1 && ins_load < 0) ins_load = (int)i;
+    else if (op == 17 && e == 1 && par == 1 && ins_mma < 0) ins_mma = (int)i;
+    else if (op == 18 && e == 1 && par == 2 && ins_spill < 0) ins_spill = (int)i;
+    else if (op == 19 && e == 2 && par == 2 && ins_epi < 0) ins_epi = (int)i;
+    else return fail(BFS_E_UNSUPPORTED, "gemm: unexpected instruction " + std::to_string(i));
+  }
+  if (ins_bias < 0 || ins_load < 0 || ins_mma < 0 || ins_spill < 0 || ins_epi < 0)
+    return fail(BFS_E_UNSUPPORTED, "gemm: needs BIAS, LOAD, MMA, SPILL and EPI");
+  const int32_t *la = &p->instr_args[8 * ins_load];
+  const int M = la[0], N = la[1], K = la[2], ring = la[3];
+  const int e_ring = p->instr_args[8 * ins_spill];
+  if (M <= 0 || N <= 0 || K <= 0 || M % kTile || N % kTile || K % kBK)
+    return fail(BFS_E_UNSUPPORTED, "gemm: M and N must be multiples of 256, K a multiple of 32");
+  if (ring < 2 || ring > 4 || e_ring < 1 || e_ring > 2)
+    return fail(BFS_E_UNSUPPORTED, "gemm: ring of 2..4 slots, epilogue ring of 1..2 slots");
+  // the epilogue ring lives in the K ring's memory: the program must order
+  // every spill after the whole K loop of every MFMA wave
+  bool spill_after_mma = false;
+  for (size_t d = 0; d < p->formulas.size(); ++d)
+    if (p->deps[3 * d] == ins_mma && p->deps[3 * d + 1] == ins_spill && p->deps[3 * d + 2] == 0) spill_after_mma = true;
+  if (!spill_after_mma || (size_t)e_ring * kESlotBytes > (size_t)ring * kSlotBytes)
+    return fail(BFS_E_UNSUPPORTED, "gemm: needs the MMA -> SPILL dependency (epilogue ring reuses the K ring)");
+  if ((M / kTile) * (N / kTile) != n_wg) return fail(BFS_E_INVALID, "gemm: n_wg must be (M / 256) * (N / 256)");
+  if (nbufs < 4 || !bufs[0] || !bufs[1] || !bufs[2] || !bufs[3]) return fail(BFS_E_INVALID, "gemm: needs [A, Bt, bias, C]");
+  if (!trips || !trip_off) return fail(BFS_E_INVALID, "gemm: needs trip tables");
+  const std::vector<DevWait> dw = device_waits(p);
+  GemmParams P{};
+  if (!fill_waits(p, dw, ins_bias, P.bias) || !fill_waits(p, dw, ins_load, P.load) ||
+      !fill_waits(p, dw, ins_mma, P.mma) || !fill_waits(p, dw, ins_spill, P.spill) || !fill_waits(p, dw, ins_epi, P.epi))
+    return fail(BFS_E_RESOURCE, "gemm: at most 4 waits per instruction");
+  P.a = static_cast<const __bf16 *>(bufs[0]);
+  P.bt = static_cast<const __bf16 *>(bufs[1]);
+  P.bias_v = static_cast<const float *>(bufs[2]);
+  P.c = static_cast<__bf16 *>(const_cast<void *>(bufs[3]));
+  P.trips = trips;
+  P.trip_off = trip_off;
+  P.dbg = dbg;
+  P.dbg_cap = dbg_cap;
+  P.err = img->err;
+  P.stats = o.dev_stats;
+  P.watchdog = o.watchdog_polls;
+  P.fault_dep = o.fault_dep;
+  P.fault_delta = o.fault_delta;
+  P.m = M;
+  P.n = N;
+  P.k = K;
+  P.ring = ring;
+  P.e_ring = e_ring;
+  P.tiles_m = M / kTile;
+  P.tiles_n = N / kTile;
+  P.xcd_map = (n_wg % 8 == 0 && P.tiles_m % 4 == 0 && P.tiles_n % 2 == 0) ? 1 : 0;
+  const size_t lds = kCntBytes + (size_t)ring * kSlotBytes + 1024;
+  const bool instr = dbg || o.dev_stats || o.fault_dep >= 0;
+  hipStream_t s = (hipStream_t)stream;
+  auto go = [&](auto kern) -> bfs_status {
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("gemm attribute: ") + hipGetErrorString(e));
+    hipLaunchKernelGGL(kern, dim3(n_wg), dim3(64 * kWaves), lds, s, P);
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("gemm launch: ") + hipGetErrorString(e));
+    return BFS_OK;
+  };
+  if (p->mode == BFS_MODE_BARRIER) return instr ? go(gemm_kernel<BFS_MODE_BARRIER, true>) : go(gemm_kernel<BFS_MODE_BARRIER, false>);
+  return instr ? go(gemm_kernel<BFS_MODE_BARRIER_FREE, true>) : go(gemm_kernel<BFS_MODE_BARRIER_FREE, false>);
+}
+
+}  // namespace bfs

@@ -26,13 +26,16 @@ def wave_engine_map(plan):
     return out
 
 
-def log_records(plan, log_words, n_wg, cap):
-    """{(wg, dep): sorted list of (instance, threshold, observed)} over waves."""
+def log_records(plan, log_words, n_wg, cap, per_wave=False):
+    """{(wg, dep): sorted list of (instance, threshold, observed)}; with
+    per_wave the key is (wg, wave, dep) (every wave of a multi-wave engine
+    evaluates the same waits)."""
     per = parse_debug_log(log_words, n_wg, plan.n_waves, cap)
     out = {}
-    for (wg, _wave), ent in per.items():
+    for (wg, wave), ent in per.items():
         for dep, inst, thr, obs in ent.tolist():
-            out.setdefault((wg, dep), []).append((inst, thr, obs))
+            key = (wg, wave, dep) if per_wave else (wg, dep)
+            out.setdefault(key, []).append((inst, thr, obs))
     for k in out:
         out[k].sort()
     return out
@@ -56,4 +59,29 @@ def compare_log_with_oracle(prog, plan, logs, recs_by_wg, mode):
             for i, t, obs in got:
                 assert t == 0 or obs >= t, (wg, d, i, t, obs)
             n += len(got)
+    return n
+
+
+def compare_wave_logs_with_oracle(prog, plan, logs, recs_by_wg, mode):
+    """Multi-wave engines: every wave of the consumer's engine logs the same
+    waits, each equal to the oracle's threshold, observed never below it."""
+    key = "sem_thr" if mode == "barrier_free" else "barrier_thr"
+    engine_waves = {}
+    w = 0
+    for e, n in enumerate(plan.waves_per_engine):
+        engine_waves[e] = list(range(w, w + n))
+        w += n
+    n = 0
+    for wg, recs in recs_by_wg.items():
+        for d, (p, c, k) in enumerate(prog.deps):
+            r = recs[recs["dep"] == d]
+            want = [(int(i), int(t)) for i, t in zip(r["instance"], r[key])]
+            for wave in engine_waves[prog.instrs[c].engine]:
+                got = logs.get((wg, wave, d), [])
+                if mode == "barrier" and not got and all(t == 0 for _, t in want):
+                    continue
+                assert [(i, t) for i, t, _ in got] == want, (wg, wave, d)
+                for i, t, obs in got:
+                    assert t == 0 or obs >= t, (wg, wave, d, i, t, obs)
+                n += len(got)
     return n

@@ -1,0 +1,145 @@
+"""GPU parity of the GEMM + bias + GELU family (load / MFMA / epilogue engines).
+
+bf16 MFMA stages: |gpu - oracle| <= 2e-2 * max(|oracle|, rms(oracle)) per
+element against the fp64 oracle; thresholds bit-exact against the oracle's
+brute force for every wave of every consumer engine; the barrier-free and
+barrier modes produce bit-identical outputs."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import core, mathref  # noqa: E402
+from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
+from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
+from workloads import gemm_program, gemm_trips  # noqa: E402
+from workloads.tensors import bf16_to_f32, gemm_inputs  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+MODES = [("barrier_free", MODE_BARRIER_FREE), ("barrier", MODE_BARRIER)]
+RTOL = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    bfs.lib()
+
+
+def _say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+def _bits_to_dev(bits):
+    return torch.from_numpy(bits.view(np.int16)).cuda()
+
+
+def run_gemm(gi, m, n, k, mode, cap=0):
+    prog = gemm_program(m, n, k)
+    plan = Plan(prog, mode)
+    tt = gemm_trips(m, n, k)
+    trips, toff = trip_tensors(tt)
+    a, bt = _bits_to_dev(gi.a), _bits_to_dev(gi.bt)
+    bias = torch.from_numpy(gi.bias).cuda()
+    c = torch.full((m * n,), -1, dtype=torch.int16, device="cuda")
+    log = None
+    if cap:
+        log = torch.zeros(plan.debug_log_words(tt.n_wg, cap), dtype=torch.int32, device="cuda")
+    plan.run([a, bt, bias, c], trips, toff, tt.n_wg, debug_log=log, debug_capacity=cap)
+    plan.status()
+    out = bf16_to_f32(c.cpu().numpy().view(np.uint16)).reshape(m, n)
+    return prog, plan, tt, out, (log.cpu().numpy().view(np.uint32) if cap else None)
+
+
+def check_close(got, ref):
+    ref = np.asarray(ref, np.float64)
+    scale = np.maximum(np.abs(ref), np.sqrt(np.mean(ref ** 2)))
+    err = np.abs(got.astype(np.float64) - ref) / scale
+    assert np.isfinite(got).all()
+    assert err.max() <= RTOL, (err.max(), np.unravel_index(err.argmax(), err.shape))
+    return err.max()
+
+
+@pytest.mark.parametrize("shape", [(512, 512, 256), (256, 768, 96)])
+def test_gemm_small_parity_and_thresholds(shape):
+    m, n, k = shape
+    gi = gemm_inputs(seed=1, m=m, n=n, k=k)
+    ref = mathref.gemm_bias_gelu(gi.a, gi.bt, gi.bias)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[gemm-small] {shape} mode={name}")
+        prog, plan, tt, out, logw = run_gemm(gi, m, n, k, mode, cap=512)
+        check_close(out, ref)
+        trips, off = tt.flat()
+        recs = {g: core.run(prog, trips, off[g], g).recs for g in range(tt.n_wg)}
+        logs = log_records(plan, logw, tt.n_wg, 512, per_wave=True)
+        assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_gemm_special_cases():
+    """B = I gives GELU(A + bias); A = 0 gives GELU(bias) in every row."""
+    m, n, k = 256, 256, 256
+    gi = gemm_inputs(seed=2, m=m, n=n, k=k)
+    from workloads.tensors import to_bf16_bits
+    gi.bt = to_bf16_bits(np.eye(n, k, dtype=np.float32))
+    _say("[gemm-identity]")
+    _, _, _, out, _ = run_gemm(gi, m, n, k, MODE_BARRIER_FREE)
+    a = bf16_to_f32(gi.a).astype(np.float64)
+    check_close(out, mathref.gelu(a + gi.bias[None, :].astype(np.float64)))
+    gi.a = np.zeros_like(gi.a)
+    _, _, _, out, _ = run_gemm(gi, m, n, k, MODE_BARRIER_FREE)
+    check_close(out, np.broadcast_to(mathref.gelu(gi.bias.astype(np.float64)), (m, n)))
+
+
+def test_gemm_full_size_sampled():
+    """The benchmark shape 4096^3, checked on sampled elements one by one."""
+    m = n = k = 4096
+    _say("[gemm-full] generating")
+    gi = gemm_inputs(seed=0, m=m, n=n, k=k)
+    rng = np.random.default_rng(7)
+    rows, cols = rng.integers(0, m, 3000), rng.integers(0, n, 3000)
+    # every tile corner too
+    rows = np.concatenate([rows, np.repeat(np.arange(0, m, 256), 16), np.repeat(np.arange(255, m, 256), 16)])
+    cols = np.concatenate([cols, np.tile(np.arange(0, n, 256), 16), np.tile(np.arange(255, n, 256), 16)])
+    ref = mathref.gemm_bias_gelu_at(gi.a, gi.bt, gi.bias, rows, cols)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[gemm-full] mode={name}")
+        _, _, _, out, _ = run_gemm(gi, m, n, k, mode)
+        check_close(out[rows, cols], ref)
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_gemm_rejects_unsupported_shapes():
+    prog = gemm_program(300, 256, 64)
+    plan = Plan(prog)
+    t = torch.zeros(16, dtype=torch.int32, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t, t, t, t], t, t, 1)
+    assert e.value.status == bfs.E_UNSUPPORTED
+
+
+def test_gemm_watchdog():
+    m, n, k = 256, 256, 64
+    gi = gemm_inputs(seed=3, m=m, n=n, k=k)
+    prog = gemm_program(m, n, k)
+    plan = Plan(prog)
+    tt = gemm_trips(m, n, k)
+    trips, toff = trip_tensors(tt)
+    a, bt = _bits_to_dev(gi.a), _bits_to_dev(gi.bt)
+    bias = torch.from_numpy(gi.bias).cuda()
+    c = torch.zeros(m * n, dtype=torch.int16, device="cuda")
+    _say("[gemm-watchdog]")
+    plan.run([a, bt, bias, c], trips, toff, tt.n_wg, watchdog_polls=2000, fault_dep=0, fault_delta=1 << 20)
+    with pytest.raises(BfsError) as e:
+        plan.status()
+    assert e.value.status == bfs.E_DEADLOCK
+    plan.run([a, bt, bias, c], trips, toff, tt.n_wg)
+    plan.status()

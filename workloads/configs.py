@@ -19,7 +19,8 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .program import (OP_ADDC, OP_LOAD, OP_NOP, OP_SCALE_ACC, OP_STORE_ACC,
+from .program import (OP_ADDC, OP_GEMM_BIAS, OP_GEMM_EPI, OP_GEMM_LOAD, OP_GEMM_MMA,
+                      OP_GEMM_SPILL, OP_LOAD, OP_NOP, OP_SCALE_ACC, OP_STORE_ACC,
                       OP_STORE_RING, Program, ProgramBuilder, tile_args)
 
 CFG_CHAIN, CFG_STREAM, CFG_GEMM, CFG_ATTN, CFG_MOE, CFG_RANDOM = 1, 2, 3, 4, 5, 99
@@ -265,3 +266,50 @@ def random_nest(seed: int, max_depth: int = 3, n_engines: int = 3, max_items: in
         return rng.integers(0, hi + 1, size=n)
     tt = TripTables([draw_trips(prog, draw)])
     return prog, tt
+
+
+# ---------------------------------------------------------------------------
+# cfg3: GEMM + bias + GELU with load / MFMA / epilogue engines
+# ---------------------------------------------------------------------------
+GEMM_TILE = 256     # output tile edge per workgroup
+GEMM_BK = 32        # K step per ring slot
+GEMM_RING = 4       # ring slots of the K loop
+GEMM_CHUNKS = 8     # accumulator blocks spilled per MFMA wave
+
+
+def gemm_program(m: int, n: int, k: int, ring: int = GEMM_RING, e_ring: int = 2,
+                 load_waves: int = 2, mma_waves: int = 8, epi_waves: int = 2) -> Program:
+    """One 256 x 256 output tile per workgroup:
+
+      E0: BIAS
+      K{ E0: LOAD A, B tiles of the step -> ring[(rhat_K - 1) % ring]; E1: MMA }
+      C{ E1: SPILL bias + GELU of one accumulator block -> ering[(rhat_C - 1) % e_ring]; E2: EPI store }
+
+    LOAD->MMA (k=0) and MMA->LOAD (k=ring) protect the K ring, SPILL->EPI
+    (k=0) and EPI->SPILL (k=e_ring) the epilogue ring, BIAS->SPILL (k=0 at the
+    top level) the staged bias.  The epilogue ring occupies the memory of the
+    K ring, so MMA->SPILL (k=0; producer nested in K, consumer in C) lets a
+    spill start only after every MFMA wave retired its last K step."""
+    b = ProgramBuilder("gemm", n_engines=3, waves_per_engine=[load_waves, mma_waves, epi_waves])
+    b.instr(0, OP_GEMM_BIAS, [m, n, k, 0, 0, 0, 0, 0], name="BIAS")
+    with b.loop("K"):
+        b.instr(0, OP_GEMM_LOAD, [m, n, k, ring, 0, 0, 0, 0], name="LOAD")
+        b.instr(1, OP_GEMM_MMA, [0] * 8, name="MMA")
+    with b.loop("C"):
+        b.instr(1, OP_GEMM_SPILL, [e_ring, 0, 0, 0, 0, 0, 0, 0], name="SPILL")
+        b.instr(2, OP_GEMM_EPI, [0] * 8, name="EPI")
+    b.dep("LOAD", "MMA", 0)
+    b.dep("MMA", "LOAD", ring)
+    b.dep("BIAS", "SPILL", 0)
+    b.dep("SPILL", "EPI", 0)
+    b.dep("EPI", "SPILL", e_ring)
+    b.dep("MMA", "SPILL", 0)
+    return b.build()
+
+
+def gemm_trips(m: int, n: int, k: int, ring: int = GEMM_RING) -> TripTables:
+    """Every workgroup runs the K loop once with K / 32 steps and the
+    epilogue loop once with 8 chunks."""
+    n_wg = (m // GEMM_TILE) * (n // GEMM_TILE)
+    one = [np.array([1], np.int32), np.array([k // GEMM_BK], np.int32), np.array([GEMM_CHUNKS], np.int32)]
+    return TripTables([[a.copy() for a in one] for _ in range(n_wg)])

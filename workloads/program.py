@@ -43,10 +43,11 @@ OP_STORE_RING = 5 # buffer[dst] tile gidx <- ring[src][slot]
 
 # --- descriptive opcodes of the fused MFMA families (values are checked
 # against the plain mathematical definition, not interpreted) --------------
-OP_GEMM_LOAD = 16
+OP_GEMM_LOAD = 16      # args: M, N, K (the shape of the whole product)
 OP_GEMM_MMA = 17
 OP_GEMM_SPILL = 18
 OP_GEMM_EPI = 19
+OP_GEMM_BIAS = 20      # stage the workgroup's bias columns in LDS
 OP_ATTN_LOAD = 32
 OP_ATTN_QK = 33
 OP_ATTN_SM = 34
