@@ -37,8 +37,9 @@ def parse():
     ap.add_argument("--n-gen", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--modes", default="barrier_free,barrier")
-    ap.add_argument("--workload", default="stream", choices=["stream", "gemm"],
-                    help="stream: the sync-bound microbenchmark (headline); gemm: 4096^3 bf16 GEMM + bias + GELU")
+    ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn"],
+                    help="stream: the sync-bound microbenchmark (headline); gemm: 4096^3 bf16 GEMM + bias + GELU; "
+                         "attn: varlen attention forward")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference dispatch for HBM traffic counters)")
@@ -176,6 +177,53 @@ def bench_gemm(a):
     print(json.dumps(out), flush=True)
 
 
+def bench_attn(a):
+    """Variable-length attention forward: 32 sequences of U[128, 4096] tokens,
+    16 heads of 128, one workgroup per (sequence, head, 128-query tile);
+    both synchronization modes."""
+    import numpy as np
+    import torch
+    from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
+    from workloads import attn_program, attn_worklist
+    from workloads.tensors import attn_inputs
+
+    heads = 16
+    ai = attn_inputs(seed=a.seed, heads=heads)
+    wl = attn_worklist(ai.lengths, heads)
+    dev = lambda bits: torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+    q, k, v = dev(ai.q), dev(ai.k), dev(ai.v)
+    o = torch.empty(ai.q.shape, dtype=torch.int16, device="cuda")
+    work = torch.from_numpy(wl.work.reshape(-1)).cuda()
+    t_np, o_np = wl.trips.flat()
+    trips, toff = torch.from_numpy(t_np).cuda(), torch.from_numpy(o_np).cuda()
+    res = {}
+    for name in a.modes.split(","):
+        mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
+        plan = Plan(attn_program(heads), mode)
+        res[name] = time_mode(plan, [work, q, k, v, o], trips, toff, wl.trips.n_wg, a.steps, a.warmup)
+    lens = ai.lengths.astype(np.float64)
+    flop = 4.0 * 128 * heads * float(np.sum(lens * lens))
+    bf = res.get("barrier_free", next(iter(res.values())))
+    ms = bf["ms_mean"]
+    tflops = flop / (ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC, "value": tflops, "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "varlen attention forward, 32 sequences of U[128,4096] tokens (seed "
+                               f"{a.seed}: {int(lens.sum())} tokens), 16 heads x 128, bf16 N(0,1), "
+                               "KV blocks of 64, 128-query tiles", "batch": 32, "heads": heads,
+                   "head_dim": 128, "tokens": int(lens.sum()), "n_wg": wl.trips.n_wg,
+                   "parallelism": "single GPU"},
+        "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
+    }
+    if "barrier" in res and "barrier_free" in res:
+        out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
+    print(json.dumps(out), flush=True)
+
+
 def bf16_bits_as_f32(bits):
     import numpy as np
     return (bits.astype(np.uint32) << 16).view(np.float32)
@@ -195,6 +243,9 @@ def main():
     torch.cuda.set_device(0)
     if a.workload == "gemm":
         bench_gemm(a)
+        return
+    if a.workload == "attn":
+        bench_attn(a)
         return
     w = stream_workload(seed=a.seed, n_wg=a.n_wg, outer=a.outer, n_gen=a.n_gen)
     trips_np, off_np = w.trips.flat()

@@ -1,0 +1,452 @@
+// Variable-length attention forward (no causal mask), one workgroup per
+// (sequence, head, 128-query tile), five engines synchronized by LDS counters:
+//
+//   E0 (1 wave, K load)    LOADK: the 64 x 128 bf16 K block of the step into
+//                          a K ring slot with direct-to-LDS loads.
+//   E1 (2 waves, MFMA)     QK: S = Q K^T for 64 query rows per wave (Q held in
+//                          registers for the whole loop), written as fp32
+//                          into an S/P slot.
+//   E2 (4 waves, VALU)     SM: online softmax over 32 rows per wave in the
+//                          base-2 domain: running max m, rescale factor
+//                          alpha = 2^(m_old - m_new), P = 2^(S c - m_new)
+//                          written as bf16 over S in place, running sum l.
+//   E3 (2 waves, MFMA)     PV: O = alpha O + P V for 64 query rows per wave
+//                          (fp32 accumulators), then NORM: O / l to HBM.
+//   E4 (1 wave, V load)    LOADV: the V block into a V ring slot.
+//
+// The KV loop runs ceil(L / 64) steps, a trip count known only at run time.
+// Dependencies (the program's; Eq. 5 on the engines' loop registers):
+// LOADK->QK, LOADV->PV, QK->SM, SM->PV (k = 0); QK->LOADK (k = K ring
+// depth), PV->LOADV (k = V ring depth), PV->QK (k = 2: the S/P slot, its
+// alpha row and P are free once PV has read them); SM->NORM (k = 0, C2: the
+// final row sums).
+//
+// Query rows of the tile beyond the sequence are computed on a clamped copy
+// of the last row and never stored; keys beyond the sequence in the last
+// block are loaded from a clamped row and masked to probability 0.
+//
+// LDS (bytes): counters 2048 | K ring (16 KiB slots: 64 rows of 256 B, the
+// 16-byte chunk c of row r at c ^ (r mod 16)) | V ring (16 KiB slots, chunk c
+// of row r at c ^ 4 (r mod 4), the layout the transposing fragment reads need
+// to be conflict-free) | 2 S/P slots of 32 KiB (S fp32 [128][64]: 16-byte
+// chunk c of row r at c ^ (r mod 16); P bf16 overwrites it with 8 chunks per
+// row at the same permutation) | alpha [2][128] fp32 | l [128] fp32.
+//
+// MFMA v_mfma_f32_32x32x16_bf16: lane l supplies row l % 32 of the first
+// operand and column l % 32 of the second, k = 8 (l / 32) .. + 7, and holds
+// column l % 32 of the result, rows 8 (i / 4) + 4 (l / 32) + i % 4 for
+// accumulator element i.  QK passes (K fragment, Q fragment), so lane l holds
+// S[query l % 32][4-key runs]; PV passes (V^T fragment, P fragment), so lane
+// l holds O[query l % 32][4-column runs] and the per-row rescale is one
+// scalar per lane.  The V^T fragment (8 consecutive keys of one column) comes
+// from two ds_read_b64_tr_b16: within each group of 16 lanes, lane i receives
+// element i % 4 of the 8 bytes addressed by lane 4 j + i / 4 as its element j.
+//
+// Family contract (BFS_KERNEL_ATTN): loop KV below the top level holding
+// LOADK (E0, opcode 32, args [0, K ring depth, heads, 128]), LOADV (E4,
+// opcode 32, args [1, V ring depth, heads, 128]), QK (E1, 33), SM (E2, 34),
+// PV (E3, 35); NORM (E3, 36) at the top level; waves per engine 1, 2, 4, 2,
+// 1; the dependencies listed above.  Buffers: [0] work list int32 [n_wg][4]
+// = (first token of the sequence, length L, first query row of the tile,
+// head), [1] Q, [2] K, [3] V, [4] O, each bf16 [tokens][heads][128].  Trip
+// table: loop KV runs ceil(L / 64) steps (0 for an empty work item).
+#include <string>
+
+#include "engine_sync.h"
+
+using namespace bfsdev;
+
+namespace {
+
+constexpr int kD = 128, kBQ = 128, kBKV = 64;
+constexpr int kWaves = 10;
+constexpr uint32_t kKVSlot = kBKV * kD * 2;      // 16 KiB
+constexpr uint32_t kSPSlot = kBQ * kBKV * 4;     // 32 KiB
+constexpr int kMaxPend = 3;                      // load groups in flight per load wave
+
+struct AttnParams {
+  SyncCommon sc;
+  InstrWaits loadk, loadv, qk, sm, pv, norm;
+  const int32_t *work;
+  const __bf16 *q, *k, *v;
+  __bf16 *o;
+  const int32_t *trips;
+  const int64_t *trip_off;
+  int32_t heads, nk, nv;
+  float scale_log2;          // log2(e) / sqrt(128)
+};
+
+// byte offset of 16-byte chunk c of row r (256-byte rows)
+__device__ __forceinline__ uint32_t pos16(uint32_t r, uint32_t c) { return r * 256u + ((c ^ (r & 15u)) << 4); }
+
+__device__ __forceinline__ bf16x8 lds_frag(uint32_t addr) {
+  return __builtin_bit_cast(bf16x8, *(const BFS_LDS u32x4 *)(uintptr_t)addr);
+}
+
+__device__ __forceinline__ bf16x4 lds_tr(uint32_t addr) {
+  typedef __attribute__((ext_vector_type(4))) short s16x4;
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((BFS_LDS s16x4 *)(uintptr_t)addr);
+  return __builtin_bit_cast(bf16x4, v);
+}
+
+__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
+
+template <int kMode, bool kInstr>
+__global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
+  const uint32_t kring = lds_addr(lds) + kCntBytes;
+  const uint32_t vring = kring + (uint32_t)P.nk * kKVSlot;
+  const uint32_t spbuf = vring + (uint32_t)P.nv * kKVSlot;
+  const uint32_t alpha_l = spbuf + 2u * kSPSlot;
+  const uint32_t lsum_l = alpha_l + 2u * kBQ * 4u;
+  for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
+  __syncthreads();
+
+  const int hw = wave_id();
+  const uint32_t lane = lane_id(), l32 = lane & 31u, lhi = lane >> 5;
+  const int wg = blockIdx.x;
+  // hardware wave -> (engine, wave within the engine); the four MFMA waves
+  // come first so that they sit on four different SIMDs
+  int eng, ew, canon;                       // canon: engine-ordered wave index
+  if (hw < 2) { eng = 1; ew = hw; canon = 1 + ew; }
+  else if (hw < 4) { eng = 3; ew = hw - 2; canon = 7 + ew; }
+  else if (hw < 8) { eng = 2; ew = hw - 4; canon = 3 + ew; }
+  else if (hw == 8) { eng = 0; ew = 0; canon = 0; }
+  else { eng = 4; ew = 0; canon = 9; }
+  Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), canon, wg);
+  const uint32_t own = S.word((uint32_t)eng, (uint32_t)ew);   // barrier mode: one counter per engine
+
+  const int32_t s0 = ldc(P.work + 4 * wg + 0), L = ldc(P.work + 4 * wg + 1);
+  const int32_t q0 = ldc(P.work + 4 * wg + 2), head = ldc(P.work + 4 * wg + 3);
+  const int64_t *toff = P.trip_off + (int64_t)wg * 2;
+  uint32_t trip = (uint32_t)ldc(P.trips + ldc(toff + 1));
+  const uint32_t max_trip = L > 0 ? (uint32_t)((L + kBKV - 1) / kBKV) : 0u;
+  if (trip > max_trip) {
+    report_deadlock(P.sc.err, 0xffffu, (uint32_t)wg, 0, trip, max_trip, (uint32_t)hw);
+    trip = max_trip;
+  }
+  const size_t row_stride = (size_t)P.heads * kD;     // elements between tokens
+  Regs g;
+  uint32_t seen_a[kMaxWaits] = {0, 0, 0, 0}, seen_b[kMaxWaits] = {0, 0, 0, 0};
+  uint64_t mark = 0;
+
+  if (eng == 0 || eng == 4) {
+    // ------------------------------------------------------- K / V loaders
+    const bool is_v = eng == 4;
+    const InstrWaits &iw = is_v ? P.loadv : P.loadk;
+    const uint32_t depth = (uint32_t)(is_v ? P.nv : P.nk);
+    const uint32_t ring = is_v ? vring : kring;
+    const __bf16 *base = (is_v ? P.v : P.k) + (size_t)head * kD;
+    int pending = 0;
+    auto retire_one = [&]() {
+      if (pending == 3) wait_vm<32>();
+      else if (pending == 2) wait_vm<16>();
+      else wait_vm<0>();
+      S.signal(iw.update, 0);
+      pending -= 1;
+    };
+    auto retire_all = [&]() {
+      if (pending > 0) {
+        wait_vm<0>();
+        for (int i = 0; i < pending; ++i) S.signal(iw.update, 0);
+        pending = 0;
+      }
+    };
+    // lane t covers row 4 j + t / 16 of instruction j and the 16-byte chunk
+    // that belongs at position t % 16 of that row
+    const uint32_t rr = lane >> 4, pos = lane & 15u;
+    S.sync_point(own);                                       // before loop KV
+    uint32_t slot = 0;
+    for (uint32_t it = 0; it < trip; ++it, slot = (slot + 1 == depth) ? 0u : slot + 1) {
+      g.r1 += 1;
+      g.h1 = it + 1;
+      S.waits(iw, g, g.r1 - 1, seen_a, [&] { retire_all(); });
+      if (!S.aborted) {
+        const uint32_t dst = ring + slot * kKVSlot;
+        const int32_t key0 = (int32_t)it * kBKV;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const uint32_t row = 4u * j + rr;
+          const uint32_t chunk = is_v ? (pos ^ (rr << 2)) : (pos ^ (row & 15u));
+          const int32_t key = min(key0 + (int32_t)row, L - 1);
+          const __bf16 *src = base + (size_t)(s0 + key) * row_stride + 8u * chunk;
+          __builtin_amdgcn_global_load_lds((const void *)src, (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+        }
+        pending += 1;
+        if (pending == kMaxPend) retire_one();
+      } else {
+        S.signal(iw.update, 0);
+      }
+      if (kMode == BFS_MODE_BARRIER) {
+        retire_all();
+        S.sync_point(own);                                   // end of a KV iteration
+      }
+    }
+    retire_all();
+  } else if (eng == 1) {
+    // ---------------------------------------------------------- QK^T engine
+    const uint32_t qr = 64u * ew;
+    bf16x8 qf[2][8];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int32_t row = min(q0 + (int32_t)(qr + 32u * qb + l32), L - 1);
+      const __bf16 *src = P.q + (size_t)(s0 + max(row, 0)) * row_stride + (size_t)head * kD + 8u * lhi;
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        qf[qb][s] = L > 0 ? __builtin_bit_cast(bf16x8, *(const u32x4 *)(src + 16 * s)) : bf16x8{};
+    }
+    S.sync_point(own);                                       // before loop KV
+    uint32_t kslot = 0;
+    for (uint32_t it = 0; it < trip; ++it, kslot = (kslot + 1 == (uint32_t)P.nk) ? 0u : kslot + 1) {
+      g.r1 += 1;
+      g.h1 = it + 1;
+      S.waits(P.qk, g, g.r1 - 1, seen_a, [] {});
+      if (!S.aborted) {
+        const uint32_t kb_base = kring + kslot * kKVSlot;
+        const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
+        f32x16 acc[2][2];
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const bf16x8 k0 = lds_frag(kb_base + pos16(l32, 2u * s + lhi));
+          const bf16x8 k1 = lds_frag(kb_base + pos16(32u + l32, 2u * s + lhi));
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb) {
+            acc[qb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[qb][s], acc[qb][0], 0, 0, 0);
+            acc[qb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[qb][s], acc[qb][1], 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const uint32_t row = qr + 32u * qb + l32;
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const f32x4 v = {acc[qb][kb][4 * j], acc[qb][kb][4 * j + 1], acc[qb][kb][4 * j + 2], acc[qb][kb][4 * j + 3]};
+              *(BFS_LDS f32x4 *)(uintptr_t)(sp + pos16(row, 8u * kb + 2u * j + lhi)) = v;
+            }
+        }
+      }
+      drain_lds();
+      S.signal(P.qk.update, (uint32_t)ew);
+      S.sync_point(own);                                     // end of a KV iteration
+    }
+  } else if (eng == 2) {
+    // ------------------------------------------------------ softmax engine
+    const uint32_t row = 32u * ew + l32;
+    const float c = P.scale_log2;
+    float m = -__builtin_inff(), lrun = 0.0f;
+    S.sync_point(own);                                       // before loop KV
+    for (uint32_t it = 0; it < trip; ++it) {
+      g.r1 += 1;
+      g.h1 = it + 1;
+      S.waits(P.sm, g, g.r1 - 1, seen_a, [] {});
+      if (!S.aborted) {
+        const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
+        float x[32];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const f32x4 v = *(const BFS_LDS f32x4 *)(uintptr_t)(sp + pos16(row, 8u * lhi + j));
+          x[4 * j] = v.x;
+          x[4 * j + 1] = v.y;
+          x[4 * j + 2] = v.z;
+          x[4 * j + 3] = v.w;
+        }
+        const int32_t key0 = (int32_t)it * kBKV + 32 * (int32_t)lhi;
+        if ((int32_t)(it + 1) * kBKV > L) {
+#pragma unroll
+          for (int t = 0; t < 32; ++t)
+            if (key0 + t >= L) x[t] = -__builtin_inff();
+        }
+        float mx = x[0];
+#pragma unroll
+        for (int t = 1; t < 32; ++t) mx = __builtin_fmaxf(mx, x[t]);
+        mx = __builtin_fmaxf(mx, xor32(mx));
+        const float m_new = __builtin_fmaxf(m, mx * c);
+        const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+        float sum = 0.0f;
+        uint32_t pk[16];
+#pragma unroll
+        for (int t = 0; t < 32; t += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(x[t], c, -m_new));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(x[t + 1], c, -m_new));
+          sum += p0 + p1;
+          pk[t / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{p0, p1}, bf16x2));
+        }
+        sum += xor32(sum);
+        lrun = alpha * lrun + sum;
+        m = m_new;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const u32x4 v = {pk[4 * j], pk[4 * j + 1], pk[4 * j + 2], pk[4 * j + 3]};
+          *(BFS_LDS u32x4 *)(uintptr_t)(sp + pos16(row, 4u * lhi + j)) = v;
+        }
+        if (lhi == 0) {
+          *(BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + row) * 4u) = alpha;
+          *(BFS_LDS float *)(uintptr_t)(lsum_l + row * 4u) = lrun;
+        }
+      }
+      drain_lds();
+      S.signal(P.sm.update, (uint32_t)ew);
+      S.sync_point(own);                                     // end of a KV iteration
+    }
+  } else {
+    // --------------------------------------------------- PV engine and NORM
+    const uint32_t qr = 64u * ew;
+    f32x16 acc[2][4];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b) acc[a][b] = f32x16{};
+    // transposing V reads: lane l addresses row 8 (l / 32) + (l % 16) / 4 (+ 16 ks + 4 hh)
+    // and columns 32 db + 16 ((l / 16) % 2) + 4 (l % 4) .. + 3
+    const uint32_t x = (lane >> 2) & 3u;
+    const uint32_t vrow = 8u * lhi + x;
+    uint32_t voff[4];
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+      voff[db] = vrow * 256u + 16u * (4u * ((uint32_t)db ^ x) + 2u * ((lane >> 4) & 1u) + ((lane >> 1) & 1u)) +
+                 8u * (lane & 1u);
+    S.sync_point(own);                                       // before loop KV
+    uint32_t vslot = 0;
+    for (uint32_t it = 0; it < trip; ++it, vslot = (vslot + 1 == (uint32_t)P.nv) ? 0u : vslot + 1) {
+      g.r1 += 1;
+      g.h1 = it + 1;
+      S.waits(P.pv, g, g.r1 - 1, seen_a, [] {});
+      if (!S.aborted) {
+        const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
+        const uint32_t vb = vring + vslot * kKVSlot;
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const float a = *(const BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + qr + 32u * qb + l32) * 4u);
+#pragma unroll
+          for (int db = 0; db < 4; ++db) acc[qb][db] *= a;
+        }
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+          bf16x8 pf[2];
+#pragma unroll
+          for (int qb = 0; qb < 2; ++qb) pf[qb] = lds_frag(sp + pos16(qr + 32u * qb + l32, 2u * ks + lhi));
+#pragma unroll
+          for (int db = 0; db < 4; ++db) {
+            const uint32_t va = vb + 16u * ks * 256u + voff[db];
+            const bf16x4 lo = lds_tr(va), hi = lds_tr(va + 4u * 256u);
+            const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb)
+              acc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb], acc[qb][db], 0, 0, 0);
+          }
+        }
+      }
+      drain_lds();
+      S.signal(P.pv.update, (uint32_t)ew);
+      S.sync_point(own);                                     // end of a KV iteration
+    }
+    mark = S.elapsed();
+    // NORM: O / l for the rows of the sequence
+    S.waits(P.norm, g, 0, seen_b, [] {});
+    if (!S.aborted) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        const uint32_t rloc = qr + 32u * qb + l32;
+        const int32_t row = q0 + (int32_t)rloc;
+        const float lr = *(const BFS_LDS float *)(uintptr_t)(lsum_l + rloc * 4u);
+        const float inv = 1.0f / lr;
+        if (row < L) {
+          __bf16 *dst = P.o + (size_t)(s0 + row) * row_stride + (size_t)head * kD;
+#pragma unroll
+          for (int db = 0; db < 4; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const f32x2 a01 = {acc[qb][db][4 * j] * inv, acc[qb][db][4 * j + 1] * inv};
+              const f32x2 a23 = {acc[qb][db][4 * j + 2] * inv, acc[qb][db][4 * j + 3] * inv};
+              const u32x2 v = {__builtin_bit_cast(uint32_t, __builtin_convertvector(a01, bf16x2)),
+                               __builtin_bit_cast(uint32_t, __builtin_convertvector(a23, bf16x2))};
+              __builtin_nontemporal_store(v, reinterpret_cast<u32x2 *>(dst + 32 * db + 8 * j + 4 * lhi));
+            }
+        }
+      }
+    }
+  }
+  drain_all();
+  S.finish(lane, mark);
+}
+
+}  // namespace
+
+namespace bfs {
+
+bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
+                       const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream, uint32_t *dbg,
+                       int64_t dbg_cap, const bfs_run_opts &o) {
+  if (p->n_loops != 2 || p->loop_parent[1] != 0) return fail(BFS_E_UNSUPPORTED, "attn: loops must be top -> KV");
+  const int want_w[5] = {1, 2, 4, 2, 1};
+  if (p->n_engines != 5) return fail(BFS_E_UNSUPPORTED, "attn: five engines");
+  for (int e = 0; e < 5; ++e)
+    if (p->waves_per_engine[e] != want_w[e]) return fail(BFS_E_UNSUPPORTED, "attn: engines of 1, 2, 4, 2, 1 waves");
+  int lk = -1, lv = -1, qk = -1, sm = -1, pv = -1, nm = -1;
+  for (size_t i = 0; i < p->instr_engine.size(); ++i) {
+    const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];
+    const int32_t *a = &p->instr_args[8 * i];
+    if (op == 32 && e == 0 && par == 1 && a[0] == 0 && lk < 0) lk = (int)i;
+    else if (op == 32 && e == 4 && par == 1 && a[0] == 1 && lv < 0) lv = (int)i;
+    else if (op == 33 && e == 1 && par == 1 && qk < 0) qk = (int)i;
+    else if (op == 34 && e == 2 && par == 1 && sm < 0) sm = (int)i;
+    else if (op == 35 && e == 3 && par == 1 && pv < 0) pv = (int)i;
+    else if (op == 36 && e == 3 && par == 0 && nm < 0) nm = (int)i;
+    else return fail(BFS_E_UNSUPPORTED, "attn: unexpected instruction " + std::to_string(i));
+  }
+  if (lk < 0 || lv < 0 || qk < 0 || sm < 0 || pv < 0 || nm < 0)
+    return fail(BFS_E_UNSUPPORTED, "attn: needs LOADK, LOADV, QK, SM, PV and NORM");
+  const int nk = p->instr_args[8 * lk + 1], nv = p->instr_args[8 * lv + 1];
+  const int heads = p->instr_args[8 * lk + 2], dim = p->instr_args[8 * lk + 3];
+  if (dim != kD || p->instr_args[8 * lv + 3] != kD) return fail(BFS_E_UNSUPPORTED, "attn: head dimension 128");
+  if (heads <= 0 || p->instr_args[8 * lv + 2] != heads) return fail(BFS_E_INVALID, "attn: heads must match");
+  const size_t lds = kCntBytes + (size_t)(nk + nv) * kKVSlot + 2 * kSPSlot + 3 * kBQ * 4;
+  if (nk < 2 || nv < 2 || lds > 160 * 1024) return fail(BFS_E_UNSUPPORTED, "attn: ring depths >= 2 within 160 KiB of LDS");
+  // the kernel's buffers are only race-free under these dependencies
+  if (!has_dep(p, lk, qk, 0) || !has_dep(p, lv, pv, 0) || !has_dep(p, qk, sm, 0) || !has_dep(p, sm, pv, 0) ||
+      !has_dep(p, qk, lk, nk) || !has_dep(p, pv, lv, nv) || !has_dep(p, pv, qk, 2) || !has_dep(p, sm, nm, 0))
+    return fail(BFS_E_UNSUPPORTED, "attn: missing a ring, S/P or row-sum dependency");
+  if (nbufs < 5) return fail(BFS_E_INVALID, "attn: needs [work, Q, K, V, O]");
+  for (int i = 0; i < 5; ++i)
+    if (!bufs[i]) return fail(BFS_E_INVALID, "attn: null buffer");
+  if (!trips || !trip_off) return fail(BFS_E_INVALID, "attn: needs trip tables");
+  if (n_wg <= 0) return fail(BFS_E_INVALID, "attn: n_wg must be positive");
+  const std::vector<DevWait> dw = device_waits(p);
+  AttnParams P{};
+  if (!fill_waits(p, dw, lk, P.loadk) || !fill_waits(p, dw, lv, P.loadv) || !fill_waits(p, dw, qk, P.qk) ||
+      !fill_waits(p, dw, sm, P.sm) || !fill_waits(p, dw, pv, P.pv) || !fill_waits(p, dw, nm, P.norm))
+    return fail(BFS_E_RESOURCE, "attn: at most 4 waits per instruction");
+  P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
+  P.work = static_cast<const int32_t *>(bufs[0]);
+  P.q = static_cast<const __bf16 *>(bufs[1]);
+  P.k = static_cast<const __bf16 *>(bufs[2]);
+  P.v = static_cast<const __bf16 *>(bufs[3]);
+  P.o = static_cast<__bf16 *>(const_cast<void *>(bufs[4]));
+  P.trips = trips;
+  P.trip_off = trip_off;
+  P.heads = heads;
+  P.nk = nk;
+  P.nv = nv;
+  P.scale_log2 = 1.4426950408889634f / 11.313708498984761f;   // log2(e) / sqrt(128)
+  const bool instr = dbg || o.dev_stats || o.fault_dep >= 0;
+  hipStream_t s = (hipStream_t)stream;
+  auto go = [&](auto kern) -> bfs_status {
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("attn attribute: ") + hipGetErrorString(e));
+    hipLaunchKernelGGL(kern, dim3(n_wg), dim3(64 * kWaves), lds, s, P);
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("attn launch: ") + hipGetErrorString(e));
+    return BFS_OK;
+  };
+  if (p->mode == BFS_MODE_BARRIER) return instr ? go(attn_kernel<BFS_MODE_BARRIER, true>) : go(attn_kernel<BFS_MODE_BARRIER, false>);
+  return instr ? go(attn_kernel<BFS_MODE_BARRIER_FREE, true>) : go(attn_kernel<BFS_MODE_BARRIER_FREE, false>);
+}
+
+}  // namespace bfs

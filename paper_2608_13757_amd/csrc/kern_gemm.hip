@@ -46,8 +46,7 @@
 // steps, loop C 8 chunks.
 #include <string>
 
-#include "bfs_internal.h"
-#include "device_sync.h"
+#include "engine_sync.h"
 
 using namespace bfsdev;
 
@@ -55,32 +54,11 @@ namespace {
 
 constexpr int kTile = 256, kBK = 32;
 constexpr int kLoadW = 2, kMmaW = 8, kEpiW = 2, kWaves = 12;
-constexpr int kMaxWaits = 4;
-constexpr uint32_t kCntBytes = bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4;
 constexpr uint32_t kSlotBytes = 2 * kTile * kBK * 2;     // A + B of one K step
 constexpr uint32_t kESlotBytes = kMmaW * 32 * 32 * 2;     // 8 bf16 blocks
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
-typedef __attribute__((ext_vector_type(16))) float f32x16;
-typedef __attribute__((ext_vector_type(2))) float f32x2;
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-
-struct Wait {
-  bfs::PackedWait w;
-  int32_t n_prd_waves;
-  int32_t pad;
-};
-
-struct InstrWaits {
-  int32_t n;
-  int32_t update;          // counter slot, -1 none
-  Wait w[kMaxWaits];
-};
-
 struct GemmParams {
+  SyncCommon sc;
   InstrWaits bias, load, mma, spill, epi;
   const __bf16 *a;
   const __bf16 *bt;
@@ -88,12 +66,6 @@ struct GemmParams {
   __bf16 *c;
   const int32_t *trips;
   const int64_t *trip_off;
-  uint32_t *dbg;
-  int64_t dbg_cap;
-  uint32_t *err;
-  uint64_t *stats;
-  uint64_t watchdog;
-  int32_t fault_dep, fault_delta;
   int32_t m, n, k;
   int32_t ring, e_ring;
   int32_t tiles_m, tiles_n;
@@ -110,108 +82,6 @@ __device__ __forceinline__ float gelu_erf(float x) {
   const float erf_z = __builtin_copysignf(erf_a, z);
   return 0.5f * x * (1.0f + erf_z);
 }
-
-// Loop registers of the GEMM nest: top (0), K (1), C (2).
-struct Regs {
-  uint32_t r1 = 0, r2 = 0, h1 = 0, h2 = 0;
-  __device__ __forceinline__ uint32_t r(uint32_t l) const { return l == 0 ? 1u : l == 1 ? r1 : r2; }
-  __device__ __forceinline__ uint32_t h(uint32_t l) const { return l == 0 ? 1u : l == 1 ? h1 : h2; }
-};
-
-template <int kMode, bool kInstr>
-struct Sync {
-  const GemmParams &P;
-  uint32_t cnt_base;
-  int wave, wg;
-  uint32_t aborted = 0;
-  uint32_t *log = nullptr;
-  uint32_t nlog = 0;
-  WaveStats st;
-
-  __device__ Sync(const GemmParams &p, uint32_t cb, int w, int g) : P(p), cnt_base(cb), wave(w), wg(g) {}
-
-  __device__ __forceinline__ uint32_t word(uint32_t slot, uint32_t w) const {
-    return cnt_base + 4u * (slot * (uint32_t)bfs::kMaxWavesPerEngine + w);
-  }
-
-  __device__ __forceinline__ uint32_t threshold(const bfs::PackedWait &w, const Regs &g) const {
-    uint32_t thr;
-    if (kMode == BFS_MODE_BARRIER) {
-      thr = ((w.w0 >> 25) & 1u) ? (w.w3 >> 16) : 0u;
-    } else {
-      thr = eq5(g.r((w.w0 >> 8) & 0xffu), g.h((w.w0 >> 16) & 0xffu), (int)(w.w2 & 0xffffu), (int)(w.w2 >> 16),
-                (int)(w.w1 & 0xffffu), (int)(w.w1 >> 16), (int)((w.w0 >> 24) & 1u));
-    }
-    if (kInstr && (int)(w.w3 & 0xffffu) == P.fault_dep) thr += (uint32_t)P.fault_delta;
-    return thr;
-  }
-
-  // All waits of one instruction.  on_block() retires what this wave holds
-  // before it would block.  seen[] keeps, per wait of this instruction, the
-  // last counter value observed: counters only grow, so it stays a valid lower
-  // bound (barrier mode resets counters, so there every wait polls).
-  template <class OnBlock>
-  __device__ __forceinline__ void waits(const InstrWaits &iw, const Regs &g, uint32_t instance,
-                                        uint32_t (&seen)[kMaxWaits], OnBlock on_block) {
-    for (int j = 0; j < iw.n; ++j) {
-      const bfs::PackedWait w = iw.w[j].w;
-      const int nw = iw.w[j].n_prd_waves;
-      const uint32_t thr = threshold(w, g);
-      uint32_t obs = kMode == BFS_MODE_BARRIER ? 0u : seen[j];
-      if (!aborted && thr > 0 && (obs < thr || (kInstr && log))) {
-        const uint32_t a = word(w.w0 & 0xffu, 0);
-        WaitResult res = wait_geq(a, nw, thr, 0);   // one poll
-        if (!res.ok) {
-          on_block();
-          const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
-          res = wait_geq(a, nw, thr, P.watchdog);
-          if (kInstr && st.on) {
-            st.blocked += now_ticks() - t0;
-            st.n_blocked += 1;
-          }
-          if (!res.ok) {
-            report_deadlock(P.err, w.w3 & 0xffffu, (uint32_t)wg, instance, thr, res.observed, (uint32_t)wave);
-            aborted = 1u;
-          }
-        }
-        obs = res.observed;
-        seen[j] = obs;
-      }
-      if (kInstr && log) {
-        on_block();
-        log_wait(log, P.dbg_cap, nlog, w.w3 & 0xffffu, instance, thr, thr > 0 ? obs : 0u);
-      }
-    }
-  }
-
-  __device__ __forceinline__ void signal(int update, uint32_t ew) {
-    if (update >= 0) lds_add(word((uint32_t)update, ew), 1u);
-  }
-
-  __device__ __forceinline__ void sync_point(uint32_t own_word) {
-    if (kMode == BFS_MODE_BARRIER) {
-      const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
-      region_sync(own_word, 1);
-      if (kInstr && st.on) st.barrier += now_ticks() - t0;
-    }
-  }
-
-  __device__ void finish(uint32_t lane) {
-    if (!kInstr) return;
-    if (P.dbg && lane == 0) P.dbg[(int64_t)wg * kWaves + wave] = nlog;
-    if (st.on && lane == 0) {
-      uint64_t *o = P.stats + ((int64_t)wg * kWaves + wave) * 8;
-      o[0] = now_ticks() - st.t_start;
-      o[1] = st.blocked;
-      o[2] = st.n_blocked;
-      o[3] = st.barrier;
-      o[4] = st.own_loads;
-      o[5] = 0;
-      o[6] = st.polls;          // time at the end of the K loop
-      o[7] = 0;
-    }
-  }
-};
 
 __device__ __forceinline__ uint32_t swz(uint32_t row, uint32_t chunk) {
   return row * 64u + ((chunk ^ ((row >> 2) & 3u)) << 4);
@@ -243,19 +113,13 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
   }
   const int m0 = tm * kTile, n0 = tn * kTile;
 
-  Sync<kMode, kInstr> S(P, lds_addr(cnt), wave, wg);
-  if (kInstr) {
-    if (P.dbg) S.log = P.dbg + (int64_t)gridDim.x * kWaves + ((int64_t)wg * kWaves + wave) * 4 * P.dbg_cap;
-    if (P.stats) {
-      S.st.on = true;
-      S.st.t_start = now_ticks();
-    }
-  }
+  Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), wave, wg);
+  uint64_t k_end = 0;                      // statistics: end of the K loop
   const int64_t *toff = P.trip_off + (int64_t)wg * 3;
   uint32_t trip_k = (uint32_t)ldc(P.trips + ldc(toff + 1));
   uint32_t trip_c = (uint32_t)ldc(P.trips + ldc(toff + 2));
   if (trip_k > (uint32_t)(P.k / kBK) || trip_c > 8u) {
-    report_deadlock(P.err, 0xffffu, (uint32_t)wg, 0, trip_k, trip_c, (uint32_t)wave);
+    report_deadlock(P.sc.err, 0xffffu, (uint32_t)wg, 0, trip_k, trip_c, (uint32_t)wave);
     trip_k = min(trip_k, (uint32_t)(P.k / kBK));
     trip_c = min(trip_c, 8u);
   }
@@ -315,7 +179,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       }
     }
     retire_all();
-    if (kInstr && S.st.on) S.st.polls = now_ticks() - S.st.t_start;   // K loop done
+    k_end = S.elapsed();
     S.sync_point(S.word(0, ew));                            // before loop C
     for (uint32_t it = 0; it < trip_c; ++it) {
       g.r2 += 1;
@@ -374,7 +238,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       S.signal(P.mma.update, ew);
       S.sync_point(S.word(1, ew));                          // end of a K iteration (barrier mode)
     }
-    if (kInstr && S.st.on) S.st.polls = now_ticks() - S.st.t_start;   // K loop done
+    k_end = S.elapsed();
     S.sync_point(S.word(1, ew));                            // before loop C
     // The chunk loop is unrolled so that each chunk names its accumulator
     // block statically; trip_c <= 8 chunks run.
@@ -445,20 +309,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     }
   }
   drain_all();
-  S.finish(lane);
-}
-
-bool fill_waits(const bfs_plan *p, const std::vector<bfs::DevWait> &dw, int ins, InstrWaits &out) {
-  out.n = 0;
-  out.update = p->instr_update[ins];
-  for (int wi = p->instr_wait_off[ins]; wi < p->instr_wait_off[ins + 1]; ++wi) {
-    if (out.n == kMaxWaits) return false;
-    const bfs::DevWait &d = dw[p->instr_wait_list[wi]];
-    if (!bfs::pack_wait(d, out.w[out.n].w)) return false;
-    out.w[out.n].n_prd_waves = p->waves_per_engine[d.prd_engine];
-    out.n += 1;
-  }
-  return true;
+  S.finish(lane, k_end);
 }
 
 }  // namespace
@@ -495,10 +346,7 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
     return fail(BFS_E_UNSUPPORTED, "gemm: ring of 2..4 slots, epilogue ring of 1..2 slots");
   // the epilogue ring lives in the K ring's memory: the program must order
   // every spill after the whole K loop of every MFMA wave
-  bool spill_after_mma = false;
-  for (size_t d = 0; d < p->formulas.size(); ++d)
-    if (p->deps[3 * d] == ins_mma && p->deps[3 * d + 1] == ins_spill && p->deps[3 * d + 2] == 0) spill_after_mma = true;
-  if (!spill_after_mma || (size_t)e_ring * kESlotBytes > (size_t)ring * kSlotBytes)
+  if (!has_dep(p, ins_mma, ins_spill, 0) || (size_t)e_ring * kESlotBytes > (size_t)ring * kSlotBytes)
     return fail(BFS_E_UNSUPPORTED, "gemm: needs the MMA -> SPILL dependency (epilogue ring reuses the K ring)");
   if ((M / kTile) * (N / kTile) != n_wg) return fail(BFS_E_INVALID, "gemm: n_wg must be (M / 256) * (N / 256)");
   if (nbufs < 4 || !bufs[0] || !bufs[1] || !bufs[2] || !bufs[3]) return fail(BFS_E_INVALID, "gemm: needs [A, Bt, bias, C]");
@@ -514,13 +362,7 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
   P.c = static_cast<__bf16 *>(const_cast<void *>(bufs[3]));
   P.trips = trips;
   P.trip_off = trip_off;
-  P.dbg = dbg;
-  P.dbg_cap = dbg_cap;
-  P.err = img->err;
-  P.stats = o.dev_stats;
-  P.watchdog = o.watchdog_polls;
-  P.fault_dep = o.fault_dep;
-  P.fault_delta = o.fault_delta;
+  P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
   P.m = M;
   P.n = N;
   P.k = K;

@@ -1,0 +1,157 @@
+"""GPU parity of the variable-length attention family (K load / QK^T MFMA /
+online softmax / PV MFMA / V load engines).
+
+bf16 MFMA stages: |gpu - oracle| <= 2e-2 * max(|oracle|, rms(oracle)) per
+element against the fp64 oracle; thresholds bit-exact against the oracle's
+brute force for every wave of every consumer engine; the barrier-free and
+barrier modes produce bit-identical outputs."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import core, mathref  # noqa: E402
+from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
+from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
+from workloads import attn_program, attn_worklist  # noqa: E402
+from workloads.tensors import attn_inputs, bf16_to_f32  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+MODES = [("barrier_free", MODE_BARRIER_FREE), ("barrier", MODE_BARRIER)]
+RTOL = 2e-2
+SCALE = 1.0 / np.sqrt(128.0)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    bfs.lib()
+
+
+def _say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+def _dev16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+
+
+def run_attn(ai, heads, mode, cap=0, nk=3, nv=2):
+    prog = attn_program(heads, nk=nk, nv=nv)
+    plan = Plan(prog, mode)
+    wl = attn_worklist(ai.lengths, heads)
+    trips, toff = trip_tensors(wl.trips)
+    work = torch.from_numpy(wl.work.reshape(-1)).cuda()
+    q, k, v = _dev16(ai.q), _dev16(ai.k), _dev16(ai.v)
+    o = torch.full(ai.q.shape, -1, dtype=torch.int16, device="cuda")
+    n_wg = wl.trips.n_wg
+    log = None
+    if cap:
+        log = torch.zeros(plan.debug_log_words(n_wg, cap), dtype=torch.int32, device="cuda")
+    plan.run([work, q, k, v, o], trips, toff, n_wg, debug_log=log, debug_capacity=cap)
+    plan.status()
+    out = bf16_to_f32(o.cpu().numpy().view(np.uint16))
+    return prog, plan, wl, out, (log.cpu().numpy().view(np.uint32) if cap else None)
+
+
+def check_close(got, ref):
+    ref = np.asarray(ref, np.float64)
+    scale = np.maximum(np.abs(ref), np.sqrt(np.mean(ref ** 2)))
+    err = np.abs(got.astype(np.float64) - ref) / scale
+    assert np.isfinite(got).all()
+    assert err.max() <= RTOL, (err.max(), np.unravel_index(err.argmax(), err.shape))
+    return err.max()
+
+
+# lengths: one key, exactly one block, a ragged block, two query tiles with
+# a one-row tail, several blocks with a ragged last block
+SMALL = [1, 64, 100, 129, 300]
+
+
+@pytest.mark.parametrize("rings", [(3, 2), (2, 2), (2, 3)])
+def test_attn_small_parity_and_thresholds(rings):
+    nk, nv = rings
+    heads = 2
+    ai = attn_inputs(seed=1, heads=heads, lengths=SMALL)
+    ref = mathref.attention(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[attn-small] rings={rings} mode={name}")
+        prog, plan, wl, out, logw = run_attn(ai, heads, mode, cap=64, nk=nk, nv=nv)
+        check_close(out, ref)
+        trips, off = wl.trips.flat()
+        recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
+        logs = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
+        assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_attn_special_cases():
+    """Constant V rows give O = that row; a one-token sequence returns its V."""
+    heads = 2
+    ai = attn_inputs(seed=2, heads=heads, lengths=[1, 200])
+    const = ai.v[1].copy()                          # token 1 is the first of sequence 1
+    ai.v[1:] = const[None]
+    _say("[attn-special]")
+    _, _, _, out, _ = run_attn(ai, heads, MODE_BARRIER_FREE)
+    check_close(out[0], bf16_to_f32(ai.v[0]))
+    check_close(out[1:], np.broadcast_to(bf16_to_f32(const), out[1:].shape))
+
+
+def test_attn_full_size_sampled():
+    """The benchmark shape (32 sequences of U[128, 4096] tokens, 16 heads),
+    checked on sampled rows one by one."""
+    heads = 16
+    _say("[attn-full] generating")
+    ai = attn_inputs(seed=0, heads=heads)
+    rng = np.random.default_rng(11)
+    items = []
+    for _ in range(200):
+        b = int(rng.integers(0, len(ai.lengths)))
+        items.append((b, int(rng.integers(0, heads)), int(rng.integers(0, ai.lengths[b]))))
+    for b in range(len(ai.lengths)):                # first and last row of every sequence
+        L = int(ai.lengths[b])
+        items += [(b, b % heads, 0), (b, (b + 7) % heads, L - 1), (b, (b + 3) % heads, (L - 1) // 128 * 128)]
+    ref = mathref.attention_rows(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE, items)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[attn-full] mode={name}")
+        _, _, _, out, _ = run_attn(ai, heads, mode)
+        got = np.array([out[ai.cu_seqlens[b] + i, h] for b, h, i in items])
+        check_close(got, ref)
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_attn_rejects_missing_dependency():
+    prog = attn_program(2)
+    prog.deps = [d for d in prog.deps if not (prog.instrs[d[0]].name == "PV" and prog.instrs[d[1]].name == "QK")]
+    plan = Plan(prog)
+    t = torch.zeros(16, dtype=torch.int32, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t, t, t, t, t], t, t, 1)
+    assert e.value.status == bfs.E_UNSUPPORTED
+
+
+def test_attn_watchdog():
+    heads = 1
+    ai = attn_inputs(seed=3, heads=heads, lengths=[300])
+    prog = attn_program(heads)
+    plan = Plan(prog)
+    wl = attn_worklist(ai.lengths, heads)
+    trips, toff = trip_tensors(wl.trips)
+    work = torch.from_numpy(wl.work.reshape(-1)).cuda()
+    q, k, v = _dev16(ai.q), _dev16(ai.k), _dev16(ai.v)
+    o = torch.zeros(ai.q.shape, dtype=torch.int16, device="cuda")
+    _say("[attn-watchdog]")
+    plan.run([work, q, k, v, o], trips, toff, wl.trips.n_wg, watchdog_polls=2000, fault_dep=2, fault_delta=1 << 20)
+    with pytest.raises(BfsError) as e:
+        plan.status()
+    assert e.value.status == bfs.E_DEADLOCK
+    plan.run([work, q, k, v, o], trips, toff, wl.trips.n_wg)
+    plan.status()

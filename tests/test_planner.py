@@ -15,8 +15,8 @@ from oracle import core
 from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER, MODE_BARRIER_FREE,
                                   BfsError, Plan, bfs)
 from tests import fixtures
-from workloads import (OP_NOP, ProgramBuilder, TripTables, chain_workload, draw_trips, random_nest,
-                       stream_workload)
+from workloads import (OP_NOP, ProgramBuilder, TripTables, attn_program, attn_worklist, chain_workload,
+                       draw_trips, gemm_program, gemm_trips, random_nest, stream_workload)
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -138,6 +138,32 @@ def test_workload_programs():
         _check_against_oracle(prog, tt)
     s = stream_workload(seed=0, n_wg=1, outer=5, with_data=False)
     _check_against_oracle(s.prog, s.trips)
+    g = gemm_program(512, 256, 128)
+    _check_against_oracle(g, TripTables([gemm_trips(512, 256, 128).per_wg[0]]))
+    for L in (1, 64, 65, 300):
+        a = attn_program(2)
+        _check_against_oracle(a, TripTables([attn_worklist([L], 2).trips.per_wg[0]]))
+
+
+def test_fused_family_formulas():
+    """The dependencies of the GEMM and attention programs land in the cases
+    the kernels rely on: ring reuse as C1 backward with the ring depth, the
+    epilogue-after-K-loop and final-row-sum dependencies as C2."""
+    g = gemm_program(512, 256, 128)
+    fg = {(g.instrs[p].name, g.instrs[c].name): f for (p, c, k), f in zip(g.deps, Plan(g).formulas())}
+    assert fg[("MMA", "LOAD")]["kase"] == 1 and fg[("MMA", "LOAD")]["k"] == 4 and not fg[("MMA", "LOAD")]["forward"]
+    assert fg[("MMA", "SPILL")]["kase"] == 2 and fg[("BIAS", "SPILL")]["kase"] == 1
+    a = attn_program(16, nk=3, nv=2)
+    fa = {(a.instrs[p].name, a.instrs[c].name): f for (p, c, k), f in zip(a.deps, Plan(a).formulas())}
+    assert fa[("QK", "LOADK")]["k"] == 3 and fa[("PV", "LOADV")]["k"] == 2 and fa[("PV", "QK")]["k"] == 2
+    assert all(fa[x]["kase"] == 1 for x in [("LOADK", "QK"), ("QK", "SM"), ("SM", "PV"), ("LOADV", "PV")])
+    assert fa[("SM", "NORM")]["kase"] == 2
+    # the work list covers every (sequence, head, query tile) once, XCD-interleaved
+    wl = attn_worklist([1, 64, 129, 300, 4096], 3)
+    items = {tuple(r) for r in wl.work.tolist() if r[1] > 0}
+    assert len(items) == 3 * (1 + 1 + 2 + 3 + 32)
+    trips = [int(t[1][0]) for t in wl.trips.per_wg]
+    assert all(t == -(-int(r[1]) // 64) for t, r in zip(trips, wl.work))
 
 
 def test_rejections():

@@ -19,7 +19,8 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .program import (OP_ADDC, OP_GEMM_BIAS, OP_GEMM_EPI, OP_GEMM_LOAD, OP_GEMM_MMA,
+from .program import (OP_ADDC, OP_ATTN_LOAD, OP_ATTN_NORM, OP_ATTN_PV, OP_ATTN_QK, OP_ATTN_SM,
+                      OP_GEMM_BIAS, OP_GEMM_EPI, OP_GEMM_LOAD, OP_GEMM_MMA,
                       OP_GEMM_SPILL, OP_LOAD, OP_NOP, OP_SCALE_ACC, OP_STORE_ACC,
                       OP_STORE_RING, Program, ProgramBuilder, tile_args)
 
@@ -313,3 +314,88 @@ def gemm_trips(m: int, n: int, k: int, ring: int = GEMM_RING) -> TripTables:
     n_wg = (m // GEMM_TILE) * (n // GEMM_TILE)
     one = [np.array([1], np.int32), np.array([k // GEMM_BK], np.int32), np.array([GEMM_CHUNKS], np.int32)]
     return TripTables([[a.copy() for a in one] for _ in range(n_wg)])
+
+
+# ---------------------------------------------------------------------------
+# cfg4: variable-length attention forward with K load / QK^T / softmax / PV /
+# V load engines
+# ---------------------------------------------------------------------------
+ATTN_BQ = 128       # query rows per workgroup
+ATTN_BKV = 64       # keys per KV block
+ATTN_D = 128        # head dimension
+ATTN_SP = 2         # S/P buffer slots
+
+
+def attn_program(heads: int, dim: int = ATTN_D, nk: int = 3, nv: int = 2) -> Program:
+    """One workgroup per (sequence, head, 128-query tile):
+
+      KV{ E0: LOADK K block -> kring[(rhat_KV - 1) % nk]
+          E4: LOADV V block -> vring[(rhat_KV - 1) % nv]
+          E1: QK    S = Q K^T -> sp[(rhat_KV - 1) % 2]
+          E2: SM    online softmax: P over S in place, alpha, running sum l
+          E3: PV    O = alpha O + P V }
+      E3: NORM  O / l -> output
+
+    The KV loop's trip count is ceil(L / 64) for the sequence's length L.
+    LOADK->QK, LOADV->PV, QK->SM, SM->PV (k=0) carry the data forward;
+    QK->LOADK (k=nk) and PV->LOADV (k=nv) free ring slots; PV->QK (k=2) frees
+    an S/P slot; SM->NORM (k=0, producer nested in KV) delivers the final row
+    sums."""
+    b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 4, 2, 1])
+    with b.loop("KV"):
+        b.instr(0, OP_ATTN_LOAD, [0, nk, heads, dim, 0, 0, 0, 0], name="LOADK")
+        b.instr(4, OP_ATTN_LOAD, [1, nv, heads, dim, 0, 0, 0, 0], name="LOADV")
+        b.instr(1, OP_ATTN_QK, [0] * 8, name="QK")
+        b.instr(2, OP_ATTN_SM, [0] * 8, name="SM")
+        b.instr(3, OP_ATTN_PV, [0] * 8, name="PV")
+    b.instr(3, OP_ATTN_NORM, [0] * 8, name="NORM")
+    b.dep("LOADK", "QK", 0)
+    b.dep("LOADV", "PV", 0)
+    b.dep("QK", "SM", 0)
+    b.dep("SM", "PV", 0)
+    b.dep("QK", "LOADK", nk)
+    b.dep("PV", "LOADV", nv)
+    b.dep("PV", "QK", ATTN_SP)
+    b.dep("SM", "NORM", 0)
+    return b.build()
+
+
+@dataclass
+class AttnWork:
+    work: np.ndarray      # int32 [n_wg, 4]: first token, length, first query row, head
+    trips: TripTables     # per workgroup: [[1], [ceil(L / 64)]]
+
+
+def attn_worklist(lengths, heads: int, xcds: int = 8) -> AttnWork:
+    """Work items (sequence, head, 128-query tile) in launch order.
+
+    (sequence, head) pairs are taken longest first and each goes, with all
+    of its query tiles, to the XCD with the least work so far; workgroup w
+    runs on XCD w % xcds, so a pair's tiles share one L2 for their K and V
+    blocks.  Shorter XCD lists are padded with empty items (length 0, no KV
+    steps)."""
+    lengths = np.asarray(lengths, dtype=np.int64)
+    cu = np.concatenate([[0], np.cumsum(lengths)])
+    pairs = sorted(((int(lengths[b]), b, h) for b in range(len(lengths)) for h in range(heads)),
+                   key=lambda t: (-t[0], t[1], t[2]))
+    load = [0] * xcds
+    lists = [[] for _ in range(xcds)]
+    for L, b, h in pairs:
+        if L <= 0:
+            continue
+        x = min(range(xcds), key=lambda i: (load[i], i))
+        n_tiles = -(-L // ATTN_BQ)
+        load[x] += n_tiles * -(-L // ATTN_BKV)
+        for t in range(n_tiles):
+            lists[x].append((int(cu[b]), L, t * ATTN_BQ, h))
+    depth = max((len(l) for l in lists), default=0)
+    if depth == 0:
+        return AttnWork(np.zeros((0, 4), np.int32), TripTables([]))
+    items = []
+    for i in range(depth):
+        for x in range(xcds):
+            items.append(lists[x][i] if i < len(lists[x]) else (0, 0, 0, 0))
+    work = np.array(items, dtype=np.int32).reshape(-1, 4)
+    trips = TripTables([[np.array([1], np.int32), np.array([-(-int(L) // ATTN_BKV)], np.int32)]
+                        for _, L, _, _ in work])
+    return AttnWork(work, trips)
