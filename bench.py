@@ -37,9 +37,9 @@ def parse():
     ap.add_argument("--n-gen", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--modes", default="barrier_free,barrier")
-    ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn"],
+    ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn", "moe"],
                     help="stream: the sync-bound microbenchmark (headline); gemm: 4096^3 bf16 GEMM + bias + GELU; "
-                         "attn: varlen attention forward")
+                         "attn: varlen attention forward; moe: MoE grouped GEMM")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference dispatch for HBM traffic counters)")
@@ -224,6 +224,94 @@ def bench_attn(a):
     print(json.dumps(out), flush=True)
 
 
+HBM_PEAK_GBPS = 8000.0
+
+
+def bench_moe(a):
+    """MoE grouped GEMM: 32768 tokens routed top-1 to 64 experts with Zipf(1.1)
+    counts, hidden 4096, ffn 1408, SiLU-gated; one step = the gate/up launch
+    plus the down launch; both synchronization modes."""
+    import numpy as np
+    import torch
+    from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
+    from workloads import moe_program, moe_worklist
+    from workloads.tensors import moe_inputs, moe_weights_all
+
+    moe = moe_inputs(seed=a.seed)
+    H, F = moe.hidden, moe.ffn
+    dev = lambda bits: torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+    wg, wu, wd = (dev(w) for w in moe_weights_all(moe))
+    x = dev(moe.x)
+    perm = torch.from_numpy(moe.perm.astype(np.int32)).cuda()
+    eoff = torch.from_numpy(moe.expert_off.astype(np.int32)).cuda()
+    T = len(moe.assign)
+    h = torch.empty((T, F), dtype=torch.int16, device="cuda")
+    y = torch.empty((T, H), dtype=torch.int16, device="cuda")
+    launches = {}
+    for ph in (1, 2):
+        wl = moe_worklist(moe.counts, ph, H, F)
+        t_np, o_np = wl.trips.flat()
+        work = torch.from_numpy(wl.work.reshape(-1)).cuda()
+        bufs = [work, perm, eoff, x, wg, wu, h] if ph == 1 else [work, perm, eoff, h, wd, y]
+        launches[ph] = (bufs, torch.from_numpy(t_np).cuda(), torch.from_numpy(o_np).cuda(), wl.trips.n_wg)
+    stream = torch.cuda.current_stream()
+    res = {}
+    for name in a.modes.split(","):
+        mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
+        plans = {ph: Plan(moe_program(ph, H, F), mode) for ph in (1, 2)}
+
+        def step():
+            for ph in (1, 2):
+                bufs, trips, toff, n_wg = launches[ph]
+                plans[ph].run(bufs, trips, toff, n_wg, stream=stream)
+        for _ in range(a.warmup):
+            step()
+        plans[1].status(stream)
+        plans[2].status(stream)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(a.steps)]
+        torch.cuda.synchronize()
+        for i in range(a.steps):
+            ev[i][0].record(stream)
+            bufs, trips, toff, n_wg = launches[1]
+            plans[1].run(bufs, trips, toff, n_wg, stream=stream)
+            ev[i][1].record(stream)
+            bufs, trips, toff, n_wg = launches[2]
+            plans[2].run(bufs, trips, toff, n_wg, stream=stream)
+            ev[i][2].record(stream)
+        torch.cuda.synchronize()
+        plans[1].status(stream)
+        plans[2].status(stream)
+        p1 = [e[0].elapsed_time(e[1]) for e in ev]
+        p2 = [e[1].elapsed_time(e[2]) for e in ev]
+        res[name] = {"ms_mean": (sum(p1) + sum(p2)) / a.steps, "phase1_ms": sum(p1) / a.steps,
+                     "phase2_ms": sum(p2) / a.steps}
+    c = moe.counts.astype(np.float64)
+    flop = float(6.0 * c.sum() * H * F)
+    # per-expert roofline: every expert's weights and token rows cross HBM once
+    f_e = 6.0 * c * H * F
+    b_e = np.where(c > 0, 3.0 * H * F * 2, 0.0) + c * (H * 2 + F * 2 * 2 + H * 2)
+    t_roof = float(np.sum(np.maximum(f_e / (MFMA_BF16_PEAK_TFLOPS * 1e12), b_e / (HBM_PEAK_GBPS * 1e9))))
+    bf = res.get("barrier_free", next(iter(res.values())))
+    ms = bf["ms_mean"]
+    tflops = flop / (ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC, "value": tflops, "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "MoE grouped GEMM, 32768 tokens top-1 to 64 experts (Zipf 1.1 counts), hidden 4096, "
+                               "ffn 1408, SiLU-gated, bf16 weights N(0,0.02); gate/up launch + down launch",
+                   "tokens": T, "experts": len(c), "hidden": H, "ffn": F, "parallelism": "single GPU"},
+        "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "phase_us": {kk: [v["phase1_ms"] * 1e3, v["phase2_ms"] * 1e3] for kk, v in res.items()},
+        "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
+        "per_expert_roofline": {"time_us": t_roof * 1e6, "frac": t_roof / (ms * 1e-3)},
+    }
+    if "barrier" in res and "barrier_free" in res:
+        out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
+    print(json.dumps(out), flush=True)
+
+
 def bf16_bits_as_f32(bits):
     import numpy as np
     return (bits.astype(np.uint32) << 16).view(np.float32)
@@ -246,6 +334,9 @@ def main():
         return
     if a.workload == "attn":
         bench_attn(a)
+        return
+    if a.workload == "moe":
+        bench_moe(a)
         return
     w = stream_workload(seed=a.seed, n_wg=a.n_wg, outer=a.outer, n_gen=a.n_gen)
     trips_np, off_np = w.trips.flat()

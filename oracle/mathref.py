@@ -74,6 +74,21 @@ def attention(q_bits, k_bits, v_bits, cu_seqlens, scale):
 
 
 # ---- MoE: top-1 routed SiLU-gated MLP -------------------------------------
+def moe_hidden(moe, tokens, weights=None):
+    """The gated hidden rows h[t] = SiLU(x W_gate) * (x W_up) of the given
+    tokens under their routed expert (the first half of the expert MLP)."""
+    weights = weights if weights is not None else {}
+    out = []
+    for t in tokens:
+        e = int(moe.assign[t])
+        if e not in weights:
+            weights[e] = tuple(bf16_to_f32(w).astype(np.float64) for w in moe.weights(e))
+        wg, wu, _ = weights[e]
+        x = bf16_to_f32(moe.x[t]).astype(np.float64)
+        out.append(silu(wg @ x) * (wu @ x))
+    return np.array(out)
+
+
 def moe_tokens(moe, tokens, weights=None):
     """Outputs y[t] = (SiLU(x W_gate) * (x W_up)) W_down for the given tokens,
     using each token's routed expert (gate weight 1)."""

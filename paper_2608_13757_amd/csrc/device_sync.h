@@ -139,6 +139,14 @@ struct WaitResult {
 
 // Poll the counter words of the nw producer waves (consecutive words from
 // addr) until every one is >= thr.  Gives up after max_polls polls.
+// Minimum of v over lanes 0 .. nw - 1, read lane by lane into scalar
+// registers (no cross-lane LDS traffic; nw is at most kMaxWavesPerEngine).
+__device__ __forceinline__ uint32_t lane_min(uint32_t v, int nw) {
+  uint32_t m = 0xffffffffu;
+  for (int i = 0; i < nw; ++i) m = min(m, (uint32_t)__builtin_amdgcn_readlane((int)v, i));
+  return m;
+}
+
 __device__ __forceinline__ WaitResult wait_geq(uint32_t addr, int nw, uint32_t thr, uint64_t max_polls) {
   WaitResult r{0, true};
   if (thr == 0) return r;
@@ -150,16 +158,11 @@ __device__ __forceinline__ WaitResult wait_geq(uint32_t addr, int nw, uint32_t t
     uint32_t v = lds_poll(a);
     uint64_t good = __ballot(v >= thr) & want;
     if (good == want) {
-      // minimum over the producer waves
-      uint32_t m = (lane < (uint32_t)nw) ? v : 0xffffffffu;
-      for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor((int)m, off));
-      r.observed = uniform(m);
+      r.observed = lane_min(v, nw);      // minimum over the producer waves
       return r;
     }
     if (++polls > max_polls) {
-      uint32_t m = (lane < (uint32_t)nw) ? v : 0xffffffffu;
-      for (int off = 32; off > 0; off >>= 1) m = min(m, (uint32_t)__shfl_xor((int)m, off));
-      r.observed = uniform(m);
+      r.observed = lane_min(v, nw);
       r.ok = false;
       return r;
     }

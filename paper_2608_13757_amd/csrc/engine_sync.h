@@ -54,13 +54,13 @@ struct SyncCommon {
   int32_t pad;
 };
 
-// Loop registers of a nest with at most two loops below the top level:
+// Loop registers of a nest with at most three loops below the top level:
 // r counts iterations since the start of the workgroup, h (rhat) within the
 // current trip (Section 5.1).  The top-level loop runs once.
 struct Regs {
-  uint32_t r1 = 0, r2 = 0, h1 = 0, h2 = 0;
-  __device__ __forceinline__ uint32_t r(uint32_t l) const { return l == 0 ? 1u : l == 1 ? r1 : r2; }
-  __device__ __forceinline__ uint32_t h(uint32_t l) const { return l == 0 ? 1u : l == 1 ? h1 : h2; }
+  uint32_t r1 = 0, r2 = 0, r3 = 0, h1 = 0, h2 = 0, h3 = 0;
+  __device__ __forceinline__ uint32_t r(uint32_t l) const { return l == 0 ? 1u : l == 1 ? r1 : l == 2 ? r2 : r3; }
+  __device__ __forceinline__ uint32_t h(uint32_t l) const { return l == 0 ? 1u : l == 1 ? h1 : l == 2 ? h2 : h3; }
 };
 
 template <int kMode, bool kInstr>

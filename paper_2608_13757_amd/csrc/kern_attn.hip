@@ -89,7 +89,15 @@ __device__ __forceinline__ bf16x4 lds_tr(uint32_t addr) {
   return __builtin_bit_cast(bf16x4, v);
 }
 
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
+// Lanes l and l ^ 32 exchange x with v_permlane32_swap (no LDS traffic):
+// the two results hold {x[l], x[l + 32]} in the low half and
+// {x[l - 32], x[l]} in the high half, so any symmetric op of the pair
+// combines the two lanes' values.
+__device__ __forceinline__ f32x2 pair32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x), __builtin_bit_cast(uint32_t, x),
+                                                  false, false);
+  return f32x2{__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1])};
+}
 
 template <int kMode, bool kInstr>
 __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
@@ -266,7 +274,8 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
         float mx = x[0];
 #pragma unroll
         for (int t = 1; t < 32; ++t) mx = __builtin_fmaxf(mx, x[t]);
-        mx = __builtin_fmaxf(mx, xor32(mx));
+        const f32x2 mp = pair32(mx);
+        mx = __builtin_fmaxf(mp.x, mp.y);
         const float m_new = __builtin_fmaxf(m, mx * c);
         const float alpha = __builtin_amdgcn_exp2f(m - m_new);
         float sum = 0.0f;
@@ -278,7 +287,8 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
           sum += p0 + p1;
           pk[t / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{p0, p1}, bf16x2));
         }
-        sum += xor32(sum);
+        const f32x2 sums = pair32(sum);
+        sum = sums.x + sums.y;
         lrun = alpha * lrun + sum;
         m = m_new;
 #pragma unroll

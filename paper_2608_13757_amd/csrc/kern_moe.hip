@@ -1,0 +1,424 @@
+// MoE grouped GEMM with top-1 routing, two launches per layer, three engines
+// per workgroup, one workgroup per (expert, N-tile, run of 128-token M-tiles):
+//
+//   phase 1  h[rows of expert e][n0 .. n0 + 127] = SiLU(x W_gate) * (x W_up),
+//            token rows gathered from x through the expert-grouped
+//            permutation, h stored bf16 in grouped row order;
+//   phase 2  y[token][n0 .. n0 + 255] = h W_down, rows scattered back to
+//            their tokens.
+//
+//   E0 (2 waves, load)      ACQL at each M-tile; LOAD: the step's 128 token
+//                           rows (wave 0) and 256 weight rows (wave 1), 32
+//                           wide in K, into a ring slot with direct-to-LDS
+//                           loads.
+//   E1 (8 waves, MFMA)      MMA: a 64-row sub-tile per wave, fp32
+//                           accumulators (phase 1: gate and up for 32 h
+//                           columns, so SiLU(g) * u needs no exchange;
+//                           phase 2: 64 y columns); ACQE at each M-tile;
+//                           SPILL: one 32 x 32 block per chunk, packed to
+//                           bf16 into an epilogue slot.
+//   E2 (2 waves, epilogue)  EPI: 16-byte row segments of the chunk to HBM.
+//
+// The M loop runs the workgroup's M-tiles, a count derived from the routing
+// and known only at run time; K runs K / 32 steps, C 2 (phase 1) or 4
+// (phase 2) chunks per M-tile.  Dependencies: LOAD->MMA (k = 0), MMA->LOAD
+// (k = ring), MMA->ACQL (k = 1, C3: an M-tile's loads start after the
+// previous tile's MFMAs released the ring), SPILL->EPI (k = 0), EPI->SPILL
+// (k = epilogue slots), EPI->ACQE (k = 1, C3).  Token rows past the expert's
+// count are loaded from a clamped row and never stored.
+//
+// LDS (bytes): counters 2048 | ring slots of 24 KiB (token rows 128 x 64 B,
+// then weight rows 256 x 64 B; 16-byte chunk c of row r at c ^ ((r / 4) % 4))
+// | epilogue slots of 16 KiB (8 blocks of 32 x 32 bf16, row-major).
+//
+// Family contract (BFS_KERNEL_MOE): loops top -> M -> {K, C}; ACQL (E0, NOP)
+// at M before K; LOAD (E0, opcode 48, args [phase, K, N, ring]) and MMA (E1,
+// 49) in K; ACQE (E1, NOP) at M between K and C; SPILL (E1, 51, args
+// [epilogue ring]) and EPI (E2, 50) in C; waves 2, 8, 2.  Phase 1: K = hidden
+// (multiple of 32), N = ffn (multiple of 128); phase 2: K = ffn (multiple of
+// 32), N = hidden (multiple of 256).  Buffers: [0] work list int32 [n_wg][4]
+// = (expert, first output column, first M-tile, M-tiles), [1] perm int32
+// [tokens] (token ids grouped by expert), [2] expert_off int32 [experts + 1];
+// phase 1: [3] x bf16 [tokens][hidden], [4] W_gate, [5] W_up bf16
+// [experts][ffn][hidden], [6] h bf16 [tokens][ffn]; phase 2: [3] h, [4]
+// W_down bf16 [experts][hidden][ffn], [5] y bf16 [tokens][hidden].
+#include <string>
+
+#include "engine_sync.h"
+
+using namespace bfsdev;
+
+namespace {
+
+constexpr int kBM = 128, kBK = 32;
+constexpr int kLoadW = 2, kMmaW = 8, kEpiW = 2, kWaves = 12;
+constexpr uint32_t kASlot = kBM * kBK * 2;          // 8 KiB of token rows
+constexpr uint32_t kSlotBytes = kASlot + 256 * kBK * 2;
+constexpr uint32_t kESlotBytes = kMmaW * 32 * 32 * 2;
+
+struct MoeParams {
+  SyncCommon sc;
+  InstrWaits acql, load, mma, acqe, spill, epi;
+  const int32_t *work;
+  const int32_t *perm;
+  const int32_t *eoff;
+  const __bf16 *a;          // x (phase 1) or h (phase 2)
+  const __bf16 *w0;         // W_gate (phase 1) or W_down (phase 2)
+  const __bf16 *w1;         // W_up (phase 1)
+  __bf16 *out;              // h (phase 1) or y (phase 2)
+  const int32_t *trips;
+  const int64_t *trip_off;
+  int32_t kdim, ndim, ring, e_ring, n_experts, n_tokens;
+};
+
+__device__ __forceinline__ uint32_t swz(uint32_t row, uint32_t chunk) {
+  return row * 64u + ((chunk ^ ((row >> 2) & 3u)) << 4);
+}
+
+__device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
+
+template <int kPhase, int kMode, bool kInstr>
+__global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
+  const uint32_t ring = lds_addr(lds) + kCntBytes;
+  const uint32_t ering = ring + (uint32_t)P.ring * kSlotBytes;
+  for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
+  __syncthreads();
+
+  const int wave = wave_id();
+  const uint32_t lane = lane_id(), l32 = lane & 31u, lhi = lane >> 5;
+  const int wg = blockIdx.x;
+  Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), wave, wg);
+
+  const int32_t expert = ldc(P.work + 4 * wg + 0), n0 = ldc(P.work + 4 * wg + 1);
+  const int32_t mt0 = ldc(P.work + 4 * wg + 2);
+  const int32_t e_lo = ldc(P.eoff + expert), e_cnt = ldc(P.eoff + expert + 1) - e_lo;
+  const int64_t *toff = P.trip_off + (int64_t)wg * 4;
+  uint32_t trip_m = (uint32_t)ldc(P.trips + ldc(toff + 1));
+  const int64_t k_off = ldc(toff + 2), c_off = ldc(toff + 3);
+  const uint32_t ksteps = (uint32_t)(P.kdim / kBK), chunks = kPhase == 1 ? 2u : 4u;
+  const uint32_t max_m = (uint32_t)max(0, (e_cnt + kBM - 1) / kBM - mt0);
+  if (trip_m > max_m) {
+    report_deadlock(P.sc.err, 0xffffu, (uint32_t)wg, 0, trip_m, max_m, (uint32_t)wave);
+    trip_m = max_m;
+  }
+  Regs g;
+  // one monotone "seen" cache per wait site
+  uint32_t sa[kMaxWaits] = {0, 0, 0, 0}, sb[kMaxWaits] = {0, 0, 0, 0}, sc[kMaxWaits] = {0, 0, 0, 0};
+  uint64_t mark = 0;
+
+  if (wave < kLoadW) {
+    // ------------------------------------------------------------ load engine
+    const uint32_t ew = (uint32_t)wave;
+    const int per_group = wave == 0 ? 8 : 16;                 // loads per step
+    int pending = 0;
+    auto retire_one = [&]() {
+      if (pending == 3) {
+        if (per_group == 8) wait_vm<16>(); else wait_vm<32>();
+      } else if (pending == 2) {
+        if (per_group == 8) wait_vm<8>(); else wait_vm<16>();
+      } else {
+        wait_vm<0>();
+      }
+      S.signal(P.load.update, ew);
+      pending -= 1;
+    };
+    auto retire_all = [&]() {
+      if (pending > 0) {
+        wait_vm<0>();
+        for (int i = 0; i < pending; ++i) S.signal(P.load.update, ew);
+        pending = 0;
+      }
+    };
+    // lane l covers rows 16 j + l / 4 and the 16-byte chunk that belongs at
+    // position l % 4 of its row
+    const uint32_t r_in = lane >> 2, chunk = (lane & 3u) ^ ((lane >> 4) & 3u);
+    S.sync_point(S.word(0, ew));                                  // before loop M
+    for (uint32_t mi = 0; mi < trip_m; ++mi) {
+      g.r1 += 1;
+      g.h1 = mi + 1;
+      S.waits(P.acql, g, g.r1 - 1, sa, [&] { retire_all(); });   // ACQL
+      S.signal(P.acql.update, ew);
+      retire_all();
+      // the K and C loops have static trips; a trip table that disagrees is
+      // reported (the static trips run)
+      if (wave == 0) {
+        const int32_t tk = ldc(P.trips + k_off + mi), tc = ldc(P.trips + c_off + mi);
+        if (tk != (int32_t)ksteps || tc != (int32_t)chunks)
+          report_deadlock(P.sc.err, 0xffffu, (uint32_t)wg, mi, (uint32_t)tk, (uint32_t)tc, (uint32_t)wave);
+      }
+      const int32_t m0 = (mt0 + (int32_t)mi) * kBM;
+      // source rows of this M-tile
+      const __bf16 *src[16];
+      if (wave == 0) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int32_t r = min(m0 + 16 * j + (int32_t)r_in, e_cnt - 1);
+          const int32_t row = kPhase == 1 ? P.perm[e_lo + r] : e_lo + r;
+          src[j] = P.a + (size_t)row * P.kdim + 8u * chunk;
+        }
+        wait_vm<0>();
+      } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const uint32_t r = 16u * j + r_in;
+          const __bf16 *w = (kPhase == 1 && r >= 128u) ? P.w1 : P.w0;
+          const uint32_t n = kPhase == 1 ? (n0 + (r & 127u)) : (n0 + r);
+          src[j] = w + ((size_t)expert * P.ndim + n) * P.kdim + 8u * chunk;
+        }
+      }
+      S.sync_point(S.word(0, ew));                                // before loop K
+      uint32_t slot = (g.r2) % (uint32_t)P.ring;
+      for (uint32_t it = 0; it < ksteps; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
+        g.r2 += 1;
+        g.h2 = it + 1;
+        S.waits(P.load, g, g.r2 - 1, sb, [&] { retire_all(); });
+        if (!S.aborted) {
+          const uint32_t dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kASlot);
+          const uint32_t koff = it * kBK;
+          if (wave == 0) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              __builtin_amdgcn_global_load_lds((const void *)(src[j] + koff), (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+          } else {
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+              __builtin_amdgcn_global_load_lds((const void *)(src[j] + koff), (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+          }
+          pending += 1;
+          if (pending == 3) retire_one();
+        } else {
+          S.signal(P.load.update, ew);
+        }
+        if (kMode == BFS_MODE_BARRIER) {
+          retire_all();
+          S.sync_point(S.word(0, ew));                            // end of a K iteration
+        }
+      }
+      retire_all();
+      S.sync_point(S.word(0, ew));                                // before loop C
+      for (uint32_t c = 0; c < chunks; ++c) {
+        g.r3 += 1;
+        g.h3 = c + 1;
+        S.sync_point(S.word(0, ew));                              // end of a C iteration
+      }
+      S.sync_point(S.word(0, ew));                                // end of an M iteration
+    }
+  } else if (wave < kLoadW + kMmaW) {
+    // ------------------------------------------------------------ MFMA engine
+    const uint32_t ew = (uint32_t)(wave - kLoadW);
+    const uint32_t wm = ew >> 2, wn = ew & 3u;
+    const uint32_t arow = wm * 64u + l32;
+    // weight rows of the two column blocks of this wave
+    const uint32_t brow0 = kPhase == 1 ? 32u * wn + l32 : 64u * wn + l32;
+    const uint32_t brow1 = kPhase == 1 ? 128u + 32u * wn + l32 : 64u * wn + 32u + l32;
+    S.sync_point(S.word(1, ew));                                  // before loop M
+    for (uint32_t mi = 0; mi < trip_m; ++mi) {
+      g.r1 += 1;
+      g.h1 = mi + 1;
+      f32x16 acc[4];                 // [b * 2 + rb]: b = weight block (gate / up, or column block)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[i] = f32x16{};
+      S.sync_point(S.word(1, ew));                                // before loop K
+      uint32_t slot = g.r2 % (uint32_t)P.ring;
+      for (uint32_t it = 0; it < ksteps; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
+        g.r2 += 1;
+        g.h2 = it + 1;
+        S.waits(P.mma, g, g.r2 - 1, sa, [] {});
+        if (!S.aborted) {
+          const uint32_t a_base = ring + slot * kSlotBytes, b_base = a_base + kASlot;
+          auto rd = [&](uint32_t base, uint32_t row, uint32_t c) {
+            return __builtin_bit_cast(bf16x8, *(const BFS_LDS u32x4 *)(uintptr_t)(base + swz(row, c)));
+          };
+          bf16x8 a0 = rd(a_base, arow, lhi), a1 = rd(a_base, arow + 32u, lhi);
+          bf16x8 b0 = rd(b_base, brow0, lhi), b1 = rd(b_base, brow1, lhi);
+          const bf16x8 a0n = rd(a_base, arow, 2u + lhi), a1n = rd(a_base, arow + 32u, 2u + lhi);
+          const bf16x8 b0n = rd(b_base, brow0, 2u + lhi), b1n = rd(b_base, brow1, 2u + lhi);
+          acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a0, acc[0], 0, 0, 0);
+          acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a1, acc[1], 0, 0, 0);
+          acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a0, acc[2], 0, 0, 0);
+          acc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a1, acc[3], 0, 0, 0);
+          acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0n, a0n, acc[0], 0, 0, 0);
+          acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0n, a1n, acc[1], 0, 0, 0);
+          acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a0n, acc[2], 0, 0, 0);
+          acc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a1n, acc[3], 0, 0, 0);
+        }
+        drain_lds();
+        S.signal(P.mma.update, ew);
+        S.sync_point(S.word(1, ew));                              // end of a K iteration
+      }
+      mark = S.elapsed();
+      S.waits(P.acqe, g, g.r1 - 1, sb, [] {});                    // ACQE
+      S.signal(P.acqe.update, ew);
+      S.sync_point(S.word(1, ew));                                // before loop C
+#pragma unroll
+      for (uint32_t c = 0; c < 4; ++c) {
+        if (c >= chunks) break;
+        g.r3 += 1;
+        g.h3 = c + 1;
+        S.waits(P.spill, g, g.r3 - 1, sc, [] {});
+        if (!S.aborted) {
+          const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
+          const uint32_t blk = ering + eslot * kESlotBytes + ew * 2048u;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if (kPhase == 1) v[e] = silu(acc[c][4 * j + e]) * acc[2 + c][4 * j + e];   // chunk = row block
+              else v[e] = acc[(c & 1u) * 2 + (c >> 1)][4 * j + e];                        // chunk = rb * 2 + cb
+            }
+            const u32x2 q = {__builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{v[0], v[1]}, bf16x2)),
+                             __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{v[2], v[3]}, bf16x2))};
+            *(BFS_LDS u32x2 *)(uintptr_t)(blk + l32 * 64u + (8u * j + 4u * lhi) * 2u) = q;
+          }
+        }
+        drain_lds();
+        S.signal(P.spill.update, ew);
+        S.sync_point(S.word(1, ew));                              // end of a C iteration
+      }
+      S.sync_point(S.word(1, ew));                                // end of an M iteration
+    }
+  } else {
+    // -------------------------------------------------------- epilogue engine
+    const uint32_t ew = (uint32_t)(wave - kLoadW - kMmaW);
+    S.sync_point(S.word(2, ew));                                  // before loop M
+    for (uint32_t mi = 0; mi < trip_m; ++mi) {
+      g.r1 += 1;
+      g.h1 = mi + 1;
+      const int32_t m0 = (mt0 + (int32_t)mi) * kBM;
+      // this wave stores the blocks of MFMA waves 4 ew .. 4 ew + 3 (rows
+      // 64 ew ..), lane rows 16 h + lane / 4 of each 32-row block
+      int32_t tok[2][2];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int32_t r = m0 + 64 * (int32_t)ew + 32 * rb + 16 * h + (int32_t)(lane >> 2);
+          tok[rb][h] = r < e_cnt ? (kPhase == 1 ? e_lo + r : P.perm[e_lo + r]) : -1;
+        }
+      S.sync_point(S.word(2, ew));                                // before loop K
+      for (uint32_t it = 0; it < ksteps; ++it) {
+        g.r2 += 1;
+        g.h2 = it + 1;
+        S.sync_point(S.word(2, ew));                              // end of a K iteration
+      }
+      S.sync_point(S.word(2, ew));                                // before loop C
+      for (uint32_t c = 0; c < chunks; ++c) {
+        g.r3 += 1;
+        g.h3 = c + 1;
+        S.waits(P.epi, g, g.r3 - 1, sa, [] {});
+        if (!S.aborted) {
+          const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
+          const uint32_t rb = kPhase == 1 ? c : (c >> 1), cb = kPhase == 1 ? 0u : (c & 1u);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t v = ew * 4u + q;                 // MFMA wave whose block this is
+            const uint32_t blk = ering + eslot * kESlotBytes + v * 2048u;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const uint32_t row = 16u * h + (lane >> 2), cc = lane & 3u;
+              const u32x4 d = *(const BFS_LDS u32x4 *)(uintptr_t)(blk + row * 64u + cc * 16u);
+              const int32_t t = rb == 0 ? tok[0][h] : tok[1][h];
+              const uint32_t col = kPhase == 1 ? (n0 + 32u * q + 8u * cc) : (n0 + 64u * q + 32u * cb + 8u * cc);
+              if (t >= 0) {
+                u32x4 *dst = reinterpret_cast<u32x4 *>(P.out + (size_t)t * P.ndim + col);
+                if (kPhase == 1) *dst = d;
+                else __builtin_nontemporal_store(d, dst);
+              }
+            }
+          }
+        }
+        drain_lds();
+        S.signal(P.epi.update, ew);
+        S.sync_point(S.word(2, ew));                              // end of a C iteration
+      }
+      S.sync_point(S.word(2, ew));                                // end of an M iteration
+    }
+  }
+  drain_all();
+  S.finish(lane, mark);
+}
+
+}  // namespace
+
+namespace bfs {
+
+bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
+                      const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream, uint32_t *dbg,
+                      int64_t dbg_cap, const bfs_run_opts &o) {
+  // structure: top{ M{ ACQL(E0); K{ LOAD(E0) MMA(E1) }; ACQE(E1); C{ SPILL(E1) EPI(E2) } } }
+  if (p->n_loops != 4 || p->loop_parent[1] != 0 || p->loop_parent[2] != 1 || p->loop_parent[3] != 1)
+    return fail(BFS_E_UNSUPPORTED, "moe: loops must be top -> M -> {K, C}");
+  if (p->n_engines != 3 || p->waves_per_engine[0] != kLoadW || p->waves_per_engine[1] != kMmaW ||
+      p->waves_per_engine[2] != kEpiW)
+    return fail(BFS_E_UNSUPPORTED, "moe: engines of 2, 8 and 2 waves");
+  int acql = -1, load = -1, mma = -1, acqe = -1, spill = -1, epi = -1;
+  for (size_t i = 0; i < p->instr_engine.size(); ++i) {
+    const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];
+    if (op == 0 && e == 0 && par == 1 && acql < 0 && load < 0) acql = (int)i;
+    else if (op == 48 && e == 0 && par == 2 && load < 0) load = (int)i;
+    else if (op == 49 && e == 1 && par == 2 && mma < 0) mma = (int)i;
+    else if (op == 0 && e == 1 && par == 1 && acqe < 0 && mma >= 0) acqe = (int)i;
+    else if (op == 51 && e == 1 && par == 3 && spill < 0) spill = (int)i;
+    else if (op == 50 && e == 2 && par == 3 && epi < 0) epi = (int)i;
+    else return fail(BFS_E_UNSUPPORTED, "moe: unexpected instruction " + std::to_string(i));
+  }
+  if (acql < 0 || load < 0 || mma < 0 || acqe < 0 || spill < 0 || epi < 0)
+    return fail(BFS_E_UNSUPPORTED, "moe: needs ACQL, LOAD, MMA, ACQE, SPILL and EPI");
+  const int32_t *la = &p->instr_args[8 * load];
+  const int phase = la[0], K = la[1], N = la[2], ring = la[3];
+  const int e_ring = p->instr_args[8 * spill];
+  if (phase != 1 && phase != 2) return fail(BFS_E_UNSUPPORTED, "moe: phase 1 or 2");
+  if (K <= 0 || K % kBK || N <= 0 || N % (phase == 1 ? 128 : 256))
+    return fail(BFS_E_UNSUPPORTED, "moe: K a multiple of 32, N a multiple of 128 (phase 1) or 256 (phase 2)");
+  if (ring < 2 || ring > 4 || e_ring < 1 || e_ring > 2) return fail(BFS_E_UNSUPPORTED, "moe: ring 2..4, epilogue 1..2");
+  if (!has_dep(p, load, mma, 0) || !has_dep(p, mma, load, ring) || !has_dep(p, mma, acql, 1) ||
+      !has_dep(p, spill, epi, 0) || !has_dep(p, epi, spill, e_ring) || !has_dep(p, epi, acqe, 1))
+    return fail(BFS_E_UNSUPPORTED, "moe: missing a ring or M-tile dependency");
+  const int need = phase == 1 ? 7 : 6;
+  if (nbufs < need) return fail(BFS_E_INVALID, "moe: too few buffers");
+  for (int i = 0; i < need; ++i)
+    if (!bufs[i]) return fail(BFS_E_INVALID, "moe: null buffer");
+  if (!trips || !trip_off || n_wg <= 0) return fail(BFS_E_INVALID, "moe: needs trip tables and workgroups");
+  const std::vector<DevWait> dw = device_waits(p);
+  MoeParams P{};
+  if (!fill_waits(p, dw, acql, P.acql) || !fill_waits(p, dw, load, P.load) || !fill_waits(p, dw, mma, P.mma) ||
+      !fill_waits(p, dw, acqe, P.acqe) || !fill_waits(p, dw, spill, P.spill) || !fill_waits(p, dw, epi, P.epi))
+    return fail(BFS_E_RESOURCE, "moe: at most 4 waits per instruction");
+  P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
+  P.work = static_cast<const int32_t *>(bufs[0]);
+  P.perm = static_cast<const int32_t *>(bufs[1]);
+  P.eoff = static_cast<const int32_t *>(bufs[2]);
+  P.a = static_cast<const __bf16 *>(bufs[3]);
+  P.w0 = static_cast<const __bf16 *>(bufs[4]);
+  P.w1 = phase == 1 ? static_cast<const __bf16 *>(bufs[5]) : nullptr;
+  P.out = static_cast<__bf16 *>(const_cast<void *>(bufs[phase == 1 ? 6 : 5]));
+  P.trips = trips;
+  P.trip_off = trip_off;
+  P.kdim = K;
+  P.ndim = N;
+  P.ring = ring;
+  P.e_ring = e_ring;
+  const size_t lds = kCntBytes + (size_t)ring * kSlotBytes + (size_t)e_ring * kESlotBytes;
+  const bool instr = dbg || o.dev_stats || o.fault_dep >= 0;
+  hipStream_t s = (hipStream_t)stream;
+  auto go = [&](auto kern) -> bfs_status {
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("moe attribute: ") + hipGetErrorString(e));
+    hipLaunchKernelGGL(kern, dim3(n_wg), dim3(64 * kWaves), lds, s, P);
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("moe launch: ") + hipGetErrorString(e));
+    return BFS_OK;
+  };
+  const bool bar = p->mode == BFS_MODE_BARRIER;
+  if (phase == 1) {
+    if (bar) return instr ? go(moe_kernel<1, BFS_MODE_BARRIER, true>) : go(moe_kernel<1, BFS_MODE_BARRIER, false>);
+    return instr ? go(moe_kernel<1, BFS_MODE_BARRIER_FREE, true>) : go(moe_kernel<1, BFS_MODE_BARRIER_FREE, false>);
+  }
+  if (bar) return instr ? go(moe_kernel<2, BFS_MODE_BARRIER, true>) : go(moe_kernel<2, BFS_MODE_BARRIER, false>);
+  return instr ? go(moe_kernel<2, BFS_MODE_BARRIER_FREE, true>) : go(moe_kernel<2, BFS_MODE_BARRIER_FREE, false>);
+}
+
+}  // namespace bfs

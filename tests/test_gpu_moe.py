@@ -1,0 +1,170 @@
+"""GPU parity of the MoE grouped-GEMM family (load / MFMA / epilogue engines,
+runtime M-tile loop per workgroup, two phases).
+
+bf16 MFMA stages: |gpu - oracle| <= 2e-2 * max(|oracle|, rms(oracle)) per
+element against the fp64 oracle (the GPU rounds h to bf16 between the two
+phases, the oracle does not); thresholds bit-exact against the oracle's
+brute force for every wave of every consumer engine; the barrier-free and
+barrier modes produce bit-identical outputs."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import core, mathref  # noqa: E402
+from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
+from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
+from workloads import moe_program, moe_worklist  # noqa: E402
+from workloads.tensors import bf16_to_f32, moe_inputs, moe_weights_all  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+MODES = [("barrier_free", MODE_BARRIER_FREE), ("barrier", MODE_BARRIER)]
+RTOL = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    bfs.lib()
+
+
+def _say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+def _dev16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+
+
+class MoeRun:
+    """Device copies of one MoE problem and the two launches."""
+
+    def __init__(self, moe, mchunk=8):
+        self.moe = moe
+        wg, wu, wd = moe_weights_all(moe)
+        self.wg, self.wu, self.wd = _dev16(wg), _dev16(wu), _dev16(wd)
+        self.x = _dev16(moe.x)
+        self.perm = torch.from_numpy(moe.perm.astype(np.int32)).cuda()
+        self.eoff = torch.from_numpy(moe.expert_off.astype(np.int32)).cuda()
+        T = len(moe.assign)
+        self.h = torch.full((T, moe.ffn), -1, dtype=torch.int16, device="cuda")
+        self.y = torch.full((T, moe.hidden), -1, dtype=torch.int16, device="cuda")
+        self.wl = {ph: moe_worklist(moe.counts, ph, moe.hidden, moe.ffn, mchunk=mchunk) for ph in (1, 2)}
+        self.dev_wl = {}
+        for ph, wl in self.wl.items():
+            trips, toff = trip_tensors(wl.trips)
+            self.dev_wl[ph] = (torch.from_numpy(wl.work.reshape(-1)).cuda(), trips, toff, wl.trips.n_wg)
+
+    def bufs(self, ph):
+        work = self.dev_wl[ph][0]
+        if ph == 1:
+            return [work, self.perm, self.eoff, self.x, self.wg, self.wu, self.h]
+        return [work, self.perm, self.eoff, self.h, self.wd, self.y]
+
+    def run(self, mode, cap=0):
+        logs = {}
+        for ph in (1, 2):
+            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn), mode)
+            work, trips, toff, n_wg = self.dev_wl[ph]
+            log = None
+            if cap:
+                log = torch.zeros(plan.debug_log_words(n_wg, cap), dtype=torch.int32, device="cuda")
+            plan.run(self.bufs(ph), trips, toff, n_wg, debug_log=log, debug_capacity=cap)
+            plan.status()
+            if cap:
+                logs[ph] = (plan, log.cpu().numpy().view(np.uint32))
+        h = bf16_to_f32(self.h.cpu().numpy().view(np.uint16))
+        y = bf16_to_f32(self.y.cpu().numpy().view(np.uint16))
+        return h, y, logs
+
+
+def check_close(got, ref):
+    ref = np.asarray(ref, np.float64)
+    scale = np.maximum(np.abs(ref), np.sqrt(np.mean(ref ** 2)))
+    err = np.abs(got.astype(np.float64) - ref) / scale
+    assert np.isfinite(got).all()
+    assert err.max() <= RTOL, (err.max(), np.unravel_index(err.argmax(), err.shape))
+    return err.max()
+
+
+# an empty expert, a one-token expert, ragged tiles, runs of M-tiles split
+# over workgroups (mchunk 2)
+SMALL_COUNTS = [300, 0, 129, 1, 530]
+
+
+def test_moe_small_parity_and_thresholds():
+    moe = moe_inputs(seed=1, hidden=256, ffn=256, counts=SMALL_COUNTS)
+    r = MoeRun(moe, mchunk=2)
+    T = len(moe.assign)
+    ref_y = mathref.moe_tokens(moe, range(T))
+    grouped = moe.perm                                  # h rows are in expert-grouped order
+    ref_h = mathref.moe_hidden(moe, grouped)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[moe-small] mode={name}")
+        h, y, logs = r.run(mode, cap=64)
+        check_close(h, ref_h)
+        check_close(y, ref_y)
+        for ph in (1, 2):
+            plan, logw = logs[ph]
+            prog = moe_program(ph, moe.hidden, moe.ffn)
+            wl = r.wl[ph]
+            trips, off = wl.trips.flat()
+            recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
+            lg = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
+            assert compare_wave_logs_with_oracle(prog, plan, lg, recs, name) > 0
+        outs[name] = y
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_moe_full_size_sampled():
+    """The benchmark shape (32768 tokens, 64 Zipf(1.1) experts, hidden 4096,
+    ffn 1408), checked on sampled tokens one by one."""
+    _say("[moe-full] generating")
+    moe = moe_inputs(seed=0)
+    r = MoeRun(moe)
+    order = np.argsort(-moe.counts)
+    experts = list(order[:3]) + list(order[30:32]) + list(order[-3:])   # largest, middle, smallest
+    rng = np.random.default_rng(5)
+    tokens = []
+    for e in experts:
+        lo, hi = int(moe.expert_off[e]), int(moe.expert_off[e + 1])
+        group = moe.perm[lo:hi]
+        tokens += [int(group[0]), int(group[-1])] + [int(t) for t in rng.choice(group, 6)]
+    weights = {}
+    ref = mathref.moe_tokens(moe, tokens, weights)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[moe-full] mode={name}")
+        _, y, _ = r.run(mode)
+        check_close(y[tokens], ref)
+        outs[name] = y
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_moe_rejects_missing_dependency():
+    prog = moe_program(1, 256, 256)
+    prog.deps = [d for d in prog.deps if prog.instrs[d[1]].name != "ACQL"]
+    plan = Plan(prog)
+    t = torch.zeros(16, dtype=torch.int32, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t] * 7, t, t, 1)
+    assert e.value.status == bfs.E_UNSUPPORTED
+
+
+def test_moe_watchdog():
+    moe = moe_inputs(seed=3, hidden=256, ffn=256, counts=[200, 50])
+    r = MoeRun(moe)
+    plan = Plan(moe_program(1, moe.hidden, moe.ffn))
+    work, trips, toff, n_wg = r.dev_wl[1]
+    _say("[moe-watchdog]")
+    plan.run(r.bufs(1), trips, toff, n_wg, watchdog_polls=2000, fault_dep=0, fault_delta=1 << 20)
+    with pytest.raises(BfsError) as e:
+        plan.status()
+    assert e.value.status == bfs.E_DEADLOCK
+    plan.run(r.bufs(1), trips, toff, n_wg)
+    plan.status()

@@ -261,3 +261,14 @@ def test_moe_reference_properties():
     y0 = mathref.moe_tokens(m, [0], weights={e: (0 * wg, wu, wd)})
     assert np.allclose(y0, 0)
     assert mathref.silu(np.array([0.0]))[0] == 0.0
+    # SiLU(1) = 1 / (1 + e^-1) = 0.7310585786300049 (known constant)
+    assert abs(mathref.silu(np.array([1.0]))[0] - 0.7310585786300049) < 1e-15
+    # the hidden rows: with W_gate = W_up = I they are SiLU(x) * x, and the
+    # full output is W_down applied to them
+    eye = np.eye(16, 32)
+    h = mathref.moe_hidden(m, [0], weights={e: (eye, eye, wd)})
+    x = bf16_to_f32(m.x[0]).astype(np.float64)[:16]
+    assert np.allclose(h[0], x * x / (1.0 + np.exp(-x)))
+    assert np.allclose(mathref.moe_tokens(m, [0, 1]), [wd_e @ h_e for wd_e, h_e in zip(
+        [(bf16_to_f32(m.weights(int(m.assign[t]))[2]).astype(np.float64)) for t in (0, 1)],
+        mathref.moe_hidden(m, [0, 1]))])

@@ -19,7 +19,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .program import (OP_ADDC, OP_ATTN_LOAD, OP_ATTN_NORM, OP_ATTN_PV, OP_ATTN_QK, OP_ATTN_SM,
+from .program import (OP_ADDC, OP_MOE_EPI, OP_MOE_LOAD, OP_MOE_MMA, OP_MOE_SPILL, OP_ATTN_LOAD, OP_ATTN_NORM, OP_ATTN_PV, OP_ATTN_QK, OP_ATTN_SM,
                       OP_GEMM_BIAS, OP_GEMM_EPI, OP_GEMM_LOAD, OP_GEMM_MMA,
                       OP_GEMM_SPILL, OP_LOAD, OP_NOP, OP_SCALE_ACC, OP_STORE_ACC,
                       OP_STORE_RING, Program, ProgramBuilder, tile_args)
@@ -399,3 +399,99 @@ def attn_worklist(lengths, heads: int, xcds: int = 8) -> AttnWork:
     trips = TripTables([[np.array([1], np.int32), np.array([-(-int(L) // ATTN_BKV)], np.int32)]
                         for _, L, _, _ in work])
     return AttnWork(work, trips)
+
+
+# ---------------------------------------------------------------------------
+# cfg5: MoE grouped GEMM, two phases with load / MFMA / epilogue engines and a
+# runtime M-tile loop per workgroup
+# ---------------------------------------------------------------------------
+MOE_BM = 128                 # token rows per M-tile
+MOE_BK = 32                  # K step per ring slot
+MOE_BN = {1: 128, 2: 256}    # output columns per workgroup: h columns (phase 1), y columns (phase 2)
+MOE_CHUNKS = {1: 2, 2: 4}    # epilogue chunks per M-tile
+MOE_RING = 4
+MOE_MCHUNK = 8               # at most this many M-tiles per workgroup
+
+
+def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring: int = 2) -> Program:
+    """One workgroup per (expert, N-tile, run of M-tiles); phase 1 computes
+    h = SiLU(x W_gate) * (x W_up) for 128 h columns, phase 2 y = h W_down for
+    256 y columns:
+
+      M{ E0: ACQL
+         K{ E0: LOAD token rows and weight rows of the step -> ring[(rhat_K - 1) % ring]; E1: MMA }
+         E1: ACQE
+         C{ E1: SPILL one accumulator block per MFMA wave -> ering[(rhat_C - 1) % e_ring]; E2: EPI store } }
+
+    The M loop's trip count is the number of 128-token tiles of the
+    workgroup's expert it covers, known only at run time.  LOAD->MMA (k=0)
+    and MMA->LOAD (k=ring) protect the ring inside an M-tile, MMA->ACQL (k=1,
+    C3) across M-tiles (the next tile's loads reuse the slots); SPILL->EPI
+    (k=0) and EPI->SPILL (k=e_ring) protect the epilogue ring inside an
+    M-tile, EPI->ACQE (k=1, C3) across M-tiles."""
+    k_dim, n_dim = (hidden, ffn) if phase == 1 else (ffn, hidden)
+    b = ProgramBuilder("moe", n_engines=3, waves_per_engine=[2, 8, 2])
+    with b.loop("M"):
+        b.instr(0, OP_NOP, [0] * 8, name="ACQL")
+        with b.loop("K"):
+            b.instr(0, OP_MOE_LOAD, [phase, k_dim, n_dim, ring, 0, 0, 0, 0], name="LOAD")
+            b.instr(1, OP_MOE_MMA, [0] * 8, name="MMA")
+        b.instr(1, OP_NOP, [0] * 8, name="ACQE")
+        with b.loop("C"):
+            b.instr(1, OP_MOE_SPILL, [e_ring, 0, 0, 0, 0, 0, 0, 0], name="SPILL")
+            b.instr(2, OP_MOE_EPI, [0] * 8, name="EPI")
+    b.dep("LOAD", "MMA", 0)
+    b.dep("MMA", "LOAD", ring)
+    b.dep("MMA", "ACQL", 1)
+    b.dep("SPILL", "EPI", 0)
+    b.dep("EPI", "SPILL", e_ring)
+    b.dep("EPI", "ACQE", 1)
+    return b.build()
+
+
+@dataclass
+class MoeWork:
+    work: np.ndarray      # int32 [n_wg, 4]: expert, first output column, first M-tile, M-tiles
+    trips: TripTables     # per workgroup: [[1], [n_mt], [K / 32] * n_mt, [chunks] * n_mt]
+
+
+def moe_worklist(counts, phase: int, hidden: int, ffn: int, mchunk: int = MOE_MCHUNK, xcds: int = 8) -> MoeWork:
+    """Work items (expert, N-tile, run of at most ``mchunk`` M-tiles).
+
+    An expert's M-tiles are split into runs of nearly equal length; each
+    (expert, run) with all its N-tiles goes to the XCD with the least work so
+    far (largest experts first), so the N-tiles sharing the run's token rows
+    share one L2.  Workgroup w runs on XCD w % xcds; shorter XCD lists are
+    padded with empty items (no M-tiles)."""
+    k_dim, n_dim = (hidden, ffn) if phase == 1 else (ffn, hidden)
+    bn = MOE_BN[phase]
+    n_tiles = n_dim // bn
+    counts = np.asarray(counts, dtype=np.int64)
+    order = sorted(range(len(counts)), key=lambda e: (-int(counts[e]), e))
+    load = [0] * xcds
+    lists = [[] for _ in range(xcds)]
+    for e in order:
+        mt = -(-int(counts[e]) // MOE_BM)
+        if mt == 0:
+            continue
+        runs = -(-mt // mchunk)
+        base, extra = divmod(mt, runs)
+        first = 0
+        for r in range(runs):
+            n_mt = base + (1 if r < extra else 0)
+            x = min(range(xcds), key=lambda i: (load[i], i))
+            load[x] += n_mt * n_tiles
+            for t in range(n_tiles):
+                lists[x].append((e, t * bn, first, n_mt))
+            first += n_mt
+    depth = max((len(l) for l in lists), default=0)
+    items = []
+    for i in range(depth):
+        for x in range(xcds):
+            items.append(lists[x][i] if i < len(lists[x]) else (0, 0, 0, 0))
+    work = np.array(items, dtype=np.int32).reshape(-1, 4)
+    ksteps, chunks = k_dim // MOE_BK, MOE_CHUNKS[phase]
+    trips = TripTables([[np.array([1], np.int32), np.array([n_mt], np.int32),
+                         np.full(n_mt, ksteps, np.int32), np.full(n_mt, chunks, np.int32)]
+                        for _, _, _, n_mt in work])
+    return MoeWork(work, trips)

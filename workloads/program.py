@@ -53,9 +53,10 @@ OP_ATTN_QK = 33
 OP_ATTN_SM = 34
 OP_ATTN_PV = 35
 OP_ATTN_NORM = 36
-OP_MOE_LOAD = 48
+OP_MOE_LOAD = 48       # args: phase (1 gate/up, 2 down), K, N, ring depth
 OP_MOE_MMA = 49
 OP_MOE_EPI = 50
+OP_MOE_SPILL = 51      # args: epilogue ring depth
 
 KIND_BLOCK = 0
 KIND_LOOP = 1

@@ -108,15 +108,34 @@ class MoeInputs:
 
 
 def moe_inputs(seed: int = 0, tokens: int = 32768, experts: int = 64, hidden: int = 4096,
-               ffn: int = 1408, s: float = 1.1) -> MoeInputs:
-    counts_by_rank = zipf_counts(tokens, experts, s)
+               ffn: int = 1408, s: float = 1.1, counts=None) -> MoeInputs:
+    """Top-1 routing with Zipf(s) expert counts over a seeded rank -> expert
+    map (or the given per-expert ``counts``), a seeded shuffle of the token ->
+    expert assignment, and x ~ N(0, 1) rounded to bf16."""
     g = rng_for(CFG_MOE, seed, 0)
-    rank_to_expert = g.permutation(experts)
-    counts = np.zeros(experts, np.int64)
-    counts[rank_to_expert] = counts_by_rank
+    if counts is None:
+        counts_by_rank = zipf_counts(tokens, experts, s)
+        rank_to_expert = g.permutation(experts)
+        counts = np.zeros(experts, np.int64)
+        counts[rank_to_expert] = counts_by_rank
+    else:
+        counts = np.asarray(counts, np.int64)
+        experts, tokens = len(counts), int(counts.sum())
     assign = np.repeat(np.arange(experts, dtype=np.int32), counts)
     g.shuffle(assign)
     perm = np.argsort(assign, kind="stable").astype(np.int32)
     expert_off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
     x = to_bf16_bits(rng_for(CFG_MOE, seed, 1).standard_normal((tokens, hidden), dtype=np.float32))
     return MoeInputs(x, assign, counts, perm, expert_off, hidden, ffn, seed)
+
+
+def moe_weights_all(moe: MoeInputs):
+    """Every expert's weights stacked: W_gate, W_up [E][ffn][hidden] and
+    W_down [E][hidden][ffn], uint16 bf16."""
+    E = len(moe.counts)
+    wg = np.empty((E, moe.ffn, moe.hidden), np.uint16)
+    wu = np.empty((E, moe.ffn, moe.hidden), np.uint16)
+    wd = np.empty((E, moe.hidden, moe.ffn), np.uint16)
+    for e in range(E):
+        wg[e], wu[e], wd[e] = moe.weights(e)
+    return wg, wu, wd
