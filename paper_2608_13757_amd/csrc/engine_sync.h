@@ -9,7 +9,9 @@
 // threshold.
 #pragma once
 
+#include <initializer_list>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "bfs_internal.h"
@@ -29,10 +31,21 @@ typedef __attribute__((ext_vector_type(2))) float f32x2;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 
+// How a wait's threshold moves while the consumer's innermost loop L runs
+// (decided on the host from the loop tree):
+//   affine   producer and shared loop are L itself (C1 at L): Eq. 5 is
+//            base + N * rhat_L with the mask rhat_L > k, base fixed at L's entry;
+//   constant the producer's loop lies outside L's subtree and the shared loop
+//            is a proper ancestor of L: Eq. 5 does not change during L's trip
+//            (and in barrier mode every threshold is a constant ordinal);
+//   dynamic  the producer's loop is nested inside L or the shared loop is L
+//            with an outer producer: Eq. 5 is evaluated at every wait.
+constexpr int32_t kWaitAffine = 0, kWaitConst = 1, kWaitDynamic = 2;
+
 struct Wait {
   bfs::PackedWait w;
   int32_t n_prd_waves;
-  int32_t pad;
+  int32_t kind;
 };
 
 // The waits of one instruction and the counter slot it increments.
@@ -57,11 +70,55 @@ struct SyncCommon {
 // Loop registers of a nest with at most three loops below the top level:
 // r counts iterations since the start of the workgroup, h (rhat) within the
 // current trip (Section 5.1).  The top-level loop runs once.
+// Selection by bit masks keeps the registers in scalar registers (a
+// conditional chain is turned into a stack lookup table by the compiler).
 struct Regs {
   uint32_t r1 = 0, r2 = 0, r3 = 0, h1 = 0, h2 = 0, h3 = 0;
-  __device__ __forceinline__ uint32_t r(uint32_t l) const { return l == 0 ? 1u : l == 1 ? r1 : l == 2 ? r2 : r3; }
-  __device__ __forceinline__ uint32_t h(uint32_t l) const { return l == 0 ? 1u : l == 1 ? h1 : l == 2 ? h2 : h3; }
+  __device__ __forceinline__ static uint32_t sel(uint32_t l, uint32_t v1, uint32_t v2, uint32_t v3) {
+    const uint32_t m0 = 0u - (uint32_t)(l == 0), m1 = 0u - (uint32_t)(l == 1);
+    const uint32_t m2 = 0u - (uint32_t)(l == 2), m3 = 0u - (uint32_t)(l == 3);
+    return (m0 & 1u) | (m1 & v1) | (m2 & v2) | (m3 & v3);
+  }
+  __device__ __forceinline__ uint32_t r(uint32_t l) const { return sel(l, r1, r2, r3); }
+  __device__ __forceinline__ uint32_t h(uint32_t l) const { return sel(l, h1, h2, h3); }
 };
+
+// The loop-invariant part of one instruction's waits, set up at each entry
+// to the instruction's innermost loop (Section 6.2: only the iteration-
+// dependent term is evaluated per iteration), plus the monotone "seen" cache.
+// kN is the most waits the call site takes (launchers check it).  Per wait:
+// meta = counter word address (bits 0-15) | producer waves (16-19) | kind
+// (20-21); mk = mask offset k (0-15) | N (16-31); base = the affine or
+// constant part of Eq. 5.
+template <int kN>
+struct Site {
+  uint32_t n = 0;
+  uint32_t meta[kN];
+  uint32_t mk[kN];
+  int32_t base[kN];
+  uint32_t seen[kN];
+  __device__ Site() {
+#pragma unroll
+    for (int j = 0; j < kN; ++j) {
+      meta[j] = 0;
+      mk[j] = 0;
+      base[j] = 0;
+      seen[j] = 0;
+    }
+  }
+};
+
+// Minimum of v over lanes 0 .. 15 with DPP moves (no LDS traffic), read from
+// lane 0.  The counter polls put producer wave w's word in lane w and repeat
+// lane 0's word in every lane at or above the producer count, so this is the
+// minimum over the producer waves.
+__device__ __forceinline__ uint32_t min16(uint32_t v) {
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false));    // quad_perm 1,0,3,2
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, false));    // quad_perm 2,3,0,1
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x124, 0xF, 0xF, false));   // row_ror 4
+  v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, false));   // row_ror 8
+  return __builtin_amdgcn_readfirstlane(v);
+}
 
 template <int kMode, bool kInstr>
 struct Sync {
@@ -87,52 +144,103 @@ struct Sync {
     return cnt_base + 4u * (slot * (uint32_t)bfs::kMaxWavesPerEngine + w);
   }
 
-  __device__ __forceinline__ uint32_t threshold(const bfs::PackedWait &w, const Regs &g) const {
-    uint32_t thr;
-    if (kMode == BFS_MODE_BARRIER) {
-      thr = ((w.w0 >> 25) & 1u) ? (w.w3 >> 16) : 0u;
-    } else {
-      thr = eq5(g.r((w.w0 >> 8) & 0xffu), g.h((w.w0 >> 16) & 0xffu), (int)(w.w2 & 0xffffu), (int)(w.w2 >> 16),
-                (int)(w.w1 & 0xffffu), (int)(w.w1 >> 16), (int)((w.w0 >> 24) & 1u));
+  // Poll until every producer word reaches thr (one poll first; on_block()
+  // before blocking); returns the minimum observed producer word.
+  template <class OnBlock>
+  __device__ __forceinline__ uint32_t poll_geq(uint32_t addr, uint32_t nw, uint32_t thr, uint32_t dep,
+                                               uint32_t instance, OnBlock on_block) {
+    const uint32_t lane = lane_id();
+    const uint32_t a = addr + 4u * (lane < nw ? lane : 0u);
+    const uint64_t want = (1ull << nw) - 1ull;
+    uint32_t v = lds_poll(a);
+    if ((__ballot(v >= thr) & want) == want) return min16(v);
+    on_block();
+    const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
+    uint64_t polls = 0;
+    while (true) {
+      v = lds_poll(a);
+      if ((__ballot(v >= thr) & want) == want) break;
+      if (++polls > C.watchdog) {
+        const uint32_t m = min16(v);
+        report_deadlock(C.err, dep, (uint32_t)wg, instance, thr, m, (uint32_t)wave);
+        aborted = 1u;
+        return m;
+      }
+      if (polls < 4) __builtin_amdgcn_s_sleep(1);
+      else __builtin_amdgcn_s_sleep(2);
     }
-    if (kInstr && (int)(w.w3 & 0xffffu) == C.fault_dep) thr += (uint32_t)C.fault_delta;
-    return thr;
+    if (kInstr && st.on) {
+      st.blocked += now_ticks() - t0;
+      st.n_blocked += 1;
+    }
+    return min16(v);
   }
 
-  // All waits of one instruction.  on_block() retires what this wave holds
-  // before it would block.  seen[] keeps, per wait of this instruction, the
-  // last counter value observed: counters only grow, so it stays a valid lower
-  // bound (barrier mode resets counters, so there every wait polls).
-  template <class OnBlock>
-  __device__ __forceinline__ void waits(const InstrWaits &iw, const Regs &g, uint32_t instance,
-                                        uint32_t (&seen)[kMaxWaits], OnBlock on_block) {
-    for (int j = 0; j < iw.n; ++j) {
-      const bfs::PackedWait w = iw.w[j].w;
-      const int nw = iw.w[j].n_prd_waves;
-      const uint32_t thr = threshold(w, g);
-      uint32_t obs = kMode == BFS_MODE_BARRIER ? 0u : seen[j];
-      if (!aborted && thr > 0 && (obs < thr || (kInstr && log))) {
-        const uint32_t a = word(w.w0 & 0xffu, 0);
-        WaitResult res = wait_geq(a, nw, thr, 0);   // one poll
-        if (!res.ok) {
-          on_block();
-          const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
-          res = wait_geq(a, nw, thr, C.watchdog);
-          if (kInstr && st.on) {
-            st.blocked += now_ticks() - t0;
-            st.n_blocked += 1;
-          }
-          if (!res.ok) {
-            report_deadlock(C.err, w.w3 & 0xffffu, (uint32_t)wg, instance, thr, res.observed, (uint32_t)wave);
-            aborted = 1u;
-          }
+  // Set up the waits of an instruction whose innermost loop is L, before
+  // the first iteration of a trip of L (g still holds r_L of the previous
+  // trips).
+  template <int kN>
+  __device__ __forceinline__ void enter(Site<kN> &s, const InstrWaits &iw, const Regs &g, uint32_t L) {
+    s.n = (uint32_t)iw.n;
+#pragma unroll
+    for (int j = 0; j < kN; ++j) {
+      if (j < iw.n) {
+        const bfs::PackedWait w = iw.w[j].w;
+        uint32_t kind = (uint32_t)iw.w[j].kind;
+        if (kMode == BFS_MODE_BARRIER) {
+          kind = (uint32_t)kWaitConst;
+          s.base[j] = ((w.w0 >> 25) & 1u) ? (int32_t)(w.w3 >> 16) : 0;
+        } else if (kind == (uint32_t)kWaitAffine) {
+          const int32_t N = (int32_t)(w.w1 & 0xffffu), K = (int32_t)(w.w1 >> 16);
+          const int32_t sub = (int32_t)(w.w2 >> 16);
+          s.base[j] = N * ((int32_t)g.r(L) - sub) - (N - K);
+          s.mk[j] = (((w.w0 >> 24) & 1u) ? (w.w2 & 0xffffu) : 0u) | ((uint32_t)N << 16);
+        } else if (kind == (uint32_t)kWaitConst) {
+          s.base[j] = (int32_t)threshold_plain(w, g);
         }
-        obs = res.observed;
-        seen[j] = obs;
+        s.meta[j] = word(w.w0 & 0xffu, 0) | ((uint32_t)iw.w[j].n_prd_waves << 16) | (kind << 20);
       }
-      if (kInstr && log) {
-        on_block();
-        log_wait(log, C.dbg_cap, nlog, w.w3 & 0xffffu, instance, thr, thr > 0 ? obs : 0u);
+    }
+  }
+
+  // Eq. 5 (no fault injection).
+  __device__ __forceinline__ uint32_t threshold_plain(const bfs::PackedWait &w, const Regs &g) const {
+    return eq5(g.r((w.w0 >> 8) & 0xffu), g.h((w.w0 >> 16) & 0xffu), (int)(w.w2 & 0xffffu), (int)(w.w2 >> 16),
+               (int)(w.w1 & 0xffffu), (int)(w.w1 >> 16), (int)((w.w0 >> 24) & 1u));
+  }
+
+  // All waits of the instruction at iteration t (rhat of its loop, from 1).
+  template <int kN, class OnBlock>
+  __device__ __forceinline__ void wait(Site<kN> &s, const InstrWaits &iw, const Regs &g, uint32_t t,
+                                       uint32_t instance, OnBlock on_block) {
+#pragma unroll
+    for (int j = 0; j < kN; ++j) {
+      if ((uint32_t)j < s.n) {
+        const uint32_t kind = (s.meta[j] >> 20) & 3u;
+        uint32_t thr;
+        if (kind == (uint32_t)kWaitAffine) {
+          const int32_t v = s.base[j] + (int32_t)((s.mk[j] >> 16) * t);
+          thr = (t > (s.mk[j] & 0xffffu) && v > 0) ? (uint32_t)v : 0u;
+        } else if (kind == (uint32_t)kWaitConst) {
+          thr = (uint32_t)s.base[j];
+        } else {
+          thr = threshold_plain(iw.w[j].w, g);
+        }
+        uint32_t dep = 0;
+        if (kInstr) {
+          dep = iw.w[j].w.w3 & 0xffffu;
+          if ((int)dep == C.fault_dep) thr += (uint32_t)C.fault_delta;
+        }
+        uint32_t obs = kMode == BFS_MODE_BARRIER ? 0u : s.seen[j];
+        if (!aborted && thr > 0 && (obs < thr || (kInstr && log))) {
+          obs = poll_geq(s.meta[j] & 0xffffu, (s.meta[j] >> 16) & 0xfu, thr,
+                         kInstr ? dep : (iw.w[j].w.w3 & 0xffffu), instance, on_block);
+          s.seen[j] = obs;
+        }
+        if (kInstr && log) {
+          on_block();
+          log_wait(log, C.dbg_cap, nlog, dep, instance, thr, thr > 0 ? obs : 0u);
+        }
       }
     }
   }
@@ -175,14 +283,29 @@ namespace bfs {
 
 // Host: copy one instruction's waits (and its counter slot) into kernel
 // arguments.  False when the instruction has more waits than fit.
+// Host: true when loop x lies in the subtree of loop l (x == l included).
+inline bool in_subtree(const bfs_plan *p, int x, int l) {
+  for (; x >= 0; x = p->loop_parent[x])
+    if (x == l) return true;
+  return false;
+}
+
+// Host: copy one instruction's waits (and its counter slot) into kernel
+// arguments, with each wait's kind relative to the instruction's innermost
+// loop.  False when the instruction has more waits than fit.
 inline bool fill_waits(const bfs_plan *p, const std::vector<DevWait> &dw, int ins, bfsdev::InstrWaits &out) {
   out.n = 0;
   out.update = p->instr_update[ins];
+  const int L = p->instr_parent[ins];
   for (int wi = p->instr_wait_off[ins]; wi < p->instr_wait_off[ins + 1]; ++wi) {
     if (out.n == bfsdev::kMaxWaits) return false;
     const DevWait &d = dw[p->instr_wait_list[wi]];
     if (!pack_wait(d, out.w[out.n].w)) return false;
     out.w[out.n].n_prd_waves = p->waves_per_engine[d.prd_engine];
+    int kind = bfsdev::kWaitDynamic;
+    if (d.loop_P == L && d.loop_S == L) kind = bfsdev::kWaitAffine;
+    else if (!in_subtree(p, d.loop_P, L) && d.loop_S != L) kind = bfsdev::kWaitConst;
+    out.w[out.n].kind = kind;
     out.n += 1;
   }
   return true;
@@ -193,6 +316,13 @@ inline bool has_dep(const bfs_plan *p, int prd, int cns, int k) {
   for (size_t d = 0; d < p->deps.size() / 3; ++d)
     if (p->deps[3 * d] == prd && p->deps[3 * d + 1] == cns && p->deps[3 * d + 2] == k) return true;
   return false;
+}
+
+// Host: every instruction's wait count fits its kernel call site.
+inline bool waits_fit(std::initializer_list<std::pair<const bfsdev::InstrWaits *, int>> sites) {
+  for (auto &x : sites)
+    if (x.first->n > x.second) return false;
+  return true;
 }
 
 // Host: launch-wide instrumentation block from the run options.

@@ -136,7 +136,7 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
   }
   const size_t row_stride = (size_t)P.heads * kD;     // elements between tokens
   Regs g;
-  uint32_t seen_a[kMaxWaits] = {0, 0, 0, 0}, seen_b[kMaxWaits] = {0, 0, 0, 0};
+  Site<2> site;
   uint64_t mark = 0;
 
   if (eng == 0 || eng == 4) {
@@ -165,11 +165,12 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
     // that belongs at position t % 16 of that row
     const uint32_t rr = lane >> 4, pos = lane & 15u;
     S.sync_point(own);                                       // before loop KV
+    S.enter(site, iw, g, 1);
     uint32_t slot = 0;
     for (uint32_t it = 0; it < trip; ++it, slot = (slot + 1 == depth) ? 0u : slot + 1) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.waits(iw, g, g.r1 - 1, seen_a, [&] { retire_all(); });
+      S.wait(site, iw, g, it + 1, g.r1 - 1, [&] { retire_all(); });
       if (!S.aborted) {
         const uint32_t dst = ring + slot * kKVSlot;
         const int32_t key0 = (int32_t)it * kBKV;
@@ -205,11 +206,12 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
         qf[qb][s] = L > 0 ? __builtin_bit_cast(bf16x8, *(const u32x4 *)(src + 16 * s)) : bf16x8{};
     }
     S.sync_point(own);                                       // before loop KV
+    S.enter(site, P.qk, g, 1);
     uint32_t kslot = 0;
     for (uint32_t it = 0; it < trip; ++it, kslot = (kslot + 1 == (uint32_t)P.nk) ? 0u : kslot + 1) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.waits(P.qk, g, g.r1 - 1, seen_a, [] {});
+      S.wait(site, P.qk, g, it + 1, g.r1 - 1, [] {});
       if (!S.aborted) {
         const uint32_t kb_base = kring + kslot * kKVSlot;
         const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
@@ -250,10 +252,11 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
     const float c = P.scale_log2;
     float m = -__builtin_inff(), lrun = 0.0f;
     S.sync_point(own);                                       // before loop KV
+    S.enter(site, P.sm, g, 1);
     for (uint32_t it = 0; it < trip; ++it) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.waits(P.sm, g, g.r1 - 1, seen_a, [] {});
+      S.wait(site, P.sm, g, it + 1, g.r1 - 1, [] {});
       if (!S.aborted) {
         const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
         float x[32];
@@ -323,11 +326,12 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
       voff[db] = vrow * 256u + 16u * (4u * ((uint32_t)db ^ x) + 2u * ((lane >> 4) & 1u) + ((lane >> 1) & 1u)) +
                  8u * (lane & 1u);
     S.sync_point(own);                                       // before loop KV
+    S.enter(site, P.pv, g, 1);
     uint32_t vslot = 0;
     for (uint32_t it = 0; it < trip; ++it, vslot = (vslot + 1 == (uint32_t)P.nv) ? 0u : vslot + 1) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.waits(P.pv, g, g.r1 - 1, seen_a, [] {});
+      S.wait(site, P.pv, g, it + 1, g.r1 - 1, [] {});
       if (!S.aborted) {
         const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
         const uint32_t vb = vring + vslot * kKVSlot;
@@ -359,7 +363,9 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
     }
     mark = S.elapsed();
     // NORM: O / l for the rows of the sequence
-    S.waits(P.norm, g, 0, seen_b, [] {});
+    Site<1> s_norm;
+    S.enter(s_norm, P.norm, g, 0);
+    S.wait(s_norm, P.norm, g, 1, 0, [] {});
     if (!S.aborted) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
@@ -433,6 +439,8 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   if (!fill_waits(p, dw, lk, P.loadk) || !fill_waits(p, dw, lv, P.loadv) || !fill_waits(p, dw, qk, P.qk) ||
       !fill_waits(p, dw, sm, P.sm) || !fill_waits(p, dw, pv, P.pv) || !fill_waits(p, dw, nm, P.norm))
     return fail(BFS_E_RESOURCE, "attn: at most 4 waits per instruction");
+  if (!waits_fit({{&P.loadk, 2}, {&P.loadv, 2}, {&P.qk, 2}, {&P.sm, 2}, {&P.pv, 2}, {&P.norm, 1}}))
+    return fail(BFS_E_RESOURCE, "attn: more waits on an instruction than its engine loop takes");
   P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
   P.work = static_cast<const int32_t *>(bufs[0]);
   P.q = static_cast<const __bf16 *>(bufs[1]);

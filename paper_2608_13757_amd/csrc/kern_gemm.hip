@@ -144,9 +144,10 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
         pending = 0;
       }
     };
-    uint32_t seen_bias[kMaxWaits] = {0, 0, 0, 0}, seen_load[kMaxWaits] = {0, 0, 0, 0};
+    Site<1> s_bias, s_load;
     // BIAS (top level)
-    S.waits(P.bias, g, 0, seen_bias, [] {});
+    S.enter(s_bias, P.bias, g, 0);
+    S.wait(s_bias, P.bias, g, 1, 0, [] {});
     if (wave == 0 && !S.aborted)
       __builtin_amdgcn_global_load_lds((const void *)(P.bias_v + n0 + 4 * lane), (BFS_LDS void *)bias_l, 16, 0, 0);
     wait_vm<0>();
@@ -155,13 +156,14 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     // per-lane source rows: lane l covers row 16 j + l / 4, logical chunk
     // (l % 4) ^ ((l / 16) % 4), so its 16 bytes land at the swizzled place.
     const uint32_t r_in = lane >> 2, chunk = (lane & 3u) ^ ((lane >> 4) & 3u);
+    S.enter(s_load, P.load, g, 1);
     const __bf16 *src = (wave == 0 ? P.a + (size_t)(m0 + r_in) * P.k : P.bt + (size_t)(n0 + r_in) * P.k) + 8 * chunk;
     const size_t row16 = (size_t)16 * P.k;
     uint32_t slot = 0;
     for (uint32_t it = 0; it < trip_k; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.waits(P.load, g, g.r1 - 1, seen_load, [&] { retire_all(); });
+      S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { retire_all(); });
       if (!S.aborted) {
         unsigned char *dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kSlotBytes / 2);
         const __bf16 *s0 = src + (size_t)it * kBK;
@@ -193,14 +195,16 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     f32x16 acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = f32x16{};
-    uint32_t seen_mma[kMaxWaits] = {0, 0, 0, 0}, seen_spill[kMaxWaits] = {0, 0, 0, 0};
+    Site<1> s_mma;
+    Site<3> s_spill;
     S.sync_point(S.word(1, ew));                            // before loop K
+    S.enter(s_mma, P.mma, g, 1);
     const uint32_t l32 = lane & 31u, lhi = lane >> 5;
     uint32_t slot = 0;
     for (uint32_t it = 0; it < trip_k; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.waits(P.mma, g, g.r1 - 1, seen_mma, [] {});
+      S.wait(s_mma, P.mma, g, it + 1, g.r1 - 1, [] {});
       const uint32_t a_base = ring_base + slot * kSlotBytes, b_base = a_base + kSlotBytes / 2;
       if (!S.aborted) {
         // Fragments are read one block ahead of the MFMAs that use them, so
@@ -240,6 +244,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     }
     k_end = S.elapsed();
     S.sync_point(S.word(1, ew));                            // before loop C
+    S.enter(s_spill, P.spill, g, 2);
     // The chunk loop is unrolled so that each chunk names its accumulator
     // block statically; trip_c <= 8 chunks run.
 #pragma unroll
@@ -247,7 +252,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       if (it >= trip_c) break;
       g.r2 += 1;
       g.h2 = it + 1;
-      S.waits(P.spill, g, g.r2 - 1, seen_spill, [] {});
+      S.wait(s_spill, P.spill, g, it + 1, g.r2 - 1, [] {});
       if (!S.aborted) {
         const uint32_t b = it, bm = b >> 1, bn = b & 1u;
         const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
@@ -273,7 +278,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
   } else {
     // -------------------------------------------------------- epilogue engine
     const uint32_t ew = (uint32_t)(wave - kLoadW - kMmaW);
-    uint32_t seen_epi[kMaxWaits] = {0, 0, 0, 0};
+    Site<1> s_epi;
     S.sync_point(S.word(2, ew));                            // before loop K
     for (uint32_t it = 0; it < trip_k; ++it) {
       g.r1 += 1;
@@ -281,10 +286,11 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       S.sync_point(S.word(2, ew));                          // end of a K iteration
     }
     S.sync_point(S.word(2, ew));                            // before loop C
+    S.enter(s_epi, P.epi, g, 2);
     for (uint32_t it = 0; it < trip_c; ++it) {
       g.r2 += 1;
       g.h2 = it + 1;
-      S.waits(P.epi, g, g.r2 - 1, seen_epi, [] {});
+      S.wait(s_epi, P.epi, g, it + 1, g.r2 - 1, [] {});
       if (!S.aborted) {
         const uint32_t b = it, bm = b >> 1, bn = b & 1u;
         const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
@@ -356,6 +362,8 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
   if (!fill_waits(p, dw, ins_bias, P.bias) || !fill_waits(p, dw, ins_load, P.load) ||
       !fill_waits(p, dw, ins_mma, P.mma) || !fill_waits(p, dw, ins_spill, P.spill) || !fill_waits(p, dw, ins_epi, P.epi))
     return fail(BFS_E_RESOURCE, "gemm: at most 4 waits per instruction");
+  if (!waits_fit({{&P.bias, 1}, {&P.load, 1}, {&P.mma, 1}, {&P.spill, 3}, {&P.epi, 1}}))
+    return fail(BFS_E_RESOURCE, "gemm: more waits on an instruction than its engine loop takes");
   P.a = static_cast<const __bf16 *>(bufs[0]);
   P.bt = static_cast<const __bf16 *>(bufs[1]);
   P.bias_v = static_cast<const float *>(bufs[2]);

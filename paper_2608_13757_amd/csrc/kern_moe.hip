@@ -104,8 +104,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
     trip_m = max_m;
   }
   Regs g;
-  // one monotone "seen" cache per wait site
-  uint32_t sa[kMaxWaits] = {0, 0, 0, 0}, sb[kMaxWaits] = {0, 0, 0, 0}, sc[kMaxWaits] = {0, 0, 0, 0};
+  Site<2> sa, sb, sc;               // one per wait site of the engine
   uint64_t mark = 0;
 
   if (wave < kLoadW) {
@@ -135,10 +134,11 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
     // position l % 4 of its row
     const uint32_t r_in = lane >> 2, chunk = (lane & 3u) ^ ((lane >> 4) & 3u);
     S.sync_point(S.word(0, ew));                                  // before loop M
+    S.enter(sa, P.acql, g, 1);
     for (uint32_t mi = 0; mi < trip_m; ++mi) {
       g.r1 += 1;
       g.h1 = mi + 1;
-      S.waits(P.acql, g, g.r1 - 1, sa, [&] { retire_all(); });   // ACQL
+      S.wait(sa, P.acql, g, mi + 1, g.r1 - 1, [&] { retire_all(); });   // ACQL
       S.signal(P.acql.update, ew);
       retire_all();
       // the K and C loops have static trips; a trip table that disagrees is
@@ -169,11 +169,12 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
         }
       }
       S.sync_point(S.word(0, ew));                                // before loop K
+      S.enter(sb, P.load, g, 2);
       uint32_t slot = (g.r2) % (uint32_t)P.ring;
       for (uint32_t it = 0; it < ksteps; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
         g.r2 += 1;
         g.h2 = it + 1;
-        S.waits(P.load, g, g.r2 - 1, sb, [&] { retire_all(); });
+        S.wait(sb, P.load, g, it + 1, g.r2 - 1, [&] { retire_all(); });
         if (!S.aborted) {
           const uint32_t dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kASlot);
           const uint32_t koff = it * kBK;
@@ -214,6 +215,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
     const uint32_t brow0 = kPhase == 1 ? 32u * wn + l32 : 64u * wn + l32;
     const uint32_t brow1 = kPhase == 1 ? 128u + 32u * wn + l32 : 64u * wn + 32u + l32;
     S.sync_point(S.word(1, ew));                                  // before loop M
+    S.enter(sb, P.acqe, g, 1);
     for (uint32_t mi = 0; mi < trip_m; ++mi) {
       g.r1 += 1;
       g.h1 = mi + 1;
@@ -221,11 +223,12 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc[i] = f32x16{};
       S.sync_point(S.word(1, ew));                                // before loop K
+      S.enter(sa, P.mma, g, 2);
       uint32_t slot = g.r2 % (uint32_t)P.ring;
       for (uint32_t it = 0; it < ksteps; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
         g.r2 += 1;
         g.h2 = it + 1;
-        S.waits(P.mma, g, g.r2 - 1, sa, [] {});
+        S.wait(sa, P.mma, g, it + 1, g.r2 - 1, [] {});
         if (!S.aborted) {
           const uint32_t a_base = ring + slot * kSlotBytes, b_base = a_base + kASlot;
           auto rd = [&](uint32_t base, uint32_t row, uint32_t c) {
@@ -249,15 +252,16 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
         S.sync_point(S.word(1, ew));                              // end of a K iteration
       }
       mark = S.elapsed();
-      S.waits(P.acqe, g, g.r1 - 1, sb, [] {});                    // ACQE
+      S.wait(sb, P.acqe, g, mi + 1, g.r1 - 1, [] {});                    // ACQE
       S.signal(P.acqe.update, ew);
       S.sync_point(S.word(1, ew));                                // before loop C
+      S.enter(sc, P.spill, g, 3);
 #pragma unroll
       for (uint32_t c = 0; c < 4; ++c) {
         if (c >= chunks) break;
         g.r3 += 1;
         g.h3 = c + 1;
-        S.waits(P.spill, g, g.r3 - 1, sc, [] {});
+        S.wait(sc, P.spill, g, c + 1, g.r3 - 1, [] {});
         if (!S.aborted) {
           const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
           const uint32_t blk = ering + eslot * kESlotBytes + ew * 2048u;
@@ -305,10 +309,11 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
         S.sync_point(S.word(2, ew));                              // end of a K iteration
       }
       S.sync_point(S.word(2, ew));                                // before loop C
+      S.enter(sa, P.epi, g, 3);
       for (uint32_t c = 0; c < chunks; ++c) {
         g.r3 += 1;
         g.h3 = c + 1;
-        S.waits(P.epi, g, g.r3 - 1, sa, [] {});
+        S.wait(sa, P.epi, g, c + 1, g.r3 - 1, [] {});
         if (!S.aborted) {
           const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
           const uint32_t rb = kPhase == 1 ? c : (c >> 1), cb = kPhase == 1 ? 0u : (c & 1u);
@@ -387,6 +392,8 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   if (!fill_waits(p, dw, acql, P.acql) || !fill_waits(p, dw, load, P.load) || !fill_waits(p, dw, mma, P.mma) ||
       !fill_waits(p, dw, acqe, P.acqe) || !fill_waits(p, dw, spill, P.spill) || !fill_waits(p, dw, epi, P.epi))
     return fail(BFS_E_RESOURCE, "moe: at most 4 waits per instruction");
+  if (!waits_fit({{&P.acql, 2}, {&P.load, 2}, {&P.mma, 2}, {&P.acqe, 2}, {&P.spill, 2}, {&P.epi, 2}}))
+    return fail(BFS_E_RESOURCE, "moe: more waits on an instruction than its engine loop takes");
   P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
   P.work = static_cast<const int32_t *>(bufs[0]);
   P.perm = static_cast<const int32_t *>(bufs[1]);
