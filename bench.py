@@ -68,27 +68,22 @@ def time_mode(plan, bufs, trips, toff, n_wg, steps, warmup):
             "wall_ms_per_step": 1e3 * wall / steps}
 
 
-def kernel_source_digest():
-    import hashlib
-    h = hashlib.sha256()
-    for f in ("kern_stream3.hip", "device_sync.h"):
-        with open(os.path.join(ROOT, "paper_2608_13757_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
-def recorded_traffic():
-    """HBM bytes per launch of the stream kernel measured with rocprofv3
-    FETCH_SIZE / WRITE_SIZE (profiles/stream3_traffic.json), or None when the
-    kernel source changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", "stream3_traffic.json")
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        rec = json.load(f)
-    if rec.get("kernel_source_digest") != kernel_source_digest():
-        return None
-    return rec.get("traffic_bytes_per_launch")
+def emit(out, a, kernel):
+    """Attach the recorded HBM traffic of the kernel (when its profile matches
+    the current sources), run the copy that calibrates traffic counters if
+    asked, and print the JSON line."""
+    import torch
+    from paper_2608_13757_amd.profiles import recorded_traffic
+    tr = recorded_traffic(kernel)
+    if tr is not None:
+        out["roofline"]["traffic"] = tr
+    if a.copy_calibration_mib:
+        src = torch.empty(a.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+    print(json.dumps(out), flush=True)
 
 
 def cpu_baseline(w, budget_s=20.0):
@@ -174,7 +169,7 @@ def bench_gemm(a):
     }
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
-    print(json.dumps(out), flush=True)
+    emit(out, a, "gemm")
 
 
 def bench_attn(a):
@@ -221,10 +216,7 @@ def bench_attn(a):
     }
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
-    print(json.dumps(out), flush=True)
-
-
-HBM_PEAK_GBPS = 8000.0
+    emit(out, a, "attn")
 
 
 def bench_moe(a):
@@ -290,7 +282,7 @@ def bench_moe(a):
     # per-expert roofline: every expert's weights and token rows cross HBM once
     f_e = 6.0 * c * H * F
     b_e = np.where(c > 0, 3.0 * H * F * 2, 0.0) + c * (H * 2 + F * 2 * 2 + H * 2)
-    t_roof = float(np.sum(np.maximum(f_e / (MFMA_BF16_PEAK_TFLOPS * 1e12), b_e / (HBM_PEAK_GBPS * 1e9))))
+    t_roof = float(np.sum(np.maximum(f_e / (MFMA_BF16_PEAK_TFLOPS * 1e12), b_e / (HBM_PEAK_GBS * 1e9))))
     bf = res.get("barrier_free", next(iter(res.values())))
     ms = bf["ms_mean"]
     tflops = flop / (ms * 1e-3) / 1e12
@@ -309,7 +301,7 @@ def bench_moe(a):
     }
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
-    print(json.dumps(out), flush=True)
+    emit(out, a, "moe")
 
 
 def bf16_bits_as_f32(bits):
@@ -384,18 +376,9 @@ def main():
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
         out["barrier_ops_per_s"] = ops / (res["barrier"]["ms_mean"] * 1e-3)
-    tr = recorded_traffic()
-    if tr is not None:
-        out["roofline"]["traffic"] = tr
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
-    if a.copy_calibration_mib:
-        src = torch.empty(a.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-    print(json.dumps(out), flush=True)
+    emit(out, a, "stream3")
 
 
 if __name__ == "__main__":
