@@ -144,8 +144,11 @@ struct Sync {
     return cnt_base + 4u * (slot * (uint32_t)bfs::kMaxWavesPerEngine + w);
   }
 
-  // Poll until every producer word reaches thr (one poll first; on_block()
-  // before blocking); returns the minimum observed producer word.
+  // Poll until every producer word reaches thr; returns the minimum
+  // observed producer word.  on_block() runs before every repeated poll: a
+  // producer that holds unretired work retires its oldest piece there, one
+  // at a time, so the consumers it may be waiting for make progress while
+  // its younger loads stay in flight.
   template <class OnBlock>
   __device__ __forceinline__ uint32_t poll_geq(uint32_t addr, uint32_t nw, uint32_t thr, uint32_t dep,
                                                uint32_t instance, OnBlock on_block) {
@@ -160,6 +163,7 @@ struct Sync {
     while (true) {
       v = lds_poll(a);
       if ((__ballot(v >= thr) & want) == want) break;
+      on_block();
       if (++polls > C.watchdog) {
         const uint32_t m = min16(v);
         report_deadlock(C.err, dep, (uint32_t)wg, instance, thr, m, (uint32_t)wave);
@@ -245,6 +249,12 @@ struct Sync {
     }
   }
 
+  // Retirement: add 1 to this wave's word of the instruction's counter.
+  // LDS executes one wave's DS instructions in issue order, so an add issued
+  // after the instruction's LDS writes (its results) and LDS reads (its last
+  // use of a slot) takes effect after them: engines whose effects are LDS
+  // accesses signal without waiting.  Direct-to-LDS loads are retired by
+  // their issuer after a counted vmcnt wait instead.
   __device__ __forceinline__ void signal(int update, uint32_t ew) {
     if (update >= 0) lds_add(word((uint32_t)update, ew), 1u);
   }

@@ -163,7 +163,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     for (uint32_t it = 0; it < trip_k; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { retire_all(); });
+      S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
       if (!S.aborted) {
         unsigned char *dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kSlotBytes / 2);
         const __bf16 *s0 = src + (size_t)it * kBK;
@@ -237,8 +237,6 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
           b1 = nb1;
         }
       }
-      // the slot's LDS reads have completed (the MFMAs consumed them)
-      drain_lds();
       S.signal(P.mma.update, ew);
       S.sync_point(S.word(1, ew));                          // end of a K iteration (barrier mode)
     }
@@ -271,7 +269,6 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
         }
         (void)bm;
       }
-      drain_lds();
       S.signal(P.spill.update, ew);
       S.sync_point(S.word(1, ew));                          // end of a C iteration
     }
@@ -309,7 +306,6 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
           }
         }
       }
-      drain_lds();
       S.signal(P.epi.update, ew);
       S.sync_point(S.word(2, ew));                          // end of a C iteration
     }

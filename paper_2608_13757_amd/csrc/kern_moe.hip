@@ -138,7 +138,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
     for (uint32_t mi = 0; mi < trip_m; ++mi) {
       g.r1 += 1;
       g.h1 = mi + 1;
-      S.wait(sa, P.acql, g, mi + 1, g.r1 - 1, [&] { retire_all(); });   // ACQL
+      S.wait(sa, P.acql, g, mi + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });   // ACQL
       S.signal(P.acql.update, ew);
       retire_all();
       // the K and C loops have static trips; a trip table that disagrees is
@@ -174,7 +174,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
       for (uint32_t it = 0; it < ksteps; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
         g.r2 += 1;
         g.h2 = it + 1;
-        S.wait(sb, P.load, g, it + 1, g.r2 - 1, [&] { retire_all(); });
+        S.wait(sb, P.load, g, it + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
         if (!S.aborted) {
           const uint32_t dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kASlot);
           const uint32_t koff = it * kBK;
@@ -247,7 +247,6 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
           acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a0n, acc[2], 0, 0, 0);
           acc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a1n, acc[3], 0, 0, 0);
         }
-        drain_lds();
         S.signal(P.mma.update, ew);
         S.sync_point(S.word(1, ew));                              // end of a K iteration
       }
@@ -278,7 +277,6 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
             *(BFS_LDS u32x2 *)(uintptr_t)(blk + l32 * 64u + (8u * j + 4u * lhi) * 2u) = q;
           }
         }
-        drain_lds();
         S.signal(P.spill.update, ew);
         S.sync_point(S.word(1, ew));                              // end of a C iteration
       }
@@ -335,7 +333,6 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
             }
           }
         }
-        drain_lds();
         S.signal(P.epi.update, ew);
         S.sync_point(S.word(2, ew));                              // end of a C iteration
       }

@@ -341,7 +341,7 @@ def attn_program(heads: int, dim: int = ATTN_D, nk: int = 3, nv: int = 2) -> Pro
     QK->LOADK (k=nk) and PV->LOADV (k=nv) free ring slots; PV->QK (k=2) frees
     an S/P slot; SM->NORM (k=0, producer nested in KV) delivers the final row
     sums."""
-    b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 4, 2, 1])
+    b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 2, 2, 1])
     with b.loop("KV"):
         b.instr(0, OP_ATTN_LOAD, [0, nk, heads, dim, 0, 0, 0, 0], name="LOADK")
         b.instr(4, OP_ATTN_LOAD, [1, nv, heads, dim, 0, 0, 0, 0], name="LOADV")
@@ -456,34 +456,46 @@ class MoeWork:
 
 
 def moe_worklist(counts, phase: int, hidden: int, ffn: int, mchunk: int = MOE_MCHUNK, xcds: int = 8) -> MoeWork:
-    """Work items (expert, N-tile, run of at most ``mchunk`` M-tiles).
+    """Work items (expert, N-tile, run of at most ``mchunk`` M-tiles) in launch
+    order.
 
-    An expert's M-tiles are split into runs of nearly equal length; each
-    (expert, run) with all its N-tiles goes to the XCD with the least work so
-    far (largest experts first), so the N-tiles sharing the run's token rows
-    share one L2.  Workgroup w runs on XCD w % xcds; shorter XCD lists are
-    padded with empty items (no M-tiles)."""
+    An expert's M-tiles are split into runs of nearly equal length.  The unit
+    placed on an XCD is one (expert, N-tile) with all its runs: those
+    workgroups stream the same weight rows in the same K order, so on one L2
+    each weight chunk is fetched once for all runs.  Experts are taken
+    largest first and each fills the least-loaded XCD up to an even share
+    before spilling to the next, so an expert's token rows are shared by the
+    N-tiles on the same XCD.  Workgroup w runs on XCD w % xcds; shorter XCD
+    lists are padded with empty items (no M-tiles)."""
     k_dim, n_dim = (hidden, ffn) if phase == 1 else (ffn, hidden)
     bn = MOE_BN[phase]
     n_tiles = n_dim // bn
     counts = np.asarray(counts, dtype=np.int64)
     order = sorted(range(len(counts)), key=lambda e: (-int(counts[e]), e))
+    mtiles = {e: -(-int(counts[e]) // MOE_BM) for e in order}
+    share = sum(mtiles.values()) * n_tiles / xcds
     load = [0] * xcds
     lists = [[] for _ in range(xcds)]
     for e in order:
-        mt = -(-int(counts[e]) // MOE_BM)
+        mt = mtiles[e]
         if mt == 0:
             continue
-        runs = -(-mt // mchunk)
-        base, extra = divmod(mt, runs)
-        first = 0
-        for r in range(runs):
+        runs_n = -(-mt // mchunk)
+        base, extra = divmod(mt, runs_n)
+        runs, first = [], 0
+        for r in range(runs_n):
             n_mt = base + (1 if r < extra else 0)
-            x = min(range(xcds), key=lambda i: (load[i], i))
-            load[x] += n_mt * n_tiles
-            for t in range(n_tiles):
-                lists[x].append((e, t * bn, first, n_mt))
+            runs.append((first, n_mt))
             first += n_mt
+        t = 0
+        while t < n_tiles:
+            x = min(range(xcds), key=lambda i: (load[i], i))
+            room = max(1, int((share - load[x]) // mt)) if load[x] < share else 1
+            for tt in range(t, min(n_tiles, t + room)):
+                for first, n_mt in runs:
+                    lists[x].append((e, tt * bn, first, n_mt))
+                load[x] += mt
+            t += room
     depth = max((len(l) for l in lists), default=0)
     items = []
     for i in range(depth):
