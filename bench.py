@@ -34,7 +34,7 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--n-wg", type=int, default=1024)
     ap.add_argument("--outer", type=int, default=256)
-    ap.add_argument("--n-gen", type=int, default=8)
+    ap.add_argument("--n-gen", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--modes", default="barrier_free,barrier")
     ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn", "moe"],
@@ -366,7 +366,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": "sync-bound stream: load/add/store engines, nest 256 x U[1,16] x U[1,4], "
-                               "64-fp32 tiles, 1024 workgroups",
+                               "64-fp32 tiles, 1024 workgroups, one in-place LDS ring",
                    "n_wg": a.n_wg, "outer": a.outer, "innermost_iterations": inner,
                    "ring_generations": a.n_gen, "seed": a.seed, "parallelism": "single GPU"},
         "latency_us": {k: v["ms_mean"] * 1e3 for k, v in res.items()},

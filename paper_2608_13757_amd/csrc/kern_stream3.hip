@@ -32,8 +32,10 @@
 // engines of one wave, tile_elems 64; the I body holds exactly one load
 // (engine 0), one add-constant (engine 1) and one store-slot (engine 2), all
 // addressed with slot = ((r_M - 1) % n_gen) * per_gen + (rhat_I - 1) % per_gen
-// and tile index base[wg] + r_I - 1.  Buffers: [0] int64 tile base per
+// (at most 128 slots per ring, rings 0 and 1; the add may write the ring it
+// reads) and tile index base[wg] + r_I - 1.  Buffers: [0] int64 tile base per
 // workgroup, [1] fp32 input tiles, [2] fp32 output tiles.
+#include <algorithm>
 #include <string>
 
 #include "bfs_internal.h"
@@ -75,6 +77,7 @@ struct Stream3Params {
   uint64_t watchdog;
   int32_t fault_dep, fault_delta;
   int32_t n_gen, per_gen, n_slots;
+  int32_t ring_ld, ring_add_src, ring_add_dst, ring_st;   // ring id of each access
   float addc;
 };
 
@@ -424,8 +427,8 @@ template <int kMode, bool kInstr, int kInflight>
 __global__ void __launch_bounds__(192) stream3_kernel(Stream3Params P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
-  float *ring_x = reinterpret_cast<float *>(lds + bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4);
-  float *ring_y = ring_x + P.n_slots * 64;
+  float *rings = reinterpret_cast<float *>(lds + bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4);
+  const int ring_floats = P.n_slots * 64;
   for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
   __syncthreads();
   const uint32_t cb = lds_addr(cnt);
@@ -433,9 +436,17 @@ __global__ void __launch_bounds__(192) stream3_kernel(Stream3Params P) {
   // The add engine has the most work per tile; it wins issue arbitration
   // against the load and store waves, which mostly poll.
   if (wave == ROLE_ADD) __builtin_amdgcn_s_setprio(2);
-  if (wave == ROLE_LOAD) run_engine<ROLE_LOAD, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
-  else if (wave == ROLE_ADD) run_engine<ROLE_ADD, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
-  else run_engine<ROLE_STORE, kMode, kInstr, kInflight>(P, cb, ring_x, ring_y);
+  // run_engine(ring read or loaded into, ring written or read from)
+  if (wave == ROLE_LOAD) {
+    float *r = rings + P.ring_ld * ring_floats;
+    run_engine<ROLE_LOAD, kMode, kInstr, kInflight>(P, cb, r, r);
+  } else if (wave == ROLE_ADD) {
+    run_engine<ROLE_ADD, kMode, kInstr, kInflight>(P, cb, rings + P.ring_add_src * ring_floats,
+                                                   rings + P.ring_add_dst * ring_floats);
+  } else {
+    float *r = rings + P.ring_st * ring_floats;
+    run_engine<ROLE_STORE, kMode, kInstr, kInflight>(P, cb, r, r);
+  }
 }
 
 template <int kMode, bool kInstr>
@@ -486,6 +497,7 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
   Stream3Params P{};
   const int want_op[3] = {1, 4, 5};
   int n_gen = -1, per_gen = -1;
+  int ring_of[4] = {0, 0, 0, 0};      // load dst, add src, add dst, store src
   float addc = 0.f;
   for (int e = 0; e < 3; ++e) {
     HostEngine H;
@@ -507,6 +519,9 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
         if (n_gen == -1) { n_gen = a[3]; per_gen = a[5]; }
         if (a[3] != n_gen || a[5] != per_gen) return fail(BFS_E_UNSUPPORTED, "stream3: inconsistent ring geometry");
         if (e == 1) addc = __builtin_bit_cast(float, a[7]);
+        if (e == 0) ring_of[0] = a[1];
+        if (e == 1) { ring_of[1] = a[0]; ring_of[2] = a[1]; }
+        if (e == 2) ring_of[3] = a[0];
       }
     }
     if (H.inner == -1) return fail(BFS_E_UNSUPPORTED, "stream3: every engine needs its instruction in I");
@@ -538,9 +553,14 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
     if (!ok || C.inner.n > kMaxInnerWaits)
       return fail(BFS_E_RESOURCE, "stream3: too many waits per engine (16) or per inner instruction (2)");
   }
-  if (n_gen < 1 || per_gen < 1 || n_gen * per_gen > 64) return fail(BFS_E_RESOURCE, "stream3: at most 64 ring slots");
-  if (p->ring_slots[0] < n_gen * per_gen || p->ring_slots[1] < n_gen * per_gen)
-    return fail(BFS_E_INVALID, "stream3: ring_slots smaller than the addressed slots");
+  if (n_gen < 1 || per_gen < 1 || n_gen * per_gen > 128) return fail(BFS_E_RESOURCE, "stream3: at most 128 ring slots");
+  int n_rings = 0;
+  for (int i = 0; i < 4; ++i) {
+    if (ring_of[i] < 0 || ring_of[i] > 1) return fail(BFS_E_UNSUPPORTED, "stream3: rings 0 and 1 only");
+    n_rings = std::max(n_rings, ring_of[i] + 1);
+    if (p->ring_slots[ring_of[i]] < n_gen * per_gen)
+      return fail(BFS_E_INVALID, "stream3: ring_slots smaller than the addressed slots");
+  }
   P.trips = trips;
   P.trip_off = trip_off;
   P.base = static_cast<const int64_t *>(bufs[0]);
@@ -557,7 +577,11 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
   P.per_gen = per_gen;
   P.n_slots = n_gen * per_gen;
   P.addc = addc;
-  const size_t lds_bytes = (size_t)kMaxSlots * kMaxWavesPerEngine * 4 + 2ull * P.n_slots * 64 * 4;
+  P.ring_ld = ring_of[0];
+  P.ring_add_src = ring_of[1];
+  P.ring_add_dst = ring_of[2];
+  P.ring_st = ring_of[3];
+  const size_t lds_bytes = (size_t)kMaxSlots * kMaxWavesPerEngine * 4 + (size_t)n_rings * P.n_slots * 64 * 4;
   const bool instr = dbg || o.dev_stats || o.fault_dep >= 0;
   hipStream_t s = (hipStream_t)stream;
   if (p->mode == BFS_MODE_BARRIER) {

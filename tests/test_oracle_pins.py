@@ -164,6 +164,32 @@ def test_hazard_coverage_of_workload_programs(mode):
     assert hazard.check(s.prog, res, mode) == []
 
 
+@pytest.mark.parametrize("layout", ["inplace", "two_rings"])
+def test_stream_layouts_race_free(layout):
+    """Both ring layouts of the stream program order every conflicting
+    access (CPU happens-before check over whole workgroups)."""
+    s = stream_workload(seed=4, n_wg=3, outer=12, with_data=False, layout=layout,
+                        n_gen=32 if layout == "inplace" else 8)
+    trips, off = s.trips.flat()
+    for wg in range(3):
+        res = core.run(s.prog, trips, off[wg], wg)
+        assert hazard.check(s.prog, res, "barrier_free") == []
+        assert hazard.check(s.prog, res, "barrier") == []
+
+
+def test_stream_inplace_needs_its_o_dependency_and_generations():
+    """Planted mistakes the race check must catch: the in-place layout without
+    MARK_O -> ACQ_O, and with too few generations for two O iterations."""
+    s = stream_workload(seed=4, n_wg=2, outer=12, with_data=False)
+    trips, off = s.trips.flat()
+    p = copy.deepcopy(s.prog)
+    p.deps = [d for d in p.deps if p.instrs[d[1]].name != "ACQ_O"]
+    assert hazard.check(p, core.run(p, trips, off[0], 0)) != []
+    from workloads import stream_program
+    few = stream_program(n_gen=16)      # M trips up to 16: o and o + 2 may now share slots with o + 1
+    assert hazard.check(few, core.run(few, trips, off[0], 0)) != []
+
+
 def test_hazard_catches_dropped_dependencies():
     w = chain_workload(seed=0)
     trips, off = w.trips.flat()

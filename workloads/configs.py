@@ -141,15 +141,30 @@ def chain_workload(seed: int = 0, outer: int = 16, inner_max: int = 8, n_wg: int
 # ---------------------------------------------------------------------------
 # cfg2: sync-bound 3-engine stream, 1024 workgroups
 # ---------------------------------------------------------------------------
-def stream_program(n_gen: int = 8, per_gen: int = 4, inner_war: bool = False) -> Program:
+STREAM_GENERATIONS = 32   # ring generations of the in-place layout (>= twice the largest M trip)
+
+
+def stream_program(n_gen: int = STREAM_GENERATIONS, per_gen: int = 4, inner_war: bool = False,
+                   layout: str = "inplace") -> Program:
     """Load / vector-add / store engines over a 3-level nest O{M{I{...}}}.
 
     Ring slot = ((r_M - 1) % n_gen) * per_gen + (rhat_I - 1): each M iteration
     owns one generation of per_gen slots.  With inner trips of at most per_gen
-    a slot is never reused inside one trip of I; ``inner_war`` adds the two
+    a slot is never reused inside one trip of I; ``inner_war`` adds the
     offset-per_gen dependencies that would order such reuse.
-    Markers at the end of each M / O iteration let the acquire instructions of
-    a later iteration wait for the previous users of a generation:
+
+    ``layout="inplace"`` (default): one ring; the add engine rewrites the slot
+    in place and the store engine reads it back:
+
+      O{ E0:ACQ_O  M{ I{ E0:LOAD X->r[slot]  E1:ADD r[slot]+1->r[slot]  E2:STORE r[slot]->Y } }  E2:MARK_O }
+
+    With M trips of at most n_gen / 2, the generations of two consecutive O
+    iterations are disjoint, so MARK_O -> ACQ_O at offset 2 (the store engine
+    has finished O iteration o - 2) orders every slot reuse and no M-level
+    instruction is needed: the load engine may run a whole O iteration ahead.
+
+    ``layout="two_rings"``: rings X (load -> add) and Y (add -> store) with
+    acquire / marker instructions at M (offset n_gen) and O (offset 1):
 
       O{ E0:ACQX_O E1:ACQY_O
          M{ E0:ACQX_M E1:ACQY_M
@@ -158,6 +173,27 @@ def stream_program(n_gen: int = 8, per_gen: int = 4, inner_war: bool = False) ->
          E1:MARKX_O E2:MARKY_O }
     """
     b = ProgramBuilder("stream3", n_engines=3)
+    if layout == "inplace":
+        with b.loop("O"):
+            b.instr(0, OP_NOP, name="ACQ_O")
+            with b.loop("M") as M:
+                with b.loop("I") as I:
+                    slot = dict(gen_loop=M, n_gen=n_gen, pos_loop=I, per_gen=per_gen)
+                    b.instr(0, OP_LOAD, tile_args(src=1, dst=0, idx_loop=I, **slot), name="LOAD")
+                    b.instr(1, OP_ADDC, tile_args(src=0, dst=0, const=1.0, **slot), name="ADD")
+                    b.instr(2, OP_STORE_RING, tile_args(src=0, dst=2, idx_loop=I, **slot), name="STORE")
+            b.instr(2, OP_NOP, name="MARK_O")
+        b.dep("LOAD", "ADD", 0)
+        b.dep("ADD", "STORE", 0)
+        if inner_war:
+            b.dep("STORE", "LOAD", per_gen)
+        b.dep("MARK_O", "ACQ_O", 2)
+        p = b.build()
+        p.tile_elems = 64
+        p.ring_slots = [n_gen * per_gen]
+        return p
+    if layout != "two_rings":
+        raise ValueError(layout)
     with b.loop("O"):
         b.instr(0, OP_NOP, name="ACQX_O")
         b.instr(1, OP_NOP, name="ACQY_O")
@@ -201,9 +237,11 @@ class StreamWorkload:
 
 
 def stream_workload(seed: int = 0, n_wg: int = 1024, outer: int = 256, mid_max: int = 16,
-                    inner_max: int = 4, n_gen: int = 8, with_data: bool = True,
-                    inner_war: bool = False) -> StreamWorkload:
-    prog = stream_program(n_gen=n_gen, per_gen=inner_max, inner_war=inner_war)
+                    inner_max: int = 4, n_gen: int = STREAM_GENERATIONS, with_data: bool = True,
+                    inner_war: bool = False, layout: str = "inplace") -> StreamWorkload:
+    if layout == "inplace" and n_gen < 2 * mid_max:
+        raise ValueError("the in-place layout needs at least twice the largest M trip in generations")
+    prog = stream_program(n_gen=n_gen, per_gen=inner_max, inner_war=inner_war, layout=layout)
     per = []
     for w in range(n_wg):
         rng = rng_for(CFG_STREAM, seed, w)
