@@ -142,9 +142,10 @@ def trace(args):
     lines += ["Template arguments: <mode, instrumented> (mode 0 = barrier-free, 1 = barrier); "
               "MoE: <phase, mode, instrumented>.", "",
               "| Kernel | Calls | Average ns | Min ns | Max ns |", "|---|---|---|---|---|"]
+    stems = ("stream3_kernel<", "gemm_kernel<", "attn_kernel<", "moe_kernel<")
     for r in rows:
         name = r["Name"]
-        if "_kernel<" not in name:
+        if not any(t in name for t in stems):
             continue
         short = name[name.index("::") + 2:] if "::" in name else name
         short = short.split("(")[0]
