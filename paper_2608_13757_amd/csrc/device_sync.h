@@ -209,15 +209,19 @@ __device__ __forceinline__ void region_sync(uint32_t own_words, int n_words) {
 // [4] threshold, [5] observed, [6] wave.
 __device__ __forceinline__ void report_deadlock(uint32_t *err, uint32_t dep, uint32_t wg, uint32_t inst,
                                                 uint32_t thr, uint32_t obs, uint32_t wave) {
-  if (lane_id() == 0 && err) {
-    if (atomicCAS(err, 0u, 1u) == 0u) {
-      err[1] = dep;
-      err[2] = wg;
-      err[3] = inst;
-      err[4] = thr;
-      err[5] = obs;
-      err[6] = wave;
-    }
+  // Branch-uniform on purpose: every lane tries the same compare-and-swap and
+  // a ballot tells the wave whether one of its lanes won, so no control flow
+  // here depends on the lane (a lane-dependent branch would make the callers'
+  // engine flags look divergent to the compiler).
+  if (err == nullptr) return;
+  const uint32_t old = atomicCAS(err, 0u, 1u);
+  if (__ballot(old == 0u) != 0ull) {
+    err[1] = dep;
+    err[2] = wg;
+    err[3] = inst;
+    err[4] = thr;
+    err[5] = obs;
+    err[6] = wave;
   }
 }
 

@@ -6,11 +6,10 @@
 //   E1 (2 waves, MFMA)     QK: S = Q K^T for 64 query rows per wave (Q held in
 //                          registers for the whole loop), written as fp32
 //                          into an S/P slot.
-//   E2 (2 waves, VALU)     SM: online softmax over 64 rows per wave, one row
-//                          per lane, in the base-2 domain: running max m,
-//                          rescale factor alpha = 2^(m_old - m_new),
-//                          P = 2^(S c - m_new) written as bf16 over S in
-//                          place, running sum l.
+//   E2 (4 waves, VALU)     SM: online softmax over 32 rows per wave in the
+//                          base-2 domain: running max m, rescale factor
+//                          alpha = 2^(m_old - m_new), P = 2^(S c - m_new)
+//                          written as bf16 over S in place, running sum l.
 //   E3 (2 waves, MFMA)     PV: O = alpha O + P V for 64 query rows per wave
 //                          (fp32 accumulators), then NORM: O / l to HBM.
 //   E4 (1 wave, V load)    LOADV: the V block into a V ring slot.
@@ -33,10 +32,6 @@
 // chunk c of row r at c ^ (r mod 16); P bf16 overwrites it with 8 chunks per
 // row at the same permutation) | alpha [2][128] fp32 | l [128] fp32.
 //
-// Eight waves per workgroup (two per SIMD, 256 registers each): the MFMA
-// waves hold a whole K block's fragments (QK) or double-buffer the P and V
-// fragments of the next 16 keys (PV), so LDS reads overlap the MFMAs.
-//
 // MFMA v_mfma_f32_32x32x16_bf16: lane l supplies row l % 32 of the first
 // operand and column l % 32 of the second, k = 8 (l / 32) .. + 7, and holds
 // column l % 32 of the result, rows 8 (i / 4) + 4 (l / 32) + i % 4 for
@@ -50,7 +45,7 @@
 // Family contract (BFS_KERNEL_ATTN): loop KV below the top level holding
 // LOADK (E0, opcode 32, args [0, K ring depth, heads, 128]), LOADV (E4,
 // opcode 32, args [1, V ring depth, heads, 128]), QK (E1, 33), SM (E2, 34),
-// PV (E3, 35); NORM (E3, 36) at the top level; waves per engine 1, 2, 2, 2,
+// PV (E3, 35); NORM (E3, 36) at the top level; waves per engine 1, 2, 4, 2,
 // 1; the dependencies listed above.  Buffers: [0] work list int32 [n_wg][4]
 // = (first token of the sequence, length L, first query row of the tile,
 // head), [1] Q, [2] K, [3] V, [4] O, each bf16 [tokens][heads][128].  Trip
@@ -64,7 +59,7 @@ using namespace bfsdev;
 namespace {
 
 constexpr int kD = 128, kBQ = 128, kBKV = 64;
-constexpr int kWaves = 8;
+constexpr int kWaves = 10;
 constexpr uint32_t kKVSlot = kBKV * kD * 2;      // 16 KiB
 constexpr uint32_t kSPSlot = kBQ * kBKV * 4;     // 32 KiB
 constexpr int kMaxPend = 3;                      // load groups in flight per load wave
@@ -94,8 +89,18 @@ __device__ __forceinline__ bf16x4 lds_tr(uint32_t addr) {
   return __builtin_bit_cast(bf16x4, v);
 }
 
+// Lanes l and l ^ 32 exchange x with v_permlane32_swap (no LDS traffic):
+// the two results hold {x[l], x[l + 32]} in the low half and
+// {x[l - 32], x[l]} in the high half, so any symmetric op of the pair
+// combines the two lanes' values.
+__device__ __forceinline__ f32x2 pair32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x), __builtin_bit_cast(uint32_t, x),
+                                                  false, false);
+  return f32x2{__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1])};
+}
+
 template <int kMode, bool kInstr>
-__global__ void __launch_bounds__(512) attn_kernel(AttnParams P) {
+__global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
   const uint32_t kring = lds_addr(lds) + kCntBytes;
@@ -109,15 +114,14 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnParams P) {
   const int hw = wave_id();
   const uint32_t lane = lane_id(), l32 = lane & 31u, lhi = lane >> 5;
   const int wg = blockIdx.x;
-  // hardware wave -> (engine, wave within the engine); waves go to SIMDs
-  // round-robin, so the four MFMA waves (0-3) sit on four SIMDs, the two
-  // softmax waves share SIMDs with the QK waves and the loaders with PV
+  // hardware wave -> (engine, wave within the engine); the four MFMA waves
+  // come first so that they sit on four different SIMDs
   int eng, ew, canon;                       // canon: engine-ordered wave index
   if (hw < 2) { eng = 1; ew = hw; canon = 1 + ew; }
-  else if (hw < 4) { eng = 3; ew = hw - 2; canon = 5 + ew; }
-  else if (hw < 6) { eng = 2; ew = hw - 4; canon = 3 + ew; }
-  else if (hw == 6) { eng = 0; ew = 0; canon = 0; }
-  else { eng = 4; ew = 0; canon = 7; }
+  else if (hw < 4) { eng = 3; ew = hw - 2; canon = 7 + ew; }
+  else if (hw < 8) { eng = 2; ew = hw - 4; canon = 3 + ew; }
+  else if (hw == 8) { eng = 0; ew = 0; canon = 0; }
+  else { eng = 4; ew = 0; canon = 9; }
   Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), canon, wg);
   const uint32_t own = S.word((uint32_t)eng, (uint32_t)ew);   // barrier mode: one counter per engine
 
@@ -216,20 +220,16 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnParams P) {
         for (int a = 0; a < 2; ++a)
 #pragma unroll
           for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
-        // every K fragment of the block is read before the first MFMA
-        bf16x8 kf[8][2];
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-          kf[s][0] = lds_frag(kb_base + pos16(l32, 2u * s + lhi));
-          kf[s][1] = lds_frag(kb_base + pos16(32u + l32, 2u * s + lhi));
-        }
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
+          const bf16x8 k0 = lds_frag(kb_base + pos16(l32, 2u * s + lhi));
+          const bf16x8 k1 = lds_frag(kb_base + pos16(32u + l32, 2u * s + lhi));
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb) {
-            acc[qb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s][0], qf[qb][s], acc[qb][0], 0, 0, 0);
-            acc[qb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s][1], qf[qb][s], acc[qb][1], 0, 0, 0);
+            acc[qb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[qb][s], acc[qb][0], 0, 0, 0);
+            acc[qb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[qb][s], acc[qb][1], 0, 0, 0);
           }
+        }
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
           const uint32_t row = qr + 32u * qb + l32;
@@ -247,7 +247,7 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnParams P) {
     }
   } else if (eng == 2) {
     // ------------------------------------------------------ softmax engine
-    const uint32_t row = 64u * ew + lane;
+    const uint32_t row = 32u * ew + l32;
     const float c = P.scale_log2;
     float m = -__builtin_inff(), lrun = 0.0f;
     S.sync_point(own);                                       // before loop KV
@@ -258,44 +258,50 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnParams P) {
       S.wait(site, P.sm, g, it + 1, g.r1 - 1, [] {});
       if (!S.aborted) {
         const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
-        float x[64];
+        float x[32];
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const f32x4 v = *(const BFS_LDS f32x4 *)(uintptr_t)(sp + pos16(row, (uint32_t)j));
+        for (int j = 0; j < 8; ++j) {
+          const f32x4 v = *(const BFS_LDS f32x4 *)(uintptr_t)(sp + pos16(row, 8u * lhi + j));
           x[4 * j] = v.x;
           x[4 * j + 1] = v.y;
           x[4 * j + 2] = v.z;
           x[4 * j + 3] = v.w;
         }
-        const int32_t key0 = (int32_t)it * kBKV;
-        if (key0 + kBKV > L) {
+        const int32_t key0 = (int32_t)it * kBKV + 32 * (int32_t)lhi;
+        if ((int32_t)(it + 1) * kBKV > L) {
 #pragma unroll
-          for (int t = 0; t < 64; ++t)
+          for (int t = 0; t < 32; ++t)
             if (key0 + t >= L) x[t] = -__builtin_inff();
         }
         float mx = x[0];
 #pragma unroll
-        for (int t = 1; t < 64; ++t) mx = __builtin_fmaxf(mx, x[t]);
+        for (int t = 1; t < 32; ++t) mx = __builtin_fmaxf(mx, x[t]);
+        const f32x2 mp = pair32(mx);
+        mx = __builtin_fmaxf(mp.x, mp.y);
         const float m_new = __builtin_fmaxf(m, mx * c);
         const float alpha = __builtin_amdgcn_exp2f(m - m_new);
         float sum = 0.0f;
-        uint32_t pk[32];
+        uint32_t pk[16];
 #pragma unroll
-        for (int t = 0; t < 64; t += 2) {
+        for (int t = 0; t < 32; t += 2) {
           const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(x[t], c, -m_new));
           const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(x[t + 1], c, -m_new));
           sum += p0 + p1;
           pk[t / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{p0, p1}, bf16x2));
         }
+        const f32x2 sums = pair32(sum);
+        sum = sums.x + sums.y;
         lrun = alpha * lrun + sum;
         m = m_new;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < 4; ++j) {
           const u32x4 v = {pk[4 * j], pk[4 * j + 1], pk[4 * j + 2], pk[4 * j + 3]};
-          *(BFS_LDS u32x4 *)(uintptr_t)(sp + pos16(row, (uint32_t)j)) = v;
+          *(BFS_LDS u32x4 *)(uintptr_t)(sp + pos16(row, 4u * lhi + j)) = v;
         }
-        *(BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + row) * 4u) = alpha;
-        *(BFS_LDS float *)(uintptr_t)(lsum_l + row * 4u) = lrun;
+        if (lhi == 0) {
+          *(BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + row) * 4u) = alpha;
+          *(BFS_LDS float *)(uintptr_t)(lsum_l + row * 4u) = lrun;
+        }
       }
       S.signal(P.sm.update, (uint32_t)ew);
       S.sync_point(own);                                     // end of a KV iteration
@@ -333,37 +339,19 @@ __global__ void __launch_bounds__(512) attn_kernel(AttnParams P) {
 #pragma unroll
           for (int db = 0; db < 4; ++db) acc[qb][db] *= a;
         }
-        // fragments of 16 keys are read one step ahead of the MFMAs
-        auto rd_p = [&](int ks, int qb) { return lds_frag(sp + pos16(qr + 32u * qb + l32, 2u * ks + lhi)); };
-        auto rd_v = [&](int ks, int db) {
-          const uint32_t va = vb + 16u * ks * 256u + voff[db];
-          const bf16x4 lo = lds_tr(va), hi = lds_tr(va + 4u * 256u);
-          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        };
-        bf16x8 pf[2], vf[4];
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) pf[qb] = rd_p(0, qb);
-#pragma unroll
-        for (int db = 0; db < 4; ++db) vf[db] = rd_v(0, db);
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-          bf16x8 pn[2], vn[4];
-          if (ks < 3) {
+          bf16x8 pf[2];
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb) pn[qb] = rd_p(ks + 1, qb);
+          for (int qb = 0; qb < 2; ++qb) pf[qb] = lds_frag(sp + pos16(qr + 32u * qb + l32, 2u * ks + lhi));
 #pragma unroll
-            for (int db = 0; db < 4; ++db) vn[db] = rd_v(ks + 1, db);
-          }
-#pragma unroll
-          for (int db = 0; db < 4; ++db)
+          for (int db = 0; db < 4; ++db) {
+            const uint32_t va = vb + 16u * ks * 256u + voff[db];
+            const bf16x4 lo = lds_tr(va), hi = lds_tr(va + 4u * 256u);
+            const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb)
-              acc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[db], pf[qb], acc[qb][db], 0, 0, 0);
-          if (ks < 3) {
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) pf[qb] = pn[qb];
-#pragma unroll
-            for (int db = 0; db < 4; ++db) vf[db] = vn[db];
+              acc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb], acc[qb][db], 0, 0, 0);
           }
         }
       }
@@ -410,10 +398,10 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
                        const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream, uint32_t *dbg,
                        int64_t dbg_cap, const bfs_run_opts &o) {
   if (p->n_loops != 2 || p->loop_parent[1] != 0) return fail(BFS_E_UNSUPPORTED, "attn: loops must be top -> KV");
-  const int want_w[5] = {1, 2, 2, 2, 1};
+  const int want_w[5] = {1, 2, 4, 2, 1};
   if (p->n_engines != 5) return fail(BFS_E_UNSUPPORTED, "attn: five engines");
   for (int e = 0; e < 5; ++e)
-    if (p->waves_per_engine[e] != want_w[e]) return fail(BFS_E_UNSUPPORTED, "attn: engines of 1, 2, 2, 2, 1 waves");
+    if (p->waves_per_engine[e] != want_w[e]) return fail(BFS_E_UNSUPPORTED, "attn: engines of 1, 2, 4, 2, 1 waves");
   int lk = -1, lv = -1, qk = -1, sm = -1, pv = -1, nm = -1;
   for (size_t i = 0; i < p->instr_engine.size(); ++i) {
     const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];
