@@ -207,7 +207,6 @@ void bfs_plan_destroy(bfs_plan *plan);
  *   dev_trips    int32 trip counts; dev_trip_off int64 [n_wg][n_loops]: the
  *                j-th execution of loop l in workgroup w runs
  *                dev_trips[dev_trip_off[w*n_loops + l] + j] iterations.
- *                (gemm / attn / moe derive trips on the device and accept NULL.)
  *   n_wg         workgroups.
  *   dev_debug_log  NULL, or a uint32 buffer of n_wg * W * (1 + 4 * debug_capacity)
  *                words (W = waves per workgroup): per (workgroup, wave) the
@@ -223,8 +222,11 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
                    struct ihipStream_t *stream, uint32_t *dev_debug_log, int64_t debug_capacity,
                    const bfs_run_opts *opts);
 
-/* Synchronizes stream, then reports (and clears) the plan's watchdog word:
- * BFS_E_DEADLOCK if any wait gave up since the last call. */
+/* Synchronizes stream, then reports (and clears) the plan's error word:
+ * BFS_E_DEADLOCK if any wait gave up since the last call, BFS_E_INVALID if a
+ * workgroup rejected a run-time input (a trip count beyond its work item, a
+ * trip table that disagrees with a loop the kernel runs statically, a load
+ * offset beyond 32 bits); the first error since the last call is reported. */
 bfs_status bfs_run_status(const bfs_plan *plan, struct ihipStream_t *stream);
 
 const char *bfs_status_string(bfs_status s);

@@ -205,24 +205,39 @@ __device__ __forceinline__ void region_sync(uint32_t own_words, int n_words) {
   __builtin_amdgcn_s_barrier();
 }
 
-// Watchdog word layout: [0] code (1 = deadlock), [1] dep, [2] wg, [3] instance,
-// [4] threshold, [5] observed, [6] wave.
+// Error word layout: [0] code, then six code-specific words.
+//   code 1 (a wait gave up): [1] dep, [2] wg, [3] instance, [4] threshold,
+//          [5] observed, [6] wave;
+//   code 2 (a run-time input was rejected): [1] what (1 trip count beyond
+//          the work item, 2 trip table disagrees with a static loop, 3 load
+//          offset beyond 32 bits), [2] wg, [3] index, [4] value, [5] limit,
+//          [6] wave.
+// Branch-uniform on purpose: every lane tries the same compare-and-swap and
+// a ballot tells the wave whether one of its lanes won, so no control flow
+// here depends on the lane (a lane-dependent branch would make the callers'
+// engine flags look divergent to the compiler).  The first error wins.
+__device__ __forceinline__ void report_error(uint32_t *err, uint32_t code, uint32_t w1, uint32_t w2, uint32_t w3,
+                                             uint32_t w4, uint32_t w5, uint32_t w6) {
+  if (err == nullptr) return;
+  const uint32_t old = atomicCAS(err, 0u, code);
+  if (__ballot(old == 0u) != 0ull) {
+    err[1] = w1;
+    err[2] = w2;
+    err[3] = w3;
+    err[4] = w4;
+    err[5] = w5;
+    err[6] = w6;
+  }
+}
+
 __device__ __forceinline__ void report_deadlock(uint32_t *err, uint32_t dep, uint32_t wg, uint32_t inst,
                                                 uint32_t thr, uint32_t obs, uint32_t wave) {
-  // Branch-uniform on purpose: every lane tries the same compare-and-swap and
-  // a ballot tells the wave whether one of its lanes won, so no control flow
-  // here depends on the lane (a lane-dependent branch would make the callers'
-  // engine flags look divergent to the compiler).
-  if (err == nullptr) return;
-  const uint32_t old = atomicCAS(err, 0u, 1u);
-  if (__ballot(old == 0u) != 0ull) {
-    err[1] = dep;
-    err[2] = wg;
-    err[3] = inst;
-    err[4] = thr;
-    err[5] = obs;
-    err[6] = wave;
-  }
+  report_error(err, 1u, dep, wg, inst, thr, obs, wave);
+}
+
+__device__ __forceinline__ void report_input(uint32_t *err, uint32_t what, uint32_t wg, uint32_t index,
+                                             uint32_t value, uint32_t limit, uint32_t wave) {
+  report_error(err, 2u, what, wg, index, value, limit, wave);
 }
 
 // Debug log entry (dependency, consumer instance, threshold, observed).

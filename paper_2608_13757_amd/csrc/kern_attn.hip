@@ -131,7 +131,7 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
   uint32_t trip = (uint32_t)ldc(P.trips + ldc(toff + 1));
   const uint32_t max_trip = L > 0 ? (uint32_t)((L + kBKV - 1) / kBKV) : 0u;
   if (trip > max_trip) {
-    report_deadlock(P.sc.err, 0xffffu, (uint32_t)wg, 0, trip, max_trip, (uint32_t)hw);
+    report_input(P.sc.err, 1u, (uint32_t)wg, 1u, trip, max_trip, (uint32_t)hw);
     trip = max_trip;
   }
   const size_t row_stride = (size_t)P.heads * kD;     // elements between tokens
@@ -164,6 +164,18 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
     // lane t covers row 4 j + t / 16 of instruction j and the 16-byte chunk
     // that belongs at position t % 16 of that row
     const uint32_t rr = lane >> 4, pos = lane & 15u;
+    // full blocks: a wave-uniform base (the block's first key) plus fixed
+    // 32-bit per-lane byte offsets, so the loads take the scalar-base address
+    // form and need no vector address arithmetic (which would compete for
+    // issue with the MFMA waves on this SIMD); the block holding the
+    // sequence's last key clamps rows one by one
+    uint32_t voff[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const uint32_t row = 4u * j + rr;
+      const uint32_t chunk = is_v ? (pos ^ (rr << 2)) : (pos ^ (row & 15u));
+      voff[j] = (row * (uint32_t)row_stride + 8u * chunk) * 2u;
+    }
     S.sync_point(own);                                       // before loop KV
     S.enter(site, iw, g, 1);
     uint32_t slot = 0;
@@ -174,13 +186,23 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
       if (!S.aborted) {
         const uint32_t dst = ring + slot * kKVSlot;
         const int32_t key0 = (int32_t)it * kBKV;
+        if (key0 + kBKV <= L) {
+          const char *sb = reinterpret_cast<const char *>(base + (size_t)(s0 + key0) * row_stride);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const uint32_t row = 4u * j + rr;
-          const uint32_t chunk = is_v ? (pos ^ (rr << 2)) : (pos ^ (row & 15u));
-          const int32_t key = min(key0 + (int32_t)row, L - 1);
-          const __bf16 *src = base + (size_t)(s0 + key) * row_stride + 8u * chunk;
-          __builtin_amdgcn_global_load_lds((const void *)src, (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+          for (int j = 0; j < 16; ++j) {
+            asm volatile("" : "+v"(voff[j]));   // keep the offset a 32-bit value at its use
+            __builtin_amdgcn_global_load_lds((const void *)(sb + voff[j]), (BFS_LDS void *)(uintptr_t)(dst + 1024u * j),
+                                             16, 0, 0);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const uint32_t row = 4u * j + rr;
+            const uint32_t chunk = is_v ? (pos ^ (rr << 2)) : (pos ^ (row & 15u));
+            const int32_t key = min(key0 + (int32_t)row, L - 1);
+            const __bf16 *src = base + (size_t)(s0 + key) * row_stride + 8u * chunk;
+            __builtin_amdgcn_global_load_lds((const void *)src, (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+          }
         }
         pending += 1;
         if (pending == kMaxPend) retire_one();

@@ -119,7 +119,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
   uint32_t trip_k = (uint32_t)ldc(P.trips + ldc(toff + 1));
   uint32_t trip_c = (uint32_t)ldc(P.trips + ldc(toff + 2));
   if (trip_k > (uint32_t)(P.k / kBK) || trip_c > 8u) {
-    report_deadlock(P.sc.err, 0xffffu, (uint32_t)wg, 0, trip_k, trip_c, (uint32_t)wave);
+    report_input(P.sc.err, 2u, (uint32_t)wg, 0u, trip_k, trip_c, (uint32_t)wave);
     trip_k = min(trip_k, (uint32_t)(P.k / kBK));
     trip_c = min(trip_c, 8u);
   }
@@ -157,8 +157,14 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     // (l % 4) ^ ((l / 16) % 4), so its 16 bytes land at the swizzled place.
     const uint32_t r_in = lane >> 2, chunk = (lane & 3u) ^ ((lane >> 4) & 3u);
     S.enter(s_load, P.load, g, 1);
-    const __bf16 *src = (wave == 0 ? P.a + (size_t)(m0 + r_in) * P.k : P.bt + (size_t)(n0 + r_in) * P.k) + 8 * chunk;
-    const size_t row16 = (size_t)16 * P.k;
+    // A wave-uniform base that advances one K step per iteration plus fixed
+    // 32-bit per-lane byte offsets (one per 16-row group): the loads take the
+    // scalar-base address form and need no vector address arithmetic, which
+    // would compete for issue with the MFMA waves sharing this SIMD.
+    const char *sbase = reinterpret_cast<const char *>(wave == 0 ? P.a + (size_t)m0 * P.k : P.bt + (size_t)n0 * P.k);
+    uint32_t voff[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) voff[j] = ((16u * j + r_in) * (uint32_t)P.k + 8u * chunk) * 2u;
     uint32_t slot = 0;
     for (uint32_t it = 0; it < trip_k; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
       g.r1 += 1;
@@ -166,10 +172,12 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
       if (!S.aborted) {
         unsigned char *dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kSlotBytes / 2);
-        const __bf16 *s0 = src + (size_t)it * kBK;
-#pragma unroll 4
-        for (int j = 0; j < 16; ++j)
-          __builtin_amdgcn_global_load_lds((const void *)(s0 + j * row16), (BFS_LDS void *)(dst + j * 1024), 16, 0, 0);
+        const char *sb = sbase + (size_t)it * (kBK * 2);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          asm volatile("" : "+v"(voff[j]));   // keep the offset a 32-bit value at its use
+          __builtin_amdgcn_global_load_lds((const void *)(sb + voff[j]), (BFS_LDS void *)(dst + j * 1024), 16, 0, 0);
+        }
         pending += 1;
         if (pending == 3) retire_one();
       } else {
@@ -344,6 +352,7 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
   const int e_ring = p->instr_args[8 * ins_spill];
   if (M <= 0 || N <= 0 || K <= 0 || M % kTile || N % kTile || K % kBK)
     return fail(BFS_E_UNSUPPORTED, "gemm: M and N must be multiples of 256, K a multiple of 32");
+  if ((uint64_t)kTile * K * 2 > 0xffffffffull) return fail(BFS_E_UNSUPPORTED, "gemm: K too large for 32-bit load offsets");
   if (ring < 2 || ring > 4 || e_ring < 1 || e_ring > 2)
     return fail(BFS_E_UNSUPPORTED, "gemm: ring of 2..4 slots, epilogue ring of 1..2 slots");
   // the epilogue ring lives in the K ring's memory: the program must order

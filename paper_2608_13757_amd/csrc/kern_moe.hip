@@ -100,7 +100,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
   const uint32_t ksteps = (uint32_t)(P.kdim / kBK), chunks = kPhase == 1 ? 2u : 4u;
   const uint32_t max_m = (uint32_t)max(0, (e_cnt + kBM - 1) / kBM - mt0);
   if (trip_m > max_m) {
-    report_deadlock(P.sc.err, 0xffffu, (uint32_t)wg, 0, trip_m, max_m, (uint32_t)wave);
+    report_input(P.sc.err, 1u, (uint32_t)wg, 1u, trip_m, max_m, (uint32_t)wave);
     trip_m = max_m;
   }
   Regs g;
@@ -146,26 +146,35 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
       if (wave == 0) {
         const int32_t tk = ldc(P.trips + k_off + mi), tc = ldc(P.trips + c_off + mi);
         if (tk != (int32_t)ksteps || tc != (int32_t)chunks)
-          report_deadlock(P.sc.err, 0xffffu, (uint32_t)wg, mi, (uint32_t)tk, (uint32_t)tc, (uint32_t)wave);
+          report_input(P.sc.err, 2u, (uint32_t)wg, mi, (uint32_t)tk, (uint32_t)tc, (uint32_t)wave);
       }
       const int32_t m0 = (mt0 + (int32_t)mi) * kBM;
-      // source rows of this M-tile
-      const __bf16 *src[16];
+      // source rows of this M-tile as 32-bit per-lane byte offsets from a
+      // wave-uniform base that advances one K step per iteration: the loads
+      // take the scalar-base address form and need no vector address
+      // arithmetic (which would compete for issue with the MFMA waves)
+      uint32_t voff[16];
       if (wave == 0) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int32_t r = min(m0 + 16 * j + (int32_t)r_in, e_cnt - 1);
           const int32_t row = kPhase == 1 ? P.perm[e_lo + r] : e_lo + r;
-          src[j] = P.a + (size_t)row * P.kdim + 8u * chunk;
+          const uint64_t off = ((uint64_t)(uint32_t)row * (uint32_t)P.kdim + 8u * chunk) * 2u;
+          if (__ballot((off >> 32) != 0) != 0ull) {
+            report_input(P.sc.err, 3u, (uint32_t)wg, mi, (uint32_t)row, 0u, (uint32_t)wave);
+            S.aborted = 1u;
+          }
+          voff[j] = (uint32_t)off;
         }
+#pragma unroll
+        for (int j = 8; j < 16; ++j) voff[j] = 0u;
         wait_vm<0>();
       } else {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const uint32_t r = 16u * j + r_in;
-          const __bf16 *w = (kPhase == 1 && r >= 128u) ? P.w1 : P.w0;
           const uint32_t n = kPhase == 1 ? (n0 + (r & 127u)) : (n0 + r);
-          src[j] = w + ((size_t)expert * P.ndim + n) * P.kdim + 8u * chunk;
+          voff[j] = (n * (uint32_t)P.kdim + 8u * chunk) * 2u;      // within the expert's matrix
         }
       }
       S.sync_point(S.word(0, ew));                                // before loop K
@@ -177,15 +186,26 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
         S.wait(sb, P.load, g, it + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
         if (!S.aborted) {
           const uint32_t dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kASlot);
-          const uint32_t koff = it * kBK;
+          const size_t kb = (size_t)it * (kBK * 2);
           if (wave == 0) {
+            const char *sb = reinterpret_cast<const char *>(P.a) + kb;
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-              __builtin_amdgcn_global_load_lds((const void *)(src[j] + koff), (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+            for (int j = 0; j < 8; ++j) {
+              asm volatile("" : "+v"(voff[j]));   // keep the offset a 32-bit value at its use
+              __builtin_amdgcn_global_load_lds((const void *)(sb + voff[j]), (BFS_LDS void *)(uintptr_t)(dst + 1024u * j),
+                                               16, 0, 0);
+            }
           } else {
+            // phase 1: weight rows 0..127 are W_gate's, 128..255 W_up's
+            const size_t eb = (size_t)expert * P.ndim * P.kdim * 2 + kb;
+            const char *sb0 = reinterpret_cast<const char *>(P.w0) + eb;
+            const char *sb1 = kPhase == 1 ? reinterpret_cast<const char *>(P.w1) + eb : sb0;
 #pragma unroll
-            for (int j = 0; j < 16; ++j)
-              __builtin_amdgcn_global_load_lds((const void *)(src[j] + koff), (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+            for (int j = 0; j < 16; ++j) {
+              asm volatile("" : "+v"(voff[j]));
+              __builtin_amdgcn_global_load_lds((const void *)((j < 8 ? sb0 : sb1) + voff[j]),
+                                               (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+            }
           }
           pending += 1;
           if (pending == 3) retire_one();
@@ -376,6 +396,7 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   if (K <= 0 || K % kBK || N <= 0 || N % (phase == 1 ? 128 : 256))
     return fail(BFS_E_UNSUPPORTED, "moe: K a multiple of 32, N a multiple of 128 (phase 1) or 256 (phase 2)");
   if (ring < 2 || ring > 4 || e_ring < 1 || e_ring > 2) return fail(BFS_E_UNSUPPORTED, "moe: ring 2..4, epilogue 1..2");
+  if ((uint64_t)N * K * 2 > 0xffffffffull) return fail(BFS_E_UNSUPPORTED, "moe: one expert's matrix must stay below 4 GiB");
   if (!has_dep(p, load, mma, 0) || !has_dep(p, mma, load, ring) || !has_dep(p, mma, acql, 1) ||
       !has_dep(p, spill, epi, 0) || !has_dep(p, epi, spill, e_ring) || !has_dep(p, epi, acqe, 1))
     return fail(BFS_E_UNSUPPORTED, "moe: missing a ring or M-tile dependency");

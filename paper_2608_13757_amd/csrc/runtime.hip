@@ -185,6 +185,14 @@ bfs_status bfs_run_status(const bfs_plan *plan, struct ihipStream_t *stream) {
   if (w[0] != 0) {
     uint32_t z[8] = {0};
     (void)hipMemcpy(img->err, z, sizeof z, hipMemcpyHostToDevice);
+    if (w[0] == 2) {
+      static const char *what[4] = {"?", "trip count beyond the work item", "trip table disagrees with a static loop",
+                                    "load offset beyond 32 bits"};
+      return fail(BFS_E_INVALID, std::string("run-time input rejected in workgroup ") + std::to_string(w[2]) +
+                                     " (wave " + std::to_string(w[6]) + "): " + what[w[1] < 4 ? w[1] : 0] +
+                                     " (index " + std::to_string(w[3]) + ", value " + std::to_string(w[4]) +
+                                     ", limit " + std::to_string(w[5]) + ")");
+    }
     return fail(BFS_E_DEADLOCK, "wait of dependency " + std::to_string(w[1]) + " in workgroup " +
                                     std::to_string(w[2]) + " (wave " + std::to_string(w[6]) + ", instance " +
                                     std::to_string(w[3]) + ") saw " + std::to_string(w[5]) + " < threshold " +

@@ -155,3 +155,23 @@ def test_attn_watchdog():
     assert e.value.status == bfs.E_DEADLOCK
     plan.run([work, q, k, v, o], trips, toff, wl.trips.n_wg)
     plan.status()
+
+
+def test_attn_rejects_trip_beyond_sequence():
+    """A KV trip count longer than the sequence's blocks is clamped on the
+    device and reported by bfs_run_status as an invalid input."""
+    heads = 1
+    ai = attn_inputs(seed=3, heads=heads, lengths=[100])
+    prog = attn_program(heads)
+    plan = Plan(prog)
+    wl = attn_worklist(ai.lengths, heads)
+    wl.trips.per_wg[0][1][0] += 1            # one KV block too many
+    trips, toff = trip_tensors(wl.trips)
+    work = torch.from_numpy(wl.work.reshape(-1)).cuda()
+    q, k, v = _dev16(ai.q), _dev16(ai.k), _dev16(ai.v)
+    o = torch.zeros(ai.q.shape, dtype=torch.int16, device="cuda")
+    _say("[attn-bad-trip]")
+    plan.run([work, q, k, v, o], trips, toff, wl.trips.n_wg)
+    with pytest.raises(BfsError) as e:
+        plan.status()
+    assert e.value.status == bfs.E_INVALID
