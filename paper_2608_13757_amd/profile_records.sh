@@ -1,0 +1,28 @@
+#!/bin/bash
+# Writes profiles/<kernel>_traffic.json and profiles/<kernel>_kernel_trace.md
+# from the rocprofv3 output of these runs under one output root R (repository
+# root, TMPDIR=/tmp):
+#   rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 20 --warmup 3 --no-cpu-baseline
+#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/pf_$wl -o f -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024
+#   rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/pw_$wl -o w -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024
+# for wl in stream gemm attn moe.  Algorithmic bytes per step: stream 512 B per
+# innermost iteration (5568928 for seed 0); GEMM A + B + C + bias; attention
+# Q + K + V + O; MoE all weights + x + h written and read + y.
+set -e
+R=${1:?usage: profile_records.sh <rocprofv3 output root>}
+for wl in ${WLS:-stream gemm attn moe}; do
+  case $wl in
+    stream) k=stream3; ab=2851291136; wk="sync-bound stream, 1024 workgroups, seed 0, 5568928 innermost iterations, one in-place ring";;
+    gemm) k=gemm; ab=100679680; wk="GEMM + bias + GELU 4096^3 bf16, seed 0";;
+    attn) k=attn; ab=1336737792; wk="varlen attention forward, 32 sequences U[128,4096] (81588 tokens), 16 heads x 128, seed 0";;
+    moe) k=moe; ab=2936012800; wk="MoE grouped GEMM, 32768 tokens, 64 Zipf(1.1) experts, hidden 4096, ffn 1408, seed 0 (both launches)";;
+  esac
+  python -m paper_2608_13757_amd.profiles traffic --kernel $k --fetch-dir $R/pf_$wl --write-dir $R/pw_$wl --copy-mib 1024 \
+    --algorithmic-bytes $ab --workload "$wk" \
+    --command "rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/pf_$wl -o f -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024" \
+    --command "rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/pw_$wl -o w -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024" \
+    --command "WLS=$wl bash paper_2608_13757_amd/profile_records.sh $R"
+  python -m paper_2608_13757_amd.profiles trace --kernel $k --stats-dir $R/pt_$wl --workload "$wk" \
+    --command "rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 20 --warmup 3 --no-cpu-baseline" \
+    --command "WLS=$wl bash paper_2608_13757_amd/profile_records.sh $R"
+done

@@ -13,9 +13,9 @@ Turns rocprofv3 output into the short records kept under ``profiles/``:
 Usage (from the repository root, after the rocprofv3 runs)::
 
     python -m paper_2608_13757_amd.profiles traffic --kernel gemm \\
-        --fetch-dir gpurun_out/pf --write-dir gpurun_out/pw --copy-mib 1024 \\
+        --fetch-dir OUT/pf --write-dir OUT/pw --copy-mib 1024 \\
         --algorithmic-bytes 100679680 --workload "..." --command "..." --command "..."
-    python -m paper_2608_13757_amd.profiles trace --kernel gemm --stats-dir gpurun_out/pt \\
+    python -m paper_2608_13757_amd.profiles trace --kernel gemm --stats-dir OUT/pt \\
         --workload "..." --command "..."
 """
 import argparse
