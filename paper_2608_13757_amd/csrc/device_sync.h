@@ -174,17 +174,19 @@ __device__ __forceinline__ WaitResult wait_geq(uint32_t addr, int nw, uint32_t t
 // loop body is a handful of scalar instructions, so a blocked wave takes few
 // issue slots from the working waves of its compute unit.  Returns the last
 // value seen; ok = false when max_polls polls did not suffice.
+// Poll one counter word until it reaches thr.  max_polls is clamped to 32
+// bits so the poll count stays a scalar 32-bit value (a 64-bit count is
+// compared with vector instructions).
 __device__ __forceinline__ WaitResult spin_geq(uint32_t addr, uint32_t thr, uint64_t max_polls) {
-  uint64_t polls = 0;
+  const uint32_t limit = max_polls > 0xffffffffull ? 0xffffffffu : (uint32_t)max_polls;
+  uint32_t polls = 0;
   while (true) {
     const uint32_t v = uniform(lds_poll(addr));
     if (v >= thr) return WaitResult{v, true};
-    if (++polls > max_polls) return WaitResult{v, false};
-    // back off: 64, 128, 256 then 512 clocks between polls
-    if (polls < 4) __builtin_amdgcn_s_sleep(1);
-    else if (polls < 16) __builtin_amdgcn_s_sleep(2);
-    else if (polls < 64) __builtin_amdgcn_s_sleep(4);
-    else __builtin_amdgcn_s_sleep(8);
+    if (++polls > limit) return WaitResult{v, false};
+    // back off: 64 clocks between the first polls, then 256
+    if (polls < 8) __builtin_amdgcn_s_sleep(1);
+    else __builtin_amdgcn_s_sleep(4);
   }
 }
 

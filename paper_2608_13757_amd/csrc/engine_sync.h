@@ -159,12 +159,13 @@ struct Sync {
     if ((__ballot(v >= thr) & want) == want) return min16(v);
     on_block();
     const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
-    uint64_t polls = 0;
+    const uint32_t limit = C.watchdog > 0xffffffffull ? 0xffffffffu : (uint32_t)C.watchdog;
+    uint32_t polls = 0;
     while (true) {
       v = lds_poll(a);
       if ((__ballot(v >= thr) & want) == want) break;
       on_block();
-      if (++polls > C.watchdog) {
+      if (++polls > limit) {
         const uint32_t m = min16(v);
         report_deadlock(C.err, dep, (uint32_t)wg, instance, thr, m, (uint32_t)wave);
         aborted = 1u;

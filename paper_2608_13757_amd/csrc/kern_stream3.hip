@@ -102,10 +102,23 @@ struct Engine {
   int pending = 0;                        // issued, not yet retired (loads or LDS ops)
   uint32_t own_counter = 0;               // LDS address of the inner instruction's counter
   uint32_t has_own_counter = 0;
+  // Retirement add with every lane active: lane 0 adds to the counter, the
+  // other lanes add 0 to this wave's private scratch words, so no exec-mask
+  // save / restore is needed around the add.
+  uint32_t own_vaddr = 0, one_v = 0, scratch_v = 0;
   WaveStats st;
 
   __device__ Engine(const Stream3Params &p, const EngineCode &c, uint32_t cb, int w, int g)
       : P(p), C(c), cnt_base(cb), wave(w), wg(g) {}
+
+  __device__ __forceinline__ void add_own(uint32_t n) {
+    const uint32_t v = n == 1u ? one_v : (lane_id() == 0 ? n : 0u);
+    asm volatile("ds_add_u32 %0, %1" ::"v"(own_vaddr), "v"(v) : "memory");
+  }
+  __device__ __forceinline__ void add_one(uint32_t addr) {
+    const uint32_t a = lane_id() == 0 ? addr : scratch_v;
+    asm volatile("ds_add_u32 %0, %1" ::"v"(a), "v"(one_v) : "memory");
+  }
 
   __device__ __forceinline__ uint32_t counter_addr(uint32_t slot) const {
     return cnt_base + 4u * slot * (uint32_t)bfs::kMaxWavesPerEngine;
@@ -131,7 +144,7 @@ struct Engine {
     const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
     wait_vm<kInflight - 1>();
     if (kInstr && st.on) st.own_loads += now_ticks() - t0;
-    if (has_own_counter) lds_add(own_counter, 1u);
+    if (has_own_counter) add_own(1u);
     pending = (int)uniform((uint32_t)pending - 1u);
   }
   // Retire everything held.
@@ -144,7 +157,7 @@ struct Engine {
       } else {
         drain_lds();
       }
-      if (has_own_counter) lds_add(own_counter, (uint32_t)pending);
+      if (has_own_counter) add_own((uint32_t)pending);
       pending = 0;
     }
   }
@@ -153,7 +166,7 @@ struct Engine {
   __device__ __forceinline__ void retire_some() {
     if (kRole == ROLE_LOAD) {
       wait_vm_dyn(pending - 1);
-      if (has_own_counter) lds_add(own_counter, 1u);
+      if (has_own_counter) add_own(1u);
       pending -= 1;
     } else {
       retire_all();
@@ -210,7 +223,7 @@ struct Engine {
     if (s.update >= 0) {
       retire_all();
       drain_lds();
-      lds_add(counter_addr((uint32_t)s.update), 1u);
+      add_one(counter_addr((uint32_t)s.update));
     }
   }
 
@@ -302,6 +315,12 @@ __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_
     E.own_counter = E.counter_addr((uint32_t)C.inner.update);
     E.has_own_counter = 1u;
   }
+  {
+    const uint32_t scratch = cnt_base + (uint32_t)bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4u + 256u * (uint32_t)wave;
+    E.scratch_v = scratch + 4u * lane;
+    E.own_vaddr = lane == 0 ? E.own_counter : E.scratch_v;
+    E.one_v = lane == 0 ? 1u : 0u;
+  }
   const int64_t *toff = P.trip_off + (int64_t)wg * 4;
   const int64_t tbase = ldc(P.base + wg);
   // per-lane addresses of the rings and of this workgroup's tiles
@@ -375,7 +394,7 @@ __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_
             asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
                          : "=v"(v) : "v"(xl + 256u * (slot + lo)) : "memory");
             // the read returned, so every earlier LDS write of this wave is done
-            if (E.pending > 0) lds_add(E.own_counter, 1u);
+            if (E.pending > 0) E.add_own(1u);
             v = v + addc;
             asm volatile("ds_write_b32 %0, %1" ::"v"(yl + 256u * (slot + lo)), "v"(v) : "memory");
             E.pending = (int)E.has_own_counter;
@@ -385,11 +404,11 @@ __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_
                          : "=v"(v) : "v"(yl + 256u * (slot + lo)) : "memory");
             __builtin_nontemporal_store(v, yg + (int64_t)instance * 64);
             // the slot has been read: the store retires now
-            if (E.has_own_counter) lds_add(E.own_counter, 1u);
+            if (E.has_own_counter) E.add_own(1u);
           }
         } else {
           E.retire_all();
-          if (E.has_own_counter) lds_add(E.own_counter, 1u);
+          if (E.has_own_counter) E.add_own(1u);
         }
         lo = (lo + 1 == per_gen) ? 0u : lo + 1;
         if (kMode == BFS_MODE_BARRIER) {
@@ -427,7 +446,8 @@ template <int kMode, bool kInstr, int kInflight>
 __global__ void __launch_bounds__(192) stream3_kernel(Stream3Params P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
-  float *rings = reinterpret_cast<float *>(lds + bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4);
+  // counters | 3 x 256 B of per-wave scratch words for the retirement adds | rings
+  float *rings = reinterpret_cast<float *>(lds + bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4 + 768);
   const int ring_floats = P.n_slots * 64;
   for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
   __syncthreads();
@@ -581,7 +601,7 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
   P.ring_add_src = ring_of[1];
   P.ring_add_dst = ring_of[2];
   P.ring_st = ring_of[3];
-  const size_t lds_bytes = (size_t)kMaxSlots * kMaxWavesPerEngine * 4 + (size_t)n_rings * P.n_slots * 64 * 4;
+  const size_t lds_bytes = (size_t)kMaxSlots * kMaxWavesPerEngine * 4 + 768 + (size_t)n_rings * P.n_slots * 64 * 4;
   const bool instr = dbg || o.dev_stats || o.fault_dep >= 0;
   hipStream_t s = (hipStream_t)stream;
   if (p->mode == BFS_MODE_BARRIER) {
