@@ -16,9 +16,9 @@
 // Retirement is in issue order:
 //   * the load engine keeps up to kInflight direct-to-LDS loads outstanding
 //     and retires the oldest with a counted vmcnt wait;
-//   * the add and store engines retire tile n once a later LDS read has
-//     returned (LDS operations of one wave complete in order), i.e. one
-//     round trip per tile instead of two;
+//   * the add engine signals right after its ring write and the store
+//     engine right after its ring read returned: LDS executes the operations
+//     of one wave in issue order, so the counter add lands after the write;
 //   * markers retire at once, after everything before them.
 // Before blocking on a wait that is not met, an engine retires what it holds
 // (the load engine one load at a time), so a consumer never waits on a
@@ -81,6 +81,18 @@ struct Stream3Params {
   float addc;
 };
 
+// The launch arguments are read in place from the kernel-argument segment
+// (scalar loads, also at run-time indices) through references of this type.
+// (The host pass of the compiler, which only parses device code, sees plain
+// const references.)
+#if defined(__HIP_DEVICE_COMPILE__)
+template <typename T>
+using kconst = const __attribute__((address_space(4))) T;
+#else
+template <typename T>
+using kconst = const T;
+#endif
+
 __device__ __forceinline__ uint32_t sel4(uint32_t a, uint32_t b, uint32_t c, uint32_t d, uint32_t i) {
   return i == 0 ? a : i == 1 ? b : i == 2 ? c : d;
 }
@@ -90,8 +102,8 @@ enum { ROLE_LOAD = 0, ROLE_ADD = 1, ROLE_STORE = 2 };
 // One engine wave: loop registers, counters, waits and retirement.
 template <int kRole, int kMode, bool kInstr, int kInflight>
 struct Engine {
-  const Stream3Params &P;
-  const EngineCode &C;
+  kconst<Stream3Params> &P;
+  kconst<EngineCode> &C;
   uint32_t r1 = 0, r2 = 0, r3 = 0;        // r of O, M, I (r of the top level is 1)
   uint32_t h1 = 0, h2 = 0, h3 = 0;        // rhat of O, M, I
   uint32_t cnt_base;
@@ -99,16 +111,15 @@ struct Engine {
   uint32_t aborted = 0;                   // a wait gave up: finish without waiting
   uint32_t *log = nullptr;
   uint32_t nlog = 0;
-  int pending = 0;                        // issued, not yet retired (loads or LDS ops)
-  uint32_t own_counter = 0;               // LDS address of the inner instruction's counter
-  uint32_t has_own_counter = 0;
-  // Retirement add with every lane active: lane 0 adds to the counter, the
-  // other lanes add 0 to this wave's private scratch words, so no exec-mask
-  // save / restore is needed around the add.
+  int pending = 0;                        // load engine: loads issued, not yet retired
+  // Retirement add with every lane active: lane 0 adds to the inner
+  // instruction's counter (or to its own scratch word when the instruction
+  // has no consumer), the other lanes add 0 to this wave's private scratch
+  // words, so no exec-mask save / restore or branch is needed around the add.
   uint32_t own_vaddr = 0, one_v = 0, scratch_v = 0;
   WaveStats st;
 
-  __device__ Engine(const Stream3Params &p, const EngineCode &c, uint32_t cb, int w, int g)
+  __device__ Engine(kconst<Stream3Params> &p, kconst<EngineCode> &c, uint32_t cb, int w, int g)
       : P(p), C(c), cnt_base(cb), wave(w), wg(g) {}
 
   __device__ __forceinline__ void add_own(uint32_t n) {
@@ -144,7 +155,7 @@ struct Engine {
     const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
     wait_vm<kInflight - 1>();
     if (kInstr && st.on) st.own_loads += now_ticks() - t0;
-    if (has_own_counter) add_own(1u);
+    add_own(1u);
     pending = (int)uniform((uint32_t)pending - 1u);
   }
   // Retire everything held.
@@ -157,7 +168,7 @@ struct Engine {
       } else {
         drain_lds();
       }
-      if (has_own_counter) add_own((uint32_t)pending);
+      add_own((uint32_t)pending);
       pending = 0;
     }
   }
@@ -166,14 +177,14 @@ struct Engine {
   __device__ __forceinline__ void retire_some() {
     if (kRole == ROLE_LOAD) {
       wait_vm_dyn(pending - 1);
-      if (has_own_counter) add_own(1u);
+      add_own(1u);
       pending -= 1;
     } else {
       retire_all();
     }
   }
 
-  __device__ WaitResult block(uint32_t addr, uint32_t thr, uint32_t dep, uint32_t instance) {
+  __device__ __forceinline__ WaitResult block(uint32_t addr, uint32_t thr, uint32_t dep, uint32_t instance) {
     const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
     if (kInstr && st.on) st.n_blocked += 1;
     while (pending > 0) {
@@ -215,7 +226,7 @@ struct Engine {
   }
 
   // A marker / acquire instruction: its waits, then retirement in order.
-  __device__ void nop(const InstrSync &s, uint32_t instance) {
+  __device__ __forceinline__ void nop(kconst<InstrSync> &s, uint32_t instance) {
     for (int j = 0; j < s.n; ++j) {
       const bfs::PackedWait w = C.waits[s.first + j];
       wait_one(w, threshold(w), 0u, instance);
@@ -227,7 +238,7 @@ struct Engine {
     }
   }
 
-  __device__ __forceinline__ void nops(const InstrSync *list, int n, uint32_t instance) {
+  __device__ __forceinline__ void nops(kconst<InstrSync> *list, int n, uint32_t instance) {
     for (int i = 0; i < n; ++i) nop(list[i], instance);
   }
 
@@ -246,27 +257,44 @@ struct Engine {
 //     thr(i) = [rhat_I > kk] * max(run(i), 0),   run(i) = N * r_P - c,
 // where run grows by N per iteration when P is loop I and is constant
 // otherwise, and kk is k when the mask reads rhat_I, 0 when no mask applies,
-// and "never" when a mask on an outer loop is 0 for this trip.  Everything
-// except run and the comparison is computed once at the loop statement
-// (loop-invariant code motion of the wait value, Section 6.2); the values
-// are exactly those of Eq. 5.
+// and "never" when a mask on an outer loop is 0 for this trip.  The fields of
+// the packed wait are decoded once per run, run and kk once per trip of I
+// (loop-invariant code motion of the wait value, Section 6.2); the values are
+// exactly those of Eq. 5.
 struct InnerWait {
-  uint32_t packed_w0, packed_w1, packed_w2, packed_w3;
-  uint32_t run;        // N * r_P - c for the current iteration (as int)
-  uint32_t step;       // N when P is loop I, else 0
-  uint32_t kk;         // threshold is 0 while rhat_I <= kk
-  uint32_t seen;       // last observed counter value
+  uint32_t addr;       // LDS address of the producer's counter word
+  uint32_t dep;        // dependency id (debug log, error word)
+  uint32_t bar_thr;    // barrier mode: the static ordinal, 0 when nothing is owed
+  uint32_t N, c;       // run = N * r_P - c
+  uint32_t lp;         // loop level of P: 0 top, 1 O, 2 M, 3 I
+  uint32_t k;          // the mask is rhat_S > k
+  uint32_t kk_lvl;     // 1 / 2: the mask reads rhat of O / M and kk is set per trip; 0: kk is fixed
+  int32_t step;        // N when P is loop I, else 0
+  int32_t run;         // N * r_P - c for the current iteration
+  uint32_t kk;         // the threshold is 0 while rhat_I <= kk
+  int32_t seen;        // last observed counter value
 };
 
-__device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait &w) {
+// Counter values stay below 2^31; an engine that gave up on a wait marks
+// every inner wait as satisfied with this value and finishes without waiting.
+constexpr int32_t kSeenAll = 0x7fffffff;
+
+__device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait w, uint32_t cnt_base) {
   InnerWait iw;
-  iw.packed_w0 = w.w0;
-  iw.packed_w1 = w.w1;
-  iw.packed_w2 = w.w2;
-  iw.packed_w3 = w.w3;
+  const uint32_t N = w.w1 & 0xffffu, K = w.w1 >> 16, k = w.w2 & 0xffffu, sub = w.w2 >> 16;
+  const uint32_t ls = (w.w0 >> 16) & 0xffu, mask = (w.w0 >> 24) & 1u;
+  iw.addr = cnt_base + 4u * (w.w0 & 0xffu) * (uint32_t)bfs::kMaxWavesPerEngine;
+  iw.dep = w.w3 & 0xffffu;
+  iw.bar_thr = ((w.w0 >> 25) & 1u) ? (w.w3 >> 16) : 0u;
+  iw.N = N;
+  iw.c = N * sub + (N - K);
+  iw.lp = (w.w0 >> 8) & 0xffu;
+  iw.k = k;
+  iw.step = iw.lp == 3u ? (int32_t)N : 0;
+  iw.kk_lvl = (mask && (ls == 1u || ls == 2u)) ? ls : 0u;
+  // fixed kk: no mask, a mask on rhat_I, or a mask on the top level (rhat 1)
+  iw.kk = !mask ? 0u : ls == 3u ? k : (1u > k ? 0u : 0xffffffffu);
   iw.run = 0;
-  iw.step = 0;
-  iw.kk = 0;
   iw.seen = 0;
   return iw;
 }
@@ -275,29 +303,24 @@ __device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait &w) {
 // rhat_O, rhat_M are the engine's registers; r_I has not been incremented yet.
 __device__ __forceinline__ void enter_inner(InnerWait &iw, uint32_t r1, uint32_t r2, uint32_t r3, uint32_t h1,
                                             uint32_t h2) {
-  const uint32_t N = iw.packed_w1 & 0xffffu, K = iw.packed_w1 >> 16;
-  const uint32_t k = iw.packed_w2 & 0xffffu, sub = iw.packed_w2 >> 16;
-  const uint32_t lp = (iw.packed_w0 >> 8) & 0xffu, ls = (iw.packed_w0 >> 16) & 0xffu;
-  const uint32_t mask = (iw.packed_w0 >> 24) & 1u;
-  const uint32_t c = N * sub + (N - K);
-  // run before the first iteration; the loop adds step before each evaluation
-  const uint32_t rP = lp == 3u ? r3 : sel4(1u, r1, r2, r3, lp);
-  iw.step = lp == 3u ? N : 0u;
-  iw.run = uniform(N * rP - c);
-  uint32_t kk = 0;
-  if (mask) {
-    if (ls == 3u) kk = k;
-    else kk = (sel4(1u, h1, h2, 0u, ls) > k) ? 0u : 0xffffffffu;
-  }
-  iw.kk = uniform(kk);
+  const uint32_t rP = iw.lp == 3u ? r3 : iw.lp == 2u ? r2 : iw.lp == 1u ? r1 : 1u;
+  iw.run = (int32_t)(iw.N * rP - iw.c);
+  if (iw.kk_lvl != 0u) iw.kk = ((iw.kk_lvl == 1u ? h1 : h2) > iw.k) ? 0u : 0xffffffffu;
 }
 
-template <int kRole, int kMode, bool kInstr, int kInflight>
-__device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_base, float *ring_x, float *ring_y) {
+// kNW >= 0: the inner instruction has exactly kNW waits and trips of I that
+// fit one generation of slots take the short loop (barrier-free,
+// uninstrumented launches only).  kNW < 0: up to kMaxInnerWaits waits, counted
+// at run time, every trip on the general loop.
+template <int kRole, int kMode, bool kInstr, int kInflight, int kNW>
+__device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cnt_base, float *ring_x,
+                                           float *ring_y) {
+  constexpr bool kShort = kNW >= 0;
+  constexpr int kSlots = kShort ? kNW : kMaxInnerWaits;
   const int wave = kRole;
   const uint32_t lane = lane_id();
   const int wg = blockIdx.x;
-  const EngineCode &C = P.eng[kRole];
+  kconst<EngineCode> &C = P.eng[kRole];
   Engine<kRole, kMode, kInstr, kInflight> E(P, C, cnt_base, wave, wg);
   if (kInstr) {
     if (P.dbg) E.log = P.dbg + (int64_t)gridDim.x * 3 + ((int64_t)wg * 3 + wave) * 4 * P.dbg_cap;
@@ -306,19 +329,18 @@ __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_
       E.st.t_start = now_ticks();
     }
   }
-  const int n_iw = C.inner.n;
-  InnerWait iw[kMaxInnerWaits];
+  const int n_iw = kShort ? kNW : C.inner.n;
+  InnerWait iw[kSlots > 0 ? kSlots : 1];
 #pragma unroll
-  for (int j = 0; j < kMaxInnerWaits; ++j)
-    iw[j] = make_inner(j < n_iw ? C.waits[C.inner.first + j] : bfs::PackedWait{0, 0, 0, 0});
-  if (C.inner.update >= 0) {
-    E.own_counter = E.counter_addr((uint32_t)C.inner.update);
-    E.has_own_counter = 1u;
-  }
+  for (int j = 0; j < kSlots; ++j)
+    if (j < n_iw) iw[j] = make_inner(C.waits[C.inner.first + j], cnt_base);
   {
+    // lane 0 adds to the inner instruction's counter, or to its own scratch
+    // word when the instruction has no consumer
     const uint32_t scratch = cnt_base + (uint32_t)bfs::kMaxSlots * bfs::kMaxWavesPerEngine * 4u + 256u * (uint32_t)wave;
     E.scratch_v = scratch + 4u * lane;
-    E.own_vaddr = lane == 0 ? E.own_counter : E.scratch_v;
+    const bool counted = C.inner.update >= 0;
+    E.own_vaddr = (lane == 0 && counted) ? E.counter_addr((uint32_t)C.inner.update) : E.scratch_v;
     E.one_v = lane == 0 ? 1u : 0u;
   }
   const int64_t *toff = P.trip_off + (int64_t)wg * 4;
@@ -350,71 +372,117 @@ __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_
       // loop-invariant parts of the inner waits for this trip of I
       if (kMode == BFS_MODE_BARRIER_FREE) {
 #pragma unroll
-        for (int j = 0; j < kMaxInnerWaits; ++j)
+        for (int j = 0; j < kSlots; ++j)
           if (j < n_iw) enter_inner(iw[j], E.r1, E.r2, E.r3, E.h1, E.h2);
       }
-      uint32_t slot = gen * per_gen, lo = 0;
-      for (uint32_t i = 0; i < trip_i; ++i) {
-        E.r3 += 1;
-        E.h3 = i + 1;
-        const uint32_t instance = E.r3 - 1;
+      const uint32_t slot0 = gen * per_gen;
+      if (kShort && trip_i <= per_gen) {
+        // Short loop: slot = slot0 + i, no wrap; the thresholds are compared
+        // with the last observation before any counter is read.
+        const uint32_t r3_0 = E.r3;
+        const float *xp = xg + (int64_t)r3_0 * 64;
+        float *yp = yg + (int64_t)r3_0 * 64;
+        uint32_t soff = 256u * slot0;
+        for (uint32_t i = 0; i < trip_i; ++i) {
 #pragma unroll
-        for (int j = 0; j < kMaxInnerWaits; ++j) {
-          if (j < n_iw) {
-            uint32_t thr;
-            if (kMode == BFS_MODE_BARRIER) {
-              thr = ((iw[j].packed_w0 >> 25) & 1u) ? (iw[j].packed_w3 >> 16) : 0u;
-            } else {
-              iw[j].run = uniform(iw[j].run + iw[j].step);
-              thr = (E.h3 > iw[j].kk && (int)iw[j].run > 0) ? iw[j].run : 0u;
-            }
-            const uint32_t dep = iw[j].packed_w3 & 0xffffu;
-            if (kInstr && (int)dep == P.fault_dep) thr += (uint32_t)P.fault_delta;
-            if (thr > iw[j].seen || (kInstr && E.log)) {
-              uint32_t obs = 0;
-              if (!E.aborted && thr > 0) {
-                const uint32_t addr = E.counter_addr(iw[j].packed_w0 & 0xffu);
-                obs = uniform(lds_poll(addr));
-                if (kInstr && E.st.on) E.st.polls += 1;
-                if (obs < thr) obs = E.block(addr, thr, dep, instance).observed;
-                iw[j].seen = obs;
+          for (int j = 0; j < kSlots; ++j) {
+            iw[j].run += iw[j].step;
+            if (iw[j].run > iw[j].seen && i >= iw[j].kk) {
+              int32_t obs = (int32_t)uniform(lds_poll(iw[j].addr));
+              if (obs < iw[j].run) {
+                const WaitResult r = E.block(iw[j].addr, (uint32_t)iw[j].run, iw[j].dep, r3_0 + i);
+                obs = (int32_t)r.observed;
+                if (!r.ok) {
+#pragma unroll
+                  for (int jj = 0; jj < kSlots; ++jj) iw[jj].seen = kSeenAll;
+                  obs = kSeenAll;
+                }
               }
-              E.logit(dep, instance, thr, obs);
+              iw[j].seen = obs;
             }
           }
-        }
-        if (!E.aborted) {
           if (kRole == ROLE_LOAD) {
-            __builtin_amdgcn_global_load_lds((const void *)(xg + (int64_t)instance * 64),
-                                             (BFS_LDS void *)(ring_x + (slot + lo) * 64), 4, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void *)xp, (BFS_LDS void *)(ring_x + (slot0 + i) * 64), 4, 0, 0);
             E.pending = (int)uniform((uint32_t)E.pending + 1u);
             if (E.pending == kInflight) E.retire_oldest_of_full();
           } else if (kRole == ROLE_ADD) {
             float v;
-            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-                         : "=v"(v) : "v"(xl + 256u * (slot + lo)) : "memory");
-            // the read returned, so every earlier LDS write of this wave is done
-            if (E.pending > 0) E.add_own(1u);
+            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(xl + soff) : "memory");
             v = v + addc;
-            asm volatile("ds_write_b32 %0, %1" ::"v"(yl + 256u * (slot + lo)), "v"(v) : "memory");
-            E.pending = (int)E.has_own_counter;
+            asm volatile("ds_write_b32 %0, %1" ::"v"(yl + soff), "v"(v) : "memory");
+            E.add_own(1u);   // executed by LDS after the write
           } else {
             float v;
-            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-                         : "=v"(v) : "v"(yl + 256u * (slot + lo)) : "memory");
-            __builtin_nontemporal_store(v, yg + (int64_t)instance * 64);
-            // the slot has been read: the store retires now
-            if (E.has_own_counter) E.add_own(1u);
+            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(yl + soff) : "memory");
+            __builtin_nontemporal_store(v, yp);
+            E.add_own(1u);   // the slot has been read: the store retires now
           }
-        } else {
-          E.retire_all();
-          if (E.has_own_counter) E.add_own(1u);
+          xp += 64;
+          yp += 64;
+          soff += 256u;
         }
-        lo = (lo + 1 == per_gen) ? 0u : lo + 1;
-        if (kMode == BFS_MODE_BARRIER) {
-          E.sync_point();                                 // end of an iteration of I
+        E.r3 = r3_0 + trip_i;
+        E.h3 = trip_i;
+      } else {
+        uint32_t lo = 0;
+        for (uint32_t i = 0; i < trip_i; ++i) {
+          E.r3 += 1;
+          E.h3 = i + 1;
+          const uint32_t instance = E.r3 - 1;
 #pragma unroll
-          for (int j = 0; j < kMaxInnerWaits; ++j) iw[j].seen = 0;   // counters were reset
+          for (int j = 0; j < kSlots; ++j) {
+            if (j < n_iw) {
+              uint32_t thr;
+              if (kMode == BFS_MODE_BARRIER) {
+                thr = iw[j].bar_thr;
+              } else {
+                iw[j].run += iw[j].step;
+                thr = (E.h3 > iw[j].kk && iw[j].run > 0) ? (uint32_t)iw[j].run : 0u;
+              }
+              const uint32_t dep = iw[j].dep;
+              if (kInstr && (int)dep == P.fault_dep) thr += (uint32_t)P.fault_delta;
+              if (thr > (uint32_t)iw[j].seen || (kInstr && E.log)) {
+                uint32_t obs = 0;
+                if (!E.aborted && thr > 0) {
+                  obs = uniform(lds_poll(iw[j].addr));
+                  if (kInstr && E.st.on) E.st.polls += 1;
+                  if (obs < thr) obs = E.block(iw[j].addr, thr, dep, instance).observed;
+                  iw[j].seen = (int32_t)obs;
+                }
+                E.logit(dep, instance, thr, obs);
+              }
+            }
+          }
+          if (!E.aborted) {
+            if (kRole == ROLE_LOAD) {
+              __builtin_amdgcn_global_load_lds((const void *)(xg + (int64_t)instance * 64),
+                                               (BFS_LDS void *)(ring_x + (slot0 + lo) * 64), 4, 0, 0);
+              E.pending = (int)uniform((uint32_t)E.pending + 1u);
+              if (E.pending == kInflight) E.retire_oldest_of_full();
+            } else if (kRole == ROLE_ADD) {
+              float v;
+              asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+                           : "=v"(v) : "v"(xl + 256u * (slot0 + lo)) : "memory");
+              v = v + addc;
+              asm volatile("ds_write_b32 %0, %1" ::"v"(yl + 256u * (slot0 + lo)), "v"(v) : "memory");
+              E.add_own(1u);
+            } else {
+              float v;
+              asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
+                           : "=v"(v) : "v"(yl + 256u * (slot0 + lo)) : "memory");
+              __builtin_nontemporal_store(v, yg + (int64_t)instance * 64);
+              E.add_own(1u);
+            }
+          } else {
+            E.retire_all();
+            E.add_own(1u);
+          }
+          lo = (lo + 1 == per_gen) ? 0u : lo + 1;
+          if (kMode == BFS_MODE_BARRIER) {
+            E.sync_point();                               // end of an iteration of I
+#pragma unroll
+            for (int j = 0; j < kSlots; ++j) iw[j].seen = 0;   // counters were reset
+          }
         }
       }
       gen = (gen + 1 == n_gen) ? 0u : gen + 1;
@@ -442,8 +510,22 @@ __device__ __forceinline__ void run_engine(const Stream3Params &P, uint32_t cnt_
   }
 }
 
+// The exact count of inner waits selects the short-loop engine.
+template <int kRole, int kMode, bool kInstr, int kInflight>
+__device__ __forceinline__ void run_role(kconst<Stream3Params> &P, uint32_t cb, float *rx, float *ry) {
+  if constexpr (kMode == BFS_MODE_BARRIER_FREE && !kInstr) {
+    const int n = P.eng[kRole].inner.n;
+    if (n == 0) run_engine<kRole, kMode, kInstr, kInflight, 0>(P, cb, rx, ry);
+    else if (n == 1) run_engine<kRole, kMode, kInstr, kInflight, 1>(P, cb, rx, ry);
+    else run_engine<kRole, kMode, kInstr, kInflight, 2>(P, cb, rx, ry);
+  } else {
+    run_engine<kRole, kMode, kInstr, kInflight, -1>(P, cb, rx, ry);
+  }
+}
+
 template <int kMode, bool kInstr, int kInflight>
-__global__ void __launch_bounds__(192) stream3_kernel(Stream3Params P) {
+__global__ void __launch_bounds__(192) stream3_kernel(Stream3Params) {
+  kconst<Stream3Params> &P = *(kconst<Stream3Params> *)__builtin_amdgcn_kernarg_segment_ptr();
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
   // counters | 3 x 256 B of per-wave scratch words for the retirement adds | rings
@@ -456,16 +538,16 @@ __global__ void __launch_bounds__(192) stream3_kernel(Stream3Params P) {
   // The add engine has the most work per tile; it wins issue arbitration
   // against the load and store waves, which mostly poll.
   if (wave == ROLE_ADD) __builtin_amdgcn_s_setprio(2);
-  // run_engine(ring read or loaded into, ring written or read from)
+  // run_role(ring read or loaded into, ring written or read from)
   if (wave == ROLE_LOAD) {
     float *r = rings + P.ring_ld * ring_floats;
-    run_engine<ROLE_LOAD, kMode, kInstr, kInflight>(P, cb, r, r);
+    run_role<ROLE_LOAD, kMode, kInstr, kInflight>(P, cb, r, r);
   } else if (wave == ROLE_ADD) {
-    run_engine<ROLE_ADD, kMode, kInstr, kInflight>(P, cb, rings + P.ring_add_src * ring_floats,
-                                                   rings + P.ring_add_dst * ring_floats);
+    run_role<ROLE_ADD, kMode, kInstr, kInflight>(P, cb, rings + P.ring_add_src * ring_floats,
+                                                 rings + P.ring_add_dst * ring_floats);
   } else {
     float *r = rings + P.ring_st * ring_floats;
-    run_engine<ROLE_STORE, kMode, kInstr, kInflight>(P, cb, r, r);
+    run_role<ROLE_STORE, kMode, kInstr, kInflight>(P, cb, r, r);
   }
 }
 

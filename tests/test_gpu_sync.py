@@ -177,6 +177,50 @@ def test_stream_full_size_values(seed):
     assert torch.equal(outs["barrier_free"], outs["barrier"])
 
 
+# Launches without the debug log run engines specialised on their exact number
+# of inner waits: trips of I that fit one generation of slots take the short
+# loop, longer trips (slots reused within the trip, ordered by the offset
+# per_gen dependencies) the general one; two_rings gives the add engine two
+# inner waits.
+UNINSTRUMENTED = [("inplace", 4, False), ("inplace", 2, True), ("two_rings", 4, True), ("two_rings", 2, True)]
+
+
+@pytest.mark.parametrize("layout,per_gen,inner_war", UNINSTRUMENTED)
+def test_stream_uninstrumented_values(layout, per_gen, inner_war):
+    w = stream_workload(seed=5, n_wg=64, outer=32, inner_war=inner_war, layout=layout)
+    w.prog = stream_program(per_gen=per_gen, inner_war=inner_war, layout=layout)
+    trips, toff = trip_tensors(w.trips)
+    base, x = dev(w.base), dev(w.x)
+    ref = torch.from_numpy(w.x.reshape(-1)).cuda() + 1.0
+    for name, mode in MODES:
+        _say(f"[stream-uninstr] {layout} per_gen={per_gen} inner_war={inner_war} mode={name}")
+        y = torch.full((w.n_tiles * 64,), float("nan"), dtype=torch.float32, device="cuda")
+        plan = Plan(w.prog, mode)
+        plan.run([base, x, y], trips, toff, w.trips.n_wg)
+        plan.status()
+        assert torch.equal(y, ref)
+
+
+def test_stream_uninstrumented_watchdog_ends():
+    """A one-poll watchdog on the uninstrumented kernel: every engine that
+    gives up finishes its trips without waiting, so the launch ends, with the
+    deadlock reported or not; the plan runs normally afterwards."""
+    w = stream_workload(seed=6, n_wg=64, outer=16)
+    plan = Plan(w.prog)
+    trips, toff = trip_tensors(w.trips)
+    base, x = dev(w.base), dev(w.x)
+    y = torch.zeros(w.n_tiles * 64, dtype=torch.float32, device="cuda")
+    _say("[stream-watchdog-uninstr]")
+    plan.run([base, x, y], trips, toff, w.trips.n_wg, watchdog_polls=1)
+    try:
+        plan.status()
+    except BfsError as e:
+        assert e.status == bfs.E_DEADLOCK
+    plan.run([base, x, y], trips, toff, w.trips.n_wg)
+    plan.status()
+    assert torch.equal(y, torch.from_numpy(w.x.reshape(-1)).cuda() + 1.0)
+
+
 # ---------------------------------------------------------------------------
 # failure handling: an unsatisfiable wait is reported, and the kernel ends
 # ---------------------------------------------------------------------------

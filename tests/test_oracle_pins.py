@@ -177,6 +177,22 @@ def test_stream_layouts_race_free(layout):
         assert hazard.check(s.prog, res, "barrier") == []
 
 
+@pytest.mark.parametrize("layout", ["inplace", "two_rings"])
+def test_stream_slot_reuse_within_a_trip_race_free(layout):
+    """Two slots per generation with inner trips up to 4: the offset-per_gen
+    dependencies order the reuse of a slot within one trip of I."""
+    from workloads import stream_program
+    s = stream_workload(seed=5, n_wg=2, outer=12, with_data=False, layout=layout, inner_war=True)
+    p = stream_program(per_gen=2, inner_war=True, layout=layout)
+    trips, off = s.trips.flat()
+    assert int(trips.max()) >= 3
+    for wg in range(2):
+        res = core.run(p, trips, off[wg], wg)
+        assert hazard.check(p, res, "barrier_free") == []
+    bare = stream_program(per_gen=2, inner_war=False, layout=layout)
+    assert hazard.check(bare, core.run(bare, trips, off[0], 0)) != []
+
+
 def test_stream_inplace_needs_its_o_dependency_and_generations():
     """Planted mistakes the race check must catch: the in-place layout without
     MARK_O -> ACQ_O, and with too few generations for two O iterations."""
