@@ -253,70 +253,74 @@ struct Engine {
 };
 
 // One wait of the innermost instruction in the form evaluated per iteration.
-// Within one trip of loop I the threshold of Eq. 5 is
-//     thr(i) = [rhat_I > kk] * max(run(i), 0),   run(i) = N * r_P - c,
-// where run grows by N per iteration when P is loop I and is constant
-// otherwise, and kk is k when the mask reads rhat_I, 0 when no mask applies,
-// and "never" when a mask on an outer loop is 0 for this trip.  The fields of
-// the packed wait are decoded once per run, run and kk once per trip of I
-// (loop-invariant code motion of the wait value, Section 6.2); the values are
-// exactly those of Eq. 5.
+// With r_P the loop register of the producer's loop P, the threshold of Eq. 5
+// at an iteration of loop I is
+//     thr = [rhat_S > k] * max(run, 0),   run = N * r_P - c,
+// and run is carried incrementally (loop-invariant code motion of the wait
+// value, Section 6.2): it grows by N whenever r_P is incremented, i.e. per
+// iteration of I, M or O according to P, and is never recomputed.  The mask
+// reads rhat of loop S: for S = I it becomes "rhat_I > kk" with kk fixed; for
+// S = O or M, kk is 0 or "never" per trip of I.  The values are exactly those
+// of Eq. 5.
+//
+// Trips of I that fit one generation of slots (1 <= trip <= per_gen) run in a
+// short loop when every wait's mask is either always 1 (kk = 0) or always 0
+// (kk >= per_gen) there; such a loop compares run with `cmp`, its own last
+// observation of the counter (kSeenAll for a wait that never applies).
 struct InnerWait {
   uint32_t addr;       // LDS address of the producer's counter word
   uint32_t dep;        // dependency id (debug log, error word)
   uint32_t bar_thr;    // barrier mode: the static ordinal, 0 when nothing is owed
-  uint32_t N, c;       // run = N * r_P - c
-  uint32_t lp;         // loop level of P: 0 top, 1 O, 2 M, 3 I
   uint32_t k;          // the mask is rhat_S > k
   uint32_t kk_lvl;     // 1 / 2: the mask reads rhat of O / M and kk is set per trip; 0: kk is fixed
-  int32_t step;        // N when P is loop I, else 0
-  int32_t run;         // N * r_P - c for the current iteration
   uint32_t kk;         // the threshold is 0 while rhat_I <= kk
-  int32_t seen;        // last observed counter value
+  int32_t step_i, step_m, step_o;   // N added to run per iteration of I / M / O
+  int32_t run;         // N * r_P - c at the current iteration
+  int32_t seen;        // last observed counter value (general loop)
+  int32_t cmp;         // short loop: last observed value, kSeenAll, or kNoShort
 };
 
 // Counter values stay below 2^31; an engine that gave up on a wait marks
 // every inner wait as satisfied with this value and finishes without waiting.
 constexpr int32_t kSeenAll = 0x7fffffff;
+constexpr int32_t kNoShort = -1;
 
-__device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait w, uint32_t cnt_base) {
+__device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait w, uint32_t cnt_base, uint32_t per_gen) {
   InnerWait iw;
   const uint32_t N = w.w1 & 0xffffu, K = w.w1 >> 16, k = w.w2 & 0xffffu, sub = w.w2 >> 16;
-  const uint32_t ls = (w.w0 >> 16) & 0xffu, mask = (w.w0 >> 24) & 1u;
+  const uint32_t lp = (w.w0 >> 8) & 0xffu, ls = (w.w0 >> 16) & 0xffu, mask = (w.w0 >> 24) & 1u;
+  const uint32_t c = N * sub + (N - K);
   iw.addr = cnt_base + 4u * (w.w0 & 0xffu) * (uint32_t)bfs::kMaxWavesPerEngine;
   iw.dep = w.w3 & 0xffffu;
   iw.bar_thr = ((w.w0 >> 25) & 1u) ? (w.w3 >> 16) : 0u;
-  iw.N = N;
-  iw.c = N * sub + (N - K);
-  iw.lp = (w.w0 >> 8) & 0xffu;
   iw.k = k;
-  iw.step = iw.lp == 3u ? (int32_t)N : 0;
   iw.kk_lvl = (mask && (ls == 1u || ls == 2u)) ? ls : 0u;
   // fixed kk: no mask, a mask on rhat_I, or a mask on the top level (rhat 1)
   iw.kk = !mask ? 0u : ls == 3u ? k : (1u > k ? 0u : 0xffffffffu);
-  iw.run = 0;
+  iw.step_i = lp == 3u ? (int32_t)N : 0;
+  iw.step_m = lp == 2u ? (int32_t)N : 0;
+  iw.step_o = lp == 1u ? (int32_t)N : 0;
+  iw.run = (int32_t)((lp == 0u ? N : 0u) - c);   // r of the top level is 1, the others start at 0
   iw.seen = 0;
+  iw.cmp = iw.kk_lvl != 0u ? kNoShort : iw.kk == 0u ? 0 : iw.kk >= per_gen ? kSeenAll : kNoShort;
   return iw;
 }
 
-// At the statement of loop I (before its first iteration): r_O, r_M, r_I and
-// rhat_O, rhat_M are the engine's registers; r_I has not been incremented yet.
-__device__ __forceinline__ void enter_inner(InnerWait &iw, uint32_t r1, uint32_t r2, uint32_t r3, uint32_t h1,
-                                            uint32_t h2) {
-  const uint32_t rP = iw.lp == 3u ? r3 : iw.lp == 2u ? r2 : iw.lp == 1u ? r1 : 1u;
-  iw.run = (int32_t)(iw.N * rP - iw.c);
+// kk of a mask on rhat of O or M, at the statement of loop I.
+__device__ __forceinline__ void enter_inner(InnerWait &iw, uint32_t h1, uint32_t h2) {
   if (iw.kk_lvl != 0u) iw.kk = ((iw.kk_lvl == 1u ? h1 : h2) > iw.k) ? 0u : 0xffffffffu;
 }
 
-// kNW >= 0: the inner instruction has exactly kNW waits and trips of I that
-// fit one generation of slots take the short loop (barrier-free,
-// uninstrumented launches only).  kNW < 0: up to kMaxInnerWaits waits, counted
-// at run time, every trip on the general loop.
+// kNW >= 0: the inner instruction has exactly kNW waits and eligible trips of
+// I take the short loop (barrier-free, uninstrumented launches only).
+// kNW < 0: up to kMaxInnerWaits waits, counted at run time, every trip on
+// the general loop.
 template <int kRole, int kMode, bool kInstr, int kInflight, int kNW>
 __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cnt_base, float *ring_x,
                                            float *ring_y) {
   constexpr bool kShort = kNW >= 0;
   constexpr int kSlots = kShort ? kNW : kMaxInnerWaits;
+  constexpr bool kBF = kMode == BFS_MODE_BARRIER_FREE;
   const int wave = kRole;
   const uint32_t lane = lane_id();
   const int wg = blockIdx.x;
@@ -329,11 +333,16 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
       E.st.t_start = now_ticks();
     }
   }
+  const uint32_t per_gen = (uint32_t)P.per_gen, n_gen = (uint32_t)P.n_gen;
   const int n_iw = kShort ? kNW : C.inner.n;
   InnerWait iw[kSlots > 0 ? kSlots : 1];
+  bool short_ok = kShort;
 #pragma unroll
   for (int j = 0; j < kSlots; ++j)
-    if (j < n_iw) iw[j] = make_inner(C.waits[C.inner.first + j], cnt_base);
+    if (j < n_iw) {
+      iw[j] = make_inner(C.waits[C.inner.first + j], cnt_base, per_gen);
+      short_ok = short_ok && iw[j].cmp != kNoShort;
+    }
   {
     // lane 0 adds to the inner instruction's counter, or to its own scratch
     // word when the instruction has no consumer
@@ -351,79 +360,96 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
   float *yg = P.y + tbase * 64 + lane;
   float addc;   // held in a vector register for the whole run
   asm volatile("v_mov_b32 %0, %1" : "=v"(addc) : "s"(P.addc));
-  const uint32_t per_gen = (uint32_t)P.per_gen, n_gen = (uint32_t)P.n_gen;
+  const uint32_t gen_bytes = 256u * per_gen, ring_bytes = gen_bytes * n_gen;
 
   E.sync_point();                                         // before loop O
   const uint32_t trip_o = (uint32_t)ldc(P.trips + ldc(toff + 1));
   const int64_t off_m = ldc(toff + 2), off_i = ldc(toff + 3);
-  uint32_t gen = 0;                                       // (r_M - 1) % n_gen
+  uint32_t soff0 = 0;                                     // byte offset of slot ((r_M - 1) % n_gen) * per_gen
   for (uint32_t o = 0; o < trip_o; ++o) {
     E.r1 += 1;
     E.h1 = o + 1;
+#pragma unroll
+    for (int j = 0; j < kSlots; ++j)
+      if (kBF && j < n_iw) iw[j].run += iw[j].step_o;
     E.nops(C.o_pre, C.n_o_pre, E.r1 - 1);
     E.sync_point();                                       // before loop M
     const uint32_t trip_m = (uint32_t)ldc(P.trips + off_m + E.r1 - 1);
+    const int32_t *trip_i_of = P.trips + off_i + E.r2;    // trips of I for this O iteration's M iterations
     for (uint32_t m = 0; m < trip_m; ++m) {
       E.r2 += 1;
       E.h2 = m + 1;
+#pragma unroll
+      for (int j = 0; j < kSlots; ++j)
+        if (kBF && j < n_iw) iw[j].run += iw[j].step_m;
       E.nops(C.m_pre, C.n_m_pre, E.r2 - 1);
       E.sync_point();                                     // before loop I
-      const uint32_t trip_i = (uint32_t)ldc(P.trips + off_i + E.r2 - 1);
-      // loop-invariant parts of the inner waits for this trip of I
-      if (kMode == BFS_MODE_BARRIER_FREE) {
-#pragma unroll
-        for (int j = 0; j < kSlots; ++j)
-          if (j < n_iw) enter_inner(iw[j], E.r1, E.r2, E.r3, E.h1, E.h2);
-      }
-      const uint32_t slot0 = gen * per_gen;
-      if (kShort && trip_i <= per_gen) {
-        // Short loop: slot = slot0 + i, no wrap; the thresholds are compared
-        // with the last observation before any counter is read.
+      const uint32_t trip_i = (uint32_t)ldc(trip_i_of + m);
+      if (kShort && short_ok && trip_i - 1u < per_gen) {
+        // Short loop: 1 <= trip_i <= per_gen, slot = slot0 + i with no wrap.
         const uint32_t r3_0 = E.r3;
         const float *xp = xg + (int64_t)r3_0 * 64;
         float *yp = yg + (int64_t)r3_0 * 64;
-        uint32_t soff = 256u * slot0;
-        for (uint32_t i = 0; i < trip_i; ++i) {
+        uint32_t vx = xl + soff0, vy = yl + soff0;
+        BFS_LDS float *lp = (BFS_LDS float *)(ring_x + soff0 / 4u);
+        // load engine: loads issued before this trip are still held; the
+        // oldest retires at every iteration from index `ir` on
+        int32_t p0 = E.pending, ir = kInflight - 1 - E.pending;
+        uint32_t i = 0;
+        do {
 #pragma unroll
           for (int j = 0; j < kSlots; ++j) {
-            iw[j].run += iw[j].step;
-            if (iw[j].run > iw[j].seen && i >= iw[j].kk) {
+            iw[j].run += iw[j].step_i;
+            if (iw[j].run > iw[j].cmp) {
               int32_t obs = (int32_t)uniform(lds_poll(iw[j].addr));
               if (obs < iw[j].run) {
+                if (kRole == ROLE_LOAD) E.pending = min(p0 + (int32_t)i, kInflight - 1);
                 const WaitResult r = E.block(iw[j].addr, (uint32_t)iw[j].run, iw[j].dep, r3_0 + i);
+                if (kRole == ROLE_LOAD) {
+                  p0 = E.pending - (int32_t)i;
+                  ir = kInflight - 1 - p0;
+                }
                 obs = (int32_t)r.observed;
                 if (!r.ok) {
 #pragma unroll
-                  for (int jj = 0; jj < kSlots; ++jj) iw[jj].seen = kSeenAll;
+                  for (int jj = 0; jj < kSlots; ++jj) iw[jj].cmp = iw[jj].seen = kSeenAll;
                   obs = kSeenAll;
                 }
               }
-              iw[j].seen = obs;
+              iw[j].cmp = obs;
             }
           }
           if (kRole == ROLE_LOAD) {
-            __builtin_amdgcn_global_load_lds((const void *)xp, (BFS_LDS void *)(ring_x + (slot0 + i) * 64), 4, 0, 0);
-            E.pending = (int)uniform((uint32_t)E.pending + 1u);
-            if (E.pending == kInflight) E.retire_oldest_of_full();
+            __builtin_amdgcn_global_load_lds((const void *)xp, (BFS_LDS void *)lp, 4, 0, 0);
+            if ((int32_t)i >= ir) {
+              wait_vm<kInflight - 1>();
+              E.add_own(1u);
+            }
           } else if (kRole == ROLE_ADD) {
             float v;
-            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(xl + soff) : "memory");
+            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(vx) : "memory");
             v = v + addc;
-            asm volatile("ds_write_b32 %0, %1" ::"v"(yl + soff), "v"(v) : "memory");
+            asm volatile("ds_write_b32 %0, %1" ::"v"(vy), "v"(v) : "memory");
             E.add_own(1u);   // executed by LDS after the write
           } else {
             float v;
-            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(yl + soff) : "memory");
+            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(vy) : "memory");
             __builtin_nontemporal_store(v, yp);
             E.add_own(1u);   // the slot has been read: the store retires now
           }
           xp += 64;
           yp += 64;
-          soff += 256u;
-        }
+          vx += 256u;
+          vy += 256u;
+          lp += 64;
+        } while (++i != trip_i);
+        if (kRole == ROLE_LOAD) E.pending = min(p0 + (int32_t)trip_i, kInflight - 1);
         E.r3 = r3_0 + trip_i;
         E.h3 = trip_i;
       } else {
+#pragma unroll
+        for (int j = 0; j < kSlots; ++j)
+          if (kBF && j < n_iw) enter_inner(iw[j], E.h1, E.h2);
         uint32_t lo = 0;
         for (uint32_t i = 0; i < trip_i; ++i) {
           E.r3 += 1;
@@ -433,10 +459,10 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
           for (int j = 0; j < kSlots; ++j) {
             if (j < n_iw) {
               uint32_t thr;
-              if (kMode == BFS_MODE_BARRIER) {
+              if (!kBF) {
                 thr = iw[j].bar_thr;
               } else {
-                iw[j].run += iw[j].step;
+                iw[j].run += iw[j].step_i;
                 thr = (E.h3 > iw[j].kk && iw[j].run > 0) ? (uint32_t)iw[j].run : 0u;
               }
               const uint32_t dep = iw[j].dep;
@@ -446,30 +472,36 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
                 if (!E.aborted && thr > 0) {
                   obs = uniform(lds_poll(iw[j].addr));
                   if (kInstr && E.st.on) E.st.polls += 1;
-                  if (obs < thr) obs = E.block(iw[j].addr, thr, dep, instance).observed;
+                  if (obs < thr) {
+                    const WaitResult r = E.block(iw[j].addr, thr, dep, instance);
+                    obs = r.observed;
+                    if (!r.ok) {
+#pragma unroll
+                      for (int jj = 0; jj < kSlots; ++jj) iw[jj].cmp = kSeenAll;
+                    }
+                  }
                   iw[j].seen = (int32_t)obs;
                 }
                 E.logit(dep, instance, thr, obs);
               }
             }
           }
+          const uint32_t so = soff0 + 256u * lo;
           if (!E.aborted) {
             if (kRole == ROLE_LOAD) {
               __builtin_amdgcn_global_load_lds((const void *)(xg + (int64_t)instance * 64),
-                                               (BFS_LDS void *)(ring_x + (slot0 + lo) * 64), 4, 0, 0);
+                                               (BFS_LDS void *)(ring_x + so / 4u), 4, 0, 0);
               E.pending = (int)uniform((uint32_t)E.pending + 1u);
               if (E.pending == kInflight) E.retire_oldest_of_full();
             } else if (kRole == ROLE_ADD) {
               float v;
-              asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-                           : "=v"(v) : "v"(xl + 256u * (slot0 + lo)) : "memory");
+              asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(xl + so) : "memory");
               v = v + addc;
-              asm volatile("ds_write_b32 %0, %1" ::"v"(yl + 256u * (slot0 + lo)), "v"(v) : "memory");
+              asm volatile("ds_write_b32 %0, %1" ::"v"(yl + so), "v"(v) : "memory");
               E.add_own(1u);
             } else {
               float v;
-              asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)"
-                           : "=v"(v) : "v"(yl + 256u * (slot0 + lo)) : "memory");
+              asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(yl + so) : "memory");
               __builtin_nontemporal_store(v, yg + (int64_t)instance * 64);
               E.add_own(1u);
             }
@@ -478,14 +510,15 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
             E.add_own(1u);
           }
           lo = (lo + 1 == per_gen) ? 0u : lo + 1;
-          if (kMode == BFS_MODE_BARRIER) {
+          if (!kBF) {
             E.sync_point();                               // end of an iteration of I
 #pragma unroll
             for (int j = 0; j < kSlots; ++j) iw[j].seen = 0;   // counters were reset
           }
         }
       }
-      gen = (gen + 1 == n_gen) ? 0u : gen + 1;
+      soff0 += gen_bytes;
+      if (soff0 == ring_bytes) soff0 = 0;
       E.nops(C.m_post, C.n_m_post, E.r2 - 1);
       E.sync_point();                                     // end of an iteration of M
     }
