@@ -48,6 +48,10 @@ namespace {
 constexpr int kMaxNops = 4;
 constexpr int kMaxWaitsPerEngine = 16;
 constexpr int kMaxInnerWaits = 2;
+// Batch loads the load engine keeps in flight beyond the one just issued:
+// more hides more HBM latency but delays every completion signal by as many
+// batches (measured best at 2 to 3).
+constexpr uint32_t kBatchQ = 2;
 
 struct InstrSync {
   int16_t first;     // index of its first wait in the engine's wait list
@@ -99,6 +103,8 @@ __device__ __forceinline__ uint32_t sel4(uint32_t a, uint32_t b, uint32_t c, uin
 
 enum { ROLE_LOAD = 0, ROLE_ADD = 1, ROLE_STORE = 2 };
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 // One engine wave: loop registers, counters, waits and retirement.
 template <int kRole, int kMode, bool kInstr, int kInflight>
 struct Engine {
@@ -112,6 +118,9 @@ struct Engine {
   uint32_t *log = nullptr;
   uint32_t nlog = 0;
   int pending = 0;                        // load engine: loads issued, not yet retired
+  // Load engine batches: lane (b % 64) of bq holds the tile count of batch b;
+  // nb batches issued so far; btiles tiles in batches not yet retired.
+  uint32_t bq = 0, nb = 0, btiles = 0;
   // Retirement add with every lane active: lane 0 adds to the inner
   // instruction's counter (or to its own scratch word when the instruction
   // has no consumer), the other lanes add 0 to this wave's private scratch
@@ -158,8 +167,29 @@ struct Engine {
     add_own(1u);
     pending = (int)uniform((uint32_t)pending - 1u);
   }
+  // Load engine: retire every outstanding batch load.
+  __device__ __forceinline__ void flush_batches() {
+    if (kRole == ROLE_LOAD && btiles != 0u) {
+      wait_vm<0>();
+      add_own(btiles);
+      btiles = 0;
+      bq = 0;   // the retired batches' entries read as 0 from now on
+    }
+  }
+  // Load engine: batch b of k tiles was issued; the batch issued kBatchQ
+  // batches earlier retires (entries of batches already flushed are 0).
+  __device__ __forceinline__ void issued_batch(uint32_t k) {
+    bq = lane_id() == (nb & 63u) ? k : bq;
+    const uint32_t t = (uint32_t)__builtin_amdgcn_readlane((int)bq, (int)((nb - kBatchQ) & 63u));
+    nb += 1;
+    btiles += k;
+    wait_vm<kBatchQ>();
+    add_own(t);
+    btiles -= t;
+  }
   // Retire everything held.
   __device__ __forceinline__ void retire_all() {
+    flush_batches();
     if (pending > 0) {
       if (kRole == ROLE_LOAD) {
         const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
@@ -187,6 +217,7 @@ struct Engine {
   __device__ __forceinline__ WaitResult block(uint32_t addr, uint32_t thr, uint32_t dep, uint32_t instance) {
     const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
     if (kInstr && st.on) st.n_blocked += 1;
+    flush_batches();
     while (pending > 0) {
       const uint32_t v = uniform(lds_poll(addr));
       if (v >= thr) {
@@ -358,6 +389,10 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
   const uint32_t xl = lds_addr(ring_x) + 4u * lane, yl = lds_addr(ring_y) + 4u * lane;
   const float *xg = P.x + tbase * 64 + lane;
   float *yg = P.y + tbase * 64 + lane;
+  // batches: lane l moves bytes [16 l, 16 l + 16) of a block of tiles
+  const uint32_t xl4 = lds_addr(ring_x) + 16u * lane, yl4 = lds_addr(ring_y) + 16u * lane;
+  const float *xb = P.x + tbase * 64 + 4 * lane;
+  float *yb = P.y + tbase * 64 + 4 * lane;
   float addc;   // held in a vector register for the whole run
   asm volatile("v_mov_b32 %0, %1" : "=v"(addc) : "s"(P.addc));
   const uint32_t gen_bytes = 256u * per_gen, ring_bytes = gen_bytes * n_gen;
@@ -376,6 +411,8 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
     E.sync_point();                                       // before loop M
     const uint32_t trip_m = (uint32_t)ldc(P.trips + off_m + E.r1 - 1);
     const int32_t *trip_i_of = P.trips + off_i + E.r2;    // trips of I for this O iteration's M iterations
+    // the trip of the next M iteration is fetched one iteration ahead
+    uint32_t trip_next = trip_m > 0 ? (uint32_t)ldc(trip_i_of) : 0u;
     for (uint32_t m = 0; m < trip_m; ++m) {
       E.r2 += 1;
       E.h2 = m + 1;
@@ -384,31 +421,28 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
         if (kBF && j < n_iw) iw[j].run += iw[j].step_m;
       E.nops(C.m_pre, C.n_m_pre, E.r2 - 1);
       E.sync_point();                                     // before loop I
-      const uint32_t trip_i = (uint32_t)ldc(trip_i_of + m);
+      const uint32_t trip_i = trip_next;
+      trip_next = (uint32_t)ldc(trip_i_of + min(m + 1u, trip_m - 1u));
       if (kShort && short_ok && trip_i - 1u < per_gen) {
-        // Short loop: 1 <= trip_i <= per_gen, slot = slot0 + i with no wrap.
-        const uint32_t r3_0 = E.r3;
-        const float *xp = xg + (int64_t)r3_0 * 64;
-        float *yp = yg + (int64_t)r3_0 * 64;
-        uint32_t vx = xl + soff0, vy = yl + soff0;
-        BFS_LDS float *lp = (BFS_LDS float *)(ring_x + soff0 / 4u);
-        // load engine: loads issued before this trip are still held; the
-        // oldest retires at every iteration from index `ir` on
-        int32_t p0 = E.pending, ir = kInflight - 1 - E.pending;
-        uint32_t i = 0;
+        // Short trip (1 <= trip_i <= per_gen): slots slot0 .. slot0 + trip_i - 1
+        // with no wrap.  It runs in batches of up to 4 instances: the tiles
+        // of consecutive r_I are adjacent in HBM and their slots adjacent in
+        // LDS, so each engine moves a batch as one contiguous block with one
+        // 16-byte-per-lane access (lanes from 16 * k idle), waits once for
+        // the threshold of the batch's last instance and adds k to its
+        // counter once.  Waiting for a later instance than required and
+        // signalling completions together only delays the engines.
+        if (kRole == ROLE_LOAD && E.pending > 0) E.retire_all();
+        uint32_t done = 0;
         do {
+          const uint32_t k = min(trip_i - done, 4u);
 #pragma unroll
           for (int j = 0; j < kSlots; ++j) {
-            iw[j].run += iw[j].step_i;
-            if (iw[j].run > iw[j].cmp) {
+            const int32_t thr = iw[j].run + (int32_t)k * iw[j].step_i;
+            if (thr > iw[j].cmp) {
               int32_t obs = (int32_t)uniform(lds_poll(iw[j].addr));
-              if (obs < iw[j].run) {
-                if (kRole == ROLE_LOAD) E.pending = min(p0 + (int32_t)i, kInflight - 1);
-                const WaitResult r = E.block(iw[j].addr, (uint32_t)iw[j].run, iw[j].dep, r3_0 + i);
-                if (kRole == ROLE_LOAD) {
-                  p0 = E.pending - (int32_t)i;
-                  ir = kInflight - 1 - p0;
-                }
+              if (obs < thr) {
+                const WaitResult r = E.block(iw[j].addr, (uint32_t)thr, iw[j].dep, E.r3 + done + k - 1u);
                 obs = (int32_t)r.observed;
                 if (!r.ok) {
 #pragma unroll
@@ -418,35 +452,38 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
               }
               iw[j].cmp = obs;
             }
+            iw[j].run = thr;
           }
+          const uint32_t boff = soff0 + 256u * done;           // LDS byte offset of the batch's first slot
+          const int64_t tile = (int64_t)(E.r3 + done) * 64;    // element offset of its first tile
+          const bool act = lane < 16u * k;
           if (kRole == ROLE_LOAD) {
-            __builtin_amdgcn_global_load_lds((const void *)xp, (BFS_LDS void *)lp, 4, 0, 0);
-            if ((int32_t)i >= ir) {
-              wait_vm<kInflight - 1>();
-              E.add_own(1u);
-            }
+            if (act)
+              __builtin_amdgcn_global_load_lds((const void *)(xb + tile), (BFS_LDS void *)(ring_x + boff / 4u), 16, 0,
+                                               0);
+            E.issued_batch(k);   // batch loads land in issue order
           } else if (kRole == ROLE_ADD) {
-            float v;
-            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(vx) : "memory");
-            v = v + addc;
-            asm volatile("ds_write_b32 %0, %1" ::"v"(vy), "v"(v) : "memory");
-            E.add_own(1u);   // executed by LDS after the write
+            if (act) {
+              f32x4 v;
+              asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(xl4 + boff) : "memory");
+              v = v + addc;
+              asm volatile("ds_write_b128 %0, %1" ::"v"(yl4 + boff), "v"(v) : "memory");
+            }
+            E.add_own(k);   // executed by LDS after the write
           } else {
-            float v;
-            asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(vy) : "memory");
-            __builtin_nontemporal_store(v, yp);
-            E.add_own(1u);   // the slot has been read: the store retires now
+            if (act) {
+              f32x4 v;
+              asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(yl4 + boff) : "memory");
+              __builtin_nontemporal_store(v, (f32x4 *)(yb + tile));
+            }
+            E.add_own(k);   // the slots have been read: the stores retire now
           }
-          xp += 64;
-          yp += 64;
-          vx += 256u;
-          vy += 256u;
-          lp += 64;
-        } while (++i != trip_i);
-        if (kRole == ROLE_LOAD) E.pending = min(p0 + (int32_t)trip_i, kInflight - 1);
-        E.r3 = r3_0 + trip_i;
+          done += k;
+        } while (done != trip_i);
+        E.r3 += trip_i;
         E.h3 = trip_i;
       } else {
+        E.flush_batches();
 #pragma unroll
         for (int j = 0; j < kSlots; ++j)
           if (kBF && j < n_iw) enter_inner(iw[j], E.h1, E.h2);
@@ -568,9 +605,11 @@ __global__ void __launch_bounds__(192) stream3_kernel(Stream3Params) {
   __syncthreads();
   const uint32_t cb = lds_addr(cnt);
   const int wave = wave_id();
-  // The add engine has the most work per tile; it wins issue arbitration
-  // against the load and store waves, which mostly poll.
-  if (wave == ROLE_ADD) __builtin_amdgcn_s_setprio(2);
+  // Issue priority follows the chain: the load engine, which every other
+  // engine waits for, wins arbitration against the add engine, and both
+  // against the store engine.
+  if (wave == ROLE_LOAD) __builtin_amdgcn_s_setprio(3);
+  else if (wave == ROLE_ADD) __builtin_amdgcn_s_setprio(2);
   // run_role(ring read or loaded into, ring written or read from)
   if (wave == ROLE_LOAD) {
     float *r = rings + P.ring_ld * ring_floats;
