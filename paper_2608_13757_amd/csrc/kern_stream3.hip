@@ -294,10 +294,10 @@ struct Engine {
 // S = O or M, kk is 0 or "never" per trip of I.  The values are exactly those
 // of Eq. 5.
 //
-// Trips of I that fit one generation of slots (1 <= trip <= per_gen) run in a
-// short loop when every wait's mask is either always 1 (kk = 0) or always 0
-// (kk >= per_gen) there; such a loop compares run with `cmp`, its own last
-// observation of the counter (kSeenAll for a wait that never applies).
+// Barrier-free, uninstrumented launches run trips of I in batches of
+// consecutive instances; a batch waits for the threshold of its last
+// instance, which is the largest of the batch (run and the mask only grow
+// with rhat_I), and compares it with `cmp`, the last observed counter value.
 struct InnerWait {
   uint32_t addr;       // LDS address of the producer's counter word
   uint32_t dep;        // dependency id (debug log, error word)
@@ -308,15 +308,16 @@ struct InnerWait {
   int32_t step_i, step_m, step_o;   // N added to run per iteration of I / M / O
   int32_t run;         // N * r_P - c at the current iteration
   int32_t seen;        // last observed counter value (general loop)
-  int32_t cmp;         // short loop: last observed value, kSeenAll, or kNoShort
+  int32_t cmp;         // last observed counter value (batches)
 };
 
 // Counter values stay below 2^31; an engine that gave up on a wait marks
 // every inner wait as satisfied with this value and finishes without waiting.
 constexpr int32_t kSeenAll = 0x7fffffff;
-constexpr int32_t kNoShort = -1;
+// Instances per batch: 64 lanes move 16 bytes each, four 256-byte tiles.
+constexpr uint32_t kBatchMax = 4;
 
-__device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait w, uint32_t cnt_base, uint32_t per_gen) {
+__device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait w, uint32_t cnt_base) {
   InnerWait iw;
   const uint32_t N = w.w1 & 0xffffu, K = w.w1 >> 16, k = w.w2 & 0xffffu, sub = w.w2 >> 16;
   const uint32_t lp = (w.w0 >> 8) & 0xffu, ls = (w.w0 >> 16) & 0xffu, mask = (w.w0 >> 24) & 1u;
@@ -333,7 +334,7 @@ __device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait w, uint32_
   iw.step_o = lp == 1u ? (int32_t)N : 0;
   iw.run = (int32_t)((lp == 0u ? N : 0u) - c);   // r of the top level is 1, the others start at 0
   iw.seen = 0;
-  iw.cmp = iw.kk_lvl != 0u ? kNoShort : iw.kk == 0u ? 0 : iw.kk >= per_gen ? kSeenAll : kNoShort;
+  iw.cmp = 0;
   return iw;
 }
 
@@ -367,12 +368,12 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
   const uint32_t per_gen = (uint32_t)P.per_gen, n_gen = (uint32_t)P.n_gen;
   const int n_iw = kShort ? kNW : C.inner.n;
   InnerWait iw[kSlots > 0 ? kSlots : 1];
-  bool short_ok = kShort;
+  bool outer_masks = false;   // some wait's mask reads rhat of O or M
 #pragma unroll
   for (int j = 0; j < kSlots; ++j)
     if (j < n_iw) {
-      iw[j] = make_inner(C.waits[C.inner.first + j], cnt_base, per_gen);
-      short_ok = short_ok && iw[j].cmp != kNoShort;
+      iw[j] = make_inner(C.waits[C.inner.first + j], cnt_base);
+      outer_masks = outer_masks || iw[j].kk_lvl != 0u;
     }
   {
     // lane 0 adds to the inner instruction's counter, or to its own scratch
@@ -423,39 +424,34 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
       E.sync_point();                                     // before loop I
       const uint32_t trip_i = trip_next;
       trip_next = (uint32_t)ldc(trip_i_of + min(m + 1u, trip_m - 1u));
-      if (kShort && short_ok && trip_i - 1u < per_gen) {
-        // Short trip (1 <= trip_i <= per_gen): slots slot0 .. slot0 + trip_i - 1
-        // with no wrap.  It runs in batches of up to 4 instances: the tiles
-        // of consecutive r_I are adjacent in HBM and their slots adjacent in
-        // LDS, so each engine moves a batch as one contiguous block with one
-        // 16-byte-per-lane access (lanes from 16 * k idle), waits once for
-        // the threshold of the batch's last instance and adds k to its
-        // counter once.  Waiting for a later instance than required and
-        // signalling completions together only delays the engines.
-        if (kRole == ROLE_LOAD && E.pending > 0) E.retire_all();
-        uint32_t done = 0;
-        do {
-          const uint32_t k = min(trip_i - done, 4u);
+      if (kShort) {
+        // Batches of up to kBatchMax instances within one generation of
+        // slots: the tiles of consecutive r_I are adjacent in HBM and their
+        // slots adjacent in LDS, so each engine moves a batch as one
+        // contiguous block with one 16-byte-per-lane access (lanes from
+        // 16 k idle), waits once and adds k to its counter once.  Waiting for
+        // the batch's last instance and signalling completions together only
+        // delays the engines.
+        auto batch = [&](uint32_t k, uint32_t done, uint32_t boff) __attribute__((always_inline)) {
 #pragma unroll
           for (int j = 0; j < kSlots; ++j) {
-            const int32_t thr = iw[j].run + (int32_t)k * iw[j].step_i;
-            if (thr > iw[j].cmp) {
+            const int32_t run_last = iw[j].run + (int32_t)k * iw[j].step_i;
+            iw[j].run = run_last;
+            if (run_last > iw[j].cmp && done + k > iw[j].kk) {
               int32_t obs = (int32_t)uniform(lds_poll(iw[j].addr));
-              if (obs < thr) {
-                const WaitResult r = E.block(iw[j].addr, (uint32_t)thr, iw[j].dep, E.r3 + done + k - 1u);
+              if (obs < run_last) {
+                const WaitResult r = E.block(iw[j].addr, (uint32_t)run_last, iw[j].dep, E.r3 + done + k - 1u);
                 obs = (int32_t)r.observed;
                 if (!r.ok) {
 #pragma unroll
-                  for (int jj = 0; jj < kSlots; ++jj) iw[jj].cmp = iw[jj].seen = kSeenAll;
+                  for (int jj = 0; jj < kSlots; ++jj) iw[jj].cmp = kSeenAll;
                   obs = kSeenAll;
                 }
               }
               iw[j].cmp = obs;
             }
-            iw[j].run = thr;
           }
-          const uint32_t boff = soff0 + 256u * done;           // LDS byte offset of the batch's first slot
-          const int64_t tile = (int64_t)(E.r3 + done) * 64;    // element offset of its first tile
+          const int64_t tile = (int64_t)(E.r3 + done) * 64;    // element offset of the batch's first tile
           const bool act = lane < 16u * k;
           if (kRole == ROLE_LOAD) {
             if (act)
@@ -478,8 +474,24 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
             }
             E.add_own(k);   // the slots have been read: the stores retire now
           }
-          done += k;
-        } while (done != trip_i);
+        };
+        if (outer_masks) {
+#pragma unroll
+          for (int j = 0; j < kSlots; ++j) enter_inner(iw[j], E.h1, E.h2);
+        }
+        if (trip_i - 1u < min(kBatchMax, per_gen)) {
+          batch(trip_i, 0u, soff0);                         // the whole trip in one batch
+        } else {
+          // slot = slot0 + (rhat_I - 1) % per_gen: batches never straddle a wrap
+          uint32_t done = 0, pos = 0;
+          while (done != trip_i) {
+            const uint32_t k = min(min(trip_i - done, kBatchMax), per_gen - pos);
+            batch(k, done, soff0 + 256u * pos);
+            done += k;
+            pos += k;
+            if (pos == per_gen) pos = 0;
+          }
+        }
         E.r3 += trip_i;
         E.h3 = trip_i;
       } else {
