@@ -414,6 +414,7 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
     const int32_t *trip_i_of = P.trips + off_i + E.r2;    // trips of I for this O iteration's M iterations
     // the trip of the next M iteration is fetched one iteration ahead
     uint32_t trip_next = trip_m > 0 ? (uint32_t)ldc(trip_i_of) : 0u;
+    asm volatile("" ::"s"(trip_next));   // waited for here, once per O iteration
     for (uint32_t m = 0; m < trip_m; ++m) {
       E.r2 += 1;
       E.h2 = m + 1;
@@ -457,11 +458,17 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
             if (act)
               __builtin_amdgcn_global_load_lds((const void *)(xb + tile), (BFS_LDS void *)(ring_x + boff / 4u), 16, 0,
                                                0);
+            // the next trip has arrived by now; taking it here keeps its
+            // wait ahead of the counter add, which then never holds up the
+            // next M iteration
+            asm volatile("" ::"s"(trip_next));
             E.issued_batch(k);   // batch loads land in issue order
           } else if (kRole == ROLE_ADD) {
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (act)
+              asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "+v"(v) : "v"(xl4 + boff) : "memory");
+            asm volatile("" ::"s"(trip_next));   // arrived by now (see the load engine)
             if (act) {
-              f32x4 v;
-              asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(xl4 + boff) : "memory");
               v = v + addc;
               asm volatile("ds_write_b128 %0, %1" ::"v"(yl4 + boff), "v"(v) : "memory");
             }
@@ -472,15 +479,18 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
               asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(yl4 + boff) : "memory");
               __builtin_nontemporal_store(v, (f32x4 *)(yb + tile));
             }
+            asm volatile("" ::"s"(trip_next));   // arrived by now (see the load engine)
             E.add_own(k);   // the slots have been read: the stores retire now
           }
         };
-        if (outer_masks) {
+        if (__builtin_expect(outer_masks, 0)) {
 #pragma unroll
           for (int j = 0; j < kSlots; ++j) enter_inner(iw[j], E.h1, E.h2);
         }
         if (trip_i - 1u < min(kBatchMax, per_gen)) {
           batch(trip_i, 0u, soff0);                         // the whole trip in one batch
+        } else if (trip_i == 0u) {
+          asm volatile("" ::"s"(trip_next));
         } else {
           // slot = slot0 + (rhat_I - 1) % per_gen: batches never straddle a wrap
           uint32_t done = 0, pos = 0;
