@@ -397,6 +397,10 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
   float addc;   // held in a vector register for the whole run
   asm volatile("v_mov_b32 %0, %1" : "=v"(addc) : "s"(P.addc));
   const uint32_t gen_bytes = 256u * per_gen, ring_bytes = gen_bytes * n_gen;
+  const uint32_t kb = min(kBatchMax, per_gen);            // the largest trip one batch holds
+  // M iterations run in pairs when the engine has no M-level instruction and
+  // no wait whose mask reads rhat of O or M
+  const bool pair_ok = kShort && C.n_m_pre == 0 && C.n_m_post == 0 && !outer_masks;
 
   E.sync_point();                                         // before loop O
   const uint32_t trip_o = (uint32_t)ldc(P.trips + ldc(toff + 1));
@@ -412,10 +416,88 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
     E.sync_point();                                       // before loop M
     const uint32_t trip_m = (uint32_t)ldc(P.trips + off_m + E.r1 - 1);
     const int32_t *trip_i_of = P.trips + off_i + E.r2;    // trips of I for this O iteration's M iterations
-    // the trip of the next M iteration is fetched one iteration ahead
-    uint32_t trip_next = trip_m > 0 ? (uint32_t)ldc(trip_i_of) : 0u;
-    asm volatile("" ::"s"(trip_next));   // waited for here, once per O iteration
-    for (uint32_t m = 0; m < trip_m; ++m) {
+    // The trips of the next two M iterations are fetched ahead: tq0 for
+    // M iteration m + 1, tq1 for m + 2 (indices clamped to the table).
+    uint32_t tq0 = trip_m > 0u ? (uint32_t)ldc(trip_i_of) : 0u;
+    uint32_t tq1 = trip_m > 1u ? (uint32_t)ldc(trip_i_of + 1) : 0u;
+    asm volatile("" ::"s"(tq0), "s"(tq1));   // waited for here, once per O iteration
+    uint32_t m = 0;
+    while (m < trip_m) {
+      if (kShort && pair_ok && m + 1u < trip_m && tq0 - 1u < kb && tq1 - 1u < kb) {
+        // Two M iterations whose trips each fit one batch: one wait, one
+        // LDS round trip and one counter add for both.
+        const uint32_t ta = tq0, tb = tq1;
+        tq0 = (uint32_t)ldc(trip_i_of + min(m + 2u, trip_m - 1u));
+        tq1 = (uint32_t)ldc(trip_i_of + min(m + 3u, trip_m - 1u));
+        E.r2 += 2;
+        E.h2 = m + 2;
+        const uint32_t sa = soff0;
+        uint32_t sb = soff0 + gen_bytes;
+        if (sb == ring_bytes) sb = 0;
+        // the largest threshold of the two trips: the second trip's last
+        // instance, or the first's while the second's mask is still 0
+#pragma unroll
+        for (int j = 0; j < kSlots; ++j) {
+          const int32_t run_a = iw[j].run + iw[j].step_m + (int32_t)ta * iw[j].step_i;
+          const int32_t run_b = run_a + iw[j].step_m + (int32_t)tb * iw[j].step_i;
+          iw[j].run = run_b;
+          const int32_t thr = tb > iw[j].kk ? run_b : ta > iw[j].kk ? run_a : 0;
+          if (thr > iw[j].cmp) {
+            int32_t obs = (int32_t)uniform(lds_poll(iw[j].addr));
+            if (obs < thr) {
+              const WaitResult r = E.block(iw[j].addr, (uint32_t)thr, iw[j].dep, E.r3 + ta + tb - 1u);
+              obs = (int32_t)r.observed;
+              if (!r.ok) {
+#pragma unroll
+                for (int jj = 0; jj < kSlots; ++jj) iw[jj].cmp = kSeenAll;
+                obs = kSeenAll;
+              }
+            }
+            iw[j].cmp = obs;
+          }
+        }
+        const int64_t tile_a = (int64_t)E.r3 * 64, tile_b = tile_a + (int64_t)ta * 64;
+        const uint32_t kmax = max(ta, tb);
+        if (kRole == ROLE_LOAD) {
+          if (lane < 16u * ta)
+            __builtin_amdgcn_global_load_lds((const void *)(xb + tile_a), (BFS_LDS void *)(ring_x + sa / 4u), 16, 0, 0);
+          asm volatile("" ::"s"(tq0), "s"(tq1));   // arrived by now (see the single batch)
+          E.issued_batch(ta);
+          if (lane < 16u * tb)
+            __builtin_amdgcn_global_load_lds((const void *)(xb + tile_b), (BFS_LDS void *)(ring_x + sb / 4u), 16, 0, 0);
+          E.issued_batch(tb);
+        } else {
+          // both blocks read with the lanes of the longer trip: the extra
+          // lanes read slots of the same generations that no engine uses in
+          // these M iterations, and their values are dropped
+          const uint32_t base = kRole == ROLE_ADD ? xl4 : yl4;
+          f32x4 va = {0.f, 0.f, 0.f, 0.f}, vb = {0.f, 0.f, 0.f, 0.f};
+          if (lane < 16u * kmax)
+            asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3\n\ts_waitcnt lgkmcnt(0)"
+                         : "+v"(va), "+v"(vb) : "v"(base + sa), "v"(base + sb) : "memory");
+          asm volatile("" ::"s"(tq0), "s"(tq1));   // arrived by now (see the single batch)
+          if (kRole == ROLE_ADD) {
+            if (lane < 16u * ta) {
+              va = va + addc;
+              asm volatile("ds_write_b128 %0, %1" ::"v"(yl4 + sa), "v"(va) : "memory");
+            }
+            if (lane < 16u * tb) {
+              vb = vb + addc;
+              asm volatile("ds_write_b128 %0, %1" ::"v"(yl4 + sb), "v"(vb) : "memory");
+            }
+          } else {
+            if (lane < 16u * ta) __builtin_nontemporal_store(va, (f32x4 *)(yb + tile_a));
+            if (lane < 16u * tb) __builtin_nontemporal_store(vb, (f32x4 *)(yb + tile_b));
+          }
+          E.add_own(ta + tb);
+        }
+        E.r3 += ta + tb;
+        E.h3 = tb;
+        soff0 = sb + gen_bytes;
+        if (soff0 == ring_bytes) soff0 = 0;
+        m += 2;
+        continue;
+      }
       E.r2 += 1;
       E.h2 = m + 1;
 #pragma unroll
@@ -423,8 +505,9 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
         if (kBF && j < n_iw) iw[j].run += iw[j].step_m;
       E.nops(C.m_pre, C.n_m_pre, E.r2 - 1);
       E.sync_point();                                     // before loop I
-      const uint32_t trip_i = trip_next;
-      trip_next = (uint32_t)ldc(trip_i_of + min(m + 1u, trip_m - 1u));
+      const uint32_t trip_i = tq0;
+      tq0 = tq1;
+      tq1 = (uint32_t)ldc(trip_i_of + min(m + 2u, trip_m - 1u));
       if (kShort) {
         // Batches of up to kBatchMax instances within one generation of
         // slots: the tiles of consecutive r_I are adjacent in HBM and their
@@ -461,13 +544,13 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
             // the next trip has arrived by now; taking it here keeps its
             // wait ahead of the counter add, which then never holds up the
             // next M iteration
-            asm volatile("" ::"s"(trip_next));
+            asm volatile("" ::"s"(tq1));
             E.issued_batch(k);   // batch loads land in issue order
           } else if (kRole == ROLE_ADD) {
             f32x4 v = {0.f, 0.f, 0.f, 0.f};
             if (act)
               asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "+v"(v) : "v"(xl4 + boff) : "memory");
-            asm volatile("" ::"s"(trip_next));   // arrived by now (see the load engine)
+            asm volatile("" ::"s"(tq1));   // arrived by now (see the load engine)
             if (act) {
               v = v + addc;
               asm volatile("ds_write_b128 %0, %1" ::"v"(yl4 + boff), "v"(v) : "memory");
@@ -479,7 +562,7 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
               asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(yl4 + boff) : "memory");
               __builtin_nontemporal_store(v, (f32x4 *)(yb + tile));
             }
-            asm volatile("" ::"s"(trip_next));   // arrived by now (see the load engine)
+            asm volatile("" ::"s"(tq1));   // arrived by now (see the load engine)
             E.add_own(k);   // the slots have been read: the stores retire now
           }
         };
@@ -487,10 +570,10 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
 #pragma unroll
           for (int j = 0; j < kSlots; ++j) enter_inner(iw[j], E.h1, E.h2);
         }
-        if (trip_i - 1u < min(kBatchMax, per_gen)) {
+        if (trip_i - 1u < kb) {
           batch(trip_i, 0u, soff0);                         // the whole trip in one batch
         } else if (trip_i == 0u) {
-          asm volatile("" ::"s"(trip_next));
+          asm volatile("" ::"s"(tq1));
         } else {
           // slot = slot0 + (rhat_I - 1) % per_gen: batches never straddle a wrap
           uint32_t done = 0, pos = 0;
@@ -580,6 +663,7 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
       if (soff0 == ring_bytes) soff0 = 0;
       E.nops(C.m_post, C.n_m_post, E.r2 - 1);
       E.sync_point();                                     // end of an iteration of M
+      m += 1;
     }
     E.nops(C.o_post, C.n_o_post, E.r1 - 1);
     E.sync_point();                                       // end of an iteration of O
