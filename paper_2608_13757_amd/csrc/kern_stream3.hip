@@ -50,8 +50,8 @@ constexpr int kMaxWaitsPerEngine = 16;
 constexpr int kMaxInnerWaits = 2;
 // Batch loads the load engine keeps in flight beyond the one just issued:
 // more hides more HBM latency but delays every completion signal by as many
-// batches (measured best at 2 to 3).
-constexpr uint32_t kBatchQ = 2;
+// batches (measured best at 2 to 3, 3 with M iterations in pairs).
+constexpr uint32_t kBatchQ = 3;
 
 struct InstrSync {
   int16_t first;     // index of its first wait in the engine's wait list
