@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--n-gen", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--modes", default="barrier_free,barrier")
+    ap.add_argument("--alloc", default="per_loop", choices=["per_loop", "per_instr"],
+                    help="counter allocation of the barrier-free plans (Eq. 5 per loop and engine, "
+                         "or Eq. 3 one counter per producer instruction)")
     ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn", "moe"],
                     help="stream: the sync-bound microbenchmark (headline); gemm: 4096^3 bf16 GEMM + bias + GELU; "
                          "attn: varlen attention forward; moe: MoE grouped GEMM")
@@ -44,6 +47,15 @@ def parse():
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference dispatch for HBM traffic counters)")
     return ap.parse_args()
+
+
+def alloc_of(a, mode):
+    """Counter allocation of a plan: the requested one for barrier-free plans
+    (barrier mode keeps its one counter per engine)."""
+    from paper_2608_13757_amd import ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER_FREE
+    if mode != MODE_BARRIER_FREE:
+        return ALLOC_PER_LOOP
+    return ALLOC_PER_INSTR if a.alloc == "per_instr" else ALLOC_PER_LOOP
 
 
 def time_mode(plan, bufs, trips, toff, n_wg, steps, warmup):
@@ -135,7 +147,7 @@ def bench_gemm(a):
     res = {}
     for name in a.modes.split(","):
         mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
-        plan = Plan(gemm_program(m, n, k), mode)
+        plan = Plan(gemm_program(m, n, k), mode, alloc_of(a, mode))
         res[name] = time_mode(plan, [A, Bt, bias, C], trips, toff, tt.n_wg, a.steps, a.warmup)
     flop = 2.0 * m * n * k
     bf = res.get("barrier_free", next(iter(res.values())))
@@ -194,7 +206,7 @@ def bench_attn(a):
     res = {}
     for name in a.modes.split(","):
         mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
-        plan = Plan(attn_program(heads), mode)
+        plan = Plan(attn_program(heads), mode, alloc_of(a, mode))
         res[name] = time_mode(plan, [work, q, k, v, o], trips, toff, wl.trips.n_wg, a.steps, a.warmup)
     lens = ai.lengths.astype(np.float64)
     flop = 4.0 * 128 * heads * float(np.sum(lens * lens))
@@ -250,7 +262,7 @@ def bench_moe(a):
     res = {}
     for name in a.modes.split(","):
         mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
-        plans = {ph: Plan(moe_program(ph, H, F), mode) for ph in (1, 2)}
+        plans = {ph: Plan(moe_program(ph, H, F), mode, alloc_of(a, mode)) for ph in (1, 2)}
 
         def step():
             for ph in (1, 2):
@@ -344,7 +356,9 @@ def main():
     modes = a.modes.split(",")
     for name in modes:
         mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
-        plan = Plan(w.prog, mode)
+        plan = Plan(w.prog, mode, alloc_of(a, mode))
+        if mode == MODE_BARRIER_FREE:
+            resources = plan.stats()
         res[name] = time_mode(plan, [base, x, y], trips, toff, a.n_wg, a.steps, a.warmup)
         ok = torch.equal(y, x.reshape(-1) + 1.0)
         if not ok:
@@ -368,7 +382,7 @@ def main():
         "config": {"workload": "sync-bound stream: load/add/store engines, nest 256 x U[1,16] x U[1,4], "
                                "64-fp32 tiles, 1024 workgroups, one in-place LDS ring",
                    "n_wg": a.n_wg, "outer": a.outer, "innermost_iterations": inner,
-                   "ring_generations": a.n_gen, "seed": a.seed, "parallelism": "single GPU"},
+                   "ring_generations": a.n_gen, "seed": a.seed, "alloc": a.alloc, "parallelism": "single GPU"},
         "latency_us": {k: v["ms_mean"] * 1e3 for k, v in res.items()},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": None},
@@ -376,6 +390,8 @@ def main():
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
         out["barrier_ops_per_s"] = ops / (res["barrier"]["ms_mean"] * 1e-3)
+    if "barrier_free" in res:
+        out["resources"] = resources
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     emit(out, a, "stream3")

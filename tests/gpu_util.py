@@ -43,8 +43,10 @@ def log_records(plan, log_words, n_wg, cap, per_wave=False):
 
 def compare_log_with_oracle(prog, plan, logs, recs_by_wg, mode):
     """Every emitted wait's logged threshold equals the oracle's, bit-exact,
-    and the observed counter was never below it."""
-    key = "sem_thr" if mode == "barrier_free" else "barrier_thr"
+    and the observed counter was never below it.  mode "per_instr": a
+    barrier-free plan with one counter per instruction, whose thresholds are
+    the Eq. 1 counts."""
+    key = {"barrier_free": "sem_thr", "barrier": "barrier_thr", "per_instr": "count_thr"}[mode]
     n = 0
     for wg, recs in recs_by_wg.items():
         for d in range(len(prog.deps)):
@@ -65,7 +67,7 @@ def compare_log_with_oracle(prog, plan, logs, recs_by_wg, mode):
 def compare_wave_logs_with_oracle(prog, plan, logs, recs_by_wg, mode):
     """Multi-wave engines: every wave of the consumer's engine logs the same
     waits, each equal to the oracle's threshold, observed never below it."""
-    key = "sem_thr" if mode == "barrier_free" else "barrier_thr"
+    key = {"barrier_free": "sem_thr", "barrier": "barrier_thr", "per_instr": "count_thr"}[mode]
     engine_waves = {}
     w = 0
     for e, n in enumerate(plan.waves_per_engine):

@@ -13,7 +13,8 @@ import pytest
 torch = pytest.importorskip("torch")
 
 from oracle import core, mathref  # noqa: E402
-from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
+from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER, MODE_BARRIER_FREE,  # noqa: E402
+                                  BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import attn_program, attn_worklist  # noqa: E402
 from workloads.tensors import attn_inputs, bf16_to_f32  # noqa: E402
@@ -40,9 +41,9 @@ def _dev16(bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
 
 
-def run_attn(ai, heads, mode, cap=0, nk=3, nv=2):
+def run_attn(ai, heads, mode, cap=0, nk=3, nv=2, alloc=ALLOC_PER_LOOP):
     prog = attn_program(heads, nk=nk, nv=nv)
-    plan = Plan(prog, mode)
+    plan = Plan(prog, mode, alloc)
     wl = attn_worklist(ai.lengths, heads)
     trips, toff = trip_tensors(wl.trips)
     work = torch.from_numpy(wl.work.reshape(-1)).cuda()
@@ -89,6 +90,22 @@ def test_attn_small_parity_and_thresholds(rings):
         assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
         outs[name] = out
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_attn_per_instr():
+    """One counter per producer instruction (Eq. 3): thresholds equal the
+    Eq. 1 counts for every wave, values as with per-loop counters."""
+    heads = 2
+    ai = attn_inputs(seed=4, heads=heads, lengths=SMALL)
+    _say("[attn-per-instr]")
+    prog, plan, wl, out, logw = run_attn(ai, heads, MODE_BARRIER_FREE, cap=64, alloc=ALLOC_PER_INSTR)
+    check_close(out, mathref.attention(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE))
+    trips, off = wl.trips.flat()
+    recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
+    logs = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
+    assert compare_wave_logs_with_oracle(prog, plan, logs, recs, "per_instr") > 0
+    _, _, _, out2, _ = run_attn(ai, heads, MODE_BARRIER_FREE)
+    assert np.array_equal(out.view(np.uint32), out2.view(np.uint32))
 
 
 def test_attn_special_cases():

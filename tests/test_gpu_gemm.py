@@ -12,7 +12,8 @@ import pytest
 torch = pytest.importorskip("torch")
 
 from oracle import core, mathref  # noqa: E402
-from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
+from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER, MODE_BARRIER_FREE,  # noqa: E402
+                                  BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import gemm_program, gemm_trips  # noqa: E402
 from workloads.tensors import bf16_to_f32, gemm_inputs  # noqa: E402
@@ -38,9 +39,9 @@ def _bits_to_dev(bits):
     return torch.from_numpy(bits.view(np.int16)).cuda()
 
 
-def run_gemm(gi, m, n, k, mode, cap=0):
+def run_gemm(gi, m, n, k, mode, cap=0, alloc=ALLOC_PER_LOOP):
     prog = gemm_program(m, n, k)
-    plan = Plan(prog, mode)
+    plan = Plan(prog, mode, alloc)
     tt = gemm_trips(m, n, k)
     trips, toff = trip_tensors(tt)
     a, bt = _bits_to_dev(gi.a), _bits_to_dev(gi.bt)
@@ -62,6 +63,22 @@ def check_close(got, ref):
     assert np.isfinite(got).all()
     assert err.max() <= RTOL, (err.max(), np.unravel_index(err.argmax(), err.shape))
     return err.max()
+
+
+def test_gemm_per_instr():
+    """One counter per producer instruction (Eq. 3): thresholds equal the
+    Eq. 1 counts for every wave, values as with per-loop counters."""
+    m, n, k = 512, 512, 256
+    gi = gemm_inputs(seed=2, m=m, n=n, k=k)
+    _say("[gemm-per-instr]")
+    prog, plan, tt, out, logw = run_gemm(gi, m, n, k, MODE_BARRIER_FREE, cap=512, alloc=ALLOC_PER_INSTR)
+    check_close(out, mathref.gemm_bias_gelu(gi.a, gi.bt, gi.bias))
+    trips, off = tt.flat()
+    recs = {g: core.run(prog, trips, off[g], g).recs for g in range(tt.n_wg)}
+    logs = log_records(plan, logw, tt.n_wg, 512, per_wave=True)
+    assert compare_wave_logs_with_oracle(prog, plan, logs, recs, "per_instr") > 0
+    _, _, _, out2, _ = run_gemm(gi, m, n, k, MODE_BARRIER_FREE)
+    assert np.array_equal(out.view(np.uint32), out2.view(np.uint32))
 
 
 @pytest.mark.parametrize("shape", [(512, 512, 256), (256, 768, 96)])

@@ -14,7 +14,8 @@ import pytest
 torch = pytest.importorskip("torch")
 
 from oracle import core, mathref  # noqa: E402
-from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
+from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER, MODE_BARRIER_FREE,  # noqa: E402
+                                  BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import moe_program, moe_worklist  # noqa: E402
 from workloads.tensors import bf16_to_f32, moe_inputs, moe_weights_all  # noqa: E402
@@ -65,10 +66,10 @@ class MoeRun:
             return [work, self.perm, self.eoff, self.x, self.wg, self.wu, self.h]
         return [work, self.perm, self.eoff, self.h, self.wd, self.y]
 
-    def run(self, mode, cap=0):
+    def run(self, mode, cap=0, alloc=ALLOC_PER_LOOP):
         logs = {}
         for ph in (1, 2):
-            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn), mode)
+            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn), mode, alloc)
             work, trips, toff, n_wg = self.dev_wl[ph]
             log = None
             if cap:
@@ -119,6 +120,26 @@ def test_moe_small_parity_and_thresholds():
             assert compare_wave_logs_with_oracle(prog, plan, lg, recs, name) > 0
         outs[name] = y
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_moe_per_instr():
+    """One counter per producer instruction (Eq. 3): thresholds equal the
+    Eq. 1 counts for every wave, values as with per-loop counters."""
+    moe = moe_inputs(seed=3, hidden=256, ffn=256, counts=SMALL_COUNTS)
+    r = MoeRun(moe, mchunk=2)
+    _say("[moe-per-instr]")
+    h, y, logs = r.run(MODE_BARRIER_FREE, cap=64, alloc=ALLOC_PER_INSTR)
+    check_close(y, mathref.moe_tokens(moe, range(len(moe.assign))))
+    for ph in (1, 2):
+        plan, logw = logs[ph]
+        prog = moe_program(ph, moe.hidden, moe.ffn)
+        wl = r.wl[ph]
+        trips, off = wl.trips.flat()
+        recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
+        lg = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
+        assert compare_wave_logs_with_oracle(prog, plan, lg, recs, "per_instr") > 0
+    _, y2, _ = r.run(MODE_BARRIER_FREE)
+    assert np.array_equal(y.view(np.uint32), y2.view(np.uint32))
 
 
 def test_moe_full_size_sampled():

@@ -12,7 +12,8 @@ import pytest
 torch = pytest.importorskip("torch")
 
 from oracle import core  # noqa: E402
-from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
+from paper_2608_13757_amd import (ALLOC_PER_INSTR, MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan,  # noqa: E402
+                                  bfs)
 from tests.gpu_util import compare_log_with_oracle, dev, log_records, trip_tensors  # noqa: E402
 from workloads import chain_workload, random_nest, stream_program, stream_workload  # noqa: E402
 
@@ -108,6 +109,63 @@ def test_random_nests_interp_thresholds():
             logs = log_records(plan, log.cpu().numpy().view(np.uint32), 1, cap)
             checked += compare_log_with_oracle(prog, plan, logs, {0: res.recs}, name)
     assert checked == expected and checked > 500
+
+
+# ---------------------------------------------------------------------------
+# per-instruction allocation (Section 5.4, Eq. 3): one counter per producer
+# instruction, thresholds equal to the Eq. 1 counts
+# ---------------------------------------------------------------------------
+def test_random_nests_interp_thresholds_per_instr():
+    checked = expected = 0
+    for seed in range(150):
+        prog, tt = random_nest(seed, max_trip=4 if seed % 2 else 3)
+        prog.deps = _allocatable(prog)
+        if not prog.deps:
+            continue
+        trips, off = tt.flat()
+        res = core.run(prog, trips, off[0], 0)
+        plan = Plan(prog, MODE_BARRIER_FREE, ALLOC_PER_INSTR)
+        expected += len(res.recs)
+        t_trips, t_off = trip_tensors(tt)
+        base = torch.zeros(1, dtype=torch.int64, device="cuda")
+        x = torch.zeros(64, dtype=torch.float32, device="cuda")
+        out = torch.zeros(64, dtype=torch.float32, device="cuda")
+        cap = 256
+        log = torch.zeros(plan.debug_log_words(1, cap), dtype=torch.int32, device="cuda")
+        plan.run([base, x, out], t_trips, t_off, 1, debug_log=log, debug_capacity=cap)
+        plan.status()
+        logs = log_records(plan, log.cpu().numpy().view(np.uint32), 1, cap)
+        checked += compare_log_with_oracle(prog, plan, logs, {0: res.recs}, "per_instr")
+    assert checked == expected and checked > 500
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_chain_interp_per_instr(seed):
+    _say(f"[chain-per-instr] seed={seed}")
+    w = chain_workload(seed)
+    trips, off = w.trips.flat()
+    res = core.run(w.prog, trips, off[0], 0, w.base, w.x, 256)
+    plan = Plan(w.prog, MODE_BARRIER_FREE, ALLOC_PER_INSTR)
+    out, logw = _run_tile_machine(w, plan, 256, cap=512)
+    assert np.abs(out - res.out).max() <= 1e-5
+    assert compare_log_with_oracle(w.prog, plan, log_records(plan, logw, 1, 512), {0: res.recs}, "per_instr") > 0
+
+
+@pytest.mark.parametrize("layout", ["inplace", "two_rings"])
+def test_stream_per_instr(layout):
+    """Thresholds of every wait logged on a few workgroups, and the values of
+    an uninstrumented launch (the batched engines)."""
+    w = stream_workload(seed=7, n_wg=6, outer=12, layout=layout, inner_war=True)
+    trips, off = w.trips.flat()
+    recs = {g: core.run(w.prog, trips, off[g], g).recs for g in range(w.trips.n_wg)}
+    plan = Plan(w.prog, MODE_BARRIER_FREE, ALLOC_PER_INSTR)
+    _say(f"[stream-per-instr] {layout} log")
+    out, logw = _run_tile_machine(w, plan, w.n_tiles * 64, cap=4096)
+    assert np.array_equal(out, w.x.reshape(-1) + np.float32(1.0))
+    assert compare_log_with_oracle(w.prog, plan, log_records(plan, logw, w.trips.n_wg, 4096), recs, "per_instr") > 0
+    _say(f"[stream-per-instr] {layout} values")
+    out, _ = _run_tile_machine(w, plan, w.n_tiles * 64)
+    assert np.array_equal(out, w.x.reshape(-1) + np.float32(1.0))
 
 
 # ---------------------------------------------------------------------------
