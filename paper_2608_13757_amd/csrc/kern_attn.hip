@@ -10,7 +10,7 @@
 //                          base-2 domain: running max m, rescale factor
 //                          alpha = 2^(m_old - m_new), P = 2^(S c - m_new)
 //                          written as bf16 over S in place, running sum l.
-//   E3 (2 waves, MFMA)     PV: O = alpha O + P V for 64 query rows per wave
+//   E3 (4 waves, MFMA)     PV: O = alpha O + P V for 32 query rows per wave
 //                          (fp32 accumulators), then NORM: O / l to HBM.
 //   E4 (1 wave, V load)    LOADV: the V block into a V ring slot.
 //
@@ -45,7 +45,7 @@
 // Family contract (BFS_KERNEL_ATTN): loop KV below the top level holding
 // LOADK (E0, opcode 32, args [0, K ring depth, heads, 128]), LOADV (E4,
 // opcode 32, args [1, V ring depth, heads, 128]), QK (E1, 33), SM (E2, 34),
-// PV (E3, 35); NORM (E3, 36) at the top level; waves per engine 1, 2, 4, 2,
+// PV (E3, 35); NORM (E3, 36) at the top level; waves per engine 1, 2, 4, 4,
 // 1; the dependencies listed above.  Buffers: [0] work list int32 [n_wg][4]
 // = (first token of the sequence, length L, first query row of the tile,
 // head), [1] Q, [2] K, [3] V, [4] O, each bf16 [tokens][heads][128].  Trip
@@ -59,7 +59,7 @@ using namespace bfsdev;
 namespace {
 
 constexpr int kD = 128, kBQ = 128, kBKV = 64;
-constexpr int kWaves = 10;
+constexpr int kWaves = 12;
 constexpr uint32_t kKVSlot = kBKV * kD * 2;      // 16 KiB
 constexpr uint32_t kSPSlot = kBQ * kBKV * 4;     // 32 KiB
 constexpr int kMaxPend = 3;                      // load groups in flight per load wave
@@ -100,7 +100,7 @@ __device__ __forceinline__ f32x2 pair32(float x) {
 }
 
 template <int kMode, bool kInstr>
-__global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
+__global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
   const uint32_t kring = lds_addr(lds) + kCntBytes;
@@ -114,14 +114,16 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
   const int hw = wave_id();
   const uint32_t lane = lane_id(), l32 = lane & 31u, lhi = lane >> 5;
   const int wg = blockIdx.x;
-  // hardware wave -> (engine, wave within the engine); the four MFMA waves
-  // come first so that they sit on four different SIMDs
+  // hardware wave -> (engine, wave within the engine), hardware wave w on
+  // SIMD w % 4: the two QK waves on SIMDs 0 and 1, the four PV waves two
+  // each on SIMDs 2 and 3 (equal MFMA work per SIMD), softmax on 0 and 1,
+  // the K and V loaders on 2 and 3
   int eng, ew, canon;                       // canon: engine-ordered wave index
   if (hw < 2) { eng = 1; ew = hw; canon = 1 + ew; }
-  else if (hw < 4) { eng = 3; ew = hw - 2; canon = 7 + ew; }
-  else if (hw < 8) { eng = 2; ew = hw - 4; canon = 3 + ew; }
-  else if (hw == 8) { eng = 0; ew = 0; canon = 0; }
-  else { eng = 4; ew = 0; canon = 9; }
+  else if (hw == 2 || hw == 3 || hw == 6 || hw == 7) { eng = 3; ew = (hw & 1) + ((hw >> 2) << 1); canon = 7 + ew; }
+  else if (hw == 4 || hw == 5 || hw == 8 || hw == 9) { eng = 2; ew = (hw & 1) + ((hw >> 3) << 1); canon = 3 + ew; }
+  else if (hw == 10) { eng = 0; ew = 0; canon = 0; }
+  else { eng = 4; ew = 0; canon = 11; }
   Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), canon, wg);
   const uint32_t own = S.word((uint32_t)eng, (uint32_t)ew);   // barrier mode: one counter per engine
 
@@ -242,15 +244,26 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
         for (int a = 0; a < 2; ++a)
 #pragma unroll
           for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+        // the K fragments of each 16-wide slice of d are read one slice
+        // ahead of the MFMAs that use them
+        bf16x8 k0 = lds_frag(kb_base + pos16(l32, lhi));
+        bf16x8 k1 = lds_frag(kb_base + pos16(32u + l32, lhi));
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
-          const bf16x8 k0 = lds_frag(kb_base + pos16(l32, 2u * s + lhi));
-          const bf16x8 k1 = lds_frag(kb_base + pos16(32u + l32, 2u * s + lhi));
+          bf16x8 n0 = k0, n1 = k1;
+          if (s < 7) {
+            n0 = lds_frag(kb_base + pos16(l32, 2u * (s + 1) + lhi));
+            n1 = lds_frag(kb_base + pos16(32u + l32, 2u * (s + 1) + lhi));
+          }
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb) {
             acc[qb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[qb][s], acc[qb][0], 0, 0, 0);
             acc[qb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[qb][s], acc[qb][1], 0, 0, 0);
           }
+          if (s < 7) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+          k0 = n0;
+          k1 = n1;
         }
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
@@ -330,12 +343,10 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
     }
   } else {
     // --------------------------------------------------- PV engine and NORM
-    const uint32_t qr = 64u * ew;
-    f32x16 acc[2][4];
+    const uint32_t qr = 32u * ew;
+    f32x16 acc[4];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a][b] = f32x16{};
+    for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
     // transposing V reads: lane l addresses row 8 (l / 32) + (l % 16) / 4 (+ 16 ks + 4 hh)
     // and columns 32 db + 16 ((l / 16) % 2) + 4 (l % 4) .. + 3
     const uint32_t x = (lane >> 2) & 3u;
@@ -355,26 +366,37 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
       if (!S.aborted) {
         const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
         const uint32_t vb = vring + vslot * kKVSlot;
+        auto vfrag = [&](int ks, int db) {
+          const uint32_t va = vb + 16u * (uint32_t)ks * 256u + voff[db];
+          const bf16x4 lo = lds_tr(va), hi = lds_tr(va + 4u * 256u);
+          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        };
+        // the first fragments are read before the rescale so that their
+        // latency overlaps it
+        bf16x8 pf = lds_frag(sp + pos16(qr + l32, lhi));
+        bf16x8 vf = vfrag(0, 0);
+        const float a = *(const BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + qr + l32) * 4u);
+        // a block whose rows all keep their running maximum needs no rescale
+        if (__builtin_amdgcn_ballot_w64(a != 1.0f) != 0) {
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const float a = *(const BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + qr + 32u * qb + l32) * 4u);
-#pragma unroll
-          for (int db = 0; db < 4; ++db) acc[qb][db] *= a;
+          for (int db = 0; db < 4; ++db) acc[db] *= a;
         }
+        // each V fragment is read one MFMA ahead of its use
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-          bf16x8 pf[2];
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) pf[qb] = lds_frag(sp + pos16(qr + 32u * qb + l32, 2u * ks + lhi));
+          bf16x8 pf_next = pf;
+          if (ks < 3) pf_next = lds_frag(sp + pos16(qr + l32, 2u * (uint32_t)(ks + 1) + lhi));
 #pragma unroll
           for (int db = 0; db < 4; ++db) {
-            const uint32_t va = vb + 16u * ks * 256u + voff[db];
-            const bf16x4 lo = lds_tr(va), hi = lds_tr(va + 4u * 256u);
-            const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
-              acc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb], acc[qb][db], 0, 0, 0);
+            bf16x8 vf_next = vf;
+            if (db < 3) vf_next = vfrag(ks, db + 1);
+            else if (ks < 3) vf_next = vfrag(ks + 1, 0);
+            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[db], 0, 0, 0);
+            if (db < 3 || ks < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            vf = vf_next;
           }
+          pf = pf_next;
         }
       }
       S.signal(P.pv.update, (uint32_t)ew);
@@ -386,25 +408,22 @@ __global__ void __launch_bounds__(640) attn_kernel(AttnParams P) {
     S.enter(s_norm, P.norm, g, 0);
     S.wait(s_norm, P.norm, g, 1, 0, [] {});
     if (!S.aborted) {
+      const uint32_t rloc = qr + l32;
+      const int32_t row = q0 + (int32_t)rloc;
+      const float lr = *(const BFS_LDS float *)(uintptr_t)(lsum_l + rloc * 4u);
+      const float inv = 1.0f / lr;
+      if (row < L) {
+        __bf16 *dst = P.o + (size_t)(s0 + row) * row_stride + (size_t)head * kD;
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        const uint32_t rloc = qr + 32u * qb + l32;
-        const int32_t row = q0 + (int32_t)rloc;
-        const float lr = *(const BFS_LDS float *)(uintptr_t)(lsum_l + rloc * 4u);
-        const float inv = 1.0f / lr;
-        if (row < L) {
-          __bf16 *dst = P.o + (size_t)(s0 + row) * row_stride + (size_t)head * kD;
+        for (int db = 0; db < 4; ++db)
 #pragma unroll
-          for (int db = 0; db < 4; ++db)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const f32x2 a01 = {acc[qb][db][4 * j] * inv, acc[qb][db][4 * j + 1] * inv};
-              const f32x2 a23 = {acc[qb][db][4 * j + 2] * inv, acc[qb][db][4 * j + 3] * inv};
-              const u32x2 v = {__builtin_bit_cast(uint32_t, __builtin_convertvector(a01, bf16x2)),
-                               __builtin_bit_cast(uint32_t, __builtin_convertvector(a23, bf16x2))};
-              __builtin_nontemporal_store(v, reinterpret_cast<u32x2 *>(dst + 32 * db + 8 * j + 4 * lhi));
-            }
-        }
+          for (int j = 0; j < 4; ++j) {
+            const f32x2 a01 = {acc[db][4 * j] * inv, acc[db][4 * j + 1] * inv};
+            const f32x2 a23 = {acc[db][4 * j + 2] * inv, acc[db][4 * j + 3] * inv};
+            const u32x2 v = {__builtin_bit_cast(uint32_t, __builtin_convertvector(a01, bf16x2)),
+                             __builtin_bit_cast(uint32_t, __builtin_convertvector(a23, bf16x2))};
+            __builtin_nontemporal_store(v, reinterpret_cast<u32x2 *>(dst + 32 * db + 8 * j + 4 * lhi));
+          }
       }
     }
   }
@@ -420,10 +439,10 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
                        const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream, uint32_t *dbg,
                        int64_t dbg_cap, const bfs_run_opts &o) {
   if (p->n_loops != 2 || p->loop_parent[1] != 0) return fail(BFS_E_UNSUPPORTED, "attn: loops must be top -> KV");
-  const int want_w[5] = {1, 2, 4, 2, 1};
+  const int want_w[5] = {1, 2, 4, 4, 1};
   if (p->n_engines != 5) return fail(BFS_E_UNSUPPORTED, "attn: five engines");
   for (int e = 0; e < 5; ++e)
-    if (p->waves_per_engine[e] != want_w[e]) return fail(BFS_E_UNSUPPORTED, "attn: engines of 1, 2, 4, 2, 1 waves");
+    if (p->waves_per_engine[e] != want_w[e]) return fail(BFS_E_UNSUPPORTED, "attn: engines of 1, 2, 4, 4, 1 waves");
   int lk = -1, lv = -1, qk = -1, sm = -1, pv = -1, nm = -1;
   for (size_t i = 0; i < p->instr_engine.size(); ++i) {
     const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];

@@ -379,7 +379,7 @@ def attn_program(heads: int, dim: int = ATTN_D, nk: int = 3, nv: int = 2) -> Pro
     QK->LOADK (k=nk) and PV->LOADV (k=nv) free ring slots; PV->QK (k=2) frees
     an S/P slot; SM->NORM (k=0, producer nested in KV) delivers the final row
     sums."""
-    b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 4, 2, 1])
+    b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 4, 4, 1])
     with b.loop("KV"):
         b.instr(0, OP_ATTN_LOAD, [0, nk, heads, dim, 0, 0, 0, 0], name="LOADK")
         b.instr(4, OP_ATTN_LOAD, [1, nv, heads, dim, 0, 0, 0, 0], name="LOADV")
