@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--n-gen", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--modes", default="barrier_free,barrier")
+    ap.add_argument("--k-unroll", type=int, default=0, choices=[0, 1, 2, 4, 8],
+                    help="GEMM: K steps per copy of the loop bodies (static-trip unrolling)")
     ap.add_argument("--alloc", default="per_loop", choices=["per_loop", "per_instr"],
                     help="counter allocation of the barrier-free plans (Eq. 5 per loop and engine, "
                          "or Eq. 3 one counter per producer instruction)")
@@ -58,11 +60,11 @@ def alloc_of(a, mode):
     return ALLOC_PER_INSTR if a.alloc == "per_instr" else ALLOC_PER_LOOP
 
 
-def time_mode(plan, bufs, trips, toff, n_wg, steps, warmup):
+def time_mode(plan, bufs, trips, toff, n_wg, steps, warmup, **run_kw):
     import torch
     stream = torch.cuda.current_stream()
     for _ in range(warmup):
-        plan.run(bufs, trips, toff, n_wg, stream=stream)
+        plan.run(bufs, trips, toff, n_wg, stream=stream, **run_kw)
     plan.status(stream)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
@@ -70,7 +72,7 @@ def time_mode(plan, bufs, trips, toff, n_wg, steps, warmup):
     t0 = time.perf_counter()
     for i in range(steps):
         starts[i].record(stream)
-        plan.run(bufs, trips, toff, n_wg, stream=stream)
+        plan.run(bufs, trips, toff, n_wg, stream=stream, **run_kw)
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -148,7 +150,8 @@ def bench_gemm(a):
     for name in a.modes.split(","):
         mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
         plan = Plan(gemm_program(m, n, k), mode, alloc_of(a, mode))
-        res[name] = time_mode(plan, [A, Bt, bias, C], trips, toff, tt.n_wg, a.steps, a.warmup)
+        res[name] = time_mode(plan, [A, Bt, bias, C], trips, toff, tt.n_wg, a.steps, a.warmup,
+                              k_unroll=a.k_unroll)
     flop = 2.0 * m * n * k
     bf = res.get("barrier_free", next(iter(res.values())))
     ms = bf["ms_mean"]
@@ -173,7 +176,7 @@ def bench_gemm(a):
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "GEMM + bias + GELU, A, B bf16 4096 x 4096 ~ N(0,1)/64, 256 x 256 tiles, "
                                f"K steps of {GEMM_BK} through a {GEMM_RING}-slot LDS ring", "m": m, "n": n, "k": k,
-                   "parallelism": "single GPU"},
+                   "k_unroll": a.k_unroll or 1, "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None},

@@ -162,6 +162,13 @@ typedef struct {
                                     workgroup), in 100 MHz ticks: [0] wave run time, [1] time
                                     blocked in waits, [2] blocked waits, [3] time in barriers,
                                     [4] time waiting for own loads to land, [5] polls, [6-7] 0 */
+  int32_t k_unroll;              /* GEMM family: iterations of the static-trip K loop per
+                                    loop-body copy in uninstrumented launches (0 or 1: none,
+                                    2, 4, 8; unrolled bodies see their thresholds as fixed
+                                    offsets of one loop-invariant value, the code-size versus
+                                    regOp trade-off of static loops); other families ignore it.
+                                    Other values: BFS_E_INVALID */
+  int32_t reserved;              /* must be 0 */
 } bfs_run_opts;
 
 /*

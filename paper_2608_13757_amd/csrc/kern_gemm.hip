@@ -87,7 +87,10 @@ __device__ __forceinline__ uint32_t swz(uint32_t row, uint32_t chunk) {
   return row * 64u + ((chunk ^ ((row >> 2) & 3u)) << 4);
 }
 
-template <int kMode, bool kInstr>
+// kUnroll: K steps per copy of the load and MFMA loop bodies (the trip of
+// loop K is static, so an unrolled body sees its thresholds as fixed offsets
+// of one value per copy); a remainder of trip_k % kUnroll steps runs singly.
+template <int kMode, bool kInstr, int kUnroll>
 __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
@@ -166,7 +169,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
 #pragma unroll
     for (int j = 0; j < 16; ++j) voff[j] = ((16u * j + r_in) * (uint32_t)P.k + 8u * chunk) * 2u;
     uint32_t slot = 0;
-    for (uint32_t it = 0; it < trip_k; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
+    auto load_step = [&](uint32_t it) __attribute__((always_inline)) {
       g.r1 += 1;
       g.h1 = it + 1;
       S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
@@ -187,7 +190,14 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
         retire_all();
         S.sync_point(S.word(0, ew));                        // end of a K iteration
       }
+      slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1;
+    };
+    uint32_t it = 0;
+    for (; it + kUnroll <= trip_k; it += kUnroll) {
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) load_step(it + u);
     }
+    for (; it < trip_k; ++it) load_step(it);
     retire_all();
     k_end = S.elapsed();
     S.sync_point(S.word(0, ew));                            // before loop C
@@ -209,7 +219,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     S.enter(s_mma, P.mma, g, 1);
     const uint32_t l32 = lane & 31u, lhi = lane >> 5;
     uint32_t slot = 0;
-    for (uint32_t it = 0; it < trip_k; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
+    auto mma_step = [&](uint32_t it) __attribute__((always_inline)) {
       g.r1 += 1;
       g.h1 = it + 1;
       S.wait(s_mma, P.mma, g, it + 1, g.r1 - 1, [] {});
@@ -247,7 +257,14 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       }
       S.signal(P.mma.update, ew);
       S.sync_point(S.word(1, ew));                          // end of a K iteration (barrier mode)
+      slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1;
+    };
+    uint32_t it = 0;
+    for (; it + kUnroll <= trip_k; it += kUnroll) {
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) mma_step(it + u);
     }
+    for (; it < trip_k; ++it) mma_step(it);
     k_end = S.elapsed();
     S.sync_point(S.word(1, ew));                            // before loop C
     S.enter(s_spill, P.spill, g, 2);
@@ -395,8 +412,24 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
     if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("gemm launch: ") + hipGetErrorString(e));
     return BFS_OK;
   };
-  if (p->mode == BFS_MODE_BARRIER) return instr ? go(gemm_kernel<BFS_MODE_BARRIER, true>) : go(gemm_kernel<BFS_MODE_BARRIER, false>);
-  return instr ? go(gemm_kernel<BFS_MODE_BARRIER_FREE, true>) : go(gemm_kernel<BFS_MODE_BARRIER_FREE, false>);
+  // instrumented launches (debug log, statistics, injected faults) keep the
+  // loop bodies single
+  if (p->mode == BFS_MODE_BARRIER) {
+    if (instr) return go(gemm_kernel<BFS_MODE_BARRIER, true, 1>);
+    switch (o.k_unroll) {
+      case 2: return go(gemm_kernel<BFS_MODE_BARRIER, false, 2>);
+      case 4: return go(gemm_kernel<BFS_MODE_BARRIER, false, 4>);
+      case 8: return go(gemm_kernel<BFS_MODE_BARRIER, false, 8>);
+      default: return go(gemm_kernel<BFS_MODE_BARRIER, false, 1>);
+    }
+  }
+  if (instr) return go(gemm_kernel<BFS_MODE_BARRIER_FREE, true, 1>);
+  switch (o.k_unroll) {
+    case 2: return go(gemm_kernel<BFS_MODE_BARRIER_FREE, false, 2>);
+    case 4: return go(gemm_kernel<BFS_MODE_BARRIER_FREE, false, 4>);
+    case 8: return go(gemm_kernel<BFS_MODE_BARRIER_FREE, false, 8>);
+    default: return go(gemm_kernel<BFS_MODE_BARRIER_FREE, false, 1>);
+  }
 }
 
 }  // namespace bfs

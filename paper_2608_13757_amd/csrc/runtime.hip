@@ -142,11 +142,15 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
   o.fault_dep = -1;
   o.fault_delta = 0;
   o.dev_stats = nullptr;
+  o.k_unroll = 1;
   if (opts) {
     if (opts->watchdog_polls) o.watchdog_polls = opts->watchdog_polls;
     o.fault_dep = opts->fault_dep;
     o.fault_delta = opts->fault_delta;
     o.dev_stats = opts->dev_stats;
+    if (opts->k_unroll > 1) o.k_unroll = opts->k_unroll;
+    if (opts->k_unroll < 0 || (o.k_unroll != 1 && o.k_unroll != 2 && o.k_unroll != 4 && o.k_unroll != 8))
+      return fail(BFS_E_INVALID, "k_unroll must be 0, 1, 2, 4 or 8");
   }
   DevImage *img = nullptr;
   bfs_status st = device_image(plan, &img);

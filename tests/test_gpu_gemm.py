@@ -65,6 +65,44 @@ def check_close(got, ref):
     return err.max()
 
 
+@pytest.mark.parametrize("shape", [(512, 512, 256), (256, 768, 96)])
+def test_gemm_k_unroll(shape):
+    """K-loop bodies unrolled 2, 4 and 8 times (a remainder of single steps
+    when the trip is not a multiple): bit-identical to the single bodies, in
+    both modes."""
+    m, n, k = shape
+    gi = gemm_inputs(seed=3, m=m, n=n, k=k)
+    prog = gemm_program(m, n, k)
+    tt = gemm_trips(m, n, k)
+    trips, toff = trip_tensors(tt)
+    a, bt = _bits_to_dev(gi.a), _bits_to_dev(gi.bt)
+    bias = torch.from_numpy(gi.bias).cuda()
+    for name, mode in MODES:
+        plan = Plan(prog, mode)
+        outs = {}
+        for u in (1, 2, 4, 8):
+            _say(f"[gemm-unroll] {shape} mode={name} k_unroll={u}")
+            c = torch.full((m * n,), -1, dtype=torch.int16, device="cuda")
+            plan.run([a, bt, bias, c], trips, toff, tt.n_wg, k_unroll=u)
+            plan.status()
+            outs[u] = c.cpu().numpy()
+        for u in (2, 4, 8):
+            assert np.array_equal(outs[u], outs[1]), (name, u)
+    check_close(bf16_to_f32(outs[1].view(np.uint16)).reshape(m, n), mathref.gemm_bias_gelu(gi.a, gi.bt, gi.bias))
+
+
+def test_gemm_k_unroll_rejects_other_factors():
+    m, n, k = 256, 256, 64
+    prog = gemm_program(m, n, k)
+    plan = Plan(prog)
+    tt = gemm_trips(m, n, k)
+    trips, toff = trip_tensors(tt)
+    t = torch.zeros(m * k, dtype=torch.int16, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t, t, torch.zeros(n, device="cuda"), t], trips, toff, tt.n_wg, k_unroll=3)
+    assert e.value.status == bfs.E_INVALID
+
+
 def test_gemm_per_instr():
     """One counter per producer instruction (Eq. 3): thresholds equal the
     Eq. 1 counts for every wave, values as with per-loop counters."""
