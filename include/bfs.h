@@ -62,6 +62,21 @@ typedef enum {
 
 typedef enum { BFS_MODE_BARRIER_FREE = 0, BFS_MODE_BARRIER = 1 } bfs_mode;
 
+/* Flags of bfs_plan_create.
+ *
+ * BFS_PLAN_BARRIER_FALLBACK: a dependency outside the allocatable cases of
+ * Section 5.2 (a producer nested below the shared loop S with an offset other
+ * than 0 forward or 1 backward) is kept instead of failing with
+ * BFS_E_NOT_ALLOCATABLE and falls back to the barrier scheme, as Section 5.2
+ * prescribes: every engine drains its in-flight instructions and meets the
+ * others at the end of every iteration of S (no counter is reset, so the
+ * monotone semaphores of the other dependencies stay valid).  Such a
+ * dependency gets no counter and no wait.  When S is the top-level loop the
+ * dependency is never owed (its single iteration has rhat_S = 1 <= k) and no
+ * barrier is placed.  Only the interpreter family executes these barriers;
+ * bfs_run of another family's plan that has one returns BFS_E_UNSUPPORTED. */
+#define BFS_PLAN_BARRIER_FALLBACK 1u
+
 /* Semaphore granularity (Section 5.4 per-instruction, Section 5.5 per-loop). */
 typedef enum { BFS_ALLOC_PER_LOOP = 0, BFS_ALLOC_PER_INSTR = 1 } bfs_alloc;
 
@@ -123,7 +138,9 @@ typedef struct {
 /* One dependency's barrier-free wait (Eq. 5). */
 typedef struct {
   int32_t dep;
-  int32_t kase;          /* 1 = C1 (P == S), 2 = C2 (nested, forward), 3 = C3 (nested, backward) */
+  int32_t kase;          /* 1 = C1 (P == S), 2 = C2 (nested, forward), 3 = C3 (nested, backward),
+                            4 = barrier fallback (BFS_PLAN_BARRIER_FALLBACK; counter -1, no wait,
+                            ordered by the barriers at the end of every iteration of loop_S) */
   int32_t loop_S;        /* innermost loop enclosing producer and consumer */
   int32_t loop_P;        /* producer's parent loop */
   int32_t k;             /* offset on S */
@@ -150,7 +167,9 @@ typedef struct {
   int32_t regs_per_engine;       /* loop registers r, rhat plus the wait register */
   int32_t salu_ops_per_wait;     /* 5 per-loop, 3 per-instruction, 0 barrier */
   int32_t n_waits;               /* waits emitted */
-  int32_t n_sync_points;         /* barrier mode: loop statements + iteration ends in the tree */
+  int32_t n_sync_points;         /* barrier mode: loop statements + iteration ends in the tree;
+                                    barrier-free: loops whose iteration ends carry a fallback barrier */
+  int32_t n_fallback;            /* dependencies handled by the barrier fallback */
 } bfs_stats;
 
 /* Options of one launch; NULL selects the defaults. */
@@ -175,10 +194,11 @@ typedef struct {
  * Plan the synchronization of prog (Sections 5.2-5.5, or Section 3.4 in
  * barrier mode).  Validates the tree, classifies every dependency, assigns
  * counter slots and computes N, K and the barrier ordinals.  Host only; needs
- * no GPU.  flags must be 0.
+ * no GPU.  flags: 0 or BFS_PLAN_BARRIER_FALLBACK (other bits: BFS_E_INVALID).
  * Errors: BFS_E_INVALID, BFS_E_ORDER (offset 0 with the producer not before
  * the consumer, or a nested backward producer at offset 0),
- * BFS_E_NOT_ALLOCATABLE (nested producer with another offset), BFS_E_RESOURCE.
+ * BFS_E_NOT_ALLOCATABLE (nested producer with another offset, without
+ * BFS_PLAN_BARRIER_FALLBACK), BFS_E_RESOURCE.
  */
 bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc alloc, uint32_t flags,
                            bfs_plan **out);
@@ -196,7 +216,8 @@ bfs_status bfs_plan_stats(const bfs_plan *plan, bfs_stats *out);
  * Host evaluation of dependency dep's threshold for the consumer engine's
  * registers r_P (entries of the producer's parent loop) and rhat_S (entries of
  * the shared loop in its current trip): Eq. 5 in barrier-free mode, the static
- * ordinal (or 0) in barrier mode.  This is the value the device computes.
+ * ordinal (or 0) in barrier mode, 0 for a barrier-fallback dependency.  This
+ * is the value the device computes.
  */
 bfs_status bfs_eval_threshold(const bfs_plan *plan, int32_t dep, uint32_t r_P, uint32_t rhat_S,
                               uint32_t *out);
@@ -223,6 +244,8 @@ void bfs_plan_destroy(bfs_plan *plan);
  *   opts         NULL for defaults.
  * The first launch of a plan on a device uploads its tables (one allocation
  * per plan and device).  Device-side deadlock is reported by bfs_run_status.
+ * BFS_E_UNSUPPORTED: a barrier-free plan with barrier-fallback dependencies
+ * of a family other than the interpreter.
  */
 bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t n_buffers,
                    const int32_t *dev_trips, const int64_t *dev_trip_off, int32_t n_wg,

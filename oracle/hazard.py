@@ -13,7 +13,9 @@ from the tile-machine semantics.  Happens-before is built from
     retirement brought the counter to that value, hence (in-order
     retirement) after everything earlier on that engine, and
   * in the barrier-based scheme, every barrier: everything before it happens
-    before everything after it (Section 3.4).
+    before everything after it (Section 3.4); in the barrier-free scheme with
+    the fallback of Section 5.2, the barrier at the end of every iteration of
+    each loop in ``barrier_loops``.
 
 A conflicting pair of accesses (same location, at least one write) on two
 different engines must be ordered.  The trace order is a topological order of
@@ -77,7 +79,15 @@ def _parents(prog):
     return par
 
 
-def check(prog, res, mode="barrier_free", thresholds=None):
+def _ancestors(prog, l):
+    out = {l}
+    while prog.loop_parent[l] >= 0:
+        l = prog.loop_parent[l]
+        out.add(l)
+    return out
+
+
+def check(prog, res, mode="barrier_free", thresholds=None, barrier_loops=()):
     """Return a list of unordered conflicting pairs (empty = covered).
 
     ``res`` is an ``oracle.core.OracleResult``.  ``thresholds`` optionally
@@ -108,9 +118,26 @@ def check(prog, res, mode="barrier_free", thresholds=None):
     region_join = np.zeros(E, np.int64)
     cur_region = inst["region"][0] if n else 0
     region_members = []
+    # fallback barriers: an instance after the b-th barrier of loop S (b =
+    # completed iterations of S) follows every instance before it
+    fb = sorted(barrier_loops) if mode == "barrier_free" else []
+    anc = {i: _ancestors(prog, par[i]) for i in par}
+    fb_phase = {S: 0 for S in fb}
+    fb_join = {S: np.zeros(E, np.int64) for S in fb}
+    fb_members = {S: [] for S in fb}
     for x in range(n):
         ins_id = int(inst["instr"][x])
         e = int(inst["engine"][x])
+        fb_vc = np.zeros(E, np.int64)
+        for S in fb:
+            b = int(res.r_snap[x][S]) - (1 if S in anc[ins_id] else 0)
+            if b > fb_phase[S]:
+                for y in fb_members[S]:
+                    fb_join[S] = np.maximum(fb_join[S], vc[y])
+                fb_members[S] = []
+                fb_phase[S] = b
+            fb_vc = np.maximum(fb_vc, fb_join[S])
+            fb_members[S].append(x)
         if mode == "barrier" and inst["region"][x] != cur_region:
             # a barrier separates everything before from everything after
             for y in region_members:
@@ -120,6 +147,7 @@ def check(prog, res, mode="barrier_free", thresholds=None):
         base_vc = vc[last_on[e]].copy() if last_on[e] >= 0 else np.zeros(E, np.int64)
         if mode == "barrier":
             base_vc = np.maximum(base_vc, region_join)
+        base_vc = np.maximum(base_vc, fb_vc)
         k = exec_idx[ins_id]
         exec_idx[ins_id] += 1
         for dep, val in waits.get((ins_id, k), []):

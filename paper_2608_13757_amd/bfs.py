@@ -18,6 +18,8 @@ LIB_PATH = os.path.join(_HERE, "libbfs.so")
 OK, E_INVALID, E_ORDER, E_NOT_ALLOCATABLE, E_RESOURCE, E_DEVICE, E_DEADLOCK, E_UNSUPPORTED = range(8)
 MODE_BARRIER_FREE, MODE_BARRIER = 0, 1
 ALLOC_PER_LOOP, ALLOC_PER_INSTR = 0, 1
+PLAN_BARRIER_FALLBACK = 1
+KASE_FALLBACK = 4
 KERNELS = {"interp": 0, "stream3": 1, "gemm": 2, "attn": 3, "moe": 4}
 
 EXPORTED = ["bfs_plan_create", "bfs_plan_formulas", "bfs_plan_static_waits", "bfs_plan_stats",
@@ -54,7 +56,7 @@ class StaticWait(C.Structure):
 
 class Stats(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("n_counters", "regs_per_engine", "salu_ops_per_wait", "n_waits",
-                                          "n_sync_points")]
+                                          "n_sync_points", "n_fallback")]
 
 
 class RunOpts(C.Structure):
@@ -129,7 +131,9 @@ def _stream_handle(stream):
 class Plan:
     """A planned program (bfs_plan_create) with its owned C arrays."""
 
-    def __init__(self, program, mode=MODE_BARRIER_FREE, alloc=ALLOC_PER_LOOP):
+    def __init__(self, program, mode=MODE_BARRIER_FREE, alloc=ALLOC_PER_LOOP, fallback=False):
+        """fallback: keep dependencies outside the allocatable cases and order
+        them by barriers (BFS_PLAN_BARRIER_FALLBACK)."""
         f = program.flat() if hasattr(program, "flat") else program
         self._keep = [
             _i32(f["loop_parent"]), _i32(f["loop_is_cond"]), _i32(f["body_off"]), _i32(f["body_kind"] or [0]),
@@ -148,7 +152,8 @@ class Plan:
                               len(f["instr_engine"]), k[7].ctypes.data, k[8].ctypes.data, k[9].ctypes.data,
                               len(f["deps"]), k[10].ctypes.data, f["tile_elems"], rs, f["n_accs"])
         h = C.c_void_p()
-        _check(lib().bfs_plan_create(C.addressof(self._prog), mode, alloc, 0, C.byref(h)))
+        flags = PLAN_BARRIER_FALLBACK if fallback else 0
+        _check(lib().bfs_plan_create(C.addressof(self._prog), mode, alloc, flags, C.byref(h)))
         self.handle = h
         self.mode = mode
         self.alloc = alloc

@@ -92,6 +92,7 @@ struct bfs_plan {
   int32_t tile_elems;
   int32_t ring_slots[4];
   int32_t n_accs;
+  uint32_t flags = 0;                    // bfs_plan_create flags
 
   // derived structure
   std::vector<int32_t> instr_parent;     // innermost enclosing loop
@@ -101,6 +102,7 @@ struct bfs_plan {
   std::vector<bfs_static_wait> static_waits;
   std::vector<int32_t> instr_update;     // counter slot incremented at retirement (-1: none)
   int32_t n_counters = 0;
+  uint32_t fallback_loops = 0;           // bit l: drain barrier at the end of every iteration of loop l
   bfs_stats stats{};
   // per-instruction wait lists (dependency ids whose consumer is the instruction)
   std::vector<int32_t> instr_wait_off, instr_wait_list;

@@ -40,6 +40,7 @@ struct InterpParams {
   uint64_t watchdog;
   int32_t fault_dep, fault_delta;
   int32_t n_loops, n_engines, n_instrs, mode, tile;
+  uint32_t fallback_loops;      // bit l: drain barrier at the end of every iteration of loop l
   int32_t ring_off[4];          // float offsets in the ring area
   int32_t acc_off;
   int32_t lds_state_off, lds_exec_off, lds_data_off;   // byte offsets in dynamic LDS
@@ -105,8 +106,17 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
       continue;
     }
     if (kind == bfs::CODE_END) {
-      if (P.mode == BFS_MODE_BARRIER) region_sync(own_words, 1);
       const int l = a0;
+      if (P.mode == BFS_MODE_BARRIER) {
+        region_sync(own_words, 1);
+      } else if ((P.fallback_loops >> l) & 1u) {
+        // Section 5.2 fallback: everything issued in this iteration of l has
+        // retired on every engine before any engine starts the next one.
+        // Every engine walks the same loop tree with the same trip table, so
+        // all waves meet the same sequence of barriers.
+        drain_all();
+        __builtin_amdgcn_s_barrier();
+      }
       if (uniform(rhat[l]) < uniform(trip[l])) {
         if (lane == 0) { r[l] += 1; rhat[l] += 1; }
         pc = a1 + 1;
@@ -215,6 +225,7 @@ bfs_status launch_interp(const bfs_plan *p, DevImage *img, const void *const *bu
   P.n_engines = p->n_engines;
   P.n_instrs = (int32_t)p->instr_engine.size();
   P.mode = p->mode;
+  P.fallback_loops = p->fallback_loops;
   P.tile = p->tile_elems > 0 ? p->tile_elems : 64;
   int off = 0;
   for (int i = 0; i < 4; ++i) {

@@ -157,6 +157,7 @@ bfs_status plan_build(bfs_plan &p) {
   p.static_waits.assign(D, bfs_static_wait{});
   std::map<std::pair<int32_t, int32_t>, int32_t> slot_of_loop_engine;  // per-loop allocation
   std::map<int32_t, int32_t> slot_of_instr;                            // per-instruction allocation
+  p.fallback_loops = 0;
   for (int32_t d = 0; d < D; ++d) {
     const int32_t a = p.deps[3 * d], c = p.deps[3 * d + 1], k = p.deps[3 * d + 2];
     const int32_t P = p.instr_parent[a];
@@ -178,18 +179,28 @@ bfs_status plan_build(bfs_plan &p) {
         return fail(BFS_E_ORDER, tag + ": offset 0 needs the producer before the consumer");
       f.kase = 1;
       f.expr_sub = k;
-    } else if (forward) {                           // C2: nested producer, forward
-      if (k != 0) return fail(BFS_E_NOT_ALLOCATABLE, tag + ": nested forward producer needs offset 0");
+    } else if (forward && k == 0) {                 // C2: nested producer, forward
       f.kase = 2;
       f.expr_sub = 0;
-    } else {                                        // C3: nested producer, backward
-      if (k == 0) return fail(BFS_E_ORDER, tag + ": nested backward producer at offset 0 is unsatisfiable");
-      if (k != 1) return fail(BFS_E_NOT_ALLOCATABLE, tag + ": nested backward producer needs offset 1");
+    } else if (!forward && k == 1) {                // C3: nested producer, backward
       f.kase = 3;
+      f.expr_sub = 0;
+    } else if (!forward && k == 0) {
+      return fail(BFS_E_ORDER, tag + ": nested backward producer at offset 0 is unsatisfiable");
+    } else if (!(p.flags & BFS_PLAN_BARRIER_FALLBACK)) {
+      return fail(BFS_E_NOT_ALLOCATABLE,
+                  tag + (forward ? ": nested forward producer needs offset 0" : ": nested backward producer needs offset 1"));
+    } else {                                        // Section 5.2 fallback: barriers at S's iteration ends
+      f.kase = 4;
       f.expr_sub = 0;
     }
     f.needs_mask = k > 0 ? 1 : 0;
-    if (p.alloc == BFS_ALLOC_PER_INSTR) {
+    if (f.kase == 4) {
+      f.N = 0;
+      f.K = 0;
+      f.counter = -1;
+      if (S != 0) p.fallback_loops |= 1u << S;
+    } else if (p.alloc == BFS_ALLOC_PER_INSTR) {
       f.N = 1;
       f.K = 1;
       auto it = slot_of_instr.find(a);
@@ -260,7 +271,7 @@ bfs_status plan_build(bfs_plan &p) {
     p.instr_wait_off[i] = (int32_t)p.instr_wait_list.size();
     for (int32_t d = 0; d < D; ++d)
       if (p.deps[3 * d + 1] == i) {
-        bool needed = p.mode == BFS_MODE_BARRIER_FREE || p.static_waits[d].same_region;
+        bool needed = p.mode == BFS_MODE_BARRIER_FREE ? p.formulas[d].kase != 4 : p.static_waits[d].same_region != 0;
         if (needed) p.instr_wait_list.push_back(d);
       }
   }
@@ -317,6 +328,7 @@ bfs_status plan_build(bfs_plan &p) {
   } else {
     std::vector<char> usedP(L, 0), usedS(L, 0);
     for (auto &f : p.formulas) {
+      if (f.kase == 4) continue;
       usedP[f.loop_P] = 1;
       if (f.needs_mask) usedS[f.loop_S] = 1;
     }
@@ -324,8 +336,11 @@ bfs_status plan_build(bfs_plan &p) {
     for (int32_t l = 0; l < L; ++l) regs += usedP[l] + usedS[l];
     s.regs_per_engine = regs;
     s.salu_ops_per_wait = p.alloc == BFS_ALLOC_PER_INSTR ? 3 : 5;
-    s.n_waits = D;
+    s.n_sync_points = __builtin_popcount(p.fallback_loops);
+    s.n_waits = 0;
+    for (auto &f : p.formulas) s.n_waits += f.kase != 4;
   }
+  for (auto &f : p.formulas) s.n_fallback += f.kase == 4;
   p.stats = s;
   return BFS_OK;
 }
@@ -345,7 +360,7 @@ extern "C" {
 bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc alloc, uint32_t flags,
                            bfs_plan **out) {
   if (!prog || !out) return fail(BFS_E_INVALID, "null argument");
-  if (flags != 0) return fail(BFS_E_INVALID, "flags must be 0");
+  if (flags & ~BFS_PLAN_BARRIER_FALLBACK) return fail(BFS_E_INVALID, "unknown plan flags");
   if (mode != BFS_MODE_BARRIER_FREE && mode != BFS_MODE_BARRIER) return fail(BFS_E_INVALID, "bad mode");
   if (alloc != BFS_ALLOC_PER_LOOP && alloc != BFS_ALLOC_PER_INSTR) return fail(BFS_E_INVALID, "bad alloc");
   if (prog->kernel < BFS_KERNEL_INTERP || prog->kernel > BFS_KERNEL_MOE) return fail(BFS_E_INVALID, "bad kernel");
@@ -390,6 +405,7 @@ bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc all
   p->tile_elems = prog->tile_elems;
   for (int r = 0; r < 4; ++r) p->ring_slots[r] = prog->ring_slots[r];
   p->n_accs = prog->n_accs;
+  p->flags = flags;
   bfs_status st = plan_build(*p);
   if (st != BFS_OK) {
     delete p;
@@ -425,6 +441,8 @@ bfs_status bfs_eval_threshold(const bfs_plan *plan, int32_t dep, uint32_t r_P, u
   if (plan->mode == BFS_MODE_BARRIER) {
     const bfs_static_wait &w = plan->static_waits[dep];
     *out = w.same_region ? (uint32_t)w.ordinal : 0u;
+  } else if (plan->formulas[dep].kase == 4) {
+    *out = 0u;
   } else {
     *out = eval_formula(plan->formulas[dep], r_P, rhat_S);
   }

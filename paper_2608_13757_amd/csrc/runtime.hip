@@ -38,7 +38,7 @@ std::vector<DevWait> device_waits(const bfs_plan *p) {
       x.N = f.N;
       x.K = f.K;
       x.needs_mask = f.needs_mask;
-      x.active = 1;
+      x.active = f.kase != 4;
     }
     w[d] = x;
   }
@@ -152,6 +152,8 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
     if (opts->k_unroll < 0 || (o.k_unroll != 1 && o.k_unroll != 2 && o.k_unroll != 4 && o.k_unroll != 8))
       return fail(BFS_E_INVALID, "k_unroll must be 0, 1, 2, 4 or 8");
   }
+  if (plan->mode == BFS_MODE_BARRIER_FREE && plan->stats.n_fallback > 0 && plan->kernel != BFS_KERNEL_INTERP)
+    return fail(BFS_E_UNSUPPORTED, "barrier-fallback dependencies run on the interpreter family only");
   DevImage *img = nullptr;
   bfs_status st = device_image(plan, &img);
   if (st != BFS_OK) return st;
@@ -180,6 +182,8 @@ bfs_status bfs_run_status(const bfs_plan *plan, struct ihipStream_t *stream) {
   if (!plan) return fail(BFS_E_INVALID, "null plan");
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipStreamSynchronize: ") + hipGetErrorString(e));
+  if (plan->mode == BFS_MODE_BARRIER_FREE && plan->stats.n_fallback > 0 && plan->kernel != BFS_KERNEL_INTERP)
+    return fail(BFS_E_UNSUPPORTED, "barrier-fallback dependencies run on the interpreter family only");
   DevImage *img = nullptr;
   bfs_status st = device_image(plan, &img);
   if (st != BFS_OK) return st;

@@ -41,15 +41,19 @@ def log_records(plan, log_words, n_wg, cap, per_wave=False):
     return out
 
 
-def compare_log_with_oracle(prog, plan, logs, recs_by_wg, mode):
+def compare_log_with_oracle(prog, plan, logs, recs_by_wg, mode, no_wait=()):
     """Every emitted wait's logged threshold equals the oracle's, bit-exact,
     and the observed counter was never below it.  mode "per_instr": a
     barrier-free plan with one counter per instruction, whose thresholds are
-    the Eq. 1 counts."""
+    the Eq. 1 counts.  Dependencies in ``no_wait`` (ordered by barriers)
+    must log nothing."""
     key = {"barrier_free": "sem_thr", "barrier": "barrier_thr", "per_instr": "count_thr"}[mode]
     n = 0
     for wg, recs in recs_by_wg.items():
         for d in range(len(prog.deps)):
+            if d in no_wait:
+                assert (wg, d) not in logs, (wg, d)
+                continue
             r = recs[recs["dep"] == d]
             want = [(int(i), int(t)) for i, t in zip(r["instance"], r[key])]
             got = logs.get((wg, d), [])

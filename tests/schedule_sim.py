@@ -19,6 +19,13 @@ instruction (every wait fires if and only if its dependency is satisfied:
 safety and liveness), every schedule must run to completion, and the final
 datapath state must equal the sequential one.
 
+Dependencies of a plan's barrier fallback (Section 5.2) have no semaphore:
+the implementation orders them by a barrier at the end of every iteration of
+their shared loop S, after which an engine issues nothing until every
+instance of the earlier iterations of S, on every engine, has retired.  For
+those only safety is required (a barrier may hold back an instance whose
+dependency is met).
+
 Datapath operations are opaque, as in the paper's model: an instance's
 commit reads the cells of its read set (the tile-machine semantics of
 ``oracle.hazard.accesses``) and writes, to each cell of its write set, a
@@ -73,7 +80,7 @@ class Model:
     mistakes for the tests of this checker."""
 
     def __init__(self, prog, plan, trips, trip_off_wg, wg=0, per_instr=False, threshold_delta=None,
-                 drop_updates=()):
+                 drop_updates=(), barrier_loops=None):
         res = core.run(prog, trips, trip_off_wg, wg)
         self.prog = prog
         inst = res.inst
@@ -88,14 +95,23 @@ class Model:
             occ[i] = seen.get(self.instr[i], 0)
             seen[self.instr[i]] = occ[i] + 1
         by_occ = {(self.instr[i], occ[i]): i for i in range(n)}
-        formulas = {f["dep"]: f for f in plan.formulas()}
+        all_formulas = {f["dep"]: f for f in plan.formulas()}
+        formulas = {d: f for d, f in all_formulas.items() if f["kase"] != 4}
+        if barrier_loops is None:
+            barrier_loops = sorted({f["loop_S"] for f in all_formulas.values() if f["kase"] == 4} - {0})
+        self.barrier_loops = list(barrier_loops)
         delta = threshold_delta or {}
-        # requirements: instance -> [(dep, producer instr, Eq. 1 count, counter, implementation threshold)]
+        # requirements: instance -> [(dep, producer instr, Eq. 1 count, counter, implementation threshold)];
+        # fallback dependencies: instance -> [(dep, producer instr, Eq. 1 count)]
         self.req = [[] for _ in range(n)]
+        self.req_fb = [[] for _ in range(n)]
         for rec in res.recs:
             d = int(rec["dep"])
             prd, cns, _k = prog.deps[d]
             i = by_occ[(cns, int(rec["instance"]))]
+            if d not in formulas:
+                self.req_fb[i].append((d, prd, int(rec["count_thr"])))
+                continue
             f = formulas[d]
             thr = plan.eval_threshold(d, int(rec["r_P"]), int(rec["rhat_S"])) + delta.get(d, 0)
             self.req[i].append((d, prd, int(rec["count_thr"]), f["counter"], max(thr, 0)))
@@ -118,6 +134,27 @@ class Model:
                     self.updates[i].append(c)
         for i, c in drop_updates:
             self.updates[i] = [x for x in self.updates[i] if x != c]
+        # barrier phase of every instance per barrier loop S: the iterations
+        # of S completed before it (r_S, less the one it runs in)
+        def inside(i, S):
+            l = par[i]
+            while l >= 0:
+                if l == S:
+                    return True
+                l = prog.loop_parent[l]
+            return False
+        self.phase = [[int(res.r_snap[x][S]) - inside(self.instr[x], S) for S in self.barrier_loops]
+                      for x in range(n)]
+        # instances that precede barrier b of loop j: need[j][b]
+        self.need = []
+        for j in range(len(self.barrier_loops)):
+            top = max((ph[j] for ph in self.phase), default=0)
+            cnt = [0] * (top + 2)
+            for ph in self.phase:
+                cnt[ph[j] + 1] += 1
+            for b in range(1, len(cnt)):
+                cnt[b] += cnt[b - 1]
+            self.need.append(cnt)        # cnt[b] = instances with phase < b
         # datapath accesses of every instance
         self.reads, self.writes = [], []
         for i in range(n):
@@ -148,8 +185,17 @@ def explore(model: Model, seed: int, issue_bias: float = 0.5) -> Outcome:
     ifl = [[] for _ in range(model.n_engines)]       # [instance, committed]
     rc = {}                                          # retirements per instruction (specification)
     sema = {c: 0 for c in model.counters}            # semaphores (implementation)
+    retired_ph = [{} for _ in model.barrier_loops]   # retired instances per barrier phase
     data = {}
     steps = 0
+
+    def barriers_passed(i):
+        for j, cnt in enumerate(model.need):
+            b = model.phase[i][j]
+            if sum(v for ph, v in retired_ph[j].items() if ph < b) < cnt[b]:
+                return False
+        return True
+
     while True:
         issue, other = [], []
         for e in range(model.n_engines):
@@ -162,7 +208,11 @@ def explore(model: Model, seed: int, issue_bias: float = 0.5) -> Outcome:
                 if spec and not impl:
                     return Outcome(False, "blocked", f"engine {e} instance {i} waits with its dependency met",
                                    steps)
-                if impl:
+                if impl and barriers_passed(i):
+                    if not all(rc.get(prd, 0) >= cnt for _, prd, cnt in model.req_fb[i]):
+                        return Outcome(False, "unsafe",
+                                       f"engine {e} instance {i} passes its barriers before a fallback dependency",
+                                       steps)
                     issue.append(e)
             for j, (i, done) in enumerate(ifl[e]):
                 if not done and not any(not d2 and model.conflict(i2, i) for i2, d2 in ifl[e][:j]):
@@ -186,6 +236,9 @@ def explore(model: Model, seed: int, issue_bias: float = 0.5) -> Outcome:
         else:
             i = ifl[e].pop(0)[0]
             rc[model.instr[i]] = rc.get(model.instr[i], 0) + 1
+            for j in range(len(model.barrier_loops)):
+                b = model.phase[i][j]
+                retired_ph[j][b] = retired_ph[j].get(b, 0) + 1
             for c in model.updates[model.instr[i]]:
                 sema[c] += 1
     if data != model.sequential():

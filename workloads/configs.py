@@ -25,6 +25,7 @@ from .program import (OP_ADDC, OP_MOE_EPI, OP_MOE_LOAD, OP_MOE_MMA, OP_MOE_SPILL
                       OP_STORE_RING, Program, ProgramBuilder, tile_args)
 
 CFG_CHAIN, CFG_STREAM, CFG_GEMM, CFG_ATTN, CFG_MOE, CFG_RANDOM = 1, 2, 3, 4, 5, 99
+CFG_LAG = 6
 
 
 def rng_for(cfg_id: int, seed: int, wg: int = 0) -> np.random.Generator:
@@ -136,6 +137,70 @@ def chain_workload(seed: int = 0, outer: int = 16, inner_max: int = 8, n_wg: int
     xs = [rng_for(CFG_CHAIN, seed, 1000 + w).uniform(-1.0, 1.0, size=(int(counts[w]), 256)).astype(np.float32)
           for w in range(n_wg)]
     return ChainWorkload(prog, tt, base, np.concatenate(xs), n_tiles)
+
+
+# ---------------------------------------------------------------------------
+# A software pipeline whose dependencies need the barrier fallback
+# ---------------------------------------------------------------------------
+def lag_pipeline_program(lag: int = 2, ring_slots: int = 3, scale: float = 0.5) -> Program:
+    """Two-stage pipeline: the tile loaded in iteration o of O is consumed in
+    iteration o + lag (a prologue of ``lag`` iterations skips the consumer).
+
+      O{ C(cond: trip 1 once O has run lag iterations){ E1:CONS acc += 0.5*ring[(r_C-1) % R] }
+         M(cond: trip 1){ E0:LOAD X[r_M-1] -> ring[(r_M-1) % R] } }
+      E1:STORE acc -> out
+
+    Inside C, r_C = r_O - lag and r_M = r_O, so CONS reads the slot LOAD
+    filled lag iterations of O earlier.  LOAD->CONS (offset lag, backward:
+    C precedes M in O's body) and CONS->LOAD (offset R - lag, forward: the
+    slot's previous reader ran R - lag iterations earlier) both have the
+    producer nested below O, so for lag >= 2 and R - lag >= 1 neither is one
+    of the allocatable cases of Section 5.2; CONS->STORE (offset 0 at the top
+    level, producer nested, forward) is.  Output: 0.5 * (sum of the first
+    trip(O) - lag tiles)."""
+    assert 1 <= lag < ring_slots
+    b = ProgramBuilder("interp", n_engines=2)
+    with b.loop("O"):
+        with b.loop("C", is_cond=True) as C:
+            b.instr(1, OP_SCALE_ACC, tile_args(src=0, dst=0, gen_loop=C, n_gen=ring_slots, const=scale),
+                    name="CONS")
+        with b.loop("M", is_cond=True) as M:
+            b.instr(0, OP_LOAD, tile_args(src=1, dst=0, gen_loop=M, n_gen=ring_slots, idx_loop=M),
+                    name="LOAD")
+    b.instr(1, OP_STORE_ACC, tile_args(src=0, dst=2), name="STORE")
+    b.dep("LOAD", "CONS", lag)
+    b.dep("CONS", "LOAD", ring_slots - lag)
+    b.dep("CONS", "STORE", 0)
+    p = b.build()
+    p.tile_elems = 256
+    p.ring_slots = [ring_slots]
+    p.n_accs = 1
+    return p
+
+
+def lag_pipeline_workload(seed: int = 0, n_wg: int = 1, outer_min: int = 1, outer_max: int = 24, lag: int = 2,
+                          ring_slots: int = 3) -> ChainWorkload:
+    """Per workgroup a trip of O drawn from [outer_min, outer_max] (trips
+    below lag + 1 never consume); X ~ U(-1, 1) fp32 tiles of 256."""
+    prog = lag_pipeline_program(lag, ring_slots)
+    O, C, M = prog.loop_id("O"), prog.loop_id("C"), prog.loop_id("M")
+    per = []
+    for w in range(n_wg):
+        rng = rng_for(CFG_LAG, seed, w)
+        outer = int(rng.integers(outer_min, outer_max + 1))
+
+        def draw(l, n, outer=outer):
+            if l == O:
+                return np.full(n, outer)
+            if l == C:
+                return (np.arange(1, n + 1) > lag).astype(np.int32)
+            return np.ones(n, np.int32)
+        per.append(draw_trips(prog, draw))
+    tt = TripTables(per)
+    base, counts = tile_bases(tt, M)
+    xs = [rng_for(CFG_LAG, seed, 1000 + w).uniform(-1.0, 1.0, size=(int(counts[w]), 256)).astype(np.float32)
+          for w in range(n_wg)]
+    return ChainWorkload(prog, tt, base, np.concatenate(xs), int(counts.sum()))
 
 
 # ---------------------------------------------------------------------------
