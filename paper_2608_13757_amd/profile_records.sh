@@ -5,11 +5,16 @@
 #   rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 20 --warmup 3 --no-cpu-baseline
 #   rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/pf_$wl -o f -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024
 #   rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/pw_$wl -o w -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024
+#   rocprofv3 --pmc $SQ1 --output-format csv -d $R/ps1_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --no-cpu-baseline
+#   rocprofv3 --pmc $SQ2 --output-format csv -d $R/ps2_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --no-cpu-baseline
+# (SQ1, SQ2 below; the SQ records are written when those runs exist)
 # for wl in stream gemm attn moe.  Algorithmic bytes per step: stream 512 B per
 # innermost iteration (5568928 for seed 0); GEMM A + B + C + bias; attention
 # Q + K + V + O; MoE all weights + x + h written and read + y.
 set -e
 R=${1:?usage: profile_records.sh <rocprofv3 output root>}
+SQ1="SQ_WAVES SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY SQ_INSTS_SALU SQ_INSTS_LDS"
+SQ2="SQ_INSTS_VALU SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_BRANCH SQ_INSTS_SMEM SQ_LDS_BANK_CONFLICT SQ_WAIT_INST_LDS"
 for wl in ${WLS:-stream gemm attn moe}; do
   case $wl in
     stream) k=stream3; ab=2851291136; wk="sync-bound stream, 1024 workgroups, seed 0, 5568928 innermost iterations, one in-place ring";;
@@ -22,6 +27,12 @@ for wl in ${WLS:-stream gemm attn moe}; do
     --command "rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/pf_$wl -o f -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024" \
     --command "rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/pw_$wl -o w -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024" \
     --command "WLS=$wl bash paper_2608_13757_amd/profile_records.sh $R"
+  if [ -d $R/ps1_$wl ] && [ -d $R/ps2_$wl ]; then
+    python -m paper_2608_13757_amd.profiles sq --kernel $k --dir $R/ps1_$wl --dir $R/ps2_$wl --workload "$wk" \
+      --command "rocprofv3 --pmc $SQ1 --output-format csv -d $R/ps1_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --no-cpu-baseline" \
+      --command "rocprofv3 --pmc $SQ2 --output-format csv -d $R/ps2_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --no-cpu-baseline" \
+      --command "WLS=$wl bash paper_2608_13757_amd/profile_records.sh $R"
+  fi
   python -m paper_2608_13757_amd.profiles trace --kernel $k --stats-dir $R/pt_$wl --workload "$wk" \
     --command "rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 20 --warmup 3 --no-cpu-baseline" \
     --command "WLS=$wl bash paper_2608_13757_amd/profile_records.sh $R"

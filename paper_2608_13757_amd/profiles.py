@@ -9,6 +9,10 @@ Turns rocprofv3 output into the short records kept under ``profiles/``:
   bytes; stamped with a digest of the kernel's sources so that a stale record
   is never reported for a changed kernel.
 * ``trace``: the per-kernel table of a ``--kernel-trace --stats`` run.
+* ``sq``: shader-sequencer counters of the uninstrumented dispatches of both
+  modes from ``--pmc`` runs (at most 8 SQ counters per run): wave cycles,
+  cycles spent waiting, instruction mix, MFMA busy cycles and MFMA work, per
+  dispatch, with the wait and issue shares of the wave cycles.
 
 Usage (from the repository root, after the rocprofv3 runs)::
 
@@ -33,7 +37,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 # its barrier-free, uninstrumented dispatch in rocprofv3 output
 KERNELS = {
     "stream3": (["kern_stream3.hip", "device_sync.h", "bfs_internal.h"], ["stream3_kernel<0, false"]),
-    "gemm": (["kern_gemm.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["gemm_kernel<0, false>"]),
+    "gemm": (["kern_gemm.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["gemm_kernel<0, false, 1>"]),
     "attn": (["kern_attn.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["attn_kernel<0, false>"]),
     "moe": (["kern_moe.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"],
             ["moe_kernel<1, 0, false>", "moe_kernel<2, 0, false>"]),
@@ -157,6 +161,63 @@ def trace(args):
     print(out)
 
 
+SQ_DERIVED = [
+    ("wait share of wave cycles", "SQ_WAIT_ANY", "SQ_WAVE_CYCLES"),
+    ("issue share of wave cycles", "SQ_ACTIVE_INST_ANY", "SQ_WAVE_CYCLES"),
+    ("LDS instructions per wave", "SQ_INSTS_LDS", "SQ_WAVES"),
+    ("SALU instructions per wave", "SQ_INSTS_SALU", "SQ_WAVES"),
+    ("branches per wave", "SQ_INSTS_BRANCH", "SQ_WAVES"),
+]
+
+
+def sq(args):
+    """Per-dispatch means of every SQ counter of the runs, for each
+    uninstrumented kernel instantiation of the family."""
+    stem = {"stream3": "stream3_kernel<", "gemm": "gemm_kernel<", "attn": "attn_kernel<",
+            "moe": "moe_kernel<"}[args.kernel]
+    table = {}          # kernel -> counter -> (mean, dispatches)
+    for d in args.dir:
+        rows = _counter_rows(d)
+        names = sorted({r["Kernel_Name"] for r in rows if stem in r["Kernel_Name"]})
+        counters = sorted({r["Counter_Name"] for r in rows})
+        for n in names:
+            short = n[n.index(stem):].split("(")[0]
+            if ", true" in short:
+                continue
+            for c in counters:
+                table.setdefault(short, {})[c] = _per_dispatch(rows, c, n)
+    kernels = sorted(table)
+    counters = sorted({c for k in kernels for c in table[k]})
+    lines = [f"# {args.kernel} kernel: SQ counters, barrier-free vs barrier ({args.workload})", "",
+             "Commands (run from the repository root on one MI355X, `TMPDIR=/tmp`):", ""]
+    for c in args.command:
+        lines += ["```", c, "```", ""]
+    lines += ["Per-dispatch means over the timed and warm-up launches (counter values summed over the "
+              "hardware instances).  Template arguments: <mode, instrumented, ...> (mode 0 = barrier-free, "
+              "1 = barrier); MoE: <phase, mode, instrumented>.  Cycle counters are in the hardware's "
+              "units (quad cycles); only their ratios are used.", "",
+              "| Counter | " + " | ".join(f"`{k}`" for k in kernels) + " |",
+              "|---|" + "---|" * len(kernels)]
+    for c in counters:
+        lines.append(f"| {c} | " + " | ".join(f"{table[k][c][0]:.4g}" if c in table[k] else "" for k in kernels)
+                     + " |")
+    for label, num, den in SQ_DERIVED + ([("MFMA bf16 FLOP (512 per MOP)", "SQ_INSTS_VALU_MFMA_MOPS_BF16", None)]):
+        vals = []
+        for k in kernels:
+            t = table[k]
+            if num not in t or (den is not None and den not in t):
+                vals.append("")
+            elif den is None:
+                vals.append(f"{t[num][0] * 512:.4g}")
+            else:
+                vals.append(f"{t[num][0] / t[den][0]:.3f}")
+        lines.append(f"| *{label}* | " + " | ".join(vals) + " |")
+    out = os.path.join(PROFILES, f"{args.kernel}_sq.md")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(out)
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -173,8 +234,13 @@ def main():
     k.add_argument("--stats-dir", required=True)
     k.add_argument("--workload", required=True)
     k.add_argument("--command", action="append", default=[])
+    q = sub.add_parser("sq")
+    q.add_argument("--kernel", required=True, choices=sorted(KERNELS))
+    q.add_argument("--dir", action="append", required=True)
+    q.add_argument("--workload", required=True)
+    q.add_argument("--command", action="append", default=[])
     a = ap.parse_args()
-    traffic(a) if a.cmd == "traffic" else trace(a)
+    {"traffic": traffic, "trace": trace, "sq": sq}[a.cmd](a)
 
 
 if __name__ == "__main__":
