@@ -103,3 +103,74 @@ def moe_tokens(moe, tokens, weights=None):
         h = silu(wg @ x) * (wu @ x)
         out.append(wd @ h)
     return np.array(out)
+
+
+# ---- RMSNorm + FP8 quantization -------------------------------------------
+E4M3_MAX = 448.0      # largest finite OCP FP8 E4M3 ("fn") value: 1.75 * 2^8
+
+
+def e4m3fn_encode(v):
+    """OCP FP8 E4M3 codes (1 sign, 4 exponent bits with bias 7, 3 mantissa
+    bits; no infinities) of fp64 values with |v| <= 464, rounding to nearest
+    with ties to even.  Normal numbers are (1 + m/8) * 2^(e-7) for exponent
+    fields e = 1..15 (field 15 with mantissa 7 is NaN, so 448 is the
+    largest); subnormals are m/8 * 2^-6."""
+    v = np.asarray(v, np.float64)
+    a = np.abs(v)
+    if np.any(a > 464.0) or np.any(~np.isfinite(a)):
+        raise ValueError("outside the E4M3 range handled here")
+    code = np.zeros(a.shape, np.int64)
+    sub = a < 2.0 ** -6
+    # subnormal: a multiple of 2^-9, rounded half to even (8 * 2^-9 is the
+    # smallest normal, whose code 8 is exactly the carried value)
+    code[sub] = np.rint(a[sub] / 2.0 ** -9).astype(np.int64)
+    n = ~sub
+    e = np.floor(np.log2(a[n])).astype(np.int64)
+    # guard the log2 rounding at exact powers of two
+    e = np.where(2.0 ** e > a[n], e - 1, e)
+    e = np.where(2.0 ** (e + 1) <= a[n], e + 1, e)
+    m = np.rint((a[n] / 2.0 ** e - 1.0) * 8.0).astype(np.int64)
+    carry = m == 8
+    e = np.where(carry, e + 1, e)
+    m = np.where(carry, 0, m)
+    code[n] = ((e + 7) << 3) | m
+    code = np.minimum(code, 0x7E)          # |v| in (448, 464) rounds to 448
+    return (code | np.where(np.signbit(v), 0x80, 0)).astype(np.uint8)
+
+
+def e4m3fn_decode(c):
+    c = np.asarray(c, np.int64)
+    s = np.where(c & 0x80, -1.0, 1.0)
+    e, m = (c >> 3) & 0xF, c & 7
+    mag = np.where(e == 0, m / 8.0 * 2.0 ** -6, (1.0 + m / 8.0) * 2.0 ** (e - 7.0))
+    return s * mag
+
+
+def rmsnorm_fp8_rows(x_bits, g_bits, eps, rows):
+    """RMSNorm followed by per-row dynamic FP8 quantization, for the given
+    rows: y = x / sqrt(mean(x^2) + eps) * gamma; scale s = max|y| / 448
+    (1 for an all-zero row); codes = E4M3(y / s).  Returns (codes uint8
+    [n, H], scales fp64 [n], y / s fp64 [n, H])."""
+    g = bf16_to_f32(g_bits).astype(np.float64)
+    codes, scales, ts = [], [], []
+    for r in rows:
+        x = bf16_to_f32(x_bits[r]).astype(np.float64)
+        y = x / np.sqrt(np.mean(x * x) + eps) * g
+        amax = np.max(np.abs(y))
+        s = amax / E4M3_MAX if amax > 0 else 1.0
+        t = y / s
+        codes.append(e4m3fn_encode(t))
+        scales.append(s)
+        ts.append(t)
+    return np.array(codes), np.array(scales), np.array(ts)
+
+
+def e4m3fn_ambiguous(t, rel=2.0 ** -18):
+    """True where t lies within a relative ``rel`` of a rounding midpoint
+    between two adjacent E4M3 values: there the code depends on the last
+    bits of the fp32 arithmetic that produced t, and either neighbour is a
+    correct rounding of the exact value."""
+    t = np.asarray(t, np.float64)
+    lo = e4m3fn_encode(t * (1.0 - rel))
+    hi = e4m3fn_encode(t * (1.0 + rel))
+    return lo != hi

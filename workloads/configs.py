@@ -22,10 +22,12 @@ import numpy as np
 from .program import (OP_ADDC, OP_MOE_EPI, OP_MOE_LOAD, OP_MOE_MMA, OP_MOE_SPILL, OP_ATTN_LOAD, OP_ATTN_NORM, OP_ATTN_PV, OP_ATTN_QK, OP_ATTN_SM,
                       OP_GEMM_BIAS, OP_GEMM_EPI, OP_GEMM_LOAD, OP_GEMM_MMA,
                       OP_GEMM_SPILL, OP_LOAD, OP_NOP, OP_SCALE_ACC, OP_STORE_ACC,
-                      OP_STORE_RING, Program, ProgramBuilder, tile_args)
+                      OP_RMS_LOAD, OP_RMS_NORM, OP_RMS_STORE, OP_STORE_RING, Program, ProgramBuilder,
+                      f32_bits, tile_args)
 
 CFG_CHAIN, CFG_STREAM, CFG_GEMM, CFG_ATTN, CFG_MOE, CFG_RANDOM = 1, 2, 3, 4, 5, 99
 CFG_LAG = 6
+CFG_RMS = 7
 
 
 def rng_for(cfg_id: int, seed: int, wg: int = 0) -> np.random.Generator:
@@ -610,3 +612,44 @@ def moe_worklist(counts, phase: int, hidden: int, ffn: int, mchunk: int = MOE_MC
                          np.full(n_mt, ksteps, np.int32), np.full(n_mt, chunks, np.int32)]
                         for _, _, _, n_mt in work])
     return MoeWork(work, trips)
+
+
+# ---------------------------------------------------------------------------
+# RMSNorm + FP8 quantization: a software-pipelined row loop
+# ---------------------------------------------------------------------------
+RMS_T, RMS_H = 32768, 8192
+
+
+def rmsnorm_program(t: int = RMS_T, h: int = RMS_H, waves: int = 4, x_ring: int = 2, q_ring: int = 2,
+                    eps: float = 1e-6) -> Program:
+    """Load / vector / store engines over one row loop per workgroup, one
+    row per iteration:
+
+      R{ E0:LOAD X row -> xring[(rhat_R-1) % x_ring]
+         E1:NORM xring -> codes + scale in qring[(rhat_R-1) % q_ring]
+         E2:STORE qring -> Q, S }
+
+    LOAD->NORM and NORM->STORE at offset 0 carry the data; NORM->LOAD at
+    offset x_ring and STORE->NORM at offset q_ring keep a slot from being
+    refilled before it is read (with two slots each: double buffering,
+    offsets {0, 2}).  The vector engine's ``waves`` waves share each row
+    (one column block each)."""
+    b = ProgramBuilder("rmsnorm", n_engines=3, waves_per_engine=[1, waves, 1])
+    with b.loop("R"):
+        b.instr(0, OP_RMS_LOAD, [t, h, x_ring, 0, 0, 0, 0, 0], name="LOAD")
+        b.instr(1, OP_RMS_NORM, [q_ring, f32_bits(eps), 0, 0, 0, 0, 0, 0], name="NORM")
+        b.instr(2, OP_RMS_STORE, [0] * 8, name="STORE")
+    b.dep("LOAD", "NORM", 0)
+    b.dep("NORM", "LOAD", x_ring)
+    b.dep("NORM", "STORE", 0)
+    b.dep("STORE", "NORM", q_ring)
+    return b.build()
+
+
+def rmsnorm_worklist(t: int, n_wg: int):
+    """Contiguous, balanced runs of rows per workgroup: (first row per
+    workgroup int64 [n_wg], trip tables)."""
+    start = (np.arange(n_wg + 1, dtype=np.int64) * t) // n_wg
+    base = start[:-1].astype(np.int64)
+    per = [[np.array([1], np.int32), np.array([int(start[w + 1] - start[w])], np.int32)] for w in range(n_wg)]
+    return base, TripTables(per)

@@ -57,11 +57,14 @@ OP_MOE_LOAD = 48       # args: phase (1 gate/up, 2 down), K, N, ring depth
 OP_MOE_MMA = 49
 OP_MOE_EPI = 50
 OP_MOE_SPILL = 51      # args: epilogue ring depth
+OP_RMS_LOAD = 64       # args: T, H, x-ring depth
+OP_RMS_NORM = 65       # args: q-ring depth, eps (fp32 bits)
+OP_RMS_STORE = 66
 
 KIND_BLOCK = 0
 KIND_LOOP = 1
 
-KERNELS = ("interp", "stream3", "gemm", "attn", "moe")
+KERNELS = ("interp", "stream3", "gemm", "attn", "moe", "rmsnorm")
 
 
 def f32_bits(x: float) -> int:

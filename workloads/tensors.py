@@ -9,7 +9,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .configs import CFG_ATTN, CFG_GEMM, CFG_MOE, rng_for
+from .configs import CFG_ATTN, CFG_GEMM, CFG_MOE, CFG_RMS, rng_for
 
 
 def to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -139,3 +139,32 @@ def moe_weights_all(moe: MoeInputs):
     for e in range(E):
         wg[e], wu[e], wd[e] = moe.weights(e)
     return wg, wu, wd
+
+
+# ---------------------------------------------------------------------------
+# RMSNorm + FP8 quantization
+# ---------------------------------------------------------------------------
+@dataclass
+class RmsInputs:
+    x: np.ndarray       # uint16 bf16 [T, H]
+    gamma: np.ndarray   # uint16 bf16 [H]
+    outliers: np.ndarray  # the channels drawn with a larger scale
+
+
+def rmsnorm_inputs(seed: int = 0, t: int = 32768, h: int = 8192, outlier_frac: float = 0.005,
+                   outlier_scale: float = 20.0) -> RmsInputs:
+    """Activations x ~ N(0, 1) with a seeded 0.5 % of channels scaled by 20
+    (the outlier channels that make per-row dynamic FP8 scaling matter), and
+    gamma = 1 + N(0, 0.1) per channel; both rounded to bf16."""
+    g = rng_for(CFG_RMS, seed, 0)
+    n_out = max(1, int(round(outlier_frac * h)))
+    outliers = np.sort(g.choice(h, size=n_out, replace=False))
+    colscale = np.ones(h, np.float32)
+    colscale[outliers] = outlier_scale
+    gx = rng_for(CFG_RMS, seed, 1)
+    x = np.empty((t, h), np.uint16)
+    for r0 in range(0, t, 4096):
+        r1 = min(t, r0 + 4096)
+        x[r0:r1] = to_bf16_bits(gx.standard_normal((r1 - r0, h), dtype=np.float32) * colscale[None, :])
+    gamma = to_bf16_bits(1.0 + 0.1 * rng_for(CFG_RMS, seed, 2).standard_normal(h, dtype=np.float32))
+    return RmsInputs(x, gamma, outliers)
