@@ -42,9 +42,13 @@ def parse():
     ap.add_argument("--alloc", default="per_loop", choices=["per_loop", "per_instr"],
                     help="counter allocation of the barrier-free plans (Eq. 5 per loop and engine, "
                          "or Eq. 3 one counter per producer instruction)")
-    ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn", "moe"],
+    ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn", "moe", "rmsnorm"],
                     help="stream: the sync-bound microbenchmark (headline); gemm: 4096^3 bf16 GEMM + bias + GELU; "
-                         "attn: varlen attention forward; moe: MoE grouped GEMM")
+                         "attn: varlen attention forward; moe: MoE grouped GEMM; rmsnorm: RMSNorm + FP8 "
+                         "quantization of 32768 x 8192 bf16")
+    ap.add_argument("--rms-wg", type=int, default=768, help="rmsnorm: workgroups (3 per CU)")
+    ap.add_argument("--rms-waves", type=int, default=4, help="rmsnorm: vector-engine waves sharing each row")
+    ap.add_argument("--rms-ring", default="2,2", help="rmsnorm: x-ring and q-ring slots")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference dispatch for HBM traffic counters)")
@@ -319,6 +323,67 @@ def bench_moe(a):
     emit(out, a, "moe")
 
 
+def bench_rmsnorm(a):
+    """RMSNorm + per-row FP8 (E4M3) quantization of a 32768 x 8192 bf16
+    activation matrix: load / vector / store engines over a software-pipelined
+    row loop (x and q rings double-buffered); both synchronization modes.
+    HBM roofline: X read once, codes and scales written once."""
+    import numpy as np
+    import torch
+    from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
+    from workloads import RMS_H, RMS_T, rmsnorm_program, rmsnorm_worklist
+    from workloads.tensors import rmsnorm_inputs
+
+    t, h = RMS_T, RMS_H
+    nx, nq = (int(v) for v in a.rms_ring.split(","))
+    ri = rmsnorm_inputs(seed=a.seed, t=t, h=h)
+    X = torch.from_numpy(ri.x.view(np.int16)).cuda()
+    G = torch.from_numpy(ri.gamma.view(np.int16)).cuda()
+    Q = torch.empty(t * h, dtype=torch.uint8, device="cuda")
+    S = torch.empty(t, dtype=torch.float32, device="cuda")
+    base_np, tt = rmsnorm_worklist(t, a.rms_wg)
+    base = torch.from_numpy(base_np).cuda()
+    t_np, o_np = tt.flat()
+    trips, toff = torch.from_numpy(t_np).cuda(), torch.from_numpy(o_np).cuda()
+    res, outs = {}, {}
+    for name in a.modes.split(","):
+        mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
+        plan = Plan(rmsnorm_program(t, h, a.rms_waves, nx, nq), mode, alloc_of(a, mode))
+        res[name] = time_mode(plan, [base, X, G, Q, S], trips, toff, a.rms_wg, a.steps, a.warmup)
+        outs[name] = (Q.clone(), S.clone())
+    if len(outs) == 2 and not (torch.equal(outs["barrier_free"][0], outs["barrier"][0]) and
+                               torch.equal(outs["barrier_free"][1], outs["barrier"][1])):
+        raise SystemExit("rmsnorm: the two modes disagree")
+    bytes_alg = 2.0 * t * h + 2.0 * h + 1.0 * t * h + 4.0 * t
+    bf = res.get("barrier_free", next(iter(res.values())))
+    ms = bf["ms_mean"]
+    gbs = bytes_alg / (ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": gbs, "unit": "GB/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "RMSNorm + per-row FP8 E4M3 quantization, X bf16 32768 x 8192 ~ N(0,1) with "
+                               "0.5% outlier channels x20, gamma bf16 1 + N(0,0.1); load / vector / store engines",
+                   "t": t, "h": h, "n_wg": a.rms_wg, "vector_waves": a.rms_waves, "x_ring": nx, "q_ring": nq,
+                   "parallelism": "single GPU"},
+        "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None},
+    }
+    if "barrier" in res and "barrier_free" in res:
+        out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
+    if not a.no_cpu_baseline:
+        from oracle import mathref
+        rows, t0 = 0, time.perf_counter()
+        while rows < t and time.perf_counter() - t0 < 10.0:
+            mathref.rmsnorm_fp8_rows(ri.x, ri.gamma, 1e-6, range(rows, min(t, rows + 64)))
+            rows = min(t, rows + 64)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": rows * (3.0 * h + 4.0) / dt / 1e9, "unit": "GB/s", "cores": 1,
+                               "kind": "oracle", "sample": f"first {rows} of {t} rows in {dt:.1f} s"}
+    emit(out, a, "rms")
+
+
 def bf16_bits_as_f32(bits):
     import numpy as np
     return (bits.astype(np.uint32) << 16).view(np.float32)
@@ -344,6 +409,9 @@ def main():
         return
     if a.workload == "moe":
         bench_moe(a)
+        return
+    if a.workload == "rmsnorm":
+        bench_rmsnorm(a)
         return
     w = stream_workload(seed=a.seed, n_wg=a.n_wg, outer=a.outer, n_gen=a.n_gen)
     trips_np, off_np = w.trips.flat()

@@ -86,7 +86,8 @@ typedef enum {
   BFS_KERNEL_STREAM3 = 1,     /* load / add / store stream over a 3-level nest */
   BFS_KERNEL_GEMM = 2,        /* bf16 GEMM + bias + GELU, load / MFMA / epilogue engines */
   BFS_KERNEL_ATTN = 3,        /* variable-length attention forward */
-  BFS_KERNEL_MOE = 4          /* MoE grouped GEMM with runtime per-expert trip counts */
+  BFS_KERNEL_MOE = 4,         /* MoE grouped GEMM with runtime per-expert trip counts */
+  BFS_KERNEL_RMSNORM = 5      /* RMSNorm + per-row FP8 (E4M3) quantization, load / vector / store engines */
 } bfs_kernel;
 
 /*

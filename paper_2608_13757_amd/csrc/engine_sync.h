@@ -187,24 +187,33 @@ struct Sync {
   template <int kN>
   __device__ __forceinline__ void enter(Site<kN> &s, const InstrWaits &iw, const Regs &g, uint32_t L) {
     s.n = (uint32_t)iw.n;
+    // Every element is assigned unconditionally (selects, no stores under
+    // branches): stores of different elements merged across branches would
+    // index the arrays dynamically and move them to scratch memory.
 #pragma unroll
     for (int j = 0; j < kN; ++j) {
-      if (j < iw.n) {
-        const bfs::PackedWait w = iw.w[j].w;
-        uint32_t kind = (uint32_t)iw.w[j].kind;
-        if (kMode == BFS_MODE_BARRIER) {
-          kind = (uint32_t)kWaitConst;
-          s.base[j] = ((w.w0 >> 25) & 1u) ? (int32_t)(w.w3 >> 16) : 0;
-        } else if (kind == (uint32_t)kWaitAffine) {
-          const int32_t N = (int32_t)(w.w1 & 0xffffu), K = (int32_t)(w.w1 >> 16);
-          const int32_t sub = (int32_t)(w.w2 >> 16);
-          s.base[j] = N * ((int32_t)g.r(L) - sub) - (N - K);
-          s.mk[j] = (((w.w0 >> 24) & 1u) ? (w.w2 & 0xffffu) : 0u) | ((uint32_t)N << 16);
-        } else if (kind == (uint32_t)kWaitConst) {
-          s.base[j] = (int32_t)threshold_plain(w, g);
-        }
-        s.meta[j] = word(w.w0 & 0xffu, 0) | ((uint32_t)iw.w[j].n_prd_waves << 16) | (kind << 20);
+      const bool on = j < iw.n;
+      const bfs::PackedWait w = iw.w[j].w;
+      uint32_t kind = (uint32_t)iw.w[j].kind;
+      int32_t base = s.base[j];
+      uint32_t mk = s.mk[j];
+      if (kMode == BFS_MODE_BARRIER) {
+        kind = (uint32_t)kWaitConst;
+        base = ((w.w0 >> 25) & 1u) ? (int32_t)(w.w3 >> 16) : 0;
+      } else {
+        const int32_t N = (int32_t)(w.w1 & 0xffffu), K = (int32_t)(w.w1 >> 16);
+        const int32_t sub = (int32_t)(w.w2 >> 16);
+        const int32_t b_aff = N * ((int32_t)g.r(L) - sub) - (N - K);
+        const uint32_t mk_aff = (((w.w0 >> 24) & 1u) ? (w.w2 & 0xffffu) : 0u) | ((uint32_t)N << 16);
+        const bool aff = kind == (uint32_t)kWaitAffine, cst = kind == (uint32_t)kWaitConst;
+        const int32_t b_cst = cst ? (int32_t)threshold_plain(w, g) : 0;
+        base = aff ? b_aff : (cst ? b_cst : base);
+        mk = aff ? mk_aff : mk;
       }
+      const uint32_t meta = word(w.w0 & 0xffu, 0) | ((uint32_t)iw.w[j].n_prd_waves << 16) | (kind << 20);
+      s.base[j] = on ? base : s.base[j];
+      s.mk[j] = on ? mk : s.mk[j];
+      s.meta[j] = on ? meta : s.meta[j];
     }
   }
 

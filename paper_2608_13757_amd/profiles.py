@@ -39,6 +39,7 @@ KERNELS = {
     "stream3": (["kern_stream3.hip", "device_sync.h", "bfs_internal.h"], ["stream3_kernel<0, false"]),
     "gemm": (["kern_gemm.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["gemm_kernel<0, false, 1>"]),
     "attn": (["kern_attn.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["attn_kernel<0, false>"]),
+    "rms": (["kern_rms.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["rms_kernel<0, false, 4>"]),
     "moe": (["kern_moe.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"],
             ["moe_kernel<1, 0, false>", "moe_kernel<2, 0, false>"]),
 }
@@ -146,7 +147,7 @@ def trace(args):
     lines += ["Template arguments: <mode, instrumented> (mode 0 = barrier-free, 1 = barrier); "
               "MoE: <phase, mode, instrumented>.", "",
               "| Kernel | Calls | Average ns | Min ns | Max ns |", "|---|---|---|---|---|"]
-    stems = ("stream3_kernel<", "gemm_kernel<", "attn_kernel<", "moe_kernel<")
+    stems = ("stream3_kernel<", "gemm_kernel<", "attn_kernel<", "moe_kernel<", "rms_kernel<")
     for r in rows:
         name = r["Name"]
         if not any(t in name for t in stems):
@@ -174,7 +175,7 @@ def sq(args):
     """Per-dispatch means of every SQ counter of the runs, for each
     uninstrumented kernel instantiation of the family."""
     stem = {"stream3": "stream3_kernel<", "gemm": "gemm_kernel<", "attn": "attn_kernel<",
-            "moe": "moe_kernel<"}[args.kernel]
+            "moe": "moe_kernel<", "rms": "rms_kernel<"}[args.kernel]
     table = {}          # kernel -> counter -> (mean, dispatches)
     for d in args.dir:
         rows = _counter_rows(d)
