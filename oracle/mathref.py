@@ -174,3 +174,17 @@ def e4m3fn_ambiguous(t, rel=2.0 ** -18):
     lo = e4m3fn_encode(t * (1.0 - rel))
     hi = e4m3fn_encode(t * (1.0 + rel))
     return lo != hi
+
+
+# ---- AdamW ------------------------------------------------------------------
+def adamw_step(p, g, m, v, lr, b1, b2, eps, wd, t):
+    """One AdamW step (Adam with decoupled weight decay) in fp64:
+    m' = b1 m + (1 - b1) g, v' = b2 v + (1 - b2) g^2, bias-corrected
+    mhat = m' / (1 - b1^t), vhat = v' / (1 - b2^t), and
+    p' = p - lr (mhat / (sqrt(vhat) + eps) + wd p).  Returns (p', m', v')."""
+    p, g, m, v = (np.asarray(a, np.float64) for a in (p, g, m, v))
+    m1 = b1 * m + (1.0 - b1) * g
+    v1 = b2 * v + (1.0 - b2) * g * g
+    mhat = m1 / (1.0 - b1 ** t)
+    vhat = v1 / (1.0 - b2 ** t)
+    return p - lr * (mhat / (np.sqrt(vhat) + eps) + wd * p), m1, v1

@@ -22,12 +22,14 @@ import numpy as np
 from .program import (OP_ADDC, OP_MOE_EPI, OP_MOE_LOAD, OP_MOE_MMA, OP_MOE_SPILL, OP_ATTN_LOAD, OP_ATTN_NORM, OP_ATTN_PV, OP_ATTN_QK, OP_ATTN_SM,
                       OP_GEMM_BIAS, OP_GEMM_EPI, OP_GEMM_LOAD, OP_GEMM_MMA,
                       OP_GEMM_SPILL, OP_LOAD, OP_NOP, OP_SCALE_ACC, OP_STORE_ACC,
-                      OP_RMS_LOAD, OP_RMS_NORM, OP_RMS_STORE, OP_STORE_RING, Program, ProgramBuilder,
+                      OP_ADAM_LOAD, OP_ADAM_STORE, OP_ADAM_UPDATE, OP_RMS_LOAD, OP_RMS_NORM, OP_RMS_STORE,
+                      OP_STORE_RING, Program, ProgramBuilder,
                       f32_bits, tile_args)
 
 CFG_CHAIN, CFG_STREAM, CFG_GEMM, CFG_ATTN, CFG_MOE, CFG_RANDOM = 1, 2, 3, 4, 5, 99
 CFG_LAG = 6
 CFG_RMS = 7
+CFG_ADAM = 8
 
 
 def rng_for(cfg_id: int, seed: int, wg: int = 0) -> np.random.Generator:
@@ -653,3 +655,42 @@ def rmsnorm_worklist(t: int, n_wg: int):
     base = start[:-1].astype(np.int64)
     per = [[np.array([1], np.int32), np.array([int(start[w + 1] - start[w])], np.int32)] for w in range(n_wg)]
     return base, TripTables(per)
+
+
+# ---------------------------------------------------------------------------
+# AdamW over parameter chunks
+# ---------------------------------------------------------------------------
+ADAM_N = 1 << 20
+ADAM_HP = dict(lr=1e-3, b1=0.9, b2=0.999, eps=1e-8, wd=0.01, t=10)
+
+
+def adamw_program(n: int = ADAM_N, chunk: int = 1024, waves: int = 2, ring: int = 2, lr: float = 1e-3,
+                  b1: float = 0.9, b2: float = 0.999, eps: float = 1e-8, wd: float = 0.01, t: int = 10) -> Program:
+    """Load / vector / store engines over one loop of parameter chunks per
+    workgroup, updating in place in the ring slot:
+
+      C{ E0:LOAD p, g, m, v chunk -> ring[(rhat_C-1) % ring]
+         E1:UPDATE AdamW on the slot (p, m, v rewritten)
+         E2:STORE p, m, v -> HBM }
+
+    LOAD->UPDATE and UPDATE->STORE at offset 0, STORE->LOAD at offset ring
+    (with two slots: offsets {0, 2})."""
+    b = ProgramBuilder("adamw", n_engines=3, waves_per_engine=[1, waves, 1])
+    with b.loop("C"):
+        b.instr(0, OP_ADAM_LOAD, [n, chunk, ring, 0, 0, 0, 0, 0], name="LOAD")
+        b.instr(1, OP_ADAM_UPDATE, [f32_bits(lr), f32_bits(b1), f32_bits(b2), f32_bits(eps), f32_bits(wd), t, 0, 0],
+                name="UPDATE")
+        b.instr(2, OP_ADAM_STORE, [0] * 8, name="STORE")
+    b.dep("LOAD", "UPDATE", 0)
+    b.dep("UPDATE", "STORE", 0)
+    b.dep("STORE", "LOAD", ring)
+    return b.build()
+
+
+def adamw_worklist(n: int, chunk: int, n_wg: int):
+    """Balanced contiguous runs of chunks per workgroup (the last chunk may
+    be partial): (first chunk per workgroup int64 [n_wg], trip tables)."""
+    n_chunks = -(-n // chunk)
+    start = (np.arange(n_wg + 1, dtype=np.int64) * n_chunks) // n_wg
+    per = [[np.array([1], np.int32), np.array([int(start[w + 1] - start[w])], np.int32)] for w in range(n_wg)]
+    return start[:-1].astype(np.int64), TripTables(per)

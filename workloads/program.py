@@ -60,11 +60,14 @@ OP_MOE_SPILL = 51      # args: epilogue ring depth
 OP_RMS_LOAD = 64       # args: T, H, x-ring depth
 OP_RMS_NORM = 65       # args: q-ring depth, eps (fp32 bits)
 OP_RMS_STORE = 66
+OP_ADAM_LOAD = 80      # args: N, chunk, ring depth
+OP_ADAM_UPDATE = 81    # args: lr, beta1, beta2, eps, weight decay (fp32 bits), step t
+OP_ADAM_STORE = 82
 
 KIND_BLOCK = 0
 KIND_LOOP = 1
 
-KERNELS = ("interp", "stream3", "gemm", "attn", "moe", "rmsnorm")
+KERNELS = ("interp", "stream3", "gemm", "attn", "moe", "rmsnorm", "adamw")
 
 
 def f32_bits(x: float) -> int:

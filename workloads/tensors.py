@@ -9,7 +9,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .configs import CFG_ATTN, CFG_GEMM, CFG_MOE, CFG_RMS, rng_for
+from .configs import CFG_ADAM, CFG_ATTN, CFG_GEMM, CFG_MOE, CFG_RMS, rng_for
 
 
 def to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -168,3 +168,27 @@ def rmsnorm_inputs(seed: int = 0, t: int = 32768, h: int = 8192, outlier_frac: f
         x[r0:r1] = to_bf16_bits(gx.standard_normal((r1 - r0, h), dtype=np.float32) * colscale[None, :])
     gamma = to_bf16_bits(1.0 + 0.1 * rng_for(CFG_RMS, seed, 2).standard_normal(h, dtype=np.float32))
     return RmsInputs(x, gamma, outliers)
+
+
+# ---------------------------------------------------------------------------
+# AdamW
+# ---------------------------------------------------------------------------
+@dataclass
+class AdamInputs:
+    p: np.ndarray     # fp32 [N] parameters
+    g: np.ndarray     # fp32 [N] gradients
+    m: np.ndarray     # fp32 [N] first moments
+    v: np.ndarray     # fp32 [N] second moments (>= 0)
+
+
+def adamw_inputs(seed: int = 0, n: int = 1 << 20) -> AdamInputs:
+    """Optimizer state of a model a few steps into training: p ~ N(0, 0.02),
+    g ~ N(0, 0.01) with 1 % of entries 30x larger, m ~ N(0, 0.003),
+    v = (N(0, 0.01))^2; all fp32."""
+    g_ = rng_for(CFG_ADAM, seed, 0)
+    p = (0.02 * g_.standard_normal(n)).astype(np.float32)
+    g = 0.01 * g_.standard_normal(n)
+    g[g_.random(n) < 0.01] *= 30.0
+    m = (0.003 * g_.standard_normal(n)).astype(np.float32)
+    v = ((0.01 * g_.standard_normal(n)) ** 2).astype(np.float32)
+    return AdamInputs(p, g.astype(np.float32), m, v)
