@@ -170,6 +170,9 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
     case BFS_KERNEL_ATTN:
       return launch_attn(plan, img, dev_buffers, n_buffers, dev_trips, dev_trip_off, n_wg, stream,
                          dev_debug_log, debug_capacity, o);
+    case BFS_KERNEL_ADAMW:
+      return launch_adamw(plan, img, dev_buffers, n_buffers, dev_trips, dev_trip_off, n_wg, stream,
+                          dev_debug_log, debug_capacity, o);
     case BFS_KERNEL_RMSNORM:
       return launch_rms(plan, img, dev_buffers, n_buffers, dev_trips, dev_trip_off, n_wg, stream,
                         dev_debug_log, debug_capacity, o);

@@ -60,9 +60,11 @@ def test_matches_library_adamw():
     st["exp_avg_sq"] = torch.from_numpy(ai.v.astype(np.float64)).clone()
     opt.step()
     p1, m1, v1 = adamw_step(ai.p, ai.g, ai.m, ai.v, t=t, **HP)
-    assert np.allclose(st["exp_avg"].numpy(), m1, rtol=1e-14, atol=1e-20)
-    assert np.allclose(st["exp_avg_sq"].numpy(), v1, rtol=1e-14, atol=1e-24)
-    assert np.allclose(P.detach().numpy(), p1, rtol=1e-13, atol=1e-18)
+    # the library forms m' as m + (1 - b1)(g - m) (a lerp): equal up to fp64
+    # rounding of terms of size |m|, |g| ~ 1e-2
+    assert np.allclose(st["exp_avg"].numpy(), m1, rtol=1e-13, atol=1e-16)
+    assert np.allclose(st["exp_avg_sq"].numpy(), v1, rtol=1e-13, atol=1e-19)
+    assert np.allclose(P.detach().numpy(), p1, rtol=1e-13, atol=1e-16)
 
 
 def test_adamw_worklist_covers_chunks_once():
