@@ -40,6 +40,7 @@ KERNELS = {
     "gemm": (["kern_gemm.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["gemm_kernel<0, false, 1>"]),
     "attn": (["kern_attn.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["attn_kernel<0, false>"]),
     "rms": (["kern_rms.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["rms_kernel<0, false, 4>"]),
+    "adamw": (["kern_adamw.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["adamw_kernel<0, false>"]),
     "moe": (["kern_moe.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"],
             ["moe_kernel<1, 0, false>", "moe_kernel<2, 0, false>"]),
 }
@@ -147,7 +148,7 @@ def trace(args):
     lines += ["Template arguments: <mode, instrumented> (mode 0 = barrier-free, 1 = barrier); "
               "MoE: <phase, mode, instrumented>.", "",
               "| Kernel | Calls | Average ns | Min ns | Max ns |", "|---|---|---|---|---|"]
-    stems = ("stream3_kernel<", "gemm_kernel<", "attn_kernel<", "moe_kernel<", "rms_kernel<")
+    stems = ("stream3_kernel<", "gemm_kernel<", "attn_kernel<", "moe_kernel<", "rms_kernel<", "adamw_kernel<")
     for r in rows:
         name = r["Name"]
         if not any(t in name for t in stems):
@@ -175,7 +176,7 @@ def sq(args):
     """Per-dispatch means of every SQ counter of the runs, for each
     uninstrumented kernel instantiation of the family."""
     stem = {"stream3": "stream3_kernel<", "gemm": "gemm_kernel<", "attn": "attn_kernel<",
-            "moe": "moe_kernel<", "rms": "rms_kernel<"}[args.kernel]
+            "moe": "moe_kernel<", "rms": "rms_kernel<", "adamw": "adamw_kernel<"}[args.kernel]
     table = {}          # kernel -> counter -> (mean, dispatches)
     for d in args.dir:
         rows = _counter_rows(d)
