@@ -42,10 +42,12 @@ def parse():
     ap.add_argument("--alloc", default="per_loop", choices=["per_loop", "per_instr"],
                     help="counter allocation of the barrier-free plans (Eq. 5 per loop and engine, "
                          "or Eq. 3 one counter per producer instruction)")
-    ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn", "moe", "rmsnorm", "adamw"],
+    ap.add_argument("--workload", default="stream", choices=["stream", "gemm", "attn", "moe", "rmsnorm", "adamw", "ring"],
                     help="stream: the sync-bound microbenchmark (headline); gemm: 4096^3 bf16 GEMM + bias + GELU; "
                          "attn: varlen attention forward; moe: MoE grouped GEMM; rmsnorm: RMSNorm + FP8 "
-                         "quantization of 32768 x 8192 bf16; adamw: AdamW step over fp32 parameters")
+                         "quantization of 32768 x 8192 bf16; adamw: AdamW step over fp32 parameters; ring: "
+                         "a ring indexed across trips on the interpreter, drained by an ACQ at every trip start "
+                         "(the paper's form) vs one linearized-offset dependency (an extension)")
     ap.add_argument("--adam-params", type=int, default=1 << 20, help="adamw: parameters (the paper's 2^20 by default)")
     ap.add_argument("--adam-wg", type=int, default=0, help="adamw: workgroups (0: one per 2 chunks, at most 1024)")
     ap.add_argument("--adam-chunk", type=int, default=1024, help="adamw: parameters per chunk (256, 512, 1024)")
@@ -456,6 +458,51 @@ def bench_adamw(a):
     emit(out, a, "adamw")
 
 
+def bench_ring(a):
+    """The chain's two engines on a 4-slot ring indexed by the monotone
+    register of the inner loop, 1024 workgroups, outer trip 64, inner trips
+    U[1, 8], on the interpreter: the paper's form (an ACQ instruction whose
+    C3 dependency drains the previous trip's reads at every trip start)
+    against one linearized-offset dependency (an extension, not in the
+    paper), both barrier-free, and the barrier mode."""
+    import torch
+    from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
+    from workloads import ring_workload
+
+    n_wg = 1024
+    res, vals = {}, {}
+    for name, linear, mode in (("linearized", True, MODE_BARRIER_FREE), ("acq_drain", False, MODE_BARRIER_FREE),
+                               ("barrier", False, MODE_BARRIER)):
+        w = ring_workload(seed=a.seed, outer=64, inner_max=8, n_wg=n_wg, ring_slots=4, linear=linear)
+        t_np, o_np = w.trips.flat()
+        trips, toff = torch.from_numpy(t_np).cuda(), torch.from_numpy(o_np).cuda()
+        base, x = torch.from_numpy(w.base).cuda(), torch.from_numpy(w.x).cuda()
+        out = torch.zeros(n_wg * 256, dtype=torch.float32, device="cuda")
+        plan = Plan(w.prog, mode)
+        res[name] = time_mode(plan, [base, x, out], trips, toff, n_wg, a.steps, a.warmup)
+        vals[name] = out.clone()
+        inner = w.n_tiles
+    if not (torch.equal(vals["linearized"], vals["acq_drain"]) and torch.equal(vals["linearized"], vals["barrier"])):
+        raise SystemExit("ring: the forms disagree")
+    ms = res["linearized"]["ms_mean"]
+    bytes_alg = 256 * 4.0 * inner + n_wg * 256 * 4.0
+    gbs = bytes_alg / (ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": 2.0 * inner / (ms * 1e-3), "unit": "ops/s", "n_gpus": 1, "steps": a.steps,
+        "warmup": a.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "2-engine ring across trips (interpreter): 1024 workgroups, outer 64, inner U[1,8], "
+                               "256-fp32 tiles, 4-slot ring indexed by the monotone register",
+                   "inner_iterations": inner, "parallelism": "single GPU"},
+        "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None},
+        "speedup_linearized_vs_acq_drain": res["acq_drain"]["ms_mean"] / ms,
+        "speedup_vs_barrier": res["barrier"]["ms_mean"] / ms,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def bf16_bits_as_f32(bits):
     import numpy as np
     return (bits.astype(np.uint32) << 16).view(np.float32)
@@ -487,6 +534,9 @@ def main():
         return
     if a.workload == "adamw":
         bench_adamw(a)
+        return
+    if a.workload == "ring":
+        bench_ring(a)
         return
     w = stream_workload(seed=a.seed, n_wg=a.n_wg, outer=a.outer, n_gen=a.n_gen)
     trips_np, off_np = w.trips.flat()

@@ -109,6 +109,16 @@ typedef enum {
  *                (datapath opcode and operands; meaning set by the family).
  *   deps         deps[3*d .. 3*d+2] = producer, consumer, offset k >= 0, with
  *                k the distance on the innermost loop enclosing both.
+ *   dep_linear   NULL, or per dependency 0 (the relation of Section 4.2) or
+ *                1: EXTENSION, not in the paper.  The offset counts
+ *                iterations of S since the start of the workgroup, across
+ *                trips of S: the consumer's iteration with monotone count
+ *                r_S needs the producer's iterations up to r_S - k, also
+ *                those of earlier trips (no underflow at a trip start).  It
+ *                lets a ring indexed by a monotone register, (r_S - 1) % R,
+ *                be protected against reuse across trip boundaries by one
+ *                dependency.  Allowed only with the producer directly in S
+ *                (its threshold is Eq. 5 of C1 without the isGT mask).
  *   tile machine tile_elems fp32 values per tile (multiple of 64, <= 256),
  *                ring_slots[r] slots in LDS ring r (0 = unused), n_accs
  *                accumulator tiles.
@@ -135,6 +145,7 @@ typedef struct {
   int32_t tile_elems;
   int32_t ring_slots[4];
   int32_t n_accs;
+  const int32_t *dep_linear;       /* NULL, or [n_deps]: see above */
 } bfs_program;
 
 /* One dependency's barrier-free wait (Eq. 5). */
@@ -142,7 +153,8 @@ typedef struct {
   int32_t dep;
   int32_t kase;          /* 1 = C1 (P == S), 2 = C2 (nested, forward), 3 = C3 (nested, backward),
                             4 = barrier fallback (BFS_PLAN_BARRIER_FALLBACK; counter -1, no wait,
-                            ordered by the barriers at the end of every iteration of loop_S) */
+                            ordered by the barriers at the end of every iteration of loop_S),
+                            6 = linearized offset (extension, dep_linear; producer in S, no mask) */
   int32_t loop_S;        /* innermost loop enclosing producer and consumer */
   int32_t loop_P;        /* producer's parent loop */
   int32_t k;             /* offset on S */
@@ -200,7 +212,8 @@ typedef struct {
  * Errors: BFS_E_INVALID, BFS_E_ORDER (offset 0 with the producer not before
  * the consumer, or a nested backward producer at offset 0),
  * BFS_E_NOT_ALLOCATABLE (nested producer with another offset, without
- * BFS_PLAN_BARRIER_FALLBACK), BFS_E_RESOURCE.
+ * BFS_PLAN_BARRIER_FALLBACK; a linearized dependency whose producer is not
+ * directly in S), BFS_E_RESOURCE.
  */
 bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc alloc, uint32_t flags,
                            bfs_plan **out);

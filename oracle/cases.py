@@ -21,7 +21,9 @@ With S the top-level loop (one iteration) such a dependency is never owed.
 from __future__ import annotations
 
 ORDER = "order"        # offset 0 with the consumer not after the producer
+NOT_ALLOCATABLE = "not allocatable"
 C1, C2, C3, FALLBACK = 1, 2, 3, 4
+LINEAR = 6             # extension, not in the paper: offset counted across trips of S
 
 
 def _home(prog):
@@ -56,8 +58,9 @@ def _item_of_loop(prog, child, S):
 
 
 def classify(prog, d):
-    """(case, S, P, forward) of dependency d; case is C1, C2, C3, FALLBACK or
-    ORDER."""
+    """(case, S, P, forward) of dependency d; case is C1, C2, C3, FALLBACK,
+    ORDER, or for a dependency flagged linearized LINEAR or
+    NOT_ALLOCATABLE."""
     p, c, k = prog.deps[d]
     home, place = _home(prog)
     P = home[p]
@@ -70,6 +73,12 @@ def classify(prog, d):
         return (_item_of_loop(prog, home[i], S), -1)
 
     forward = where(p) < where(c)
+    if getattr(prog, "dep_linear", None) and prog.dep_linear[d]:
+        # the linearized reading of the offset (an extension): only for a
+        # producer directly in S, whose count of S is then its own count
+        if P != S:
+            return NOT_ALLOCATABLE, S, P, forward
+        return (ORDER if (not forward and k == 0) else LINEAR), S, P, forward
     if P == S:
         case = C1 if (forward or k >= 1) else ORDER
     elif forward:

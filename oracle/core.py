@@ -164,3 +164,29 @@ def values(prog, trips, trip_off, base, x, out_len) -> np.ndarray:
     if rc != 0:
         raise RuntimeError(f"oracle values failed: {rc}")
     return out
+
+
+def linearized_records(prog, res, d):
+    """EXTENSION, not in the paper: the requirements of dependency d when its
+    offset counts iterations of the shared loop S across all of S's trips in
+    the workgroup.  Brute force over the trace: a consumer instance whose
+    monotone count of S is r needs every producer instance whose count of S
+    is at most r - k (none if r - k <= 0); its semaphore threshold is the
+    producer's per-loop counter right after the latest such instance (0 if
+    none).  Returns the records of d (consumer-instance order) with
+    count_thr and sem_thr replaced."""
+    from oracle import cases
+    p, c, k = prog.deps[d]
+    S = cases.classify(prog, d)[1]
+    inst = res.inst
+    rS = res.r_snap[:, S].astype(np.int64)
+    prod = np.nonzero(inst["instr"] == p)[0]
+    cons = np.nonzero(inst["instr"] == c)[0]
+    recs = res.recs[res.recs["dep"] == d].copy()
+    assert len(recs) == len(cons)
+    for j, x in enumerate(cons):
+        target = rS[x] - k
+        counted = [y for y in prod if rS[y] <= target] if target > 0 else []
+        recs[j]["count_thr"] = len(counted)
+        recs[j]["sem_thr"] = inst["cnt_after"][max(counted)] if counted else 0
+    return recs

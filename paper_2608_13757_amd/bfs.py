@@ -42,6 +42,7 @@ class _Program(C.Structure):
         ("n_instrs", C.c_int32), ("instr_engine", C.c_void_p), ("instr_opcode", C.c_void_p),
         ("instr_args", C.c_void_p), ("n_deps", C.c_int32), ("deps", C.c_void_p),
         ("tile_elems", C.c_int32), ("ring_slots", C.c_int32 * 4), ("n_accs", C.c_int32),
+        ("dep_linear", C.c_void_p),
     ]
 
 
@@ -141,6 +142,7 @@ class Plan:
             _i32(f["instr_engine"] or [0]), _i32(f["instr_opcode"] or [0]),
             _i32(np.array(f["instr_args"] or [[0] * 8]).reshape(-1)),
             _i32(np.array(f["deps"] or [(0, 0, 0)]).reshape(-1)),
+            _i32(f.get("dep_linear") or [0]),
         ]
         k = self._keep
         wpe = (C.c_int32 * 8)(*f["waves_per_engine"][:8])
@@ -150,7 +152,8 @@ class Plan:
                               k[1].ctypes.data, k[2].ctypes.data, k[3].ctypes.data, k[4].ctypes.data,
                               len(f["block_off"]) - 1, k[5].ctypes.data, k[6].ctypes.data,
                               len(f["instr_engine"]), k[7].ctypes.data, k[8].ctypes.data, k[9].ctypes.data,
-                              len(f["deps"]), k[10].ctypes.data, f["tile_elems"], rs, f["n_accs"])
+                              len(f["deps"]), k[10].ctypes.data, f["tile_elems"], rs, f["n_accs"],
+                              k[11].ctypes.data if f.get("dep_linear") else None)
         h = C.c_void_p()
         flags = PLAN_BARRIER_FALLBACK if fallback else 0
         _check(lib().bfs_plan_create(C.addressof(self._prog), mode, alloc, flags, C.byref(h)))

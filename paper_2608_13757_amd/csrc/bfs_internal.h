@@ -89,6 +89,7 @@ struct bfs_plan {
   std::vector<int32_t> block_off, block_instrs;
   std::vector<int32_t> instr_engine, instr_opcode, instr_args;
   std::vector<int32_t> deps;
+  std::vector<int32_t> dep_linear;       // per dependency: 1 = linearized offset (extension)
   int32_t tile_elems;
   int32_t ring_slots[4];
   int32_t n_accs;

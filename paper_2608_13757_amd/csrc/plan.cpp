@@ -174,7 +174,13 @@ bfs_status plan_build(bfs_plan &p) {
     f.prd_engine = p.instr_engine[a];
     f.cns_engine = p.instr_engine[c];
     f.forward = forward ? 1 : 0;
-    if (P == S) {                                   // C1: producer directly in S
+    if (p.dep_linear[d]) {                          // extension: offset over all trips of S
+      if (P != S) return fail(BFS_E_NOT_ALLOCATABLE, tag + ": a linearized offset needs the producer directly in S");
+      if (!forward && k == 0)
+        return fail(BFS_E_ORDER, tag + ": offset 0 needs the producer before the consumer");
+      f.kase = 6;
+      f.expr_sub = k;
+    } else if (P == S) {                            // C1: producer directly in S
       if (!forward && k == 0)
         return fail(BFS_E_ORDER, tag + ": offset 0 needs the producer before the consumer");
       f.kase = 1;
@@ -194,7 +200,7 @@ bfs_status plan_build(bfs_plan &p) {
       f.kase = 4;
       f.expr_sub = 0;
     }
-    f.needs_mask = k > 0 ? 1 : 0;
+    f.needs_mask = (k > 0 && f.kase != 6) ? 1 : 0;
     if (f.kase == 4) {
       f.N = 0;
       f.K = 0;
@@ -402,6 +408,8 @@ bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc all
     return fail(BFS_E_INVALID, "null deps");
   }
   p->deps.assign(prog->deps, prog->deps + 3 * (size_t)D);
+  p->dep_linear.assign(D, 0);
+  if (prog->dep_linear) p->dep_linear.assign(prog->dep_linear, prog->dep_linear + D);
   p->tile_elems = prog->tile_elems;
   for (int r = 0; r < 4; ++r) p->ring_slots[r] = prog->ring_slots[r];
   p->n_accs = prog->n_accs;

@@ -208,6 +208,66 @@ def lag_pipeline_workload(seed: int = 0, n_wg: int = 1, outer_min: int = 1, oute
 
 
 # ---------------------------------------------------------------------------
+# A ring indexed across trips (linearized-offset extension)
+# ---------------------------------------------------------------------------
+def ring_program(ring_slots: int = 4, scale: float = 0.5, linear: bool = True) -> Program:
+    """The chain's two engines with the ring slot taken from the monotone
+    register of B, so that slots rotate across trips of B:
+
+      A{ [E0:ACQ] B{ E0:LOAD X[r_B-1] -> ring[(r_B-1) % R]; E1:CONS acc += 0.5*ring[(r_B-1) % R] } }
+      E1:STORE acc -> out
+
+    ``linear=True``: CONS->LOAD at offset R with the linearized reading (an
+    extension, not in the paper) orders every slot reuse, also the ones that
+    straddle a trip boundary, with one dependency and no ACQ.
+    ``linear=False``: the paper's relation: CONS->LOAD at offset R underflows
+    in the first R iterations of every trip, so an ACQ instruction with
+    CONS->ACQ at offset 1 (C3) drains the previous trip's reads at each trip
+    start."""
+    b = ProgramBuilder("interp", n_engines=2)
+    with b.loop("A"):
+        if not linear:
+            b.instr(0, OP_NOP, name="ACQ")
+        with b.loop("B") as B:
+            slot = dict(gen_loop=B, n_gen=ring_slots)
+            b.instr(0, OP_LOAD, tile_args(src=1, dst=0, idx_loop=B, **slot), name="LOAD")
+            b.instr(1, OP_SCALE_ACC, tile_args(src=0, dst=0, const=scale, **slot), name="CONS")
+    b.instr(1, OP_STORE_ACC, tile_args(src=0, dst=2), name="STORE")
+    b.dep("LOAD", "CONS", 0)
+    b.dep("CONS", "LOAD", ring_slots, linear=linear)
+    if not linear:
+        b.dep("CONS", "ACQ", 1)
+    b.dep("CONS", "STORE", 0)
+    p = b.build()
+    p.tile_elems = 256
+    p.ring_slots = [ring_slots]
+    p.n_accs = 1
+    return p
+
+
+def ring_workload(seed: int = 0, outer: int = 16, inner_max: int = 8, n_wg: int = 1, ring_slots: int = 4,
+                  linear: bool = True) -> ChainWorkload:
+    """The chain's trip recipe (outer trip fixed, inner trips U[1, inner_max]
+    per workgroup) on the ring program."""
+    prog = ring_program(ring_slots, linear=linear)
+    A, B = prog.loop_id("A"), prog.loop_id("B")
+    per = []
+    for w in range(n_wg):
+        rng = rng_for(CFG_CHAIN, seed, w)
+
+        def draw(l, n, rng=rng):
+            if l == A:
+                return np.full(n, outer)
+            return rng.integers(1, inner_max + 1, size=n)
+        per.append(draw_trips(prog, draw))
+    tt = TripTables(per)
+    base, counts = tile_bases(tt, B)
+    xs = [rng_for(CFG_CHAIN, seed, 1000 + w).uniform(-1.0, 1.0, size=(int(counts[w]), 256)).astype(np.float32)
+          for w in range(n_wg)]
+    return ChainWorkload(prog, tt, base, np.concatenate(xs), int(counts.sum()))
+
+
+# ---------------------------------------------------------------------------
 # cfg2: sync-bound 3-engine stream, 1024 workgroups
 # ---------------------------------------------------------------------------
 STREAM_GENERATIONS = 32   # ring generations of the in-place layout (>= twice the largest M trip)

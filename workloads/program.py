@@ -95,6 +95,7 @@ class Program:
     blocks: list = field(default_factory=list)             # per block: [instr id]
     instrs: list = field(default_factory=list)             # [Instr]
     deps: list = field(default_factory=list)               # [(prd, cns, k)]
+    dep_linear: list = field(default_factory=list)         # per dep: 1 = linearized offset (extension), or empty
     tile_elems: int = 64
     ring_slots: list = field(default_factory=list)         # slots per ring
     n_accs: int = 0
@@ -115,6 +116,8 @@ class Program:
 
     def flat(self) -> dict:
         """Flat integer arrays (CSR) used by both the oracle and the library."""
+        if any(self.dep_linear) and len(self.dep_linear) != len(self.deps):
+            raise ValueError("dep_linear must have one flag per dependency")
         body_off, body = [0], []
         for items in self.body:
             body.extend(items)
@@ -140,6 +143,7 @@ class Program:
             instr_opcode=[ins.opcode for ins in self.instrs],
             instr_args=[list(ins.args) + [0] * (8 - len(ins.args)) for ins in self.instrs],
             deps=[tuple(d) for d in self.deps],
+            dep_linear=[int(x) for x in self.dep_linear] if any(self.dep_linear) else [],
             tile_elems=self.tile_elems,
             ring_slots=list(self.ring_slots) + [0] * (4 - len(self.ring_slots)),
             n_accs=self.n_accs,
@@ -191,12 +195,15 @@ class ProgramBuilder:
         self.p.blocks[self._open_block[cur]].append(iid)
         return iid
 
-    def dep(self, producer, consumer, offset: int):
+    def dep(self, producer, consumer, offset: int, linear: bool = False):
+        """``linear``: the offset counts iterations of the shared loop across
+        its trips (an extension of the paper's relation; see the C header)."""
         if isinstance(producer, str):
             producer = self.p.instr_id(producer)
         if isinstance(consumer, str):
             consumer = self.p.instr_id(consumer)
         self.p.deps.append((producer, consumer, offset))
+        self.p.dep_linear.append(1 if linear else 0)
 
     def build(self) -> Program:
         # Renumber instructions so that the concatenation of the blocks (in
