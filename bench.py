@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--outer", type=int, default=256)
     ap.add_argument("--n-gen", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-measured-peak", action="store_true",
+                    help="skip the copy / library-matmul measurement of achievable peaks")
     ap.add_argument("--modes", default="barrier_free,barrier")
     ap.add_argument("--k-unroll", type=int, default=0, choices=[0, 1, 2, 4, 8],
                     help="GEMM: K steps per copy of the loop bodies (static-trip unrolling)")
@@ -93,15 +95,55 @@ def time_mode(plan, bufs, trips, toff, n_wg, steps, warmup, **run_kw):
             "wall_ms_per_step": 1e3 * wall / steps}
 
 
+def measured_peak(bound):
+    """Achievable rates measured on this GPU next to the vendor peaks: a
+    device-to-device copy of 1 GiB (bytes read + written per second) for
+    HBM-bound kernels, the vendor library's bf16 matmul at 4096^3 and 8192^3
+    for MFMA-bound ones."""
+    import torch
+
+    def timed(fn, reps):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+    if bound == "hbm":
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        t = timed(lambda: dst.copy_(src), 5)
+        del src, dst
+        return {"copy_1GiB_gbs": 2.0 * (1 << 30) / t / 1e9}
+    res = {}
+    for n in (4096, 8192):
+        x = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+        w = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+        t = timed(lambda: torch.matmul(x, w), 10)
+        res[f"library_bf16_matmul_{n}_tflops"] = 2.0 * n ** 3 / t / 1e12
+        del x, w
+    return res
+
+
 def emit(out, a, kernel):
     """Attach the recorded HBM traffic of the kernel (when its profile matches
-    the current sources), run the copy that calibrates traffic counters if
-    asked, and print the JSON line."""
+    the current sources) and the achievable peaks measured on this GPU, run
+    the copy that calibrates traffic counters if asked, and print the JSON
+    line."""
     import torch
     from paper_2608_13757_amd.profiles import recorded_traffic
     tr = recorded_traffic(kernel)
     if tr is not None:
         out["roofline"]["traffic"] = tr
+    if not a.no_measured_peak:
+        mp = measured_peak(out["roofline"]["bound"])
+        best = max(mp.values())
+        mp["frac_of_measured"] = out["roofline"]["achieved"] / best
+        out["measured_peak"] = mp
     if a.copy_calibration_mib:
         src = torch.empty(a.copy_calibration_mib << 20, dtype=torch.uint8, device="cuda").fill_(1)
         dst = torch.empty_like(src)
