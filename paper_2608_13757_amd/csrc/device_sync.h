@@ -119,6 +119,19 @@ __device__ __forceinline__ void wait_vm_dyn(int n) {
   }
 }
 
+// Wait until at most n vector-memory operations are outstanding, rounding n
+// down to a value the wait instruction encodes (waiting for more is safe).
+__device__ __forceinline__ void wait_vm_atmost(uint32_t n) {
+  if (n >= 48) wait_vm<48>();
+  else if (n >= 32) wait_vm<32>();
+  else if (n >= 16) wait_vm<16>();
+  else if (n >= 8) wait_vm<8>();
+  else if (n >= 4) wait_vm<4>();
+  else if (n >= 2) wait_vm<2>();
+  else if (n >= 1) wait_vm<1>();
+  else wait_vm<0>();
+}
+
 // Only LDS operations completed (the engine's own LDS reads and writes).
 __device__ __forceinline__ void drain_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 

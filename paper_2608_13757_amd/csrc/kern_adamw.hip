@@ -56,17 +56,6 @@ struct AdamParams {
   uint32_t slot_bytes;
 };
 
-__device__ __forceinline__ void wait_vm_atmost(uint32_t n) {
-  if (n >= 48) wait_vm<48>();
-  else if (n >= 32) wait_vm<32>();
-  else if (n >= 16) wait_vm<16>();
-  else if (n >= 8) wait_vm<8>();
-  else if (n >= 4) wait_vm<4>();
-  else if (n >= 2) wait_vm<2>();
-  else if (n >= 1) wait_vm<1>();
-  else wait_vm<0>();
-}
-
 template <int kMode, bool kInstr>
 __global__ void __launch_bounds__(64 * 6) adamw_kernel(AdamParams P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];

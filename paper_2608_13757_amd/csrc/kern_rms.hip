@@ -71,19 +71,6 @@ struct RmsParams {
   uint32_t x_slot, q_slot, q_off, red_off;  // bytes: x slot, q slot (codes + trailer), q ring, reduction area
 };
 
-// Wait until at most n vector-memory operations are outstanding, rounding n
-// down to a value the wait instruction encodes (waiting for more is safe).
-__device__ __forceinline__ void wait_vm_atmost(uint32_t n) {
-  if (n >= 48) wait_vm<48>();
-  else if (n >= 32) wait_vm<32>();
-  else if (n >= 16) wait_vm<16>();
-  else if (n >= 8) wait_vm<8>();
-  else if (n >= 4) wait_vm<4>();
-  else if (n >= 2) wait_vm<2>();
-  else if (n >= 1) wait_vm<1>();
-  else wait_vm<0>();
-}
-
 // Sum and maximum over the 64 lanes: DPP within rows of 16, then the four
 // row results read from lanes 0, 16, 32, 48 (wave-uniform result).
 __device__ __forceinline__ float wave_sum(float v) {
