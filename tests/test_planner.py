@@ -143,6 +143,21 @@ def test_workload_programs():
     for L in (1, 64, 65, 300):
         a = attn_program(2)
         _check_against_oracle(a, TripTables([attn_worklist([L], 2).trips.per_wg[0]]))
+    # the second workloads of the paper's suite and the MoE program
+    from workloads import adamw_program, adamw_worklist, moe_program, moe_worklist, rmsnorm_program, \
+        rmsnorm_worklist
+    for rows in (1, 2, 7):
+        _, tt = rmsnorm_worklist(rows, 1)
+        _check_against_oracle(rmsnorm_program(rows, 1024, 2), tt)
+        _check_against_oracle(rmsnorm_program(rows, 1024, 2, 1, 3), tt)
+    for n in (256, 3000, 8192):
+        _, tt = adamw_worklist(n, 1024, 1)
+        _check_against_oracle(adamw_program(n, 1024, 2, 2), tt)
+        _check_against_oracle(adamw_program(n, 1024, 2, 3), tt)
+    for ph in (1, 2):
+        wl = moe_worklist(np.array([300, 0, 129, 1, 530]), ph, 256, 256)
+        for w in range(0, len(wl.trips.per_wg), 3):
+            _check_against_oracle(moe_program(ph, 256, 256), TripTables([wl.trips.per_wg[w]]))
 
 
 def test_moe_worklist_covers_every_tile_once():
