@@ -129,3 +129,19 @@ def test_planted_dropped_dependency_races():
     prog = copy.deepcopy(w.prog)
     prog.deps = [d for d in prog.deps if prog.instrs[d[1]].name != "ACQ_O"]
     assert _caught(prog, w.trips, {"values"})
+
+
+@pytest.mark.parametrize("per_instr", [False, True])
+def test_rmsnorm_adamw_schedules(per_instr):
+    """The paper's software-pipelined RMSNorm and AdamW programs (offsets
+    {0, 2}) on one workgroup of 7 steps: both issue predicates agree at every
+    reachable state and no schedule deadlocks."""
+    from workloads import adamw_program, adamw_worklist, rmsnorm_program, rmsnorm_worklist
+    cases = [(rmsnorm_program(7, 1024, 2), rmsnorm_worklist(7, 1)[1]),
+             (rmsnorm_program(7, 1024, 1, 1, 3), rmsnorm_worklist(7, 1)[1]),
+             (adamw_program(7 * 256, 256, 2, 2), adamw_worklist(7 * 256, 256, 1)[1])]
+    for prog, tt in cases:
+        m = _model(prog, tt, per_instr)
+        for s in range(6):
+            out = explore(m, s, issue_bias=(0.3, 0.6, 0.95)[s % 3])
+            assert out.ok, (s, out)
