@@ -395,7 +395,9 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   if (phase != 1 && phase != 2) return fail(BFS_E_UNSUPPORTED, "moe: phase 1 or 2");
   if (K <= 0 || K % kBK || N <= 0 || N % (phase == 1 ? 128 : 256))
     return fail(BFS_E_UNSUPPORTED, "moe: K a multiple of 32, N a multiple of 128 (phase 1) or 256 (phase 2)");
-  if (ring < 2 || ring > 4 || e_ring < 1 || e_ring > 2) return fail(BFS_E_UNSUPPORTED, "moe: ring 2..4, epilogue 1..2");
+  if (ring < 2 || ring > 5 || e_ring < 1 || e_ring > 2) return fail(BFS_E_UNSUPPORTED, "moe: ring 2..5, epilogue 1..2");
+  if (kCntBytes + (size_t)ring * kSlotBytes + (size_t)e_ring * kESlotBytes > 160 * 1024)
+    return fail(BFS_E_RESOURCE, "moe: ring and epilogue slots exceed 160 KiB of LDS");
   if ((uint64_t)N * K * 2 > 0xffffffffull) return fail(BFS_E_UNSUPPORTED, "moe: one expert's matrix must stay below 4 GiB");
   if (!has_dep(p, load, mma, 0) || !has_dep(p, mma, load, ring) || !has_dep(p, mma, acql, 1) ||
       !has_dep(p, spill, epi, 0) || !has_dep(p, epi, spill, e_ring) || !has_dep(p, epi, acqe, 1))
