@@ -10,16 +10,18 @@
 //                          base-2 domain: running max m, rescale factor
 //                          alpha = 2^(m_old - m_new), P = 2^(S c - m_new)
 //                          written as bf16 over S in place, running sum l.
-//   E3 (4 waves, MFMA)     PV: O = alpha O + P V for 32 query rows per wave
-//                          (fp32 accumulators), then NORM: O / l to HBM.
+//   E3 (4 waves, MFMA)     PREAD: the P fragments and alpha of the wave's 32
+//                          query rows into registers; PV: O = alpha O + P V
+//                          (fp32 accumulators); after the loop NORM: O / l
+//                          to HBM.
 //   E4 (1 wave, V load)    LOADV: the V block into a V ring slot.
 //
 // The KV loop runs ceil(L / 64) steps, a trip count known only at run time.
 // Dependencies (the program's; Eq. 5 on the engines' loop registers):
-// LOADK->QK, LOADV->PV, QK->SM, SM->PV (k = 0); QK->LOADK (k = K ring
-// depth), PV->LOADV (k = V ring depth), PV->QK (k = 2: the S/P slot, its
-// alpha row and P are free once PV has read them); SM->NORM (k = 0, C2: the
-// final row sums).
+// LOADK->QK, LOADV->PV, QK->SM, SM->PREAD (k = 0); QK->LOADK (k = K ring
+// depth), PV->LOADV (k = V ring depth), PREAD->QK (k = 2: the S/P slot and
+// its alpha row are free once PREAD holds them in registers, before the
+// MFMAs of PV); SM->NORM (k = 0, C2: the final row sums).
 //
 // Query rows of the tile beyond the sequence are computed on a clamped copy
 // of the last row and never stored; keys beyond the sequence in the last
@@ -45,8 +47,8 @@
 // Family contract (BFS_KERNEL_ATTN): loop KV below the top level holding
 // LOADK (E0, opcode 32, args [0, K ring depth, heads, 128]), LOADV (E4,
 // opcode 32, args [1, V ring depth, heads, 128]), QK (E1, 33), SM (E2, 34),
-// PV (E3, 35); NORM (E3, 36) at the top level; waves per engine 1, 2, 4, 4,
-// 1; the dependencies listed above.  Buffers: [0] work list int32 [n_wg][4]
+// PREAD (E3, 37), PV (E3, 35); NORM (E3, 36) at the top level; waves per
+// engine 1, 2, 4, 4, 1; the dependencies listed above.  Buffers: [0] work list int32 [n_wg][4]
 // = (first token of the sequence, length L, first query row of the tile,
 // head), [1] Q, [2] K, [3] V, [4] O, each bf16 [tokens][heads][128].  Trip
 // table: loop KV runs ceil(L / 64) steps (0 for an empty work item).
@@ -66,7 +68,7 @@ constexpr int kMaxPend = 3;                      // load groups in flight per lo
 
 struct AttnParams {
   SyncCommon sc;
-  InstrWaits loadk, loadv, qk, sm, pv, norm;
+  InstrWaits loadk, loadv, qk, sm, pread, pv, norm;
   const int32_t *work;
   const __bf16 *q, *k, *v;
   __bf16 *o;
@@ -357,25 +359,36 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
       voff[db] = vrow * 256u + 16u * (4u * ((uint32_t)db ^ x) + 2u * ((lane >> 4) & 1u) + ((lane >> 1) & 1u)) +
                  8u * (lane & 1u);
     S.sync_point(own);                                       // before loop KV
+    Site<2> s_pr;
+    S.enter(s_pr, P.pread, g, 1);
     S.enter(site, P.pv, g, 1);
     uint32_t vslot = 0;
     for (uint32_t it = 0; it < trip; ++it, vslot = (vslot + 1 == (uint32_t)P.nv) ? 0u : vslot + 1) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.wait(site, P.pv, g, it + 1, g.r1 - 1, [] {});
+      // PREAD: P and alpha of the step into registers, then the S/P slot is
+      // released (LDS executes this wave's reads before its signal)
+      S.wait(s_pr, P.pread, g, it + 1, g.r1 - 1, [] {});
+      bf16x8 pf[4];
+      float a = 1.0f;
       if (!S.aborted) {
         const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) pf[ks] = lds_frag(sp + pos16(qr + l32, 2u * (uint32_t)ks + lhi));
+        a = *(const BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + qr + l32) * 4u);
+      }
+      S.signal(P.pread.update, (uint32_t)ew);
+      S.wait(site, P.pv, g, it + 1, g.r1 - 1, [] {});
+      if (!S.aborted) {
         const uint32_t vb = vring + vslot * kKVSlot;
         auto vfrag = [&](int ks, int db) {
           const uint32_t va = vb + 16u * (uint32_t)ks * 256u + voff[db];
           const bf16x4 lo = lds_tr(va), hi = lds_tr(va + 4u * 256u);
           return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         };
-        // the first fragments are read before the rescale so that their
+        // the first V fragment is read before the rescale so that its
         // latency overlaps it
-        bf16x8 pf = lds_frag(sp + pos16(qr + l32, lhi));
         bf16x8 vf = vfrag(0, 0);
-        const float a = *(const BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + qr + l32) * 4u);
         // a block whose rows all keep their running maximum needs no rescale
         if (__builtin_amdgcn_ballot_w64(a != 1.0f) != 0) {
 #pragma unroll
@@ -384,19 +397,16 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
         // each V fragment is read one MFMA ahead of its use
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-          bf16x8 pf_next = pf;
-          if (ks < 3) pf_next = lds_frag(sp + pos16(qr + l32, 2u * (uint32_t)(ks + 1) + lhi));
 #pragma unroll
           for (int db = 0; db < 4; ++db) {
             bf16x8 vf_next = vf;
             if (db < 3) vf_next = vfrag(ks, db + 1);
             else if (ks < 3) vf_next = vfrag(ks + 1, 0);
-            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[db], 0, 0, 0);
+            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], acc[db], 0, 0, 0);
             if (db < 3 || ks < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             vf = vf_next;
           }
-          pf = pf_next;
         }
       }
       S.signal(P.pv.update, (uint32_t)ew);
@@ -443,7 +453,7 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   if (p->n_engines != 5) return fail(BFS_E_UNSUPPORTED, "attn: five engines");
   for (int e = 0; e < 5; ++e)
     if (p->waves_per_engine[e] != want_w[e]) return fail(BFS_E_UNSUPPORTED, "attn: engines of 1, 2, 4, 4, 1 waves");
-  int lk = -1, lv = -1, qk = -1, sm = -1, pv = -1, nm = -1;
+  int lk = -1, lv = -1, qk = -1, sm = -1, pr = -1, pv = -1, nm = -1;
   for (size_t i = 0; i < p->instr_engine.size(); ++i) {
     const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];
     const int32_t *a = &p->instr_args[8 * i];
@@ -451,12 +461,13 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
     else if (op == 32 && e == 4 && par == 1 && a[0] == 1 && lv < 0) lv = (int)i;
     else if (op == 33 && e == 1 && par == 1 && qk < 0) qk = (int)i;
     else if (op == 34 && e == 2 && par == 1 && sm < 0) sm = (int)i;
+    else if (op == 37 && e == 3 && par == 1 && pr < 0 && pv < 0) pr = (int)i;
     else if (op == 35 && e == 3 && par == 1 && pv < 0) pv = (int)i;
     else if (op == 36 && e == 3 && par == 0 && nm < 0) nm = (int)i;
     else return fail(BFS_E_UNSUPPORTED, "attn: unexpected instruction " + std::to_string(i));
   }
-  if (lk < 0 || lv < 0 || qk < 0 || sm < 0 || pv < 0 || nm < 0)
-    return fail(BFS_E_UNSUPPORTED, "attn: needs LOADK, LOADV, QK, SM, PV and NORM");
+  if (lk < 0 || lv < 0 || qk < 0 || sm < 0 || pr < 0 || pv < 0 || nm < 0)
+    return fail(BFS_E_UNSUPPORTED, "attn: needs LOADK, LOADV, QK, SM, PREAD, PV and NORM (PREAD before PV)");
   const int nk = p->instr_args[8 * lk + 1], nv = p->instr_args[8 * lv + 1];
   const int heads = p->instr_args[8 * lk + 2], dim = p->instr_args[8 * lk + 3];
   if (dim != kD || p->instr_args[8 * lv + 3] != kD) return fail(BFS_E_UNSUPPORTED, "attn: head dimension 128");
@@ -464,8 +475,8 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   const size_t lds = kCntBytes + (size_t)(nk + nv) * kKVSlot + 2 * kSPSlot + 3 * kBQ * 4;
   if (nk < 2 || nv < 2 || lds > 160 * 1024) return fail(BFS_E_UNSUPPORTED, "attn: ring depths >= 2 within 160 KiB of LDS");
   // the kernel's buffers are only race-free under these dependencies
-  if (!has_dep(p, lk, qk, 0) || !has_dep(p, lv, pv, 0) || !has_dep(p, qk, sm, 0) || !has_dep(p, sm, pv, 0) ||
-      !has_dep(p, qk, lk, nk) || !has_dep(p, pv, lv, nv) || !has_dep(p, pv, qk, 2) || !has_dep(p, sm, nm, 0))
+  if (!has_dep(p, lk, qk, 0) || !has_dep(p, lv, pv, 0) || !has_dep(p, qk, sm, 0) || !has_dep(p, sm, pr, 0) ||
+      !has_dep(p, qk, lk, nk) || !has_dep(p, pv, lv, nv) || !has_dep(p, pr, qk, 2) || !has_dep(p, sm, nm, 0))
     return fail(BFS_E_UNSUPPORTED, "attn: missing a ring, S/P or row-sum dependency");
   if (nbufs < 5) return fail(BFS_E_INVALID, "attn: needs [work, Q, K, V, O]");
   for (int i = 0; i < 5; ++i)
@@ -475,9 +486,10 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   const std::vector<DevWait> dw = device_waits(p);
   AttnParams P{};
   if (!fill_waits(p, dw, lk, P.loadk) || !fill_waits(p, dw, lv, P.loadv) || !fill_waits(p, dw, qk, P.qk) ||
-      !fill_waits(p, dw, sm, P.sm) || !fill_waits(p, dw, pv, P.pv) || !fill_waits(p, dw, nm, P.norm))
+      !fill_waits(p, dw, sm, P.sm) || !fill_waits(p, dw, pr, P.pread) || !fill_waits(p, dw, pv, P.pv) ||
+      !fill_waits(p, dw, nm, P.norm))
     return fail(BFS_E_RESOURCE, "attn: at most 4 waits per instruction");
-  if (!waits_fit({{&P.loadk, 2}, {&P.loadv, 2}, {&P.qk, 2}, {&P.sm, 2}, {&P.pv, 2}, {&P.norm, 1}}))
+  if (!waits_fit({{&P.loadk, 2}, {&P.loadv, 2}, {&P.qk, 2}, {&P.sm, 2}, {&P.pread, 2}, {&P.pv, 2}, {&P.norm, 1}}))
     return fail(BFS_E_RESOURCE, "attn: more waits on an instruction than its engine loop takes");
   P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
   P.work = static_cast<const int32_t *>(bufs[0]);

@@ -147,7 +147,7 @@ def test_attn_full_size_sampled():
 
 def test_attn_rejects_missing_dependency():
     prog = attn_program(2)
-    prog.deps = [d for d in prog.deps if not (prog.instrs[d[0]].name == "PV" and prog.instrs[d[1]].name == "QK")]
+    prog.deps = [d for d in prog.deps if not (prog.instrs[d[0]].name == "PREAD" and prog.instrs[d[1]].name == "QK")]
     plan = Plan(prog)
     t = torch.zeros(16, dtype=torch.int32, device="cuda")
     with pytest.raises(BfsError) as e:

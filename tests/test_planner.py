@@ -191,8 +191,8 @@ def test_fused_family_formulas():
     assert fg[("MMA", "SPILL")]["kase"] == 2 and fg[("BIAS", "SPILL")]["kase"] == 1
     a = attn_program(16, nk=3, nv=2)
     fa = {(a.instrs[p].name, a.instrs[c].name): f for (p, c, k), f in zip(a.deps, Plan(a).formulas())}
-    assert fa[("QK", "LOADK")]["k"] == 3 and fa[("PV", "LOADV")]["k"] == 2 and fa[("PV", "QK")]["k"] == 2
-    assert all(fa[x]["kase"] == 1 for x in [("LOADK", "QK"), ("QK", "SM"), ("SM", "PV"), ("LOADV", "PV")])
+    assert fa[("QK", "LOADK")]["k"] == 3 and fa[("PV", "LOADV")]["k"] == 2 and fa[("PREAD", "QK")]["k"] == 2
+    assert all(fa[x]["kase"] == 1 for x in [("LOADK", "QK"), ("QK", "SM"), ("SM", "PREAD"), ("LOADV", "PV")])
     assert fa[("SM", "NORM")]["kase"] == 2
     # the work list covers every (sequence, head, query tile) once, XCD-interleaved
     wl = attn_worklist([1, 64, 129, 300, 4096], 3)

@@ -19,7 +19,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .program import (OP_ADDC, OP_MOE_EPI, OP_MOE_LOAD, OP_MOE_MMA, OP_MOE_SPILL, OP_ATTN_LOAD, OP_ATTN_NORM, OP_ATTN_PV, OP_ATTN_QK, OP_ATTN_SM,
+from .program import (OP_ADDC, OP_MOE_EPI, OP_MOE_LOAD, OP_MOE_MMA, OP_MOE_SPILL, OP_ATTN_LOAD, OP_ATTN_NORM, OP_ATTN_PREAD, OP_ATTN_PV, OP_ATTN_QK, OP_ATTN_SM,
                       OP_GEMM_BIAS, OP_GEMM_EPI, OP_GEMM_LOAD, OP_GEMM_MMA,
                       OP_GEMM_SPILL, OP_LOAD, OP_NOP, OP_SCALE_ACC, OP_STORE_ACC,
                       OP_ADAM_LOAD, OP_ADAM_STORE, OP_ADAM_UPDATE, OP_RMS_LOAD, OP_RMS_NORM, OP_RMS_STORE,
@@ -500,13 +500,15 @@ def attn_program(heads: int, dim: int = ATTN_D, nk: int = 3, nv: int = 2) -> Pro
           E4: LOADV V block -> vring[(rhat_KV - 1) % nv]
           E1: QK    S = Q K^T -> sp[(rhat_KV - 1) % 2]
           E2: SM    online softmax: P over S in place, alpha, running sum l
+          E3: PREAD P and alpha of the step into registers
           E3: PV    O = alpha O + P V }
       E3: NORM  O / l -> output
 
     The KV loop's trip count is ceil(L / 64) for the sequence's length L.
-    LOADK->QK, LOADV->PV, QK->SM, SM->PV (k=0) carry the data forward;
-    QK->LOADK (k=nk) and PV->LOADV (k=nv) free ring slots; PV->QK (k=2) frees
-    an S/P slot; SM->NORM (k=0, producer nested in KV) delivers the final row
+    LOADK->QK, LOADV->PV, QK->SM, SM->PREAD (k=0) carry the data forward;
+    QK->LOADK (k=nk) and PV->LOADV (k=nv) free ring slots; PREAD->QK (k=2)
+    frees an S/P slot as soon as its P is held in registers, before the PV
+    MFMAs; SM->NORM (k=0, producer nested in KV) delivers the final row
     sums."""
     b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 4, 4, 1])
     with b.loop("KV"):
@@ -514,15 +516,16 @@ def attn_program(heads: int, dim: int = ATTN_D, nk: int = 3, nv: int = 2) -> Pro
         b.instr(4, OP_ATTN_LOAD, [1, nv, heads, dim, 0, 0, 0, 0], name="LOADV")
         b.instr(1, OP_ATTN_QK, [0] * 8, name="QK")
         b.instr(2, OP_ATTN_SM, [0] * 8, name="SM")
+        b.instr(3, OP_ATTN_PREAD, [0] * 8, name="PREAD")
         b.instr(3, OP_ATTN_PV, [0] * 8, name="PV")
     b.instr(3, OP_ATTN_NORM, [0] * 8, name="NORM")
     b.dep("LOADK", "QK", 0)
     b.dep("LOADV", "PV", 0)
     b.dep("QK", "SM", 0)
-    b.dep("SM", "PV", 0)
+    b.dep("SM", "PREAD", 0)
     b.dep("QK", "LOADK", nk)
     b.dep("PV", "LOADV", nv)
-    b.dep("PV", "QK", ATTN_SP)
+    b.dep("PREAD", "QK", ATTN_SP)
     b.dep("SM", "NORM", 0)
     return b.build()
 

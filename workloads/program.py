@@ -53,6 +53,7 @@ OP_ATTN_QK = 33
 OP_ATTN_SM = 34
 OP_ATTN_PV = 35
 OP_ATTN_NORM = 36
+OP_ATTN_PREAD = 37     # P fragments and alpha of the step into the PV waves' registers
 OP_MOE_LOAD = 48       # args: phase (1 gate/up, 2 down), K, N, ring depth
 OP_MOE_MMA = 49
 OP_MOE_EPI = 50
