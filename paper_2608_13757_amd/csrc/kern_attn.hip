@@ -118,13 +118,13 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
   const int wg = blockIdx.x;
   // hardware wave -> (engine, wave within the engine), hardware wave w on
   // SIMD w % 4: the two QK waves on SIMDs 0 and 1, the four PV waves two
-  // each on SIMDs 2 and 3 (equal MFMA work per SIMD), softmax on 0 and 1,
-  // the K and V loaders on 2 and 3
+  // each on SIMDs 2 and 3 (equal MFMA work per SIMD), one softmax wave per
+  // SIMD (equal VALU work), the K and V loaders on 0 and 1
   int eng, ew, canon;                       // canon: engine-ordered wave index
   if (hw < 2) { eng = 1; ew = hw; canon = 1 + ew; }
-  else if (hw == 2 || hw == 3 || hw == 6 || hw == 7) { eng = 3; ew = (hw & 1) + ((hw >> 2) << 1); canon = 7 + ew; }
-  else if (hw == 4 || hw == 5 || hw == 8 || hw == 9) { eng = 2; ew = (hw & 1) + ((hw >> 3) << 1); canon = 3 + ew; }
-  else if (hw == 10) { eng = 0; ew = 0; canon = 0; }
+  else if (hw == 2 || hw == 3 || hw == 10 || hw == 11) { eng = 3; ew = (hw & 1) + ((hw >> 3) << 1); canon = 7 + ew; }
+  else if (hw < 8) { eng = 2; ew = hw - 4; canon = 3 + ew; }
+  else if (hw == 8) { eng = 0; ew = 0; canon = 0; }
   else { eng = 4; ew = 0; canon = 11; }
   Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), canon, wg);
   const uint32_t own = S.word((uint32_t)eng, (uint32_t)ew);   // barrier mode: one counter per engine
