@@ -242,6 +242,10 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
             bf16x8 a_next = a_cur;
             if (bm < 3) {
               a_next = rd(a_base, arow + 32u * (bm + 1), c);
+              // the step's last fragment read is issued: MMA retires from
+              // the slot (LDS executes this wave's reads before the signal
+              // that follows them; the remaining MFMAs use registers only)
+              if (s == 1 && bm == 2) S.signal(P.mma.update, ew);
             } else if (s == 0) {
               nb0 = rd(b_base, brow, c + 2u);
               nb1 = rd(b_base, brow + 32u, c + 2u);
@@ -254,8 +258,9 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
           b0 = nb0;
           b1 = nb1;
         }
+      } else {
+        S.signal(P.mma.update, ew);
       }
-      S.signal(P.mma.update, ew);
       S.sync_point(S.word(1, ew));                          // end of a K iteration (barrier mode)
       slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1;
     };

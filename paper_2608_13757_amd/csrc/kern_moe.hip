@@ -258,6 +258,10 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
           bf16x8 b0 = rd(b_base, brow0, lhi), b1 = rd(b_base, brow1, lhi);
           const bf16x8 a0n = rd(a_base, arow, 2u + lhi), a1n = rd(a_base, arow + 32u, 2u + lhi);
           const bf16x8 b0n = rd(b_base, brow0, 2u + lhi), b1n = rd(b_base, brow1, 2u + lhi);
+          // MMA retires from the slot once its fragments are read: LDS
+          // executes this wave's reads before the signal that follows them,
+          // and the MFMAs below use registers only
+          S.signal(P.mma.update, ew);
           acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a0, acc[0], 0, 0, 0);
           acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a1, acc[1], 0, 0, 0);
           acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a0, acc[2], 0, 0, 0);
@@ -266,8 +270,9 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
           acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0n, a1n, acc[1], 0, 0, 0);
           acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a0n, acc[2], 0, 0, 0);
           acc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a1n, acc[3], 0, 0, 0);
+        } else {
+          S.signal(P.mma.update, ew);
         }
-        S.signal(P.mma.update, ew);
         S.sync_point(S.word(1, ew));                              // end of a K iteration
       }
       mark = S.elapsed();
