@@ -580,7 +580,7 @@ MOE_BK = 32                  # K step per ring slot
 MOE_BN = {1: 128, 2: 256}    # output columns per workgroup: h columns (phase 1), y columns (phase 2)
 MOE_CHUNKS = {1: 2, 2: 4}    # epilogue chunks per M-tile
 MOE_RING = 5
-MOE_MCHUNK = 8               # at most this many M-tiles per workgroup
+MOE_MCHUNK = 4               # at most this many M-tiles per workgroup
 
 
 def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring: int = 2) -> Program:
