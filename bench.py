@@ -39,6 +39,10 @@ def parse():
     ap.add_argument("--no-measured-peak", action="store_true",
                     help="skip the copy / library-matmul measurement of achievable peaks")
     ap.add_argument("--modes", default="barrier_free,barrier")
+    ap.add_argument("--moe-ring", default="linear", choices=["linear", "acq"],
+                    help="MoE: protect the load ring across M-tiles with the linearized MMA->LOAD dependency "
+                         "(an extension of the paper's relation) or with the paper's acquire instruction that "
+                         "drains the ring at every M-tile (MMA->ACQL, k = 1)")
     ap.add_argument("--k-unroll", type=int, default=0, choices=[0, 1, 2, 4, 8],
                     help="GEMM: K steps per copy of the loop bodies (static-trip unrolling)")
     ap.add_argument("--alloc", default="per_loop", choices=["per_loop", "per_instr"],
@@ -318,7 +322,8 @@ def bench_moe(a):
     res = {}
     for name in a.modes.split(","):
         mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
-        plans = {ph: Plan(moe_program(ph, H, F), mode, alloc_of(a, mode)) for ph in (1, 2)}
+        plans = {ph: Plan(moe_program(ph, H, F, linear=a.moe_ring == "linear"), mode, alloc_of(a, mode))
+                 for ph in (1, 2)}
 
         def step():
             for ph in (1, 2):
@@ -360,7 +365,9 @@ def bench_moe(a):
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "MoE grouped GEMM, 32768 tokens top-1 to 64 experts (Zipf 1.1 counts), hidden 4096, "
                                "ffn 1408, SiLU-gated, bf16 weights N(0,0.02); gate/up launch + down launch",
-                   "tokens": T, "experts": len(c), "hidden": H, "ffn": F, "parallelism": "single GPU"},
+                   "tokens": T, "experts": len(c), "hidden": H, "ffn": F,
+                   "ring_across_m_tiles": "linearized MMA->LOAD (extension)" if a.moe_ring == "linear"
+                   else "ACQL drain (paper's relation)", "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
         "phase_us": {kk: [v["phase1_ms"] * 1e3, v["phase2_ms"] * 1e3] for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",

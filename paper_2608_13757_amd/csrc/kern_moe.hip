@@ -24,7 +24,12 @@
 // (phase 2) chunks per M-tile.  Dependencies: LOAD->MMA (k = 0), MMA->LOAD
 // (k = ring), MMA->ACQL (k = 1, C3: an M-tile's loads start after the
 // previous tile's MFMAs released the ring), SPILL->EPI (k = 0), EPI->SPILL
-// (k = epilogue slots), EPI->ACQE (k = 1, C3).  Token rows past the expert's
+// (k = epilogue slots), EPI->ACQE (k = 1, C3).  In place of MMA->ACQL the
+// program may read MMA->LOAD with the linearized offset (an extension of
+// the paper's relation: k counts K steps over all M-tiles of the
+// workgroup), which orders exactly the reuse of ring slot (r_K - 1) % ring
+// across M-tiles, so the next tile's loads overlap the previous tile's
+// MFMAs; ACQL then waits for nothing.  Token rows past the expert's
 // count are loaded from a clamped row and never stored.
 //
 // LDS (bytes): counters 2048 | ring slots of 24 KiB (token rows 128 x 64 B,
@@ -404,7 +409,13 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   if (kCntBytes + (size_t)ring * kSlotBytes + (size_t)e_ring * kESlotBytes > 160 * 1024)
     return fail(BFS_E_RESOURCE, "moe: ring and epilogue slots exceed 160 KiB of LDS");
   if ((uint64_t)N * K * 2 > 0xffffffffull) return fail(BFS_E_UNSUPPORTED, "moe: one expert's matrix must stay below 4 GiB");
-  if (!has_dep(p, load, mma, 0) || !has_dep(p, mma, load, ring) || !has_dep(p, mma, acql, 1) ||
+  // the ring is protected across M-tiles either by MMA->ACQL (k = 1) or by
+  // reading MMA->LOAD with the linearized offset (slots are indexed by r_K)
+  bool ring_linear = false;
+  for (size_t d = 0; d < p->deps.size() / 3; ++d)
+    if (p->deps[3 * d] == mma && p->deps[3 * d + 1] == load && p->deps[3 * d + 2] == ring && p->dep_linear[d])
+      ring_linear = true;
+  if (!has_dep(p, load, mma, 0) || !has_dep(p, mma, load, ring) || !(ring_linear || has_dep(p, mma, acql, 1)) ||
       !has_dep(p, spill, epi, 0) || !has_dep(p, epi, spill, e_ring) || !has_dep(p, epi, acqe, 1))
     return fail(BFS_E_UNSUPPORTED, "moe: missing a ring or M-tile dependency");
   const int need = phase == 1 ? 7 : 6;

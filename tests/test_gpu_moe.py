@@ -66,10 +66,10 @@ class MoeRun:
             return [work, self.perm, self.eoff, self.x, self.wg, self.wu, self.h]
         return [work, self.perm, self.eoff, self.h, self.wd, self.y]
 
-    def run(self, mode, cap=0, alloc=ALLOC_PER_LOOP):
+    def run(self, mode, cap=0, alloc=ALLOC_PER_LOOP, linear=False):
         logs = {}
         for ph in (1, 2):
-            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn), mode, alloc)
+            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn, linear=linear), mode, alloc)
             work, trips, toff, n_wg = self.dev_wl[ph]
             log = None
             if cap:
@@ -120,6 +120,45 @@ def test_moe_small_parity_and_thresholds():
             assert compare_wave_logs_with_oracle(prog, plan, lg, recs, name) > 0
         outs[name] = y
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_moe_linear_ring_parity_and_thresholds():
+    """MMA->LOAD read with the linearized offset (an extension) in place of
+    the M-tile drain: outputs equal the oracle's and, bit for bit, the
+    drained program's in both modes; every logged barrier-free threshold
+    equals the brute force of the linearized relation (the paper's for the
+    other dependencies), across M-tile boundaries (runs of 3 M-tiles)."""
+    moe = moe_inputs(seed=2, hidden=256, ffn=256, counts=SMALL_COUNTS)
+    r = MoeRun(moe, mchunk=3)
+    T = len(moe.assign)
+    ref_y = mathref.moe_tokens(moe, range(T))
+    ref_h = mathref.moe_hidden(moe, moe.perm)
+    _say("[moe-linear] drained program")
+    h0, y0, _ = r.run(MODE_BARRIER_FREE)
+    for name, mode in MODES:
+        _say(f"[moe-linear] mode={name}")
+        h, y, logs = r.run(mode, cap=64, linear=True)
+        check_close(h, ref_h)
+        check_close(y, ref_y)
+        assert np.array_equal(h.view(np.uint32), h0.view(np.uint32))
+        assert np.array_equal(y.view(np.uint32), y0.view(np.uint32))
+        if name != "barrier_free":
+            continue
+        for ph in (1, 2):
+            plan, logw = logs[ph]
+            prog = moe_program(ph, moe.hidden, moe.ffn, linear=True)
+            d_lin = [i for i, x in enumerate(prog.dep_linear) if x]
+            wl = r.wl[ph]
+            trips, off = wl.trips.flat()
+            recs = {}
+            for g in range(wl.trips.n_wg):
+                res = core.run(prog, trips, off[g], g)
+                rr = res.recs.copy()
+                for d in d_lin:
+                    rr[rr["dep"] == d] = core.linearized_records(prog, res, d)
+                recs[g] = rr
+            lg = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
+            assert compare_wave_logs_with_oracle(prog, plan, lg, recs, name) > 0
 
 
 def test_moe_per_instr():

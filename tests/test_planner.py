@@ -160,10 +160,42 @@ def test_workload_programs():
             _check_against_oracle(moe_program(ph, 256, 256), TripTables([wl.trips.per_wg[w]]))
 
 
+def test_moe_linear_ring_thresholds():
+    """The MoE program with MMA->LOAD read linearized (an extension): the
+    planner's thresholds equal the brute force of the linearized relation at
+    every consumer instance, across M-tile boundaries (runs of 2 and 3
+    M-tiles), and the paper's relation for every other dependency."""
+    from workloads import moe_program, moe_worklist
+    checked = 0
+    for ph in (1, 2):
+        prog = moe_program(ph, 256, 256, ring=3, linear=True)
+        d_lin = [i for i, (p, c, k) in enumerate(prog.deps)
+                 if (prog.instrs[p].name, prog.instrs[c].name) == ("MMA", "LOAD")]
+        assert d_lin and prog.dep_linear[d_lin[0]] == 1
+        assert not any((prog.instrs[p].name, prog.instrs[c].name) == ("MMA", "ACQL") for p, c, k in prog.deps)
+        plan = Plan(prog)
+        assert plan.formulas()[d_lin[0]]["kase"] == 6
+        wl = moe_worklist(np.array([300, 0, 129, 1, 530]), ph, 256, 256, mchunk=3)
+        for per in wl.trips.per_wg:
+            if int(per[1][0]) < 2:
+                continue
+            tt = TripTables([per])
+            trips, off = tt.flat()
+            res = core.run(prog, trips, off[0], 0)
+            for d in range(len(prog.deps)):
+                recs = res.recs[res.recs["dep"] == d]
+                want = core.linearized_records(prog, res, d)["sem_thr"] if d == d_lin[0] else recs["sem_thr"]
+                got = [plan.eval_threshold(d, int(r["r_P"]), int(r["rhat_S"])) for r in recs]
+                assert got == [int(x) for x in want], (ph, d)
+                checked += len(recs)
+    assert checked > 200
+
+
 def test_moe_worklist_covers_every_tile_once():
     """Every (expert, output tile, M-tile) of both phases appears in exactly
-    one work item, runs hold at most 8 M-tiles, trips match."""
+    one work item, runs hold at most MOE_MCHUNK M-tiles, trips match."""
     from workloads import MOE_BM, MOE_BN, moe_worklist
+    from workloads.configs import MOE_MCHUNK
     from workloads.tensors import zipf_counts
     for counts in (zipf_counts(32768, 64), np.array([300, 0, 129, 1, 530])):
         for ph, (hidden, ffn) in ((1, (4096, 1408)), (2, (4096, 1408)), (1, (256, 256)), (2, (256, 256))):
@@ -171,7 +203,7 @@ def test_moe_worklist_covers_every_tile_once():
             n_dim = ffn if ph == 1 else hidden
             seen = set()
             for (e, n0, mt0, n_mt), tr in zip(wl.work.tolist(), wl.trips.per_wg):
-                assert int(tr[1][0]) == n_mt and len(tr[2]) == n_mt and n_mt <= 8
+                assert int(tr[1][0]) == n_mt and len(tr[2]) == n_mt and n_mt <= MOE_MCHUNK
                 for m in range(mt0, mt0 + n_mt):
                     key = (e, n0, m)
                     assert key not in seen

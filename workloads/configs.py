@@ -583,7 +583,8 @@ MOE_RING = 5
 MOE_MCHUNK = 4               # at most this many M-tiles per workgroup
 
 
-def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring: int = 2) -> Program:
+def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring: int = 2,
+                linear: bool = False) -> Program:
     """One workgroup per (expert, N-tile, run of M-tiles); phase 1 computes
     h = SiLU(x W_gate) * (x W_up) for 128 h columns, phase 2 y = h W_down for
     256 y columns:
@@ -598,7 +599,13 @@ def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring:
     and MMA->LOAD (k=ring) protect the ring inside an M-tile, MMA->ACQL (k=1,
     C3) across M-tiles (the next tile's loads reuse the slots); SPILL->EPI
     (k=0) and EPI->SPILL (k=e_ring) protect the epilogue ring inside an
-    M-tile, EPI->ACQE (k=1, C3) across M-tiles."""
+    M-tile, EPI->ACQE (k=1, C3) across M-tiles.
+
+    ``linear``: MMA->LOAD is read with the linearized offset (an extension,
+    not the paper's relation: k counts K iterations over all M-tiles of the
+    workgroup, and the ring slot is (r_K - 1) % ring), which protects the
+    ring across M-tiles by itself, so MMA->ACQL is dropped and the next
+    tile's loads may start while the MFMAs of the previous tile run."""
     k_dim, n_dim = (hidden, ffn) if phase == 1 else (ffn, hidden)
     b = ProgramBuilder("moe", n_engines=3, waves_per_engine=[2, 8, 2])
     with b.loop("M"):
@@ -611,8 +618,9 @@ def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring:
             b.instr(1, OP_MOE_SPILL, [e_ring, 0, 0, 0, 0, 0, 0, 0], name="SPILL")
             b.instr(2, OP_MOE_EPI, [0] * 8, name="EPI")
     b.dep("LOAD", "MMA", 0)
-    b.dep("MMA", "LOAD", ring)
-    b.dep("MMA", "ACQL", 1)
+    b.dep("MMA", "LOAD", ring, linear=linear)
+    if not linear:
+        b.dep("MMA", "ACQL", 1)
     b.dep("SPILL", "EPI", 0)
     b.dep("EPI", "SPILL", e_ring)
     b.dep("EPI", "ACQE", 1)
