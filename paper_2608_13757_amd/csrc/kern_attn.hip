@@ -1,5 +1,7 @@
-// Variable-length attention forward (no causal mask), one workgroup per
-// (sequence, head, 128-query tile), five engines synchronized by LDS counters:
+// Variable-length attention forward (no causal mask).  A fixed set of
+// workgroups (one per compute unit) each runs a run-time list of (sequence,
+// head, 128-query tile) work items, with five engines synchronized by LDS
+// counters:
 //
 //   E0 (1 wave, K load)    LOADK: the 64 x 128 bf16 K block of the step into
 //                          a K ring slot with direct-to-LDS loads.
@@ -16,12 +18,18 @@
 //                          to HBM.
 //   E4 (1 wave, V load)    LOADV: the V block into a V ring slot.
 //
-// The KV loop runs ceil(L / 64) steps, a trip count known only at run time.
-// Dependencies (the program's; Eq. 5 on the engines' loop registers):
-// LOADK->QK, LOADV->PV, QK->SM, SM->PREAD (k = 0); QK->LOADK (k = K ring
-// depth), PV->LOADV (k = V ring depth), PREAD->QK (k = 2: the S/P slot and
-// its alpha row are free once PREAD holds them in registers, before the
-// MFMAs of PV); SM->NORM (k = 0, C2: the final row sums).
+// Loops top -> T -> KV: T runs the workgroup's tiles, KV ceil(L / 64) steps
+// of a tile; both trips are known only at run time.  Dependencies (the
+// program's; Eq. 5 on the engines' loop registers): LOADK->QK, LOADV->PV,
+// QK->SM, SM->PREAD (k = 0); QK->LOADK (k = K ring depth), PV->LOADV (k = V
+// ring depth), PREAD->QK (k = 2: the S/P slot and its alpha row are free
+// once PREAD holds them in registers, before the MFMAs of PV), these three
+// read with the linearized offset (an extension of the paper's relation:
+// ring slots and S/P slots follow r_KV over all tiles, so the next tile's
+// loads and QK steps overlap the end of the previous tile); SM->NORM (k = 0,
+// C2: the tile's final row sums); NORM->SM (k = 2 at T: the row sums are
+// double-buffered by tile, and a tile's softmax overwrites a buffer only
+// after NORM of the tile before last has read it).
 //
 // Query rows of the tile beyond the sequence are computed on a clamped copy
 // of the last row and never stored; keys beyond the sequence in the last
@@ -32,7 +40,7 @@
 // of row r at c ^ 4 (r mod 4), the layout the transposing fragment reads need
 // to be conflict-free) | 2 S/P slots of 32 KiB (S fp32 [128][64]: 16-byte
 // chunk c of row r at c ^ (r mod 16); P bf16 overwrites it with 8 chunks per
-// row at the same permutation) | alpha [2][128] fp32 | l [128] fp32.
+// row at the same permutation) | alpha [2][128] fp32 | l [2][128] fp32.
 //
 // MFMA v_mfma_f32_32x32x16_bf16: lane l supplies row l % 32 of the first
 // operand and column l % 32 of the second, k = 8 (l / 32) .. + 7, and holds
@@ -44,14 +52,17 @@
 // from two ds_read_b64_tr_b16: within each group of 16 lanes, lane i receives
 // element i % 4 of the 8 bytes addressed by lane 4 j + i / 4 as its element j.
 //
-// Family contract (BFS_KERNEL_ATTN): loop KV below the top level holding
-// LOADK (E0, opcode 32, args [0, K ring depth, heads, 128]), LOADV (E4,
-// opcode 32, args [1, V ring depth, heads, 128]), QK (E1, 33), SM (E2, 34),
-// PREAD (E3, 37), PV (E3, 35); NORM (E3, 36) at the top level; waves per
-// engine 1, 2, 4, 4, 1; the dependencies listed above.  Buffers: [0] work list int32 [n_wg][4]
-// = (first token of the sequence, length L, first query row of the tile,
-// head), [1] Q, [2] K, [3] V, [4] O, each bf16 [tokens][heads][128].  Trip
-// table: loop KV runs ceil(L / 64) steps (0 for an empty work item).
+// Family contract (BFS_KERNEL_ATTN): loop T below the top level and loop KV
+// in T, KV holding LOADK (E0, opcode 32, args [0, K ring depth, heads,
+// 128]), LOADV (E4, opcode 32, args [1, V ring depth, heads, 128]), QK (E1,
+// 33), SM (E2, 34), PREAD (E3, 37), PV (E3, 35); NORM (E3, 36) in T after
+// KV; waves per engine 1, 2, 4, 4, 1; the dependencies listed above.
+// Buffers: [0] work list int32 [rows][4] = (first token of the sequence,
+// length L, first query row of the tile, head), tile t of workgroup w at
+// row w + t * n_wg (the caller provides every row its trip tables reach),
+// [1] Q, [2] K, [3] V, [4] O, each bf16 [tokens][heads][128].  Trip table
+// per workgroup: T runs its number of tiles, KV ceil(L / 64) steps for
+// each (0 for an empty work item).
 #include <string>
 
 #include "engine_sync.h"
@@ -129,16 +140,32 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
   Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), canon, wg);
   const uint32_t own = S.word((uint32_t)eng, (uint32_t)ew);   // barrier mode: one counter per engine
 
-  const int32_t s0 = ldc(P.work + 4 * wg + 0), L = ldc(P.work + 4 * wg + 1);
-  const int32_t q0 = ldc(P.work + 4 * wg + 2), head = ldc(P.work + 4 * wg + 3);
-  const int64_t *toff = P.trip_off + (int64_t)wg * 2;
-  uint32_t trip = (uint32_t)ldc(P.trips + ldc(toff + 1));
-  const uint32_t max_trip = L > 0 ? (uint32_t)((L + kBKV - 1) / kBKV) : 0u;
-  if (trip > max_trip) {
-    report_input(P.sc.err, 1u, (uint32_t)wg, 1u, trip, max_trip, (uint32_t)hw);
-    trip = max_trip;
-  }
+  const int64_t *toff = P.trip_off + (int64_t)wg * 3;
+  const uint32_t trip_t = (uint32_t)ldc(P.trips + ldc(toff + 1));
+  const int64_t kv_off = ldc(toff + 2);
   const size_t row_stride = (size_t)P.heads * kD;     // elements between tokens
+  // tile t of this workgroup: row wg + t * n_wg of the work list, its KV
+  // trip from the trip table (a trip beyond the sequence is reported and
+  // clamped)
+  struct Tile {
+    int32_t s0, L, q0, head;
+    uint32_t trip;
+  };
+  auto tile = [&](uint32_t t) {
+    const int64_t row = (int64_t)wg + (int64_t)t * gridDim.x;
+    Tile x;
+    x.s0 = ldc(P.work + 4 * row + 0);
+    x.L = ldc(P.work + 4 * row + 1);
+    x.q0 = ldc(P.work + 4 * row + 2);
+    x.head = ldc(P.work + 4 * row + 3);
+    x.trip = (uint32_t)ldc(P.trips + kv_off + t);
+    const uint32_t max_trip = x.L > 0 ? (uint32_t)((x.L + kBKV - 1) / kBKV) : 0u;
+    if (x.trip > max_trip) {
+      report_input(P.sc.err, 1u, (uint32_t)wg, t, x.trip, max_trip, (uint32_t)hw);
+      x.trip = max_trip;
+    }
+    return x;
+  };
   Regs g;
   Site<2> site;
   uint64_t mark = 0;
@@ -149,7 +176,6 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
     const InstrWaits &iw = is_v ? P.loadv : P.loadk;
     const uint32_t depth = (uint32_t)(is_v ? P.nv : P.nk);
     const uint32_t ring = is_v ? vring : kring;
-    const __bf16 *base = (is_v ? P.v : P.k) + (size_t)head * kD;
     int pending = 0;
     auto retire_one = [&]() {
       if (pending == 3) wait_vm<32>();
@@ -180,261 +206,301 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
       const uint32_t chunk = is_v ? (pos ^ (rr << 2)) : (pos ^ (row & 15u));
       voff[j] = (row * (uint32_t)row_stride + 8u * chunk) * 2u;
     }
-    S.sync_point(own);                                       // before loop KV
-    S.enter(site, iw, g, 1);
+    // ring slots follow r_KV over all tiles: a tile's loads go on where the
+    // previous tile's stopped, ordered by the linearized ring dependency
     uint32_t slot = 0;
-    for (uint32_t it = 0; it < trip; ++it, slot = (slot + 1 == depth) ? 0u : slot + 1) {
+    S.sync_point(own);                                       // before loop T
+    for (uint32_t t = 0; t < trip_t; ++t) {
       g.r1 += 1;
-      g.h1 = it + 1;
-      S.wait(site, iw, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
-      if (!S.aborted) {
-        const uint32_t dst = ring + slot * kKVSlot;
-        const int32_t key0 = (int32_t)it * kBKV;
-        if (key0 + kBKV <= L) {
-          const char *sb = reinterpret_cast<const char *>(base + (size_t)(s0 + key0) * row_stride);
+      g.h1 = t + 1;
+      const Tile x = tile(t);
+      const __bf16 *base = (is_v ? P.v : P.k) + (size_t)x.head * kD;
+      S.sync_point(own);                                     // before loop KV
+      S.enter(site, iw, g, 2);
+      for (uint32_t it = 0; it < x.trip; ++it, slot = (slot + 1 == depth) ? 0u : slot + 1) {
+        g.r2 += 1;
+        g.h2 = it + 1;
+        S.wait(site, iw, g, it + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
+        if (!S.aborted) {
+          const uint32_t dst = ring + slot * kKVSlot;
+          const int32_t key0 = (int32_t)it * kBKV;
+          if (key0 + kBKV <= x.L) {
+            const char *sb = reinterpret_cast<const char *>(base + (size_t)(x.s0 + key0) * row_stride);
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            asm volatile("" : "+v"(voff[j]));   // keep the offset a 32-bit value at its use
-            __builtin_amdgcn_global_load_lds((const void *)(sb + voff[j]), (BFS_LDS void *)(uintptr_t)(dst + 1024u * j),
-                                             16, 0, 0);
+            for (int j = 0; j < 16; ++j) {
+              asm volatile("" : "+v"(voff[j]));   // keep the offset a 32-bit value at its use
+              __builtin_amdgcn_global_load_lds((const void *)(sb + voff[j]),
+                                               (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
+            }
+          } else {
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+              const uint32_t row = 4u * j + rr;
+              const uint32_t chunk = is_v ? (pos ^ (rr << 2)) : (pos ^ (row & 15u));
+              const int32_t key = min(key0 + (int32_t)row, x.L - 1);
+              const __bf16 *src = base + (size_t)(x.s0 + key) * row_stride + 8u * chunk;
+              __builtin_amdgcn_global_load_lds((const void *)src, (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16,
+                                               0, 0);
+            }
           }
+          pending += 1;
+          if (pending == kMaxPend) retire_one();
         } else {
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const uint32_t row = 4u * j + rr;
-            const uint32_t chunk = is_v ? (pos ^ (rr << 2)) : (pos ^ (row & 15u));
-            const int32_t key = min(key0 + (int32_t)row, L - 1);
-            const __bf16 *src = base + (size_t)(s0 + key) * row_stride + 8u * chunk;
-            __builtin_amdgcn_global_load_lds((const void *)src, (BFS_LDS void *)(uintptr_t)(dst + 1024u * j), 16, 0, 0);
-          }
+          S.signal(iw.update, 0);
         }
-        pending += 1;
-        if (pending == kMaxPend) retire_one();
-      } else {
-        S.signal(iw.update, 0);
+        if (kMode == BFS_MODE_BARRIER) {
+          retire_all();
+          S.sync_point(own);                                 // end of a KV iteration
+        }
       }
-      if (kMode == BFS_MODE_BARRIER) {
-        retire_all();
-        S.sync_point(own);                                   // end of a KV iteration
-      }
+      if (kMode == BFS_MODE_BARRIER) retire_all();
+      S.sync_point(own);                                     // end of a T iteration
     }
     retire_all();
   } else if (eng == 1) {
     // ---------------------------------------------------------- QK^T engine
     const uint32_t qr = 64u * ew;
-    bf16x8 qf[2][8];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      const int32_t row = min(q0 + (int32_t)(qr + 32u * qb + l32), L - 1);
-      const __bf16 *src = P.q + (size_t)(s0 + max(row, 0)) * row_stride + (size_t)head * kD + 8u * lhi;
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-        qf[qb][s] = L > 0 ? __builtin_bit_cast(bf16x8, *(const u32x4 *)(src + 16 * s)) : bf16x8{};
-    }
-    S.sync_point(own);                                       // before loop KV
-    S.enter(site, P.qk, g, 1);
+    S.sync_point(own);                                       // before loop T
     uint32_t kslot = 0;
-    for (uint32_t it = 0; it < trip; ++it, kslot = (kslot + 1 == (uint32_t)P.nk) ? 0u : kslot + 1) {
+    for (uint32_t t = 0; t < trip_t; ++t) {
       g.r1 += 1;
-      g.h1 = it + 1;
-      S.wait(site, P.qk, g, it + 1, g.r1 - 1, [] {});
-      if (!S.aborted) {
-        const uint32_t kb_base = kring + kslot * kKVSlot;
-        const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
-        f32x16 acc[2][2];
+      g.h1 = t + 1;
+      const Tile x = tile(t);
+      // the tile's 64 query rows of this wave, held in registers for its KV
+      // loop
+      bf16x8 qf[2][8];
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+      for (int qb = 0; qb < 2; ++qb) {
+        const int32_t row = min(x.q0 + (int32_t)(qr + 32u * qb + l32), x.L - 1);
+        const __bf16 *src = P.q + (size_t)(x.s0 + max(row, 0)) * row_stride + (size_t)x.head * kD + 8u * lhi;
 #pragma unroll
-          for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
-        // the K fragments of each 16-wide slice of d are read one slice
-        // ahead of the MFMAs that use them
-        bf16x8 k0 = lds_frag(kb_base + pos16(l32, lhi));
-        bf16x8 k1 = lds_frag(kb_base + pos16(32u + l32, lhi));
+        for (int s = 0; s < 8; ++s)
+          qf[qb][s] = x.L > 0 ? __builtin_bit_cast(bf16x8, *(const u32x4 *)(src + 16 * s)) : bf16x8{};
+      }
+      S.sync_point(own);                                     // before loop KV
+      S.enter(site, P.qk, g, 2);
+      for (uint32_t it = 0; it < x.trip; ++it, kslot = (kslot + 1 == (uint32_t)P.nk) ? 0u : kslot + 1) {
+        g.r2 += 1;
+        g.h2 = it + 1;
+        S.wait(site, P.qk, g, it + 1, g.r2 - 1, [] {});
+        if (!S.aborted) {
+          const uint32_t kb_base = kring + kslot * kKVSlot;
+          const uint32_t sp = spbuf + ((g.r2 - 1) & 1u) * kSPSlot;
+          f32x16 acc[2][2];
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          bf16x8 n0 = k0, n1 = k1;
-          if (s < 7) {
-            n0 = lds_frag(kb_base + pos16(l32, 2u * (s + 1) + lhi));
-            n1 = lds_frag(kb_base + pos16(32u + l32, 2u * (s + 1) + lhi));
+          for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+          // the K fragments of each 16-wide slice of d are read one slice
+          // ahead of the MFMAs that use them
+          bf16x8 k0 = lds_frag(kb_base + pos16(l32, lhi));
+          bf16x8 k1 = lds_frag(kb_base + pos16(32u + l32, lhi));
+#pragma unroll
+          for (int s = 0; s < 8; ++s) {
+            bf16x8 n0 = k0, n1 = k1;
+            if (s < 7) {
+              n0 = lds_frag(kb_base + pos16(l32, 2u * (s + 1) + lhi));
+              n1 = lds_frag(kb_base + pos16(32u + l32, 2u * (s + 1) + lhi));
+            }
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) {
+              acc[qb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[qb][s], acc[qb][0], 0, 0, 0);
+              acc[qb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[qb][s], acc[qb][1], 0, 0, 0);
+            }
+            if (s < 7) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+            k0 = n0;
+            k1 = n1;
           }
 #pragma unroll
           for (int qb = 0; qb < 2; ++qb) {
-            acc[qb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[qb][s], acc[qb][0], 0, 0, 0);
-            acc[qb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[qb][s], acc[qb][1], 0, 0, 0);
+            const uint32_t row = qr + 32u * qb + l32;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const f32x4 v = {acc[qb][kb][4 * j], acc[qb][kb][4 * j + 1], acc[qb][kb][4 * j + 2],
+                                 acc[qb][kb][4 * j + 3]};
+                *(BFS_LDS f32x4 *)(uintptr_t)(sp + pos16(row, 8u * kb + 2u * j + lhi)) = v;
+              }
           }
-          if (s < 7) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-          k0 = n0;
-          k1 = n1;
         }
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const uint32_t row = qr + 32u * qb + l32;
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const f32x4 v = {acc[qb][kb][4 * j], acc[qb][kb][4 * j + 1], acc[qb][kb][4 * j + 2], acc[qb][kb][4 * j + 3]};
-              *(BFS_LDS f32x4 *)(uintptr_t)(sp + pos16(row, 8u * kb + 2u * j + lhi)) = v;
-            }
-        }
+        S.signal(P.qk.update, (uint32_t)ew);
+        S.sync_point(own);                                   // end of a KV iteration
       }
-      S.signal(P.qk.update, (uint32_t)ew);
-      S.sync_point(own);                                     // end of a KV iteration
+      S.sync_point(own);                                     // end of a T iteration
     }
   } else if (eng == 2) {
     // ------------------------------------------------------ softmax engine
     const uint32_t row = 32u * ew + l32;
     const float c = P.scale_log2;
-    float m = -__builtin_inff(), lrun = 0.0f;
-    S.sync_point(own);                                       // before loop KV
-    S.enter(site, P.sm, g, 1);
-    for (uint32_t it = 0; it < trip; ++it) {
+    S.sync_point(own);                                       // before loop T
+    for (uint32_t t = 0; t < trip_t; ++t) {
       g.r1 += 1;
-      g.h1 = it + 1;
-      S.wait(site, P.sm, g, it + 1, g.r1 - 1, [] {});
-      if (!S.aborted) {
-        const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
-        float x[32];
+      g.h1 = t + 1;
+      const Tile x = tile(t);
+      float m = -__builtin_inff(), lrun = 0.0f;
+      S.sync_point(own);                                     // before loop KV
+      S.enter(site, P.sm, g, 2);
+      for (uint32_t it = 0; it < x.trip; ++it) {
+        g.r2 += 1;
+        g.h2 = it + 1;
+        S.wait(site, P.sm, g, it + 1, g.r2 - 1, [] {});
+        if (!S.aborted) {
+          const uint32_t par = (g.r2 - 1) & 1u;
+          const uint32_t sp = spbuf + par * kSPSlot;
+          float xs[32];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const f32x4 v = *(const BFS_LDS f32x4 *)(uintptr_t)(sp + pos16(row, 8u * lhi + j));
-          x[4 * j] = v.x;
-          x[4 * j + 1] = v.y;
-          x[4 * j + 2] = v.z;
-          x[4 * j + 3] = v.w;
-        }
-        const int32_t key0 = (int32_t)it * kBKV + 32 * (int32_t)lhi;
-        if ((int32_t)(it + 1) * kBKV > L) {
+          for (int j = 0; j < 8; ++j) {
+            const f32x4 v = *(const BFS_LDS f32x4 *)(uintptr_t)(sp + pos16(row, 8u * lhi + j));
+            xs[4 * j] = v.x;
+            xs[4 * j + 1] = v.y;
+            xs[4 * j + 2] = v.z;
+            xs[4 * j + 3] = v.w;
+          }
+          const int32_t key0 = (int32_t)it * kBKV + 32 * (int32_t)lhi;
+          if ((int32_t)(it + 1) * kBKV > x.L) {
 #pragma unroll
-          for (int t = 0; t < 32; ++t)
-            if (key0 + t >= L) x[t] = -__builtin_inff();
-        }
-        float mx = x[0];
+            for (int q = 0; q < 32; ++q)
+              if (key0 + q >= x.L) xs[q] = -__builtin_inff();
+          }
+          float mx = xs[0];
 #pragma unroll
-        for (int t = 1; t < 32; ++t) mx = __builtin_fmaxf(mx, x[t]);
-        const f32x2 mp = pair32(mx);
-        mx = __builtin_fmaxf(mp.x, mp.y);
-        const float m_new = __builtin_fmaxf(m, mx * c);
-        const float alpha = __builtin_amdgcn_exp2f(m - m_new);
-        float sum = 0.0f;
-        uint32_t pk[16];
+          for (int q = 1; q < 32; ++q) mx = __builtin_fmaxf(mx, xs[q]);
+          const f32x2 mp = pair32(mx);
+          mx = __builtin_fmaxf(mp.x, mp.y);
+          const float m_new = __builtin_fmaxf(m, mx * c);
+          const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+          float sum = 0.0f;
+          uint32_t pk[16];
 #pragma unroll
-        for (int t = 0; t < 32; t += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(x[t], c, -m_new));
-          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(x[t + 1], c, -m_new));
-          sum += p0 + p1;
-          pk[t / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{p0, p1}, bf16x2));
-        }
-        const f32x2 sums = pair32(sum);
-        sum = sums.x + sums.y;
-        lrun = alpha * lrun + sum;
-        m = m_new;
+          for (int q = 0; q < 32; q += 2) {
+            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(xs[q], c, -m_new));
+            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(xs[q + 1], c, -m_new));
+            sum += p0 + p1;
+            pk[q / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{p0, p1}, bf16x2));
+          }
+          const f32x2 sums = pair32(sum);
+          sum = sums.x + sums.y;
+          lrun = alpha * lrun + sum;
+          m = m_new;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const u32x4 v = {pk[4 * j], pk[4 * j + 1], pk[4 * j + 2], pk[4 * j + 3]};
-          *(BFS_LDS u32x4 *)(uintptr_t)(sp + pos16(row, 4u * lhi + j)) = v;
+          for (int j = 0; j < 4; ++j) {
+            const u32x4 v = {pk[4 * j], pk[4 * j + 1], pk[4 * j + 2], pk[4 * j + 3]};
+            *(BFS_LDS u32x4 *)(uintptr_t)(sp + pos16(row, 4u * lhi + j)) = v;
+          }
+          if (lhi == 0) {
+            *(BFS_LDS float *)(uintptr_t)(alpha_l + (par * kBQ + row) * 4u) = alpha;
+            *(BFS_LDS float *)(uintptr_t)(lsum_l + (((g.r1 - 1) & 1u) * kBQ + row) * 4u) = lrun;
+          }
         }
-        if (lhi == 0) {
-          *(BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + row) * 4u) = alpha;
-          *(BFS_LDS float *)(uintptr_t)(lsum_l + row * 4u) = lrun;
-        }
+        S.signal(P.sm.update, (uint32_t)ew);
+        S.sync_point(own);                                   // end of a KV iteration
       }
-      S.signal(P.sm.update, (uint32_t)ew);
-      S.sync_point(own);                                     // end of a KV iteration
+      S.sync_point(own);                                     // end of a T iteration
     }
   } else {
     // --------------------------------------------------- PV engine and NORM
     const uint32_t qr = 32u * ew;
-    f32x16 acc[4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
     // transposing V reads: lane l addresses row 8 (l / 32) + (l % 16) / 4 (+ 16 ks + 4 hh)
     // and columns 32 db + 16 ((l / 16) % 2) + 4 (l % 4) .. + 3
-    const uint32_t x = (lane >> 2) & 3u;
-    const uint32_t vrow = 8u * lhi + x;
+    const uint32_t xq = (lane >> 2) & 3u;
+    const uint32_t vrow = 8u * lhi + xq;
     uint32_t voff[4];
 #pragma unroll
     for (int db = 0; db < 4; ++db)
-      voff[db] = vrow * 256u + 16u * (4u * ((uint32_t)db ^ x) + 2u * ((lane >> 4) & 1u) + ((lane >> 1) & 1u)) +
+      voff[db] = vrow * 256u + 16u * (4u * ((uint32_t)db ^ xq) + 2u * ((lane >> 4) & 1u) + ((lane >> 1) & 1u)) +
                  8u * (lane & 1u);
-    S.sync_point(own);                                       // before loop KV
     Site<2> s_pr;
-    S.enter(s_pr, P.pread, g, 1);
-    S.enter(site, P.pv, g, 1);
-    uint32_t vslot = 0;
-    for (uint32_t it = 0; it < trip; ++it, vslot = (vslot + 1 == (uint32_t)P.nv) ? 0u : vslot + 1) {
-      g.r1 += 1;
-      g.h1 = it + 1;
-      // PREAD: P and alpha of the step into registers, then the S/P slot is
-      // released (LDS executes this wave's reads before its signal)
-      S.wait(s_pr, P.pread, g, it + 1, g.r1 - 1, [] {});
-      bf16x8 pf[4];
-      float a = 1.0f;
-      if (!S.aborted) {
-        const uint32_t sp = spbuf + (it & 1u) * kSPSlot;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) pf[ks] = lds_frag(sp + pos16(qr + l32, 2u * (uint32_t)ks + lhi));
-        a = *(const BFS_LDS float *)(uintptr_t)(alpha_l + ((it & 1u) * kBQ + qr + l32) * 4u);
-      }
-      S.signal(P.pread.update, (uint32_t)ew);
-      S.wait(site, P.pv, g, it + 1, g.r1 - 1, [] {});
-      if (!S.aborted) {
-        const uint32_t vb = vring + vslot * kKVSlot;
-        auto vfrag = [&](int ks, int db) {
-          const uint32_t va = vb + 16u * (uint32_t)ks * 256u + voff[db];
-          const bf16x4 lo = lds_tr(va), hi = lds_tr(va + 4u * 256u);
-          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        };
-        // the first V fragment is read before the rescale so that its
-        // latency overlaps it
-        bf16x8 vf = vfrag(0, 0);
-        // a block whose rows all keep their running maximum needs no rescale
-        if (__builtin_amdgcn_ballot_w64(a != 1.0f) != 0) {
-#pragma unroll
-          for (int db = 0; db < 4; ++db) acc[db] *= a;
-        }
-        // each V fragment is read one MFMA ahead of its use
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-#pragma unroll
-          for (int db = 0; db < 4; ++db) {
-            bf16x8 vf_next = vf;
-            if (db < 3) vf_next = vfrag(ks, db + 1);
-            else if (ks < 3) vf_next = vfrag(ks + 1, 0);
-            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], acc[db], 0, 0, 0);
-            if (db < 3 || ks < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            vf = vf_next;
-          }
-        }
-      }
-      S.signal(P.pv.update, (uint32_t)ew);
-      S.sync_point(own);                                     // end of a KV iteration
-    }
-    mark = S.elapsed();
-    // NORM: O / l for the rows of the sequence
     Site<1> s_norm;
-    S.enter(s_norm, P.norm, g, 0);
-    S.wait(s_norm, P.norm, g, 1, 0, [] {});
-    if (!S.aborted) {
-      const uint32_t rloc = qr + l32;
-      const int32_t row = q0 + (int32_t)rloc;
-      const float lr = *(const BFS_LDS float *)(uintptr_t)(lsum_l + rloc * 4u);
-      const float inv = 1.0f / lr;
-      if (row < L) {
-        __bf16 *dst = P.o + (size_t)(s0 + row) * row_stride + (size_t)head * kD;
+    uint32_t vslot = 0;
+    S.sync_point(own);                                       // before loop T
+    S.enter(s_norm, P.norm, g, 1);
+    for (uint32_t t = 0; t < trip_t; ++t) {
+      g.r1 += 1;
+      g.h1 = t + 1;
+      const Tile x = tile(t);
+      f32x16 acc[4];
 #pragma unroll
-        for (int db = 0; db < 4; ++db)
+      for (int b = 0; b < 4; ++b) acc[b] = f32x16{};
+      S.sync_point(own);                                     // before loop KV
+      S.enter(s_pr, P.pread, g, 2);
+      S.enter(site, P.pv, g, 2);
+      for (uint32_t it = 0; it < x.trip; ++it, vslot = (vslot + 1 == (uint32_t)P.nv) ? 0u : vslot + 1) {
+        g.r2 += 1;
+        g.h2 = it + 1;
+        // PREAD: P and alpha of the step into registers, then the S/P slot
+        // is released (LDS executes this wave's reads before its signal)
+        S.wait(s_pr, P.pread, g, it + 1, g.r2 - 1, [] {});
+        bf16x8 pf[4];
+        float a = 1.0f;
+        if (!S.aborted) {
+          const uint32_t par = (g.r2 - 1) & 1u;
+          const uint32_t sp = spbuf + par * kSPSlot;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const f32x2 a01 = {acc[db][4 * j] * inv, acc[db][4 * j + 1] * inv};
-            const f32x2 a23 = {acc[db][4 * j + 2] * inv, acc[db][4 * j + 3] * inv};
-            const u32x2 v = {__builtin_bit_cast(uint32_t, __builtin_convertvector(a01, bf16x2)),
-                             __builtin_bit_cast(uint32_t, __builtin_convertvector(a23, bf16x2))};
-            __builtin_nontemporal_store(v, reinterpret_cast<u32x2 *>(dst + 32 * db + 8 * j + 4 * lhi));
+          for (int ks = 0; ks < 4; ++ks) pf[ks] = lds_frag(sp + pos16(qr + l32, 2u * (uint32_t)ks + lhi));
+          a = *(const BFS_LDS float *)(uintptr_t)(alpha_l + (par * kBQ + qr + l32) * 4u);
+        }
+        S.signal(P.pread.update, (uint32_t)ew);
+        S.wait(site, P.pv, g, it + 1, g.r2 - 1, [] {});
+        if (!S.aborted) {
+          const uint32_t vb = vring + vslot * kKVSlot;
+          auto vfrag = [&](int ks, int db) {
+            const uint32_t va = vb + 16u * (uint32_t)ks * 256u + voff[db];
+            const bf16x4 lo = lds_tr(va), hi = lds_tr(va + 4u * 256u);
+            return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          };
+          // the first V fragment is read before the rescale so that its
+          // latency overlaps it
+          bf16x8 vf = vfrag(0, 0);
+          // a block whose rows all keep their running maximum needs no rescale
+          if (__builtin_amdgcn_ballot_w64(a != 1.0f) != 0) {
+#pragma unroll
+            for (int db = 0; db < 4; ++db) acc[db] *= a;
           }
+          // each V fragment is read one MFMA ahead of its use
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+            for (int db = 0; db < 4; ++db) {
+              bf16x8 vf_next = vf;
+              if (db < 3) vf_next = vfrag(ks, db + 1);
+              else if (ks < 3) vf_next = vfrag(ks + 1, 0);
+              acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], acc[db], 0, 0, 0);
+              if (db < 3 || ks < 3) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              vf = vf_next;
+            }
+          }
+        }
+        S.signal(P.pv.update, (uint32_t)ew);
+        S.sync_point(own);                                   // end of a KV iteration
       }
+      mark = S.elapsed();
+      // NORM: O / l for the tile's rows of the sequence; its signal lets the
+      // softmax of the tile after next overwrite these row sums
+      S.wait(s_norm, P.norm, g, t + 1, g.r1 - 1, [] {});
+      if (!S.aborted) {
+        const uint32_t rloc = qr + l32;
+        const int32_t row = x.q0 + (int32_t)rloc;
+        const float lr = *(const BFS_LDS float *)(uintptr_t)(lsum_l + (((g.r1 - 1) & 1u) * kBQ + rloc) * 4u);
+        const float inv = 1.0f / lr;
+        if (row < x.L) {
+          __bf16 *dst = P.o + (size_t)(x.s0 + row) * row_stride + (size_t)x.head * kD;
+#pragma unroll
+          for (int db = 0; db < 4; ++db)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const f32x2 a01 = {acc[db][4 * j] * inv, acc[db][4 * j + 1] * inv};
+              const f32x2 a23 = {acc[db][4 * j + 2] * inv, acc[db][4 * j + 3] * inv};
+              const u32x2 v = {__builtin_bit_cast(uint32_t, __builtin_convertvector(a01, bf16x2)),
+                               __builtin_bit_cast(uint32_t, __builtin_convertvector(a23, bf16x2))};
+              __builtin_nontemporal_store(v, reinterpret_cast<u32x2 *>(dst + 32 * db + 8 * j + 4 * lhi));
+            }
+        }
+      }
+      S.signal(P.norm.update, (uint32_t)ew);
+      S.sync_point(own);                                     // end of a T iteration
     }
   }
   drain_all();
@@ -448,7 +514,8 @@ namespace bfs {
 bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
                        const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream, uint32_t *dbg,
                        int64_t dbg_cap, const bfs_run_opts &o) {
-  if (p->n_loops != 2 || p->loop_parent[1] != 0) return fail(BFS_E_UNSUPPORTED, "attn: loops must be top -> KV");
+  if (p->n_loops != 3 || p->loop_parent[1] != 0 || p->loop_parent[2] != 1)
+    return fail(BFS_E_UNSUPPORTED, "attn: loops must be top -> T -> KV");
   const int want_w[5] = {1, 2, 4, 4, 1};
   if (p->n_engines != 5) return fail(BFS_E_UNSUPPORTED, "attn: five engines");
   for (int e = 0; e < 5; ++e)
@@ -457,13 +524,13 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   for (size_t i = 0; i < p->instr_engine.size(); ++i) {
     const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];
     const int32_t *a = &p->instr_args[8 * i];
-    if (op == 32 && e == 0 && par == 1 && a[0] == 0 && lk < 0) lk = (int)i;
-    else if (op == 32 && e == 4 && par == 1 && a[0] == 1 && lv < 0) lv = (int)i;
-    else if (op == 33 && e == 1 && par == 1 && qk < 0) qk = (int)i;
-    else if (op == 34 && e == 2 && par == 1 && sm < 0) sm = (int)i;
-    else if (op == 37 && e == 3 && par == 1 && pr < 0 && pv < 0) pr = (int)i;
-    else if (op == 35 && e == 3 && par == 1 && pv < 0) pv = (int)i;
-    else if (op == 36 && e == 3 && par == 0 && nm < 0) nm = (int)i;
+    if (op == 32 && e == 0 && par == 2 && a[0] == 0 && lk < 0) lk = (int)i;
+    else if (op == 32 && e == 4 && par == 2 && a[0] == 1 && lv < 0) lv = (int)i;
+    else if (op == 33 && e == 1 && par == 2 && qk < 0) qk = (int)i;
+    else if (op == 34 && e == 2 && par == 2 && sm < 0) sm = (int)i;
+    else if (op == 37 && e == 3 && par == 2 && pr < 0 && pv < 0) pr = (int)i;
+    else if (op == 35 && e == 3 && par == 2 && pv < 0) pv = (int)i;
+    else if (op == 36 && e == 3 && par == 1 && nm < 0 && pv >= 0) nm = (int)i;
     else return fail(BFS_E_UNSUPPORTED, "attn: unexpected instruction " + std::to_string(i));
   }
   if (lk < 0 || lv < 0 || qk < 0 || sm < 0 || pr < 0 || pv < 0 || nm < 0)
@@ -472,11 +539,20 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   const int heads = p->instr_args[8 * lk + 2], dim = p->instr_args[8 * lk + 3];
   if (dim != kD || p->instr_args[8 * lv + 3] != kD) return fail(BFS_E_UNSUPPORTED, "attn: head dimension 128");
   if (heads <= 0 || p->instr_args[8 * lv + 2] != heads) return fail(BFS_E_INVALID, "attn: heads must match");
-  const size_t lds = kCntBytes + (size_t)(nk + nv) * kKVSlot + 2 * kSPSlot + 3 * kBQ * 4;
+  const size_t lds = kCntBytes + (size_t)(nk + nv) * kKVSlot + 2 * kSPSlot + 4 * kBQ * 4;
   if (nk < 2 || nv < 2 || lds > 160 * 1024) return fail(BFS_E_UNSUPPORTED, "attn: ring depths >= 2 within 160 KiB of LDS");
-  // the kernel's buffers are only race-free under these dependencies
+  // the kernel's buffers are only race-free under these dependencies; the
+  // rings and S/P slots are indexed by r_KV over all tiles, so their reuse
+  // dependencies must be read with the linearized offset
+  auto linear_dep = [&](int prd, int cns, int k) {
+    for (size_t d = 0; d < p->deps.size() / 3; ++d)
+      if (p->deps[3 * d] == prd && p->deps[3 * d + 1] == cns && p->deps[3 * d + 2] == k && p->dep_linear[d])
+        return true;
+    return false;
+  };
   if (!has_dep(p, lk, qk, 0) || !has_dep(p, lv, pv, 0) || !has_dep(p, qk, sm, 0) || !has_dep(p, sm, pr, 0) ||
-      !has_dep(p, qk, lk, nk) || !has_dep(p, pv, lv, nv) || !has_dep(p, pr, qk, 2) || !has_dep(p, sm, nm, 0))
+      !linear_dep(qk, lk, nk) || !linear_dep(pv, lv, nv) || !linear_dep(pr, qk, 2) || !has_dep(p, sm, nm, 0) ||
+      !has_dep(p, nm, sm, 2))
     return fail(BFS_E_UNSUPPORTED, "attn: missing a ring, S/P or row-sum dependency");
   if (nbufs < 5) return fail(BFS_E_INVALID, "attn: needs [work, Q, K, V, O]");
   for (int i = 0; i < 5; ++i)

@@ -17,6 +17,7 @@ from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER,
                                   BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import attn_program, attn_worklist  # noqa: E402
+from workloads.configs import ATTN_WG  # noqa: E402
 from workloads.tensors import attn_inputs, bf16_to_f32  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -41,10 +42,10 @@ def _dev16(bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
 
 
-def run_attn(ai, heads, mode, cap=0, nk=3, nv=2, alloc=ALLOC_PER_LOOP):
+def run_attn(ai, heads, mode, cap=0, nk=3, nv=2, alloc=ALLOC_PER_LOOP, n_wg=ATTN_WG):
     prog = attn_program(heads, nk=nk, nv=nv)
     plan = Plan(prog, mode, alloc)
-    wl = attn_worklist(ai.lengths, heads)
+    wl = attn_worklist(ai.lengths, heads, n_wg=n_wg)
     trips, toff = trip_tensors(wl.trips)
     work = torch.from_numpy(wl.work.reshape(-1)).cuda()
     q, k, v = _dev16(ai.q), _dev16(ai.k), _dev16(ai.v)
@@ -57,6 +58,22 @@ def run_attn(ai, heads, mode, cap=0, nk=3, nv=2, alloc=ALLOC_PER_LOOP):
     plan.status()
     out = bf16_to_f32(o.cpu().numpy().view(np.uint16))
     return prog, plan, wl, out, (log.cpu().numpy().view(np.uint32) if cap else None)
+
+
+def oracle_recs(prog, wl):
+    """The oracle's records per workgroup; the ring and S/P reuse
+    dependencies (read with the linearized offset) take the brute force of
+    that relation."""
+    trips, off = wl.trips.flat()
+    out = {}
+    for g in range(wl.trips.n_wg):
+        res = core.run(prog, trips, off[g], g)
+        rr = res.recs.copy()
+        for d, lin in enumerate(prog.dep_linear):
+            if lin:
+                rr[rr["dep"] == d] = core.linearized_records(prog, res, d)
+        out[g] = rr
+    return out
 
 
 def check_close(got, ref):
@@ -73,20 +90,22 @@ def check_close(got, ref):
 SMALL = [1, 64, 100, 129, 300]
 
 
-@pytest.mark.parametrize("rings", [(3, 2), (2, 2), (2, 3)])
-def test_attn_small_parity_and_thresholds(rings):
+@pytest.mark.parametrize("rings,n_wg", [((3, 2), 3), ((2, 2), 3), ((2, 3), 3), ((3, 2), 64)])
+def test_attn_small_parity_and_thresholds(rings, n_wg):
+    """Three workgroups run all 16 tiles (several tiles each, so the rings,
+    S/P slots and row sums cross tile boundaries); 64 workgroups leave most
+    with one tile or none."""
     nk, nv = rings
     heads = 2
     ai = attn_inputs(seed=1, heads=heads, lengths=SMALL)
     ref = mathref.attention(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE)
     outs = {}
     for name, mode in MODES:
-        _say(f"[attn-small] rings={rings} mode={name}")
-        prog, plan, wl, out, logw = run_attn(ai, heads, mode, cap=64, nk=nk, nv=nv)
+        _say(f"[attn-small] rings={rings} n_wg={n_wg} mode={name}")
+        prog, plan, wl, out, logw = run_attn(ai, heads, mode, cap=256, nk=nk, nv=nv, n_wg=n_wg)
         check_close(out, ref)
-        trips, off = wl.trips.flat()
-        recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
-        logs = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
+        recs = oracle_recs(prog, wl)
+        logs = log_records(plan, logw, wl.trips.n_wg, 256, per_wave=True)
         assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
         outs[name] = out
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
@@ -98,13 +117,12 @@ def test_attn_per_instr():
     heads = 2
     ai = attn_inputs(seed=4, heads=heads, lengths=SMALL)
     _say("[attn-per-instr]")
-    prog, plan, wl, out, logw = run_attn(ai, heads, MODE_BARRIER_FREE, cap=64, alloc=ALLOC_PER_INSTR)
+    prog, plan, wl, out, logw = run_attn(ai, heads, MODE_BARRIER_FREE, cap=256, alloc=ALLOC_PER_INSTR, n_wg=3)
     check_close(out, mathref.attention(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE))
-    trips, off = wl.trips.flat()
-    recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
-    logs = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
+    recs = oracle_recs(prog, wl)
+    logs = log_records(plan, logw, wl.trips.n_wg, 256, per_wave=True)
     assert compare_wave_logs_with_oracle(prog, plan, logs, recs, "per_instr") > 0
-    _, _, _, out2, _ = run_attn(ai, heads, MODE_BARRIER_FREE)
+    _, _, _, out2, _ = run_attn(ai, heads, MODE_BARRIER_FREE, n_wg=3)
     assert np.array_equal(out.view(np.uint32), out2.view(np.uint32))
 
 
@@ -145,9 +163,26 @@ def test_attn_full_size_sampled():
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
 
 
+def test_attn_rejects_paper_relation_for_ring_reuse():
+    """The kernel indexes the rings and S/P slots by r_KV over all tiles:
+    a program whose reuse dependencies use the paper's per-trip relation
+    would let a tile's first loads overwrite slots the previous tile still
+    reads, so the launcher refuses it."""
+    prog = attn_program(2)
+    prog.dep_linear = [0] * len(prog.deps)
+    plan = Plan(prog)
+    t = torch.zeros(16, dtype=torch.int32, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t, t, t, t, t], t, t, 1)
+    assert e.value.status == bfs.E_UNSUPPORTED
+
+
 def test_attn_rejects_missing_dependency():
     prog = attn_program(2)
-    prog.deps = [d for d in prog.deps if not (prog.instrs[d[0]].name == "PREAD" and prog.instrs[d[1]].name == "QK")]
+    keep = [i for i, d in enumerate(prog.deps)
+            if not (prog.instrs[d[0]].name == "PREAD" and prog.instrs[d[1]].name == "QK")]
+    prog.deps = [prog.deps[i] for i in keep]
+    prog.dep_linear = [prog.dep_linear[i] for i in keep]
     plan = Plan(prog)
     t = torch.zeros(16, dtype=torch.int32, device="cuda")
     with pytest.raises(BfsError) as e:
@@ -182,7 +217,7 @@ def test_attn_rejects_trip_beyond_sequence():
     prog = attn_program(heads)
     plan = Plan(prog)
     wl = attn_worklist(ai.lengths, heads)
-    wl.trips.per_wg[0][1][0] += 1            # one KV block too many
+    wl.trips.per_wg[0][2][0] += 1            # one KV block too many
     trips, toff = trip_tensors(wl.trips)
     work = torch.from_numpy(wl.work.reshape(-1)).cuda()
     q, k, v = _dev16(ai.q), _dev16(ai.k), _dev16(ai.v)

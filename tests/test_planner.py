@@ -90,6 +90,32 @@ def _check_against_oracle(prog, tt):
     return len(res.recs)
 
 
+def _check_linear_against_oracle(prog, tt):
+    """Like _check_against_oracle for a program with linearized
+    dependencies: those are checked against the brute force of the
+    linearized relation (both allocations), the others against Eq. 1's
+    records (both allocations and the barrier mode)."""
+    trips, off = tt.flat()
+    res = core.run(prog, trips, off[0], 0)
+    pl = Plan(prog, MODE_BARRIER_FREE, ALLOC_PER_LOOP)
+    pi = Plan(prog, MODE_BARRIER_FREE, ALLOC_PER_INSTR)
+    pb = Plan(prog, MODE_BARRIER, ALLOC_PER_LOOP)
+    n = 0
+    for d in range(len(prog.deps)):
+        recs = res.recs[res.recs["dep"] == d]
+        lin = bool(prog.dep_linear and prog.dep_linear[d])
+        want = core.linearized_records(prog, res, d) if lin else recs
+        for rec, w in zip(recs, want):
+            rP, rh = int(rec["r_P"]), int(rec["rhat_S"])
+            assert pl.eval_threshold(d, rP, rh) == w["sem_thr"], (d, rec)
+            assert pi.eval_threshold(d, rP, rh) == w["count_thr"], (d, rec)
+            if not lin:
+                assert pb.eval_threshold(d, rP, rh) == rec["barrier_thr"], (d, rec)
+                assert rec["order_ok"]
+        n += len(recs)
+    return n
+
+
 def test_random_nests_bit_exact():
     n_checked, cases = 0, set()
     for seed in range(1200):
@@ -140,9 +166,9 @@ def test_workload_programs():
     _check_against_oracle(s.prog, s.trips)
     g = gemm_program(512, 256, 128)
     _check_against_oracle(g, TripTables([gemm_trips(512, 256, 128).per_wg[0]]))
-    for L in (1, 64, 65, 300):
-        a = attn_program(2)
-        _check_against_oracle(a, TripTables([attn_worklist([L], 2).trips.per_wg[0]]))
+    for lengths in ([1], [64], [65], [300], [300, 65, 1, 129]):
+        # one workgroup runs every tile: the T loop spans several tiles
+        _check_linear_against_oracle(attn_program(2), attn_worklist(lengths, 2, n_wg=1).trips)
     # the second workloads of the paper's suite and the MoE program
     from workloads import adamw_program, adamw_worklist, moe_program, moe_worklist, rmsnorm_program, \
         rmsnorm_worklist
@@ -225,13 +251,25 @@ def test_fused_family_formulas():
     fa = {(a.instrs[p].name, a.instrs[c].name): f for (p, c, k), f in zip(a.deps, Plan(a).formulas())}
     assert fa[("QK", "LOADK")]["k"] == 3 and fa[("PV", "LOADV")]["k"] == 2 and fa[("PREAD", "QK")]["k"] == 2
     assert all(fa[x]["kase"] == 1 for x in [("LOADK", "QK"), ("QK", "SM"), ("SM", "PREAD"), ("LOADV", "PV")])
+    assert all(fa[x]["kase"] == 6 for x in [("QK", "LOADK"), ("PV", "LOADV"), ("PREAD", "QK")])
     assert fa[("SM", "NORM")]["kase"] == 2
-    # the work list covers every (sequence, head, query tile) once, XCD-interleaved
-    wl = attn_worklist([1, 64, 129, 300, 4096], 3)
-    items = {tuple(r) for r in wl.work.tolist() if r[1] > 0}
-    assert len(items) == 3 * (1 + 1 + 2 + 3 + 32)
-    trips = [int(t[1][0]) for t in wl.trips.per_wg]
-    assert all(t == -(-int(r[1]) // 64) for t, r in zip(trips, wl.work))
+    assert fa[("NORM", "SM")]["kase"] == 1 and fa[("NORM", "SM")]["loop_S"] == a.loop_id("T")
+    # the work list covers every (sequence, head, query tile) once; tile j of
+    # workgroup w sits at row w + j * n_wg, on w's XCD (w % 8) with every
+    # tile of its (sequence, head)
+    for n_wg in (1, 5, 16, 256):
+        wl = attn_worklist([1, 64, 129, 300, 4096], 3, n_wg=n_wg)
+        seen, xcd_of_pair = [], {}
+        for w, per in enumerate(wl.trips.per_wg):
+            n_t = int(per[1][0])
+            assert len(per[2]) == n_t
+            for j in range(n_t):
+                r = wl.work[w + j * n_wg]
+                assert r[1] > 0 and int(per[2][j]) == -(-int(r[1]) // 64)
+                seen.append(tuple(r))
+                if n_wg >= 8:
+                    assert xcd_of_pair.setdefault((int(r[0]), int(r[3])), w % 8) == w % 8
+        assert len(seen) == len(set(seen)) == 3 * (1 + 1 + 2 + 3 + 32)
 
 
 def test_rejections():

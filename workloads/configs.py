@@ -494,56 +494,75 @@ ATTN_SP = 2         # S/P buffer slots
 
 
 def attn_program(heads: int, dim: int = ATTN_D, nk: int = 3, nv: int = 2) -> Program:
-    """One workgroup per (sequence, head, 128-query tile):
+    """A fixed set of workgroups, each running a run-time list of (sequence,
+    head, 128-query tile) work items:
 
-      KV{ E0: LOADK K block -> kring[(rhat_KV - 1) % nk]
-          E4: LOADV V block -> vring[(rhat_KV - 1) % nv]
-          E1: QK    S = Q K^T -> sp[(rhat_KV - 1) % 2]
-          E2: SM    online softmax: P over S in place, alpha, running sum l
-          E3: PREAD P and alpha of the step into registers
-          E3: PV    O = alpha O + P V }
-      E3: NORM  O / l -> output
+      T{ KV{ E0: LOADK K block -> kring[(r_KV - 1) % nk]
+             E4: LOADV V block -> vring[(r_KV - 1) % nv]
+             E1: QK    S = Q K^T -> sp[(r_KV - 1) % 2]
+             E2: SM    online softmax: P over S in place, alpha, running sum l
+             E3: PREAD P and alpha of the step into registers
+             E3: PV    O = alpha O + P V }
+         E3: NORM  O / l -> output }
 
-    The KV loop's trip count is ceil(L / 64) for the sequence's length L.
-    LOADK->QK, LOADV->PV, QK->SM, SM->PREAD (k=0) carry the data forward;
-    QK->LOADK (k=nk) and PV->LOADV (k=nv) free ring slots; PREAD->QK (k=2)
-    frees an S/P slot as soon as its P is held in registers, before the PV
-    MFMAs; SM->NORM (k=0, producer nested in KV) delivers the final row
-    sums."""
+    T's trip count is the workgroup's number of tiles, KV's ceil(L / 64) for
+    the tile's sequence length L; both known only at run time.  LOADK->QK,
+    LOADV->PV, QK->SM, SM->PREAD (k=0) carry the data forward.  The rings
+    and S/P slots are indexed by r_KV, which counts KV iterations over all
+    tiles, so their reuse dependencies QK->LOADK (k=nk), PV->LOADV (k=nv)
+    and PREAD->QK (k=2) are read with the linearized offset (an extension of
+    the paper's relation): the next tile's loads and QK steps overlap the
+    end of the previous tile.  SM->NORM (k=0, C2) delivers a tile's final
+    row sums; they are double-buffered by tile, and NORM->SM (k=2, C1 at T)
+    keeps a tile's softmax from overwriting a buffer before NORM of the tile
+    before last has read it."""
     b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 4, 4, 1])
-    with b.loop("KV"):
-        b.instr(0, OP_ATTN_LOAD, [0, nk, heads, dim, 0, 0, 0, 0], name="LOADK")
-        b.instr(4, OP_ATTN_LOAD, [1, nv, heads, dim, 0, 0, 0, 0], name="LOADV")
-        b.instr(1, OP_ATTN_QK, [0] * 8, name="QK")
-        b.instr(2, OP_ATTN_SM, [0] * 8, name="SM")
-        b.instr(3, OP_ATTN_PREAD, [0] * 8, name="PREAD")
-        b.instr(3, OP_ATTN_PV, [0] * 8, name="PV")
-    b.instr(3, OP_ATTN_NORM, [0] * 8, name="NORM")
+    with b.loop("T"):
+        with b.loop("KV"):
+            b.instr(0, OP_ATTN_LOAD, [0, nk, heads, dim, 0, 0, 0, 0], name="LOADK")
+            b.instr(4, OP_ATTN_LOAD, [1, nv, heads, dim, 0, 0, 0, 0], name="LOADV")
+            b.instr(1, OP_ATTN_QK, [0] * 8, name="QK")
+            b.instr(2, OP_ATTN_SM, [0] * 8, name="SM")
+            b.instr(3, OP_ATTN_PREAD, [0] * 8, name="PREAD")
+            b.instr(3, OP_ATTN_PV, [0] * 8, name="PV")
+        b.instr(3, OP_ATTN_NORM, [0] * 8, name="NORM")
     b.dep("LOADK", "QK", 0)
     b.dep("LOADV", "PV", 0)
     b.dep("QK", "SM", 0)
     b.dep("SM", "PREAD", 0)
-    b.dep("QK", "LOADK", nk)
-    b.dep("PV", "LOADV", nv)
-    b.dep("PREAD", "QK", ATTN_SP)
+    b.dep("QK", "LOADK", nk, linear=True)
+    b.dep("PV", "LOADV", nv, linear=True)
+    b.dep("PREAD", "QK", ATTN_SP, linear=True)
     b.dep("SM", "NORM", 0)
+    b.dep("NORM", "SM", 2)
     return b.build()
 
 
 @dataclass
 class AttnWork:
-    work: np.ndarray      # int32 [n_wg, 4]: first token, length, first query row, head
-    trips: TripTables     # per workgroup: [[1], [ceil(L / 64)]]
+    work: np.ndarray      # int32 [max tiles * n_wg, 4]: first token, length, first query row, head;
+                          # tile j of workgroup w at row w + j * n_wg
+    trips: TripTables     # per workgroup: [[1], [tiles], [ceil(L / 64) per tile]]
 
 
-def attn_worklist(lengths, heads: int, xcds: int = 8) -> AttnWork:
-    """Work items (sequence, head, 128-query tile) in launch order.
+ATTN_WG = 256                # workgroups: one per compute unit (the LDS allows one per CU)
+ATTN_TILE_COST = 14          # fixed cost of a tile in KV steps, for balancing (measured: about 20 us
+                             # per tile of fill and drain against 1.4 us per KV step with one tile
+                             # per workgroup)
+
+
+def attn_worklist(lengths, heads: int, xcds: int = 8, n_wg: int = ATTN_WG) -> AttnWork:
+    """Tiles (sequence, head, 128-query tile) assigned to ``n_wg``
+    workgroups.
 
     (sequence, head) pairs are taken longest first and each goes, with all
-    of its query tiles, to the XCD with the least work so far; workgroup w
-    runs on XCD w % xcds, so a pair's tiles share one L2 for their K and V
-    blocks.  Shorter XCD lists are padded with empty items (length 0, no KV
-    steps)."""
+    of its query tiles, to the XCD with the least work so far, so a pair's
+    tiles share one L2 for their K and V blocks (workgroup w runs on XCD
+    w % xcds).  Within an XCD, tiles in that order go to the workgroup with
+    the least work so far (KV steps plus a fixed cost per tile), so the
+    tiles of one pair run at the same time on different compute units."""
+    if n_wg <= 0:
+        raise ValueError("n_wg must be positive")
     lengths = np.asarray(lengths, dtype=np.int64)
     cu = np.concatenate([[0], np.cumsum(lengths)])
     pairs = sorted(((int(lengths[b]), b, h) for b in range(len(lengths)) for h in range(heads)),
@@ -555,19 +574,25 @@ def attn_worklist(lengths, heads: int, xcds: int = 8) -> AttnWork:
             continue
         x = min(range(xcds), key=lambda i: (load[i], i))
         n_tiles = -(-L // ATTN_BQ)
-        load[x] += n_tiles * -(-L // ATTN_BKV)
+        load[x] += n_tiles * (-(-L // ATTN_BKV) + ATTN_TILE_COST)
         for t in range(n_tiles):
             lists[x].append((int(cu[b]), L, t * ATTN_BQ, h))
-    depth = max((len(l) for l in lists), default=0)
-    if depth == 0:
-        return AttnWork(np.zeros((0, 4), np.int32), TripTables([]))
-    items = []
-    for i in range(depth):
-        for x in range(xcds):
-            items.append(lists[x][i] if i < len(lists[x]) else (0, 0, 0, 0))
-    work = np.array(items, dtype=np.int32).reshape(-1, 4)
-    trips = TripTables([[np.array([1], np.int32), np.array([-(-int(L) // ATTN_BKV)], np.int32)]
-                        for _, L, _, _ in work])
+    per_wg = [[] for _ in range(n_wg)]
+    wg_load = [0] * n_wg
+    for x in range(xcds):
+        mine = list(range(x, n_wg, xcds)) or list(range(n_wg))
+        for item in lists[x]:
+            w = min(mine, key=lambda i: (wg_load[i], i))
+            per_wg[w].append(item)
+            wg_load[w] += -(-item[1] // ATTN_BKV) + ATTN_TILE_COST
+    depth = max((len(l) for l in per_wg), default=0)
+    work = np.zeros((max(depth, 1) * n_wg, 4), np.int32)
+    for w, items in enumerate(per_wg):
+        for j, it in enumerate(items):
+            work[w + j * n_wg] = it
+    trips = TripTables([[np.array([1], np.int32), np.array([len(items)], np.int32),
+                         np.array([-(-int(L) // ATTN_BKV) for _, L, _, _ in items], np.int32)]
+                        for items in per_wg])
     return AttnWork(work, trips)
 
 
