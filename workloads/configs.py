@@ -493,7 +493,7 @@ ATTN_D = 128        # head dimension
 ATTN_SP = 2         # S/P buffer slots
 
 
-def attn_program(heads: int, dim: int = ATTN_D, nk: int = 3, nv: int = 2) -> Program:
+def attn_program(heads: int, dim: int = ATTN_D, nk: int = 2, nv: int = 3) -> Program:
     """A fixed set of workgroups, each running a run-time list of (sequence,
     head, 128-query tile) work items:
 
