@@ -246,7 +246,11 @@ void bfs_plan_destroy(bfs_plan *plan);
  *   dev_buffers  family-specific device pointers, n_buffers of them
  *                (interp / stream3: [0] int64 per-workgroup tile base,
  *                [1] fp32 input tiles, [2] fp32 output; see the family notes
- *                in the implementation files for gemm / attn / moe).
+ *                in the implementation files for gemm / attn / moe).  The
+ *                library does not know buffer lengths: the caller owns the
+ *                buffers and must size them for the trip tables it passes
+ *                (attn: the work list holds tile t of workgroup w at row
+ *                w + t * n_wg for every t below w's T trip).
  *   dev_trips    int32 trip counts; dev_trip_off int64 [n_wg][n_loops]: the
  *                j-th execution of loop l in workgroup w runs
  *                dev_trips[dev_trip_off[w*n_loops + l] + j] iterations.
