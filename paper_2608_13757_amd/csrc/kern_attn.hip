@@ -5,17 +5,17 @@
 //
 //   E0 (1 wave, K load)    LOADK: the 64 x 128 bf16 K block of the step into
 //                          a K ring slot with direct-to-LDS loads.
-//   E1 (2 waves, MFMA)     QK: S = Q K^T for 64 query rows per wave (Q held in
-//                          registers for the whole loop), written as fp32
-//                          into an S/P slot.
+//   E1 (2 waves, MFMA)     QK: S = Q K^T for 64 query rows per wave (the
+//                          tile's Q rows held in registers for its KV loop),
+//                          written as fp32 into an S/P slot.
 //   E2 (4 waves, VALU)     SM: online softmax over 32 rows per wave in the
 //                          base-2 domain: running max m, rescale factor
 //                          alpha = 2^(m_old - m_new), P = 2^(S c - m_new)
 //                          written as bf16 over S in place, running sum l.
 //   E3 (4 waves, MFMA)     PREAD: the P fragments and alpha of the wave's 32
 //                          query rows into registers; PV: O = alpha O + P V
-//                          (fp32 accumulators); after the loop NORM: O / l
-//                          to HBM.
+//                          (fp32 accumulators); after each tile's KV loop
+//                          NORM: O / l to HBM.
 //   E4 (1 wave, V load)    LOADV: the V block into a V ring slot.
 //
 // Loops top -> T -> KV: T runs the workgroup's tiles, KV ceil(L / 64) steps
