@@ -246,8 +246,8 @@ def bench_gemm(a):
 
 def bench_attn(a):
     """Variable-length attention forward: 32 sequences of U[128, 4096] tokens,
-    16 heads of 128, one workgroup per (sequence, head, 128-query tile);
-    both synchronization modes."""
+    16 heads of 128; 256 workgroups (one per compute unit) each run a list of
+    (sequence, head, 128-query tile) tiles; both synchronization modes."""
     import numpy as np
     import torch
     from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
