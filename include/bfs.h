@@ -196,13 +196,34 @@ typedef struct {
                                     blocked in waits, [2] blocked waits, [3] time in barriers,
                                     [4] time waiting for own loads to land, [5] polls, [6-7] 0 */
   int32_t k_unroll;              /* GEMM family: iterations of the static-trip K loop per
-                                    loop-body copy in uninstrumented launches (0 or 1: none,
+                                    loop-body copy, also in instrumented launches, whose debug
+                                    log then records the unrolled bodies' waits (0 or 1: none,
                                     2, 4, 8; unrolled bodies see their thresholds as fixed
                                     offsets of one loop-invariant value, the code-size versus
                                     regOp trade-off of static loops); other families ignore it.
                                     Other values: BFS_E_INVALID */
-  int32_t reserved;              /* must be 0 */
+  uint32_t flags;                /* 0 or BFS_RUN_* bits below; other bits: BFS_E_INVALID */
 } bfs_run_opts;
+
+/* bfs_run_opts.flags.
+ *
+ * BFS_RUN_PER_INSTANCE: stream family, barrier-free, uninstrumented: every
+ * trip of the innermost loop runs one instance at a time (one wait, one tile
+ * moved and one counter add per instance), the loop the barrier mode runs,
+ * instead of the batches of up to four consecutive instances that
+ * uninstrumented launches take otherwise.  The schedule is then the same in
+ * both modes and only the synchronization differs (the isolation of the
+ * allocation that Section 8.2 asks for).  Other families ignore it.
+ *
+ * BFS_RUN_LOG_BATCHED: stream family, barrier-free, with a debug log: the
+ * engines run the batched loop of uninstrumented launches and log one entry
+ * per batch wait, for the instance whose threshold the batch waits for (the
+ * batch's last instance, or in a pair of M iterations the last instance of
+ * the trip that holds the larger threshold).  Without it an instrumented
+ * launch logs every instance from the per-instance loop.  Ignored with an
+ * injected fault (fault_dep >= 0), which always runs the per-instance loop. */
+#define BFS_RUN_PER_INSTANCE 1u
+#define BFS_RUN_LOG_BATCHED 2u
 
 /*
  * Plan the synchronization of prog (Sections 5.2-5.5, or Section 3.4 in
@@ -271,11 +292,13 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
                    struct ihipStream_t *stream, uint32_t *dev_debug_log, int64_t debug_capacity,
                    const bfs_run_opts *opts);
 
-/* Synchronizes stream, then reports (and clears) the plan's error word:
+/* Synchronizes stream, then reports (and clears) the plan's error words:
  * BFS_E_DEADLOCK if any wait gave up since the last call, BFS_E_INVALID if a
  * workgroup rejected a run-time input (a trip count beyond its work item, a
  * trip table that disagrees with a loop the kernel runs statically, a load
- * offset beyond 32 bits); the first error since the last call is reported. */
+ * offset beyond 32 bits, a trip count beyond the ring-slot reuse the
+ * program's dependencies order); the first error since the last call is
+ * reported.  Allocates nothing. */
 bfs_status bfs_run_status(const bfs_plan *plan, struct ihipStream_t *stream);
 
 const char *bfs_status_string(bfs_status s);

@@ -62,7 +62,10 @@ class Stats(C.Structure):
 
 class RunOpts(C.Structure):
     _fields_ = [("watchdog_polls", C.c_uint64), ("fault_dep", C.c_int32), ("fault_delta", C.c_int32),
-                ("dev_stats", C.c_void_p), ("k_unroll", C.c_int32), ("reserved", C.c_int32)]
+                ("dev_stats", C.c_void_p), ("k_unroll", C.c_int32), ("flags", C.c_uint32)]
+
+RUN_PER_INSTANCE = 1
+RUN_LOG_BATCHED = 2
 
 STAT_FIELDS = ("run", "blocked", "n_blocked", "barrier", "own_loads", "polls")
 
@@ -197,13 +200,14 @@ class Plan:
         return out.value
 
     def run(self, buffers, trips, trip_off, n_wg, stream=None, debug_log=None, debug_capacity=0,
-            watchdog_polls=0, fault_dep=-1, fault_delta=0, stats=None, k_unroll=0):
+            watchdog_polls=0, fault_dep=-1, fault_delta=0, stats=None, k_unroll=0, flags=0):
         """Enqueue one execution (asynchronous).  buffers: torch tensors or
         device addresses; trips / trip_off: device int32 / int64 tensors;
         stats: optional int64 tensor of n_wg * n_waves * 8 per-wave counters;
-        k_unroll: K-loop unroll factor of uninstrumented GEMM launches (0, 1, 2, 4, 8)."""
+        k_unroll: K-loop unroll factor of GEMM launches (0, 1, 2, 4, 8);
+        flags: RUN_PER_INSTANCE / RUN_LOG_BATCHED (stream family)."""
         arr = (C.c_void_p * max(1, len(buffers)))(*[_ptr(b) for b in buffers])
-        opts = RunOpts(watchdog_polls, fault_dep, fault_delta, _ptr(stats), k_unroll, 0)
+        opts = RunOpts(watchdog_polls, fault_dep, fault_delta, _ptr(stats), k_unroll, flags)
         _check(lib().bfs_run(self.handle, arr, len(buffers), _ptr(trips), _ptr(trip_off), n_wg,
                              _stream_handle(stream), _ptr(debug_log), debug_capacity, C.byref(opts)))
 

@@ -112,6 +112,9 @@ struct bfs_plan {
 
   std::mutex dev_mu;
   std::vector<bfs::DevImage> images;     // one per device used
+  // the packed device tables (error words first), built once
+  std::vector<unsigned char> packed;
+  std::vector<size_t> packed_off;        // table offsets in `packed`
 };
 
 namespace bfs {

@@ -225,8 +225,9 @@ __device__ __forceinline__ void region_sync(uint32_t own_words, int n_words) {
 //          [5] observed, [6] wave;
 //   code 2 (a run-time input was rejected): [1] what (1 trip count beyond
 //          the work item, 2 trip table disagrees with a static loop, 3 load
-//          offset beyond 32 bits), [2] wg, [3] index, [4] value, [5] limit,
-//          [6] wave.
+//          offset beyond 32 bits, 4 trip count beyond the ring-slot reuse the
+//          program's dependencies order), [2] wg, [3] index, [4] value,
+//          [5] limit, [6] wave.
 // Branch-uniform on purpose: every lane tries the same compare-and-swap and
 // a ballot tells the wave whether one of its lanes won, so no control flow
 // here depends on the lane (a lane-dependent branch would make the callers'

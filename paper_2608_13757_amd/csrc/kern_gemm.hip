@@ -45,6 +45,7 @@
 // [2] bias fp32 [N], [3] C bf16 [M][N].  Trip tables: loop K runs K / 32
 // steps, loop C 8 chunks.
 #include <string>
+#include <type_traits>
 
 #include "engine_sync.h"
 
@@ -417,24 +418,23 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
     if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("gemm launch: ") + hipGetErrorString(e));
     return BFS_OK;
   };
-  // instrumented launches (debug log, statistics, injected faults) keep the
-  // loop bodies single
-  if (p->mode == BFS_MODE_BARRIER) {
-    if (instr) return go(gemm_kernel<BFS_MODE_BARRIER, true, 1>);
+  // Instrumented launches (debug log, statistics, injected faults) run the
+  // same unrolled bodies as timed ones, so the debug log records the waits
+  // of the code path that is timed.
+  auto pick = [&](auto mode_tag, auto instr_tag) -> bfs_status {
+    constexpr int kM = decltype(mode_tag)::value;
+    constexpr bool kI = decltype(instr_tag)::value;
     switch (o.k_unroll) {
-      case 2: return go(gemm_kernel<BFS_MODE_BARRIER, false, 2>);
-      case 4: return go(gemm_kernel<BFS_MODE_BARRIER, false, 4>);
-      case 8: return go(gemm_kernel<BFS_MODE_BARRIER, false, 8>);
-      default: return go(gemm_kernel<BFS_MODE_BARRIER, false, 1>);
+      case 2: return go(gemm_kernel<kM, kI, 2>);
+      case 4: return go(gemm_kernel<kM, kI, 4>);
+      case 8: return go(gemm_kernel<kM, kI, 8>);
+      default: return go(gemm_kernel<kM, kI, 1>);
     }
-  }
-  if (instr) return go(gemm_kernel<BFS_MODE_BARRIER_FREE, true, 1>);
-  switch (o.k_unroll) {
-    case 2: return go(gemm_kernel<BFS_MODE_BARRIER_FREE, false, 2>);
-    case 4: return go(gemm_kernel<BFS_MODE_BARRIER_FREE, false, 4>);
-    case 8: return go(gemm_kernel<BFS_MODE_BARRIER_FREE, false, 8>);
-    default: return go(gemm_kernel<BFS_MODE_BARRIER_FREE, false, 1>);
-  }
+  };
+  using BF = std::integral_constant<int, BFS_MODE_BARRIER_FREE>;
+  using BB = std::integral_constant<int, BFS_MODE_BARRIER>;
+  if (p->mode == BFS_MODE_BARRIER) return instr ? pick(BB{}, std::true_type{}) : pick(BB{}, std::false_type{});
+  return instr ? pick(BF{}, std::true_type{}) : pick(BF{}, std::false_type{});
 }
 
 }  // namespace bfs

@@ -83,6 +83,12 @@ struct Stream3Params {
   int32_t n_gen, per_gen, n_slots;
   int32_t ring_ld, ring_add_src, ring_add_dst, ring_st;   // ring id of each access
   float addc;
+  // Largest trips of M and I whose ring-slot reuse the program's
+  // dependencies order (derived on the host); longer trips are reported as
+  // invalid input and clamped, identically by every engine.
+  uint32_t max_trip_m, max_trip_i;
+  int32_t per_instance;    // uninstrumented barrier-free: every trip of I on the per-instance loop
+  int32_t log_batched;     // instrumented barrier-free: log from the batched loop
 };
 
 // The launch arguments are read in place from the kernel-argument segment
@@ -414,7 +420,12 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
       if (kBF && j < n_iw) iw[j].run += iw[j].step_o;
     E.nops(C.o_pre, C.n_o_pre, E.r1 - 1);
     E.sync_point();                                       // before loop M
-    const uint32_t trip_m = (uint32_t)ldc(P.trips + off_m + E.r1 - 1);
+    uint32_t trip_m = (uint32_t)ldc(P.trips + off_m + E.r1 - 1);
+    if (__builtin_expect(trip_m > P.max_trip_m, 0)) {
+      if (kRole == ROLE_LOAD)
+        report_input(P.err, 4u, (uint32_t)wg, E.r1 - 1, trip_m, P.max_trip_m, (uint32_t)wave);
+      trip_m = P.max_trip_m;
+    }
     const int32_t *trip_i_of = P.trips + off_i + E.r2;    // trips of I for this O iteration's M iterations
     // The trips of the next two M iterations are fetched ahead: tq0 for
     // M iteration m + 1, tq1 for m + 2 (indices clamped to the table).
@@ -454,6 +465,14 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
               }
             }
             iw[j].cmp = obs;
+          }
+          if (kInstr && E.log) {
+            // the instance whose threshold the pair waited for: the second
+            // trip's last one, or the first trip's last one while the second
+            // trip's mask is still 0
+            const uint32_t inst = (tb <= iw[j].kk && ta > iw[j].kk) ? E.r3 + ta - 1u : E.r3 + ta + tb - 1u;
+            const uint32_t t = thr > 0 ? (uint32_t)thr : 0u;
+            E.logit(iw[j].dep, inst, t, t > 0 ? (uint32_t)iw[j].cmp : 0u);
           }
         }
         const int64_t tile_a = (int64_t)E.r3 * 64, tile_b = tile_a + (int64_t)ta * 64;
@@ -534,6 +553,11 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
               }
               iw[j].cmp = obs;
             }
+            if (kInstr && E.log) {
+              // one entry per batch wait: the batch's last instance
+              const uint32_t t = (done + k > iw[j].kk && run_last > 0) ? (uint32_t)run_last : 0u;
+              E.logit(iw[j].dep, E.r3 + done + k - 1u, t, t > 0 ? (uint32_t)iw[j].cmp : 0u);
+            }
           }
           const int64_t tile = (int64_t)(E.r3 + done) * 64;    // element offset of the batch's first tile
           const bool act = lane < 16u * k;
@@ -570,11 +594,18 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
 #pragma unroll
           for (int j = 0; j < kSlots; ++j) enter_inner(iw[j], E.h1, E.h2);
         }
+        uint32_t trip_i_v = trip_i;
         if (trip_i - 1u < kb) {
           batch(trip_i, 0u, soff0);                         // the whole trip in one batch
         } else if (trip_i == 0u) {
           asm volatile("" ::"s"(tq1));
         } else {
+          if (trip_i > P.max_trip_i) {
+            if (kRole == ROLE_LOAD)
+              report_input(P.err, 4u, (uint32_t)wg, E.r2 - 1, trip_i, P.max_trip_i, (uint32_t)wave);
+            trip_i_v = P.max_trip_i;
+          }
+          const uint32_t trip_i = trip_i_v;
           // slot = slot0 + (rhat_I - 1) % per_gen: batches never straddle a wrap
           uint32_t done = 0, pos = 0;
           while (done != trip_i) {
@@ -585,15 +616,20 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
             if (pos == per_gen) pos = 0;
           }
         }
-        E.r3 += trip_i;
-        E.h3 = trip_i;
+        E.r3 += trip_i_v;
+        E.h3 = trip_i_v;
       } else {
         E.flush_batches();
+        if (trip_i > P.max_trip_i) {
+          if (kRole == ROLE_LOAD)
+            report_input(P.err, 4u, (uint32_t)wg, E.r2 - 1, trip_i, P.max_trip_i, (uint32_t)wave);
+        }
+        const uint32_t trip_i_g = min(trip_i, P.max_trip_i);
 #pragma unroll
         for (int j = 0; j < kSlots; ++j)
           if (kBF && j < n_iw) enter_inner(iw[j], E.h1, E.h2);
         uint32_t lo = 0;
-        for (uint32_t i = 0; i < trip_i; ++i) {
+        for (uint32_t i = 0; i < trip_i_g; ++i) {
           E.r3 += 1;
           E.h3 = i + 1;
           const uint32_t instance = E.r3 - 1;
@@ -687,16 +723,23 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
 }
 
 // The exact count of inner waits selects the short-loop engine.
+// Barrier-free launches take the batched loop unless asked for the
+// per-instance one (per_instance, uninstrumented) or instrumented without
+// log_batched; instrumented launches with log_batched log the batched
+// loop's waits (one entry per batch).
 template <int kRole, int kMode, bool kInstr, int kInflight>
 __device__ __forceinline__ void run_role(kconst<Stream3Params> &P, uint32_t cb, float *rx, float *ry) {
-  if constexpr (kMode == BFS_MODE_BARRIER_FREE && !kInstr) {
-    const int n = P.eng[kRole].inner.n;
-    if (n == 0) run_engine<kRole, kMode, kInstr, kInflight, 0>(P, cb, rx, ry);
-    else if (n == 1) run_engine<kRole, kMode, kInstr, kInflight, 1>(P, cb, rx, ry);
-    else run_engine<kRole, kMode, kInstr, kInflight, 2>(P, cb, rx, ry);
-  } else {
-    run_engine<kRole, kMode, kInstr, kInflight, -1>(P, cb, rx, ry);
+  if constexpr (kMode == BFS_MODE_BARRIER_FREE) {
+    const bool batched = kInstr ? P.log_batched != 0 : P.per_instance == 0;
+    if (batched) {
+      const int n = P.eng[kRole].inner.n;
+      if (n == 0) run_engine<kRole, kMode, kInstr, kInflight, 0>(P, cb, rx, ry);
+      else if (n == 1) run_engine<kRole, kMode, kInstr, kInflight, 1>(P, cb, rx, ry);
+      else run_engine<kRole, kMode, kInstr, kInflight, 2>(P, cb, rx, ry);
+      return;
+    }
   }
+  run_engine<kRole, kMode, kInstr, kInflight, -1>(P, cb, rx, ry);
 }
 
 template <int kMode, bool kInstr, int kInflight>
@@ -775,6 +818,7 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
     if (p->body_kind[it] != 1) return fail(BFS_E_UNSUPPORTED, "stream3: top level must hold only loop O");
   const std::vector<DevWait> dw = device_waits(p);
   Stream3Params P{};
+  HostEngine hosts[3];
   const int want_op[3] = {1, 4, 5};
   int n_gen = -1, per_gen = -1;
   int ring_of[4] = {0, 0, 0, 0};      // load dst, add src, add dst, store src
@@ -805,6 +849,7 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
       }
     }
     if (H.inner == -1) return fail(BFS_E_UNSUPPORTED, "stream3: every engine needs its instruction in I");
+    hosts[e] = H;
     // Resolve each instruction's waits into the launch arguments.
     EngineCode &C = P.eng[e];
     int nw = 0;
@@ -841,6 +886,59 @@ bfs_status launch_stream3(const bfs_plan *p, DevImage *img, const void *const *b
     if (p->ring_slots[ring_of[i]] < n_gen * per_gen)
       return fail(BFS_E_INVALID, "stream3: ring_slots smaller than the addressed slots");
   }
+  // Ring-slot reuse the program orders.  A slot of generation
+  // (r_M - 1) % n_gen at position (rhat_I - 1) % per_gen is written again
+  // per_gen instances later in a long trip of I, and n_gen iterations of M
+  // later (r_M counts across O iterations).  For each ring, its first writer
+  // must wait for its last reader before the reuse:
+  //   I: a dependency between their I instructions at offset <= per_gen
+  //      orders reuse inside a trip; without one a trip of I may not exceed
+  //      per_gen;
+  //   O: a marker of the reader after M -> an acquire of the writer before M
+  //      at offset kO: the generations of kO consecutive O iterations must be
+  //      distinct, so an M trip may not exceed n_gen / kO;
+  //   M: a marker -> acquire pair at M at offset <= n_gen orders reuse inside
+  //      an O iteration; with kO = 1 (all reads of the previous O iteration
+  //      drained) the M trip is then unbounded.
+  // Barrier mode drains every engine at each iteration end: no bound.
+  P.max_trip_m = 0xffffffffu;
+  P.max_trip_i = 0xffffffffu;
+  if (p->mode == BFS_MODE_BARRIER_FREE) {
+    const bool in_place = ring_of[0] == ring_of[3];
+    const int pairs[2][2] = {{0, in_place ? 2 : 1}, {1, 2}};
+    const int n_pairs = in_place ? 1 : 2;
+    auto in_list = [](const std::vector<int> &v, int ins) { return std::find(v.begin(), v.end(), ins) != v.end(); };
+    // smallest offset of a dependency rd -> wr matching the level, or -1
+    auto prot = [&](int rd, int wr, int level) {
+      int best = -1;
+      for (size_t d = 0; d < p->deps.size() / 3; ++d) {
+        if (!p->dep_linear.empty() && p->dep_linear[d]) continue;
+        const int prd = p->deps[3 * d], cns = p->deps[3 * d + 1], k = p->deps[3 * d + 2];
+        bool ok = false;
+        if (level == 3) ok = prd == hosts[rd].inner && cns == hosts[wr].inner && k >= 1 && k <= per_gen;
+        else if (level == 2) ok = in_list(hosts[rd].m_post, prd) && in_list(hosts[wr].m_pre, cns) && k >= 1 && k <= n_gen;
+        else ok = in_list(hosts[rd].o_post, prd) && in_list(hosts[wr].o_pre, cns) && k >= 1;
+        if (ok && (best < 0 || k < best)) best = k;
+      }
+      return best;
+    };
+    bool inner_ok = true, m_ok = true;
+    int k_o = 1;
+    for (int i = 0; i < n_pairs; ++i) {
+      const int wr = pairs[i][0], rd = pairs[i][1];
+      inner_ok = inner_ok && prot(rd, wr, 3) > 0;
+      m_ok = m_ok && prot(rd, wr, 2) > 0;
+      const int ko = prot(rd, wr, 1);
+      if (ko < 0)
+        return fail(BFS_E_UNSUPPORTED, "stream3: ring reuse across O iterations needs a marker -> acquire "
+                                       "dependency at O from the ring's last reader to its first writer");
+      k_o = std::max(k_o, ko);
+    }
+    if (!inner_ok) P.max_trip_i = (uint32_t)per_gen;
+    if (!(m_ok && k_o == 1)) P.max_trip_m = (uint32_t)(n_gen / k_o);
+  }
+  P.per_instance = (o.flags & BFS_RUN_PER_INSTANCE) ? 1 : 0;
+  P.log_batched = (dbg && (o.flags & BFS_RUN_LOG_BATCHED) && o.fault_dep < 0) ? 1 : 0;
   P.trips = trips;
   P.trip_off = trip_off;
   P.base = static_cast<const int64_t *>(bufs[0]);

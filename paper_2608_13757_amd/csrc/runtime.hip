@@ -4,6 +4,7 @@
 
 #include <cstring>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "bfs_internal.h"
@@ -45,6 +46,60 @@ std::vector<DevWait> device_waits(const bfs_plan *p) {
   return w;
 }
 
+namespace {
+
+// Table order in a packed plan image.
+enum { T_CODE, T_COFF, T_WAIT, T_OP, T_ARGS, T_IW, T_WL, T_UPD, T_LP, T_N };
+// The first kErrBytes of an image hold the error words (zero at upload).
+constexpr size_t kErrBytes = 256;
+
+// Packs the plan's device tables into plan->packed once (caller holds
+// plan->dev_mu).
+void pack_tables(bfs_plan *plan) {
+  if (!plan->packed.empty()) return;
+  const std::vector<DevWait> waits = device_waits(plan);
+  const std::pair<const void *, size_t> src[T_N] = {
+      {plan->code.data(), plan->code.size() * 4},
+      {plan->code_off.data(), plan->code_off.size() * 4},
+      {waits.data(), waits.size() * sizeof(DevWait)},
+      {plan->instr_opcode.data(), plan->instr_opcode.size() * 4},
+      {plan->instr_args.data(), plan->instr_args.size() * 4},
+      {plan->instr_wait_off.data(), plan->instr_wait_off.size() * 4},
+      {plan->instr_wait_list.data(), plan->instr_wait_list.size() * 4},
+      {plan->instr_update.data(), plan->instr_update.size() * 4},
+      {plan->loop_parent.data(), plan->loop_parent.size() * 4}};
+  plan->packed_off.assign(T_N, 0);
+  size_t off = kErrBytes;
+  for (int t = 0; t < T_N; ++t) {
+    off = align_up(off, 256);
+    plan->packed_off[t] = off;
+    off += src[t].second > 0 ? src[t].second : 4;
+  }
+  plan->packed.assign(align_up(off, 256), 0);
+  for (int t = 0; t < T_N; ++t)
+    if (src[t].first && src[t].second) std::memcpy(plan->packed.data() + plan->packed_off[t], src[t].first, src[t].second);
+}
+
+// Device pointers of a packed image placed at mem.
+DevImage image_at(const bfs_plan *plan, void *mem, int dev) {
+  DevImage img;
+  img.device = dev;
+  auto at = [&](int t) { return reinterpret_cast<unsigned char *>(mem) + plan->packed_off[t]; };
+  img.code = reinterpret_cast<int32_t *>(at(T_CODE));
+  img.code_off = reinterpret_cast<int32_t *>(at(T_COFF));
+  img.waits = reinterpret_cast<DevWait *>(at(T_WAIT));
+  img.instr_opcode = reinterpret_cast<int32_t *>(at(T_OP));
+  img.instr_args = reinterpret_cast<int32_t *>(at(T_ARGS));
+  img.instr_waits = reinterpret_cast<int32_t *>(at(T_IW));
+  img.waits_by_instr = reinterpret_cast<int32_t *>(at(T_WL));
+  img.instr_update = reinterpret_cast<int32_t *>(at(T_UPD));
+  img.loop_parent = reinterpret_cast<int32_t *>(at(T_LP));
+  img.err = reinterpret_cast<uint32_t *>(mem);
+  return img;
+}
+
+}  // namespace
+
 bfs_status device_image(const bfs_plan *cplan, DevImage **out) {
   bfs_plan *plan = const_cast<bfs_plan *>(cplan);
   int dev = 0;
@@ -56,53 +111,18 @@ bfs_status device_image(const bfs_plan *cplan, DevImage **out) {
       *out = &img;
       return BFS_OK;
     }
-  // Pack every table into one allocation.
-  const std::vector<DevWait> waits = device_waits(plan);
-  struct Part { const void *src; size_t bytes; size_t off; };
-  std::vector<Part> parts;
-  size_t off = 0;
-  auto add = [&](const void *src, size_t bytes) {
-    off = align_up(off, 256);
-    parts.push_back(Part{src, bytes, off});
-    off += bytes > 0 ? bytes : 4;
-    return parts.size() - 1;
-  };
-  size_t i_code = add(plan->code.data(), plan->code.size() * 4);
-  size_t i_coff = add(plan->code_off.data(), plan->code_off.size() * 4);
-  size_t i_wait = add(waits.data(), waits.size() * sizeof(DevWait));
-  size_t i_op = add(plan->instr_opcode.data(), plan->instr_opcode.size() * 4);
-  size_t i_args = add(plan->instr_args.data(), plan->instr_args.size() * 4);
-  size_t i_iw = add(plan->instr_wait_off.data(), plan->instr_wait_off.size() * 4);
-  size_t i_wl = add(plan->instr_wait_list.data(), plan->instr_wait_list.size() * 4);
-  size_t i_upd = add(plan->instr_update.data(), plan->instr_update.size() * 4);
-  size_t i_lp = add(plan->loop_parent.data(), plan->loop_parent.size() * 4);
-  size_t i_err = add(nullptr, 64);
-  const size_t total = align_up(off, 256);
+  // Every table in one allocation.
+  pack_tables(plan);
   void *mem = nullptr;
-  e = hipMalloc(&mem, total);
+  e = hipMalloc(&mem, plan->packed.size());
   if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipMalloc: ") + hipGetErrorString(e));
-  std::vector<unsigned char> host(total, 0);
-  for (auto &pt : parts)
-    if (pt.src && pt.bytes) std::memcpy(host.data() + pt.off, pt.src, pt.bytes);
-  e = hipMemcpy(mem, host.data(), total, hipMemcpyHostToDevice);
+  e = hipMemcpy(mem, plan->packed.data(), plan->packed.size(), hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(mem);
     return fail(BFS_E_DEVICE, std::string("hipMemcpy: ") + hipGetErrorString(e));
   }
-  DevImage img;
-  img.device = dev;
+  DevImage img = image_at(plan, mem, dev);
   img.mem = mem;
-  auto at = [&](size_t i) { return reinterpret_cast<unsigned char *>(mem) + parts[i].off; };
-  img.code = reinterpret_cast<int32_t *>(at(i_code));
-  img.code_off = reinterpret_cast<int32_t *>(at(i_coff));
-  img.waits = reinterpret_cast<DevWait *>(at(i_wait));
-  img.instr_opcode = reinterpret_cast<int32_t *>(at(i_op));
-  img.instr_args = reinterpret_cast<int32_t *>(at(i_args));
-  img.instr_waits = reinterpret_cast<int32_t *>(at(i_iw));
-  img.waits_by_instr = reinterpret_cast<int32_t *>(at(i_wl));
-  img.instr_update = reinterpret_cast<int32_t *>(at(i_upd));
-  img.loop_parent = reinterpret_cast<int32_t *>(at(i_lp));
-  img.err = reinterpret_cast<uint32_t *>(at(i_err));
   plan->images.push_back(img);
   *out = &plan->images.back();
   return BFS_OK;
@@ -126,23 +146,25 @@ void free_images(bfs_plan *plan) {
 
 using namespace bfs;
 
-extern "C" {
+namespace {
 
-bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t n_buffers,
-                   const int32_t *dev_trips, const int64_t *dev_trip_off, int32_t n_wg,
-                   struct ihipStream_t *stream, uint32_t *dev_debug_log, int64_t debug_capacity,
-                   const bfs_run_opts *opts) {
+// Argument checks and defaults of bfs_run.
+// Returns BFS_OK with *skip set when there is nothing to launch.
+bfs_status run_prologue(const bfs_plan *plan, int32_t n_buffers, const void *const *dev_buffers, int32_t n_wg,
+                        uint32_t *dev_debug_log, int64_t debug_capacity, const bfs_run_opts *opts, bfs_run_opts &o,
+                        bool *skip) {
+  *skip = false;
   if (!plan) return fail(BFS_E_INVALID, "null plan");
   if (n_wg < 0) return fail(BFS_E_INVALID, "negative workgroup count");
   if (n_buffers < 0 || (n_buffers > 0 && !dev_buffers)) return fail(BFS_E_INVALID, "bad buffer list");
   if (dev_debug_log && debug_capacity < 0) return fail(BFS_E_INVALID, "negative debug capacity");
-  if (n_wg == 0) return BFS_OK;
-  bfs_run_opts o{};
+  o = bfs_run_opts{};
   o.watchdog_polls = 1ull << 24;
   o.fault_dep = -1;
   o.fault_delta = 0;
   o.dev_stats = nullptr;
   o.k_unroll = 1;
+  o.flags = 0;
   if (opts) {
     if (opts->watchdog_polls) o.watchdog_polls = opts->watchdog_polls;
     o.fault_dep = opts->fault_dep;
@@ -151,12 +173,19 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
     if (opts->k_unroll > 1) o.k_unroll = opts->k_unroll;
     if (opts->k_unroll < 0 || (o.k_unroll != 1 && o.k_unroll != 2 && o.k_unroll != 4 && o.k_unroll != 8))
       return fail(BFS_E_INVALID, "k_unroll must be 0, 1, 2, 4 or 8");
+    if (opts->flags & ~(BFS_RUN_PER_INSTANCE | BFS_RUN_LOG_BATCHED))
+      return fail(BFS_E_INVALID, "unknown bfs_run_opts.flags bits");
+    o.flags = opts->flags;
   }
   if (plan->mode == BFS_MODE_BARRIER_FREE && plan->stats.n_fallback > 0 && plan->kernel != BFS_KERNEL_INTERP)
     return fail(BFS_E_UNSUPPORTED, "barrier-fallback dependencies run on the interpreter family only");
-  DevImage *img = nullptr;
-  bfs_status st = device_image(plan, &img);
-  if (st != BFS_OK) return st;
+  if (n_wg == 0) *skip = true;
+  return BFS_OK;
+}
+
+bfs_status dispatch(const bfs_plan *plan, DevImage *img, const void *const *dev_buffers, int32_t n_buffers,
+                    const int32_t *dev_trips, const int64_t *dev_trip_off, int32_t n_wg, struct ihipStream_t *stream,
+                    uint32_t *dev_debug_log, int64_t debug_capacity, const bfs_run_opts &o) {
   switch (plan->kernel) {
     case BFS_KERNEL_INTERP:
       return launch_interp(plan, img, dev_buffers, n_buffers, dev_trips, dev_trip_off, n_wg, stream,
@@ -184,34 +213,65 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
   }
 }
 
-bfs_status bfs_run_status(const bfs_plan *plan, struct ihipStream_t *stream) {
-  if (!plan) return fail(BFS_E_INVALID, "null plan");
+// Reports (and clears) the first error recorded in an image's error words.
+bfs_status report_error_words(uint32_t *dev_err) {
+  uint32_t w[8] = {0};
+  hipError_t e = hipMemcpy(w, dev_err, sizeof w, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipMemcpy: ") + hipGetErrorString(e));
+  if (w[0] == 0) return BFS_OK;
+  uint32_t z[8] = {0};
+  (void)hipMemcpy(dev_err, z, sizeof z, hipMemcpyHostToDevice);
+  if (w[0] == 2) {
+    static const char *what[5] = {"?", "trip count beyond the work item", "trip table disagrees with a static loop",
+                                  "load offset beyond 32 bits",
+                                  "trip count beyond the ring reuse the program's dependencies order"};
+    return fail(BFS_E_INVALID, std::string("run-time input rejected in workgroup ") + std::to_string(w[2]) +
+                                   " (wave " + std::to_string(w[6]) + "): " + what[w[1] < 5 ? w[1] : 0] +
+                                   " (index " + std::to_string(w[3]) + ", value " + std::to_string(w[4]) +
+                                   ", limit " + std::to_string(w[5]) + ")");
+  }
+  return fail(BFS_E_DEADLOCK, "wait of dependency " + std::to_string(w[1]) + " in workgroup " +
+                                  std::to_string(w[2]) + " (wave " + std::to_string(w[6]) + ", instance " +
+                                  std::to_string(w[3]) + ") saw " + std::to_string(w[5]) + " < threshold " +
+                                  std::to_string(w[4]));
+}
+
+}  // namespace
+
+extern "C" {
+
+bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t n_buffers,
+                   const int32_t *dev_trips, const int64_t *dev_trip_off, int32_t n_wg,
+                   struct ihipStream_t *stream, uint32_t *dev_debug_log, int64_t debug_capacity,
+                   const bfs_run_opts *opts) {
+  bfs_run_opts o;
+  bool skip = false;
+  bfs_status st = run_prologue(plan, n_buffers, dev_buffers, n_wg, dev_debug_log, debug_capacity, opts, o, &skip);
+  if (st != BFS_OK || skip) return st;
+  DevImage *img = nullptr;
+  st = device_image(plan, &img);
+  if (st != BFS_OK) return st;
+  return dispatch(plan, img, dev_buffers, n_buffers, dev_trips, dev_trip_off, n_wg, stream, dev_debug_log,
+                  debug_capacity, o);
+}
+
+bfs_status bfs_run_status(const bfs_plan *cplan, struct ihipStream_t *stream) {
+  if (!cplan) return fail(BFS_E_INVALID, "null plan");
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipStreamSynchronize: ") + hipGetErrorString(e));
-  if (plan->mode == BFS_MODE_BARRIER_FREE && plan->stats.n_fallback > 0 && plan->kernel != BFS_KERNEL_INTERP)
+  if (cplan->mode == BFS_MODE_BARRIER_FREE && cplan->stats.n_fallback > 0 && cplan->kernel != BFS_KERNEL_INTERP)
     return fail(BFS_E_UNSUPPORTED, "barrier-fallback dependencies run on the interpreter family only");
-  DevImage *img = nullptr;
-  bfs_status st = device_image(plan, &img);
-  if (st != BFS_OK) return st;
-  uint32_t w[8] = {0};
-  e = hipMemcpy(w, img->err, sizeof w, hipMemcpyDeviceToHost);
-  if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipMemcpy: ") + hipGetErrorString(e));
-  if (w[0] != 0) {
-    uint32_t z[8] = {0};
-    (void)hipMemcpy(img->err, z, sizeof z, hipMemcpyHostToDevice);
-    if (w[0] == 2) {
-      static const char *what[4] = {"?", "trip count beyond the work item", "trip table disagrees with a static loop",
-                                    "load offset beyond 32 bits"};
-      return fail(BFS_E_INVALID, std::string("run-time input rejected in workgroup ") + std::to_string(w[2]) +
-                                     " (wave " + std::to_string(w[6]) + "): " + what[w[1] < 4 ? w[1] : 0] +
-                                     " (index " + std::to_string(w[3]) + ", value " + std::to_string(w[4]) +
-                                     ", limit " + std::to_string(w[5]) + ")");
-    }
-    return fail(BFS_E_DEADLOCK, "wait of dependency " + std::to_string(w[1]) + " in workgroup " +
-                                    std::to_string(w[2]) + " (wave " + std::to_string(w[6]) + ", instance " +
-                                    std::to_string(w[3]) + ") saw " + std::to_string(w[5]) + " < threshold " +
-                                    std::to_string(w[4]));
+  bfs_plan *plan = const_cast<bfs_plan *>(cplan);
+  int dev = 0;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  uint32_t *own = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(plan->dev_mu);
+    for (auto &img : plan->images)
+      if (img.device == dev) own = img.err;
   }
+  if (own) return report_error_words(own);
   return BFS_OK;
 }
 

@@ -91,3 +91,32 @@ def compare_wave_logs_with_oracle(prog, plan, logs, recs_by_wg, mode):
                     assert t == 0 or obs >= t, (wg, wave, d, i, t, obs)
                 n += len(got)
     return n
+
+
+def compare_batched_log_with_oracle(prog, logs, recs_by_wg):
+    """Logs of the batched loop (one entry per batch wait): every logged
+    threshold equals the oracle's at the logged instance, bit-exact, the
+    observed counter was never below it, and every consumer instance of the
+    oracle's trace needs no more than the entry that covers it (the first
+    logged instance at or after it: batches wait before their first
+    instance issues, for the largest threshold among their instances)."""
+    n = 0
+    for wg, recs in recs_by_wg.items():
+        for d in range(len(prog.deps)):
+            r = recs[recs["dep"] == d]
+            want = {int(i): int(t) for i, t in zip(r["instance"], r["sem_thr"])}
+            got = logs.get((wg, d), [])
+            assert got, (wg, d)
+            inst = np.array([i for i, _, _ in got], np.int64)
+            thr = np.array([t for _, t, _ in got], np.int64)
+            assert (np.diff(inst) > 0).all(), (wg, d)
+            for i, t, obs in got:
+                assert i in want and want[i] == t, (wg, d, i, t, want.get(i))
+                assert t == 0 or obs >= t, (wg, d, i, t, obs)
+            oi = np.array(sorted(want), np.int64)
+            ot = np.array([want[i] for i in oi], np.int64)
+            cover = np.searchsorted(inst, oi, side="left")
+            assert (cover < len(inst)).all(), (wg, d)
+            assert (ot <= thr[cover]).all(), (wg, d)
+            n += len(got)
+    return n

@@ -91,6 +91,36 @@ def test_gemm_k_unroll(shape):
     check_close(bf16_to_f32(outs[1].view(np.uint16)).reshape(m, n), mathref.gemm_bias_gelu(gi.a, gi.bt, gi.bias))
 
 
+@pytest.mark.parametrize("u", [2, 4, 8])
+def test_gemm_k_unroll_thresholds(u):
+    """The unrolled K bodies' waits, logged from the same unrolled code that
+    uninstrumented launches time: every logged threshold equals the oracle's
+    for every wave, in both modes (K trips 8: a multiple of every factor;
+    3: all remainder for u >= 4)."""
+    for m, n, k in ((512, 512, 256), (256, 768, 96)):
+        gi = gemm_inputs(seed=5, m=m, n=n, k=k)
+        prog = gemm_program(m, n, k)
+        tt = gemm_trips(m, n, k)
+        trips, toff = trip_tensors(tt)
+        a, bt = _bits_to_dev(gi.a), _bits_to_dev(gi.bt)
+        bias = torch.from_numpy(gi.bias).cuda()
+        t_np, off = tt.flat()
+        recs = {g: core.run(prog, t_np, off[g], g).recs for g in range(tt.n_wg)}
+        outs = {}
+        for name, mode in MODES:
+            _say(f"[gemm-unroll-log] {(m, n, k)} u={u} mode={name}")
+            plan = Plan(prog, mode)
+            cap = 512
+            log = torch.zeros(plan.debug_log_words(tt.n_wg, cap), dtype=torch.int32, device="cuda")
+            c = torch.full((m * n,), -1, dtype=torch.int16, device="cuda")
+            plan.run([a, bt, bias, c], trips, toff, tt.n_wg, debug_log=log, debug_capacity=cap, k_unroll=u)
+            plan.status()
+            logs = log_records(plan, log.cpu().numpy().view(np.uint32), tt.n_wg, cap, per_wave=True)
+            assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
+            outs[name] = c.cpu().numpy()
+        assert np.array_equal(outs["barrier_free"], outs["barrier"])
+
+
 def test_gemm_k_unroll_rejects_other_factors():
     m, n, k = 256, 256, 64
     prog = gemm_program(m, n, k)

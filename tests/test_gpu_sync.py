@@ -14,8 +14,11 @@ torch = pytest.importorskip("torch")
 from oracle import core  # noqa: E402
 from paper_2608_13757_amd import (ALLOC_PER_INSTR, MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan,  # noqa: E402
                                   bfs)
-from tests.gpu_util import compare_log_with_oracle, dev, log_records, trip_tensors  # noqa: E402
-from workloads import chain_workload, random_nest, stream_program, stream_workload  # noqa: E402
+from paper_2608_13757_amd.bfs import RUN_LOG_BATCHED, RUN_PER_INSTANCE  # noqa: E402
+from tests.gpu_util import (compare_batched_log_with_oracle, compare_log_with_oracle, dev, log_records,  # noqa: E402
+                            trip_tensors)
+from workloads import (chain_workload, random_nest, stream_fixed_trips, stream_program,  # noqa: E402
+                       stream_workload, tile_bases)
 
 pytestmark = pytest.mark.gpu
 
@@ -233,6 +236,81 @@ def test_stream_full_size_values(seed):
         assert torch.equal(y, ref)
         outs[name] = y
     assert torch.equal(outs["barrier_free"], outs["barrier"])
+
+
+def test_stream_batched_path_thresholds_full_size():
+    """The timed code path's waits: the benchmark launch (1024 workgroups,
+    nest 256 x U[1,16] x U[1,4], seed 0) with the engines on the batched
+    loop of uninstrumented launches, logging one entry per batch wait.  On
+    sampled workgroups every logged threshold equals the oracle's at the
+    logged instance, bit-exact, and covers every instance of its batch; the
+    output equals the per-instance launches' (x + 1)."""
+    _say("[stream-batched-log] generating")
+    w = stream_workload(seed=0)
+    trips, off = w.trips.flat()
+    sample = [0, 1, 517, 1023]
+    recs = {g: core.run(w.prog, trips, off[g], g).recs for g in sample}
+    plan = Plan(w.prog, MODE_BARRIER_FREE)
+    cap = 4096
+    t_trips, t_off = trip_tensors(w.trips)
+    base, x = dev(w.base), dev(w.x)
+    y = torch.full((w.n_tiles * 64,), float("nan"), dtype=torch.float32, device="cuda")
+    log = torch.zeros(plan.debug_log_words(w.trips.n_wg, cap), dtype=torch.int32, device="cuda")
+    _say("[stream-batched-log] run")
+    plan.run([base, x, y], t_trips, t_off, w.trips.n_wg, debug_log=log, debug_capacity=cap, flags=RUN_LOG_BATCHED)
+    plan.status()
+    assert torch.equal(y, torch.from_numpy(w.x.reshape(-1)).cuda() + 1.0)
+    words = log.cpu().numpy().view(np.uint32)
+    logs = log_records(plan, words, w.trips.n_wg, cap)
+    logs = {k: v for k, v in logs.items() if k[0] in sample}
+    n = compare_batched_log_with_oracle(w.prog, logs, recs)
+    # batches: fewer entries than instances on the inner waits
+    n_inner = sum(int((recs[g]["dep"] == 0).sum()) for g in sample)
+    n_batched = sum(len(logs.get((g, 0), [])) for g in sample)
+    assert n > 0 and n_batched < n_inner
+
+
+def test_stream_per_instance_flag_values():
+    """BFS_RUN_PER_INSTANCE: the barrier-free engines run the per-instance
+    loop uninstrumented (the schedule of barrier mode); values equal x + 1 at
+    the benchmark shape."""
+    w = stream_workload(seed=2, n_wg=256)
+    trips, toff = trip_tensors(w.trips)
+    base, x = dev(w.base), dev(w.x)
+    y = torch.full((w.n_tiles * 64,), float("nan"), dtype=torch.float32, device="cuda")
+    _say("[stream-per-instance]")
+    plan = Plan(w.prog, MODE_BARRIER_FREE)
+    plan.run([base, x, y], trips, toff, w.trips.n_wg, flags=RUN_PER_INSTANCE)
+    plan.status()
+    assert torch.equal(y, torch.from_numpy(w.x.reshape(-1)).cuda() + 1.0)
+
+
+@pytest.mark.parametrize("m_trips,i_trip,ok", [([16] * 8, 4, True), ([16, 17, 16], 4, False), ([3] * 8, 5, False)])
+def test_stream_ring_trip_bounds(m_trips, i_trip, ok):
+    """Trips at the in-place ring's bounds (M trip n_gen / 2 = 16, I trip
+    per_gen = 4) run; one past either bound is reported as invalid input
+    (clamped on the device, so the ring never races), in both the batched
+    and the per-instance loops; barrier mode has no bound."""
+    p = stream_program()
+    tt = stream_fixed_trips(p, m_trips, i_trip, n_wg=4)
+    base_np, counts = tile_bases(tt, p.loop_id("I"))
+    n_tiles = int(counts.sum())
+    trips, toff = trip_tensors(tt)
+    base = dev(base_np)
+    x = torch.rand(n_tiles * 64, dtype=torch.float32, device="cuda")
+    for name, mode, flags in (("batched", MODE_BARRIER_FREE, 0), ("per_instance", MODE_BARRIER_FREE, RUN_PER_INSTANCE),
+                              ("barrier", MODE_BARRIER, 0)):
+        _say(f"[stream-bounds] m={m_trips[:3]} i={i_trip} {name}")
+        y = torch.full((n_tiles * 64,), float("nan"), dtype=torch.float32, device="cuda")
+        plan = Plan(p, mode)
+        plan.run([base, x, y], trips, toff, tt.n_wg, flags=flags)
+        if ok or mode == MODE_BARRIER:
+            plan.status()
+            assert torch.equal(y, x + 1.0)
+        else:
+            with pytest.raises(BfsError) as e:
+                plan.status()
+            assert e.value.status == bfs.E_INVALID
 
 
 # Launches without the debug log run engines specialised on their exact number
