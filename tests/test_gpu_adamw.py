@@ -21,7 +21,7 @@ from oracle import core  # noqa: E402
 from oracle.mathref import adamw_step  # noqa: E402
 from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan, bfs  # noqa: E402
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records  # noqa: E402
-from workloads import ADAM_HP, adamw_program, adamw_worklist  # noqa: E402
+from workloads import ADAM_HP, adamw_default_wg, adamw_program, adamw_worklist  # noqa: E402
 from workloads.tensors import AdamInputs, adamw_inputs  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -119,14 +119,16 @@ def test_adamw_zero_gradient_and_moments():
         assert not m.any() and not v.any()
 
 
-def test_adamw_full_size():
-    """2^20 parameters at the benchmark's launch shape (256 workgroups of 4
-    chunks of 1024), every element against the oracle; the modes agree."""
+@pytest.mark.parametrize("n_wg", [adamw_default_wg(1 << 20), 256], ids=["bench", "wg256"])
+def test_adamw_full_size(n_wg):
+    """2^20 parameters at the benchmark's launch shape (512 workgroups of 2
+    chunks of 1024), then 256 workgroups of 4 chunks; every element against
+    the oracle; the modes agree."""
     ai = adamw_inputs(seed=0)
     outs = {}
     for name, mode in MODES:
-        _say(f"[adamw-full] mode={name}")
-        _, _, _, p, m, v, _ = run_adam(ai, 256, mode)
+        _say(f"[adamw-full] n_wg={n_wg} mode={name}")
+        _, _, _, p, m, v, _ = run_adam(ai, n_wg, mode)
         check(ai, p, m, v)
         outs[name] = (p, m, v)
     for a, b in zip(outs["barrier_free"], outs["barrier"]):

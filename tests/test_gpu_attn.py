@@ -17,7 +17,7 @@ from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER,
                                   BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import attn_program, attn_worklist  # noqa: E402
-from workloads.configs import ATTN_WG  # noqa: E402
+from workloads.configs import ATTN_NK, ATTN_NV, ATTN_WG  # noqa: E402
 from workloads.tensors import attn_inputs, bf16_to_f32  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -42,7 +42,7 @@ def _dev16(bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
 
 
-def run_attn(ai, heads, mode, cap=0, nk=3, nv=2, alloc=ALLOC_PER_LOOP, n_wg=ATTN_WG):
+def run_attn(ai, heads, mode, cap=0, nk=ATTN_NK, nv=ATTN_NV, alloc=ALLOC_PER_LOOP, n_wg=ATTN_WG):
     prog = attn_program(heads, nk=nk, nv=nv)
     plan = Plan(prog, mode, alloc)
     wl = attn_worklist(ai.lengths, heads, n_wg=n_wg)
@@ -138,9 +138,10 @@ def test_attn_special_cases():
     check_close(out[1:], np.broadcast_to(bf16_to_f32(const), out[1:].shape))
 
 
-def test_attn_full_size_sampled():
-    """The benchmark shape (32 sequences of U[128, 4096] tokens, 16 heads),
-    checked on sampled rows one by one."""
+@pytest.fixture(scope="module")
+def full_attn():
+    """The benchmark inputs (32 sequences of U[128, 4096] tokens, 16 heads,
+    seed 0) and the oracle's rows at sampled (sequence, head, row) items."""
     heads = 16
     _say("[attn-full] generating")
     ai = attn_inputs(seed=0, heads=heads)
@@ -153,10 +154,21 @@ def test_attn_full_size_sampled():
         L = int(ai.lengths[b])
         items += [(b, b % heads, 0), (b, (b + 7) % heads, L - 1), (b, (b + 3) % heads, (L - 1) // 128 * 128)]
     ref = mathref.attention_rows(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE, items)
+    return heads, ai, items, ref
+
+
+@pytest.mark.parametrize("rings", [(ATTN_NK, ATTN_NV), (3, 2)], ids=["bench", "k3v2"])
+def test_attn_full_size_sampled(full_attn, rings):
+    """The benchmark shape and launch (256 persistent workgroups, the
+    benchmark's K and V ring depths first, then the other layout), checked
+    on sampled rows one by one; both modes bit-identical."""
+    heads, ai, items, ref = full_attn
+    nk, nv = rings
     outs = {}
     for name, mode in MODES:
-        _say(f"[attn-full] mode={name}")
-        _, _, _, out, _ = run_attn(ai, heads, mode)
+        _say(f"[attn-full] rings={rings} mode={name}")
+        _, _, wl, out, _ = run_attn(ai, heads, mode, nk=nk, nv=nv)
+        assert wl.trips.n_wg == ATTN_WG
         got = np.array([out[ai.cu_seqlens[b] + i, h] for b, h, i in items])
         check_close(got, ref)
         outs[name] = out

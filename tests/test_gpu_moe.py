@@ -18,6 +18,7 @@ from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER,
                                   BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import moe_program, moe_worklist  # noqa: E402
+from workloads.configs import MOE_LINEAR, MOE_MCHUNK  # noqa: E402
 from workloads.tensors import bf16_to_f32, moe_inputs, moe_weights_all  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -44,7 +45,7 @@ def _dev16(bits):
 class MoeRun:
     """Device copies of one MoE problem and the two launches."""
 
-    def __init__(self, moe, mchunk=8):
+    def __init__(self, moe, mchunk=MOE_MCHUNK):
         self.moe = moe
         wg, wu, wd = moe_weights_all(moe)
         self.wg, self.wu, self.wd = _dev16(wg), _dev16(wu), _dev16(wd)
@@ -54,7 +55,13 @@ class MoeRun:
         T = len(moe.assign)
         self.h = torch.full((T, moe.ffn), -1, dtype=torch.int16, device="cuda")
         self.y = torch.full((T, moe.hidden), -1, dtype=torch.int16, device="cuda")
-        self.wl = {ph: moe_worklist(moe.counts, ph, moe.hidden, moe.ffn, mchunk=mchunk) for ph in (1, 2)}
+        self.set_mchunk(mchunk)
+
+    def set_mchunk(self, mchunk):
+        """Work lists with runs of at most ``mchunk`` M-tiles per workgroup."""
+        self.mchunk = mchunk
+        self.wl = {ph: moe_worklist(self.moe.counts, ph, self.moe.hidden, self.moe.ffn, mchunk=mchunk)
+                   for ph in (1, 2)}
         self.dev_wl = {}
         for ph, wl in self.wl.items():
             trips, toff = trip_tensors(wl.trips)
@@ -181,29 +188,49 @@ def test_moe_per_instr():
     assert np.array_equal(y.view(np.uint32), y2.view(np.uint32))
 
 
-def test_moe_full_size_sampled():
-    """The benchmark shape (32768 tokens, 64 Zipf(1.1) experts, hidden 4096,
-    ffn 1408), checked on sampled tokens one by one."""
+@pytest.fixture(scope="module")
+def full_moe():
+    """The benchmark problem (32768 tokens, 64 Zipf(1.1) experts, hidden
+    4096, ffn 1408, seed 0) on the device, and the oracle's y rows of
+    sampled tokens and h rows of sampled expert-grouped positions."""
     _say("[moe-full] generating")
     moe = moe_inputs(seed=0)
     r = MoeRun(moe)
     order = np.argsort(-moe.counts)
     experts = list(order[:3]) + list(order[30:32]) + list(order[-3:])   # largest, middle, smallest
     rng = np.random.default_rng(5)
-    tokens = []
+    tokens, rows = [], []
     for e in experts:
         lo, hi = int(moe.expert_off[e]), int(moe.expert_off[e + 1])
         group = moe.perm[lo:hi]
         tokens += [int(group[0]), int(group[-1])] + [int(t) for t in rng.choice(group, 6)]
+        # h rows are in expert-grouped order: the first and last row of the
+        # expert, the first row of its last (ragged) M-tile, and random ones
+        rows += [lo, hi - 1, lo + (hi - 1 - lo) // 128 * 128] + [int(i) for i in rng.integers(lo, hi, 4)]
     weights = {}
-    ref = mathref.moe_tokens(moe, tokens, weights)
+    ref_y = mathref.moe_tokens(moe, tokens, weights)
+    ref_h = mathref.moe_hidden(moe, [int(moe.perm[i]) for i in rows], weights)
+    return r, tokens, ref_y, rows, ref_h
+
+
+@pytest.mark.parametrize("mchunk,linear", [(MOE_MCHUNK, MOE_LINEAR), (8, False)], ids=["bench", "m8_acq"])
+def test_moe_full_size_sampled(full_moe, mchunk, linear):
+    """The benchmark shape and launch (runs of at most four M-tiles, the
+    linearized ring, as timed), then runs of eight with the paper's ACQL
+    drain; sampled y tokens and h rows one by one; both modes bit-identical."""
+    r, tokens, ref_y, rows, ref_h = full_moe
+    r.set_mchunk(mchunk)
     outs = {}
     for name, mode in MODES:
-        _say(f"[moe-full] mode={name}")
-        _, y, _ = r.run(mode)
-        check_close(y[tokens], ref)
-        outs[name] = y
-    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+        _say(f"[moe-full] mchunk={mchunk} linear={linear} mode={name}")
+        r.h.fill_(-1)
+        r.y.fill_(-1)
+        h, y, _ = r.run(mode, linear=linear)
+        check_close(y[tokens], ref_y)
+        check_close(h[rows], ref_h)
+        outs[name] = (h, y)
+    for a, b in zip(outs["barrier_free"], outs["barrier"]):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
 def test_moe_rejects_missing_dependency():

@@ -206,6 +206,29 @@ def test_stream_inplace_needs_its_o_dependency_and_generations():
     assert hazard.check(few, core.run(few, trips, off[0], 0)) != []
 
 
+def test_stream_inplace_trip_bounds():
+    """The in-place ring (32 generations of 4 slots, MARK_O -> ACQ_O at
+    offset 2, no inner reuse dependency) is race-free with every M trip at
+    its bound n_gen / 2 = 16 and every I trip at per_gen = 4, and races
+    one past either bound (the launcher reports such trips as invalid)."""
+    from workloads import stream_fixed_trips, stream_program
+    p = stream_program()
+    ok = stream_fixed_trips(p, [16] * 6, 4)
+    trips, off = ok.flat()
+    res = core.run(p, trips, off[0], 0)
+    assert res.recs["order_ok"].all()
+    assert hazard.check(p, res, "barrier_free") == []
+    for m_trips, i_trip in (([16, 17, 16, 16], 4), ([16] * 4, 5)):
+        bad = stream_fixed_trips(p, m_trips, i_trip)
+        trips, off = bad.flat()
+        assert hazard.check(p, core.run(p, trips, off[0], 0), "barrier_free") != [], (m_trips, i_trip)
+    # with the inner reuse dependency a trip of I may be longer than a generation
+    pw = stream_program(inner_war=True)
+    long_i = stream_fixed_trips(pw, [16] * 3, 9)
+    trips, off = long_i.flat()
+    assert hazard.check(pw, core.run(pw, trips, off[0], 0), "barrier_free") == []
+
+
 def test_hazard_catches_dropped_dependencies():
     w = chain_workload(seed=0)
     trips, off = w.trips.flat()
@@ -288,6 +311,39 @@ def test_attention_reference_special_cases():
     rows = mathref.attention_rows(ai.q, ai.k, ai.v, ai.cu_seqlens, scale, [(1, 1, 2), (0, 0, 0)])
     s0 = ai.cu_seqlens[1]
     assert np.allclose(rows[0], full[s0 + 2, 1]) and np.allclose(rows[1], full[0, 0])
+
+
+def test_attention_softmax_weights_closed_form():
+    """Softmax weights pinned on scores with known exponentials: with scale
+    1/2, query e_0 and keys 0, 2 e_0, -2 e_0 the scores are 0, 1, -1, so with
+    V rows e_0, e_1, e_2 the output row is the softmax of (0, 1, -1) itself:
+    (1, e, 1/e) / (1 + e + 1/e).  The first two keys alone give the logistic
+    values 1/(1+e) and e/(1+e).  A zero query weights every key equally.
+    A wrong exponent base, a dropped or doubled scale, or a transposed Q K
+    product fails one of these."""
+    d, scale = 4, 0.5
+    q = np.zeros((3, 1, d), np.float32)
+    q[0, 0, 0] = 1.0                                   # row 0: e_0; rows 1, 2: zero
+    k = np.zeros((3, 1, d), np.float32)
+    k[1, 0, 0], k[2, 0, 0] = 2.0, -2.0
+    v = np.zeros((3, 1, d), np.float32)
+    v[0, 0, 0], v[1, 0, 1], v[2, 0, 2] = 1.0, 1.0, 1.0
+    q, k, v = (to_bf16_bits(a) for a in (q, k, v))
+    # softmax(0, 1, -1) = (0.24472847105479764, 0.6652409557748219, 0.09003057317038046)
+    want3 = np.array([0.24472847105479764, 0.6652409557748219, 0.09003057317038046, 0.0])
+    cu3 = np.array([0, 3])
+    full = mathref.attention(q, k, v, cu3, scale)
+    assert np.abs(full[0, 0] - want3).max() < 1e-12
+    assert np.abs(full[1, 0] - np.array([1 / 3, 1 / 3, 1 / 3, 0.0])).max() < 1e-12
+    rows = mathref.attention_rows(q, k, v, cu3, scale, [(0, 0, 0), (0, 0, 2)])
+    assert np.abs(rows[0] - want3).max() < 1e-12
+    assert np.abs(rows[1] - np.array([1 / 3, 1 / 3, 1 / 3, 0.0])).max() < 1e-12
+    # two keys: scores 0 and 1 give the logistic values 1/(1+e), e/(1+e)
+    want2 = np.array([0.2689414213699951, 0.7310585786300049, 0.0, 0.0])
+    cu2 = np.array([0, 2])
+    two = mathref.attention(q[:2], k[:2], v[:2], cu2, scale)
+    assert np.abs(two[0, 0] - want2).max() < 1e-12
+    assert np.abs(mathref.attention_rows(q[:2], k[:2], v[:2], cu2, scale, [(0, 0, 0)])[0] - want2).max() < 1e-12
 
 
 def test_moe_reference_properties():

@@ -394,6 +394,20 @@ def stream_workload(seed: int = 0, n_wg: int = 1024, outer: int = 256, mid_max: 
     return StreamWorkload(prog, tt, base, counts, x, n_tiles)
 
 
+def stream_fixed_trips(prog: Program, m_trips, i_trip: int, n_wg: int = 1) -> TripTables:
+    """Trip tables of one or more identical workgroups: O runs len(m_trips)
+    iterations with those M trips, every trip of I is i_trip."""
+    m_trips = np.asarray(m_trips, dtype=np.int32)
+
+    def draw(l, n):
+        if l == 1:
+            return np.full(n, len(m_trips))
+        if l == 2:
+            return m_trips[:n]
+        return np.full(n, i_trip)
+    return TripTables([draw_trips(prog, draw) for _ in range(n_wg)])
+
+
 # ---------------------------------------------------------------------------
 # random tiny nests (property tests of thresholds)
 # ---------------------------------------------------------------------------
@@ -491,9 +505,11 @@ ATTN_BQ = 128       # query rows per workgroup
 ATTN_BKV = 64       # keys per KV block
 ATTN_D = 128        # head dimension
 ATTN_SP = 2         # S/P buffer slots
+ATTN_NK = 2         # K ring slots of the benchmark layout
+ATTN_NV = 3         # V ring slots of the benchmark layout (2 + 3 measured 2 % faster than 3 + 2)
 
 
-def attn_program(heads: int, dim: int = ATTN_D, nk: int = 2, nv: int = 3) -> Program:
+def attn_program(heads: int, dim: int = ATTN_D, nk: int = ATTN_NK, nv: int = ATTN_NV) -> Program:
     """A fixed set of workgroups, each running a run-time list of (sequence,
     head, 128-query tile) work items:
 
@@ -606,6 +622,8 @@ MOE_BN = {1: 128, 2: 256}    # output columns per workgroup: h columns (phase 1)
 MOE_CHUNKS = {1: 2, 2: 4}    # epilogue chunks per M-tile
 MOE_RING = 5
 MOE_MCHUNK = 4               # at most this many M-tiles per workgroup
+MOE_LINEAR = True            # benchmark ring form: the linearized MMA->LOAD dependency (extension);
+                             # False selects the paper's ACQL drain at every M-tile
 
 
 def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring: int = 2,
@@ -781,6 +799,13 @@ def adamw_program(n: int = ADAM_N, chunk: int = 1024, waves: int = 2, ring: int 
     b.dep("UPDATE", "STORE", 0)
     b.dep("STORE", "LOAD", ring)
     return b.build()
+
+
+def adamw_default_wg(n: int, chunk: int = 1024) -> int:
+    """Workgroups of the benchmark launch shape: two chunks per workgroup,
+    at most 1024 workgroups (512 for 2^20 parameters in chunks of 1024)."""
+    n_chunks = -(-n // chunk)
+    return max(1, min(1024, -(-n_chunks // 2)))
 
 
 def adamw_worklist(n: int, chunk: int, n_wg: int):
