@@ -292,7 +292,40 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
                    struct ihipStream_t *stream, uint32_t *dev_debug_log, int64_t debug_capacity,
                    const bfs_run_opts *opts);
 
-/* Synchronizes stream, then reports (and clears) the plan's error words:
+/*
+ * bfs_run without any device allocation, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments, kernels and results as bfs_run.
+ *
+ * bfs_run keeps each plan's device tables and error words in an allocation
+ * of its own (made at the plan's first launch on a device).  This entry
+ * point places them instead in one fixed array of BFS_NOALLOC_MAX_IMAGE_BYTES
+ * bytes in the library's code object: each device holds its own copy from
+ * the library's load until the process ends, and every plan on that device
+ * shares it.  It calls no allocation routine (no hipMalloc, no hipFree).
+ *
+ *   - A plan whose tables exceed the array: BFS_E_RESOURCE (nothing is
+ *     launched).  Only the interpreter family reads the tables: the first
+ *     launch of an interpreter plan after another plan's writes them into
+ *     the array with an asynchronous host-to-device copy on stream (the plan
+ *     must stay alive until that work has completed); the other families read
+ *     only the error words.
+ *   - The error words are shared by every plan on the device: a device-side
+ *     error (watchdog, rejected trip count) stays recorded until
+ *     bfs_run_status of a plan that used this entry point on the device
+ *     reports and clears it.
+ *   - The array keeps the last call's contents.  Calls that overlap on one
+ *     device (several streams or threads at once) race on it.
+ */
+#define BFS_NOALLOC_MAX_IMAGE_BYTES (256u * 1024u)
+bfs_status bfs_run_noalloc(const bfs_plan *plan, const void *const *dev_buffers, int32_t n_buffers,
+                           const int32_t *dev_trips, const int64_t *dev_trip_off, int32_t n_wg,
+                           struct ihipStream_t *stream, uint32_t *dev_debug_log, int64_t debug_capacity,
+                           const bfs_run_opts *opts);
+
+/* Synchronizes stream, then reports (and clears) the plan's error words --
+ * those of its own allocation (bfs_run) and, if the plan has used
+ * bfs_run_noalloc on the current device, the fixed array's:
  * BFS_E_DEADLOCK if any wait gave up since the last call, BFS_E_INVALID if a
  * workgroup rejected a run-time input (a trip count beyond its work item, a
  * trip table that disagrees with a loop the kernel runs statically, a load

@@ -23,7 +23,7 @@ KASE_FALLBACK = 4
 KERNELS = {"interp": 0, "stream3": 1, "gemm": 2, "attn": 3, "moe": 4, "rmsnorm": 5, "adamw": 6}
 
 EXPORTED = ["bfs_plan_create", "bfs_plan_formulas", "bfs_plan_static_waits", "bfs_plan_stats",
-            "bfs_eval_threshold", "bfs_plan_destroy", "bfs_run", "bfs_run_status",
+            "bfs_eval_threshold", "bfs_plan_destroy", "bfs_run", "bfs_run_noalloc", "bfs_run_status",
             "bfs_status_string", "bfs_last_error"]
 
 
@@ -95,6 +95,8 @@ def lib():
         L.bfs_run.restype = C.c_int
         L.bfs_run.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
                               C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]
+        L.bfs_run_noalloc.restype = C.c_int
+        L.bfs_run_noalloc.argtypes = L.bfs_run.argtypes
         L.bfs_run_status.restype = C.c_int
         L.bfs_run_status.argtypes = [C.c_void_p, C.c_void_p]
         L.bfs_status_string.restype = C.c_char_p
@@ -210,6 +212,15 @@ class Plan:
         opts = RunOpts(watchdog_polls, fault_dep, fault_delta, _ptr(stats), k_unroll, flags)
         _check(lib().bfs_run(self.handle, arr, len(buffers), _ptr(trips), _ptr(trip_off), n_wg,
                              _stream_handle(stream), _ptr(debug_log), debug_capacity, C.byref(opts)))
+
+    def run_noalloc(self, buffers, trips, trip_off, n_wg, stream=None, debug_log=None, debug_capacity=0,
+                    watchdog_polls=0, fault_dep=-1, fault_delta=0, stats=None, k_unroll=0, flags=0):
+        """As run(), through bfs_run_noalloc: the plan's tables and error words
+        live in the library's fixed device array instead of an allocation."""
+        arr = (C.c_void_p * max(1, len(buffers)))(*[_ptr(b) for b in buffers])
+        opts = RunOpts(watchdog_polls, fault_dep, fault_delta, _ptr(stats), k_unroll, flags)
+        _check(lib().bfs_run_noalloc(self.handle, arr, len(buffers), _ptr(trips), _ptr(trip_off), n_wg,
+                                     _stream_handle(stream), _ptr(debug_log), debug_capacity, C.byref(opts)))
 
     def status(self, stream=None):
         """Synchronize the stream; raise BfsError(E_DEADLOCK) if a wait gave up."""

@@ -112,9 +112,13 @@ struct bfs_plan {
 
   std::mutex dev_mu;
   std::vector<bfs::DevImage> images;     // one per device used
-  // the packed device tables (error words first), built once
+  // bfs_run_noalloc: the packed tables (built once, kept for the
+  // asynchronous copies into the static device array), the plan's unique id,
+  // and the devices whose static array this plan has written (bit d).
   std::vector<unsigned char> packed;
   std::vector<size_t> packed_off;        // table offsets in `packed`
+  uint64_t uid = 0;
+  uint64_t noalloc_devices = 0;
 };
 
 namespace bfs {

@@ -1,6 +1,7 @@
 // Host-side planner: validates a structured program and computes, for every
 // dependency, the barrier-free wait of Sections 5.2-5.5 (or the barrier-mode
 // static wait of Section 3.4).  Pure host code; needs no GPU.
+#include <atomic>
 #include <algorithm>
 #include <cstring>
 #include <map>
@@ -375,6 +376,8 @@ bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc all
   if (!prog->loop_parent || !prog->body_off || !prog->block_off)
     return fail(BFS_E_INVALID, "null program array");
   bfs_plan *p = new bfs_plan();
+  static std::atomic<uint64_t> next_uid{1};
+  p->uid = next_uid.fetch_add(1);
   p->mode = mode;
   p->alloc = alloc;
   p->kernel = prog->kernel;

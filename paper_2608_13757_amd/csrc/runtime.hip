@@ -9,6 +9,10 @@
 
 #include "bfs_internal.h"
 
+// The fixed device array of bfs_run_noalloc (see below).  Host code never
+// names it except in the one hipGetSymbolAddress call.
+static __device__ __align__(256) unsigned char scratch[BFS_NOALLOC_MAX_IMAGE_BYTES];
+
 namespace bfs {
 
 namespace {
@@ -98,6 +102,38 @@ DevImage image_at(const bfs_plan *plan, void *mem, int dev) {
   return img;
 }
 
+// ---------------------------------------------------------------------------
+// The fixed device array of bfs_run_noalloc.  It holds a plan image (error
+// words, then the tables) like the allocation of bfs_run.  Each device keeps
+// its own copy at its own address, obtained with hipGetSymbolAddress; host
+// code uses that address, never the array's name.  Zero-initialized when the
+// code object is loaded; bfs_run_status clears the error words it reports.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = BFS_NOALLOC_MAX_IMAGE_BYTES;
+
+constexpr int kMaxDevices = 64;
+struct ScratchDev {
+  void *ptr = nullptr;       // device address of this device's copy of scratch
+  uint64_t tables_of = 0;    // uid of the plan whose tables it holds (0: none)
+};
+std::mutex g_scratch_mu;
+ScratchDev g_scratch[kMaxDevices];
+
+// Address of the current device's copy (looked up once per device, with the
+// device current).  Caller holds g_scratch_mu.
+bfs_status scratch_ptr(int dev, void **out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(BFS_E_DEVICE, "device index beyond 64");
+  if (!g_scratch[dev].ptr) {
+    void *p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(BFS_E_DEVICE, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch[dev].ptr = p;
+  }
+  *out = g_scratch[dev].ptr;
+  return BFS_OK;
+}
+
 }  // namespace
 
 bfs_status device_image(const bfs_plan *cplan, DevImage **out) {
@@ -148,7 +184,7 @@ using namespace bfs;
 
 namespace {
 
-// Argument checks and defaults of bfs_run.
+// Argument checks and defaults shared by bfs_run and bfs_run_noalloc.
 // Returns BFS_OK with *skip set when there is nothing to launch.
 bfs_status run_prologue(const bfs_plan *plan, int32_t n_buffers, const void *const *dev_buffers, int32_t n_wg,
                         uint32_t *dev_debug_log, int64_t debug_capacity, const bfs_run_opts *opts, bfs_run_opts &o,
@@ -255,6 +291,45 @@ bfs_status bfs_run(const bfs_plan *plan, const void *const *dev_buffers, int32_t
                   debug_capacity, o);
 }
 
+bfs_status bfs_run_noalloc(const bfs_plan *cplan, const void *const *dev_buffers, int32_t n_buffers,
+                           const int32_t *dev_trips, const int64_t *dev_trip_off, int32_t n_wg,
+                           struct ihipStream_t *stream, uint32_t *dev_debug_log, int64_t debug_capacity,
+                           const bfs_run_opts *opts) {
+  bfs_run_opts o;
+  bool skip = false;
+  bfs_status st = run_prologue(cplan, n_buffers, dev_buffers, n_wg, dev_debug_log, debug_capacity, opts, o, &skip);
+  if (st != BFS_OK || skip) return st;
+  bfs_plan *plan = const_cast<bfs_plan *>(cplan);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  DevImage img;
+  {
+    std::lock_guard<std::mutex> lk(plan->dev_mu);
+    pack_tables(plan);
+    if (plan->packed.size() > kScratchBytes)
+      return fail(BFS_E_RESOURCE, "plan image of " + std::to_string(plan->packed.size()) +
+                                      " bytes exceeds the no-allocation limit of " + std::to_string(kScratchBytes));
+    std::lock_guard<std::mutex> gk(g_scratch_mu);
+    void *mem = nullptr;
+    st = scratch_ptr(dev, &mem);
+    if (st != BFS_OK) return st;
+    // Only the interpreter reads the tables; the other families read the
+    // error words alone.  The error words are never overwritten here, so an
+    // error stays until bfs_run_status reports it.
+    if (plan->kernel == BFS_KERNEL_INTERP && g_scratch[dev].tables_of != plan->uid) {
+      e = hipMemcpyAsync(reinterpret_cast<unsigned char *>(mem) + kErrBytes, plan->packed.data() + kErrBytes,
+                         plan->packed.size() - kErrBytes, hipMemcpyHostToDevice, (hipStream_t)stream);
+      if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+      g_scratch[dev].tables_of = plan->uid;
+    }
+    plan->noalloc_devices |= 1ull << dev;
+    img = image_at(plan, mem, dev);
+  }
+  return dispatch(plan, &img, dev_buffers, n_buffers, dev_trips, dev_trip_off, n_wg, stream, dev_debug_log,
+                  debug_capacity, o);
+}
+
 bfs_status bfs_run_status(const bfs_plan *cplan, struct ihipStream_t *stream) {
   if (!cplan) return fail(BFS_E_INVALID, "null plan");
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
@@ -265,13 +340,21 @@ bfs_status bfs_run_status(const bfs_plan *cplan, struct ihipStream_t *stream) {
   int dev = 0;
   e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(BFS_E_DEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
-  uint32_t *own = nullptr;
+  uint32_t *own = nullptr, *fixed = nullptr;
   {
     std::lock_guard<std::mutex> lk(plan->dev_mu);
     for (auto &img : plan->images)
       if (img.device == dev) own = img.err;
+    if (dev >= 0 && dev < kMaxDevices && (plan->noalloc_devices >> dev) & 1ull) {
+      std::lock_guard<std::mutex> gk(g_scratch_mu);
+      fixed = static_cast<uint32_t *>(g_scratch[dev].ptr);
+    }
   }
-  if (own) return report_error_words(own);
+  if (own) {
+    bfs_status st = report_error_words(own);
+    if (st != BFS_OK) return st;
+  }
+  if (fixed) return report_error_words(fixed);
   return BFS_OK;
 }
 
