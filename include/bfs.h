@@ -88,7 +88,8 @@ typedef enum {
   BFS_KERNEL_ATTN = 3,        /* variable-length attention forward */
   BFS_KERNEL_MOE = 4,         /* MoE grouped GEMM with runtime per-expert trip counts */
   BFS_KERNEL_RMSNORM = 5,     /* RMSNorm + per-row FP8 (E4M3) quantization, load / vector / store engines */
-  BFS_KERNEL_ADAMW = 6        /* AdamW step over fp32 parameter chunks, load / vector / store engines */
+  BFS_KERNEL_ADAMW = 6,       /* AdamW step over fp32 parameter chunks, load / vector / store engines */
+  BFS_KERNEL_CHAIN = 7        /* two-engine chain: tiles loaded into an LDS ring, scaled and accumulated */
 } bfs_kernel;
 
 /*

@@ -20,7 +20,7 @@ MODE_BARRIER_FREE, MODE_BARRIER = 0, 1
 ALLOC_PER_LOOP, ALLOC_PER_INSTR = 0, 1
 PLAN_BARRIER_FALLBACK = 1
 KASE_FALLBACK = 4
-KERNELS = {"interp": 0, "stream3": 1, "gemm": 2, "attn": 3, "moe": 4, "rmsnorm": 5, "adamw": 6}
+KERNELS = {"interp": 0, "stream3": 1, "gemm": 2, "attn": 3, "moe": 4, "rmsnorm": 5, "adamw": 6, "chain": 7}
 
 EXPORTED = ["bfs_plan_create", "bfs_plan_formulas", "bfs_plan_static_waits", "bfs_plan_stats",
             "bfs_eval_threshold", "bfs_plan_destroy", "bfs_run", "bfs_run_noalloc", "bfs_run_status",

@@ -7,7 +7,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libbfs.so")
 SOURCES = ["plan.cpp", "runtime.hip", "kern_interp.hip", "kern_stream3.hip", "kern_gemm.hip", "kern_attn.hip", "kern_moe.hip",
-           "kern_rms.hip", "kern_adamw.hip"]
+           "kern_rms.hip", "kern_adamw.hip", "kern_chain.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-Wno-unused-parameter", "-Wno-unused-result"]

@@ -150,4 +150,7 @@ bfs_status launch_rms(const bfs_plan *p, DevImage *img, const void *const *bufs,
 bfs_status launch_adamw(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
                         const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream,
                         uint32_t *dbg, int64_t dbg_cap, const bfs_run_opts &o);
+bfs_status launch_chain(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
+                        const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream,
+                        uint32_t *dbg, int64_t dbg_cap, const bfs_run_opts &o);
 }  // namespace bfs

@@ -152,6 +152,32 @@ struct Sync {
   template <class OnBlock>
   __device__ __forceinline__ uint32_t poll_geq(uint32_t addr, uint32_t nw, uint32_t thr, uint32_t dep,
                                                uint32_t instance, OnBlock on_block) {
+    if (nw == 1) {
+      // one producer wave: a scalar compare of its word
+      uint32_t v = uniform(lds_poll(addr));
+      if (v >= thr) return v;
+      on_block();
+      const uint64_t t0 = (kInstr && st.on) ? now_ticks() : 0;
+      const uint32_t limit = C.watchdog > 0xffffffffull ? 0xffffffffu : (uint32_t)C.watchdog;
+      uint32_t polls = 0;
+      while (true) {
+        v = uniform(lds_poll(addr));
+        if (v >= thr) break;
+        on_block();
+        if (++polls > limit) {
+          report_deadlock(C.err, dep, (uint32_t)wg, instance, thr, v, (uint32_t)wave);
+          aborted = 1u;
+          return v;
+        }
+        if (polls < 4) __builtin_amdgcn_s_sleep(1);
+        else __builtin_amdgcn_s_sleep(2);
+      }
+      if (kInstr && st.on) {
+        st.blocked += now_ticks() - t0;
+        st.n_blocked += 1;
+      }
+      return v;
+    }
     const uint32_t lane = lane_id();
     const uint32_t a = addr + 4u * (lane < nw ? lane : 0u);
     const uint64_t want = (1ull << nw) - 1ull;

@@ -37,6 +37,7 @@ struct InterpParams {
   uint32_t *dbg;
   int64_t dbg_cap;
   uint32_t *err;
+  uint64_t *stats;              // per-wave statistics (null: off)
   uint64_t watchdog;
   int32_t fault_dep, fault_delta;
   int32_t n_loops, n_engines, n_instrs, mode, tile;
@@ -81,6 +82,11 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
     log_entries = P.dbg + nw + ((int64_t)wg * P.n_engines + wave) * 4 * P.dbg_cap;
   }
   bool aborted = false;
+  WaveStats stt;
+  if (P.stats) {
+    stt.on = true;
+    stt.t_start = now_ticks();
+  }
   if (lane == 0) { r[0] = 1; rhat[0] = 1; trip[0] = 1; }
   __builtin_amdgcn_s_waitcnt(0);
 
@@ -91,7 +97,11 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
     const int kind = code[4 * pc], a0 = code[4 * pc + 1], a1 = code[4 * pc + 2];
     if (kind == bfs::CODE_HALT) break;
     if (kind == bfs::CODE_LOOP) {
-      if (P.mode == BFS_MODE_BARRIER) region_sync(own_words, 1);
+      if (P.mode == BFS_MODE_BARRIER) {
+        const uint64_t t0 = stt.on ? now_ticks() : 0;
+        region_sync(own_words, 1);
+        if (stt.on) stt.barrier += now_ticks() - t0;
+      }
       const int l = a0;
       const uint32_t rp = uniform(r[P.loop_parent[l]]);
       const uint32_t t = (uint32_t)P.trips[toff[l] + (int64_t)rp - 1];
@@ -108,7 +118,9 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
     if (kind == bfs::CODE_END) {
       const int l = a0;
       if (P.mode == BFS_MODE_BARRIER) {
+        const uint64_t t0 = stt.on ? now_ticks() : 0;
         region_sync(own_words, 1);
+        if (stt.on) stt.barrier += now_ticks() - t0;
       } else if ((P.fallback_loops >> l) & 1u) {
         // Section 5.2 fallback: everything issued in this iteration of l has
         // retired on every engine before any engine starts the next one.
@@ -141,7 +153,13 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
       WaitResult res{0, true};
       if (!aborted) {
         const uint32_t addr = cnt_base + 4u * (uint32_t)(W.counter * bfs::kMaxWavesPerEngine);
+        const uint64_t t0 = stt.on ? now_ticks() : 0;
         res = wait_geq(addr, 1, thr, P.watchdog);
+        if (stt.on && thr > 0) {
+          const uint64_t dt = now_ticks() - t0;
+          stt.blocked += dt;
+          stt.n_blocked += 1;
+        }
         if (!res.ok) {
           report_deadlock(P.err, (uint32_t)W.dep, (uint32_t)wg, inst, thr, res.observed, (uint32_t)wave);
           aborted = true;
@@ -186,6 +204,17 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
     pc += 1;
   }
   if (P.dbg && lane == 0) P.dbg[(int64_t)wg * P.n_engines + wave] = nlog;
+  if (stt.on && lane == 0) {
+    uint64_t *o = P.stats + ((int64_t)wg * P.n_engines + wave) * 8;
+    o[0] = now_ticks() - stt.t_start;
+    o[1] = stt.blocked;
+    o[2] = stt.n_blocked;
+    o[3] = stt.barrier;
+    o[4] = 0;
+    o[5] = 0;
+    o[6] = 0;
+    o[7] = 0;
+  }
 }
 
 }  // namespace
@@ -218,6 +247,7 @@ bfs_status launch_interp(const bfs_plan *p, DevImage *img, const void *const *bu
   P.dbg = dbg;
   P.dbg_cap = dbg_cap;
   P.err = img->err;
+  P.stats = o.dev_stats;
   P.watchdog = o.watchdog_polls;
   P.fault_dep = o.fault_dep;
   P.fault_delta = o.fault_delta;

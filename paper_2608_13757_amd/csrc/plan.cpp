@@ -370,7 +370,7 @@ bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc all
   if (flags & ~BFS_PLAN_BARRIER_FALLBACK) return fail(BFS_E_INVALID, "unknown plan flags");
   if (mode != BFS_MODE_BARRIER_FREE && mode != BFS_MODE_BARRIER) return fail(BFS_E_INVALID, "bad mode");
   if (alloc != BFS_ALLOC_PER_LOOP && alloc != BFS_ALLOC_PER_INSTR) return fail(BFS_E_INVALID, "bad alloc");
-  if (prog->kernel < BFS_KERNEL_INTERP || prog->kernel > BFS_KERNEL_ADAMW) return fail(BFS_E_INVALID, "bad kernel");
+  if (prog->kernel < BFS_KERNEL_INTERP || prog->kernel > BFS_KERNEL_CHAIN) return fail(BFS_E_INVALID, "bad kernel");
   if (prog->n_loops < 1 || prog->n_blocks < 0 || prog->n_instrs < 0 || prog->n_deps < 0)
     return fail(BFS_E_INVALID, "negative sizes");
   if (!prog->loop_parent || !prog->body_off || !prog->block_off)

@@ -244,6 +244,9 @@ bfs_status dispatch(const bfs_plan *plan, DevImage *img, const void *const *dev_
     case BFS_KERNEL_MOE:
       return launch_moe(plan, img, dev_buffers, n_buffers, dev_trips, dev_trip_off, n_wg, stream,
                         dev_debug_log, debug_capacity, o);
+    case BFS_KERNEL_CHAIN:
+      return launch_chain(plan, img, dev_buffers, n_buffers, dev_trips, dev_trip_off, n_wg, stream,
+                          dev_debug_log, debug_capacity, o);
     default:
       return fail(BFS_E_UNSUPPORTED, "kernel family not built");
   }

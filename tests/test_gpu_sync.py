@@ -51,10 +51,14 @@ def _run_tile_machine(w, plan, n_out, cap=0):
 # ---------------------------------------------------------------------------
 # cfg1: two-engine chain on the interpreter
 # ---------------------------------------------------------------------------
+@pytest.mark.parametrize("kernel", ["chain", "interp"])
 @pytest.mark.parametrize("seed", [0, 1, 2])
-def test_chain_interp_parity(seed):
-    _say(f"[chain] seed={seed}")
-    w = chain_workload(seed)
+def test_chain_parity(seed, kernel):
+    """cfg1 (one workgroup, loop A of 16, inner trips U[1,8]) on the chain
+    kernel and on the generic interpreter: values within 1e-5 of the fp64
+    oracle, every threshold equal to the oracle's, both modes bit-identical."""
+    _say(f"[chain] seed={seed} kernel={kernel}")
+    w = chain_workload(seed, kernel=kernel)
     trips, off = w.trips.flat()
     res = core.run(w.prog, trips, off[0], 0, w.base, w.x, 256)
     outs = {}
@@ -142,10 +146,33 @@ def test_random_nests_interp_thresholds_per_instr():
     assert checked == expected and checked > 500
 
 
+@pytest.mark.parametrize("ring,n_wg,outer", [(2, 64, 9), (3, 5, 16), (8, 3, 12), (1, 2, 5)])
+def test_chain_kernel_rings_and_workgroups(ring, n_wg, outer):
+    """The chain kernel with other ring depths (one slot: no overlap at all)
+    and several independent workgroups: values and thresholds against the
+    oracle in both modes."""
+    w = chain_workload(seed=4, outer=outer, n_wg=n_wg, ring_slots=ring)
+    trips, off = w.trips.flat()
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[chain-rings] ring={ring} n_wg={n_wg} mode={name}")
+        plan = Plan(w.prog, mode)
+        out, logw = _run_tile_machine(w, plan, n_wg * 256, cap=512)
+        recs = {}
+        for g in range(n_wg):
+            res = core.run(w.prog, trips, off[g], g, w.base, w.x, n_wg * 256)
+            assert np.abs(out[g * 256:(g + 1) * 256] - res.out[g * 256:(g + 1) * 256]).max() <= 1e-5
+            recs[g] = res.recs
+        assert compare_log_with_oracle(w.prog, plan, log_records(plan, logw, n_wg, 512), recs, name) > 0
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+@pytest.mark.parametrize("kernel", ["chain", "interp"])
 @pytest.mark.parametrize("seed", [0, 1])
-def test_chain_interp_per_instr(seed):
-    _say(f"[chain-per-instr] seed={seed}")
-    w = chain_workload(seed)
+def test_chain_per_instr(seed, kernel):
+    _say(f"[chain-per-instr] seed={seed} kernel={kernel}")
+    w = chain_workload(seed, kernel=kernel)
     trips, off = w.trips.flat()
     res = core.run(w.prog, trips, off[0], 0, w.base, w.x, 256)
     plan = Plan(w.prog, MODE_BARRIER_FREE, ALLOC_PER_INSTR)
@@ -360,11 +387,11 @@ def test_stream_uninstrumented_watchdog_ends():
 # ---------------------------------------------------------------------------
 # failure handling: an unsatisfiable wait is reported, and the kernel ends
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("kernel", ["interp", "stream3"])
+@pytest.mark.parametrize("kernel", ["interp", "chain", "stream3"])
 def test_watchdog_reports_deadlock(kernel):
     _say(f"[watchdog] {kernel}")
-    if kernel == "interp":
-        w = chain_workload(0)
+    if kernel in ("interp", "chain"):
+        w = chain_workload(0, kernel=kernel)
         n_out = 256
     else:
         w = stream_workload(seed=0, n_wg=2, outer=3)

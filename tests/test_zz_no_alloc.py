@@ -47,7 +47,8 @@ def _tile_run(w, plan, n_out, noalloc):
 def test_noalloc_interpreter_two_calls_and_interleaved_plans(mode):
     """Chain (16 outer iterations), then a smaller chain (5), then the ring
     program, then the first chain again: each equals bfs_run bit for bit."""
-    cases = [("chain16", chain_workload(seed=0), 256), ("chain5", chain_workload(seed=1, outer=5), 256),
+    cases = [("chain16", chain_workload(seed=0, kernel="interp"), 256),
+             ("chain5", chain_workload(seed=1, outer=5, kernel="interp"), 256),
              ("ring", ring_workload(seed=2, outer=6, n_wg=3), 3 * 256)]
     plans = {name: Plan(w.prog, mode) for name, w, _ in cases}
     for name, w, n_out in cases + [cases[0]]:
@@ -91,7 +92,7 @@ def test_noalloc_reports_device_errors_then_recovers():
     """A wait that can never be met (raised threshold, short watchdog) is
     recorded in the fixed array's error words and reported by
     bfs_run_status; the next call runs cleanly."""
-    w = chain_workload(seed=0)
+    w = chain_workload(seed=0, kernel="interp")
     plan = Plan(w.prog)
     trips, toff = trip_tensors(w.trips)
     base, x = dev(w.base), dev(w.x)

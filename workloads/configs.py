@@ -87,7 +87,7 @@ def tile_bases(tt: TripTables, loop: int) -> np.ndarray:
 # ---------------------------------------------------------------------------
 # cfg1: 2-engine chain, one workgroup
 # ---------------------------------------------------------------------------
-def chain_program(ring_slots: int = 4, scale: float = 0.5) -> Program:
+def chain_program(ring_slots: int = 4, scale: float = 0.5, kernel: str = "chain") -> Program:
     """E0 loads 256-element fp32 tiles into a ring, E1 accumulates 0.5 * tile.
 
     A{ E0:ACQ; B{ E0:LOAD X[n] -> ring[(rhat_B-1) % 4]; E1:CONS acc += 0.5*ring }}
@@ -95,8 +95,10 @@ def chain_program(ring_slots: int = 4, scale: float = 0.5) -> Program:
 
     LOAD->CONS (k=0) is the read-after-write; CONS->LOAD (k=4) keeps a slot
     from being refilled before it is read within one trip of B; CONS->ACQ
-    (k=1) orders the next trip's loads after the previous trip's reads."""
-    b = ProgramBuilder("interp", n_engines=2)
+    (k=1) orders the next trip's loads after the previous trip's reads.
+    ``kernel``: "chain" (the dedicated two-wave kernel) or "interp" (the
+    generic interpreter)."""
+    b = ProgramBuilder(kernel, n_engines=2)
     with b.loop("A") as A:
         b.instr(0, OP_NOP, name="ACQ")
         with b.loop("B") as B:
@@ -124,8 +126,9 @@ class ChainWorkload:
     n_tiles: int
 
 
-def chain_workload(seed: int = 0, outer: int = 16, inner_max: int = 8, n_wg: int = 1) -> ChainWorkload:
-    prog = chain_program()
+def chain_workload(seed: int = 0, outer: int = 16, inner_max: int = 8, n_wg: int = 1,
+                   kernel: str = "chain", ring_slots: int = 4) -> ChainWorkload:
+    prog = chain_program(ring_slots=ring_slots, kernel=kernel)
     per = []
     for w in range(n_wg):
         rng = rng_for(CFG_CHAIN, seed, w)

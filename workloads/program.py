@@ -68,7 +68,7 @@ OP_ADAM_STORE = 82
 KIND_BLOCK = 0
 KIND_LOOP = 1
 
-KERNELS = ("interp", "stream3", "gemm", "attn", "moe", "rmsnorm", "adamw")
+KERNELS = ("interp", "stream3", "gemm", "attn", "moe", "rmsnorm", "adamw", "chain")
 
 
 def f32_bits(x: float) -> int:
