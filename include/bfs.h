@@ -77,8 +77,31 @@ typedef enum { BFS_MODE_BARRIER_FREE = 0, BFS_MODE_BARRIER = 1 } bfs_mode;
  * bfs_run of another family's plan that has one returns BFS_E_UNSUPPORTED. */
 #define BFS_PLAN_BARRIER_FALLBACK 1u
 
-/* Semaphore granularity (Section 5.4 per-instruction, Section 5.5 per-loop). */
-typedef enum { BFS_ALLOC_PER_LOOP = 0, BFS_ALLOC_PER_INSTR = 1 } bfs_alloc;
+/* Semaphore granularity (Section 5.4 per-instruction, Section 5.5 per-loop,
+ * Section 6.1 per-engine).
+ *
+ * BFS_ALLOC_PER_ENGINE: one counter per producer engine, incremented at the
+ * retirement of every instruction of that engine; in-order retirement makes
+ * its value the number of the engine's instructions retired so far.  A
+ * dependency's threshold is that counter's value right after the producer
+ * instance Eq. 1 requires: the number of the producer engine's instructions
+ * up to that instance in program order.  Section 6.1 gives it as a sum of
+ * loop-entry terms along the producer's path and caches the outer partial
+ * sums; here the sum is carried incrementally, in its cached form, by the
+ * consumer engine, which walks every loop: it keeps, per producer engine,
+ * the running count of that engine's instructions up to its own position
+ * (program-order counts of each block, added as it walks), and takes a
+ * snapshot of it at the producer's position.  A dependency at offset k on
+ * the producer's own loop S keeps the snapshots of the last k + 1
+ * iterations of S (indexed by r_S); a producer nested below S (C2, C3) keeps
+ * the latest one.  The threshold is the snapshot of iteration r_S - k, or
+ * the latest one, under the isGT(rhat_S, k) mask of Eq. 5 (no mask for a
+ * linearized offset, which reads r_S over all trips): one register read and
+ * the mask per issue.  Exact wherever per-loop counters are (the same Eq. 1
+ * requirement, certified on a coarser counter).  Barrier-free plans of the
+ * interpreter family only; other families return BFS_E_UNSUPPORTED at
+ * bfs_run. */
+typedef enum { BFS_ALLOC_PER_LOOP = 0, BFS_ALLOC_PER_INSTR = 1, BFS_ALLOC_PER_ENGINE = 2 } bfs_alloc;
 
 /* Datapath kernel families. */
 typedef enum {
@@ -166,6 +189,8 @@ typedef struct {
   int32_t prd_engine;
   int32_t cns_engine;
   int32_t forward;       /* producer precedes consumer in S's body */
+  int32_t snap_slots;    /* BFS_ALLOC_PER_ENGINE: snapshots the consumer keeps (k + 1 when the
+                            producer is directly in S, else 1; N and K are then 0); 0 otherwise */
 } bfs_formula;
 
 /* One dependency's barrier-mode wait (Section 3.4). */
@@ -179,8 +204,10 @@ typedef struct {
 /* Resource figures (Table alloc-resources / Table alloc-sema-combined columns). */
 typedef struct {
   int32_t n_counters;            /* semaphores used */
-  int32_t regs_per_engine;       /* loop registers r, rhat plus the wait register */
-  int32_t salu_ops_per_wait;     /* 5 per-loop, 3 per-instruction, 0 barrier */
+  int32_t regs_per_engine;       /* loop registers r, rhat plus the wait register; per-engine:
+                                    plus the running counts and snapshots (most of any engine) */
+  int32_t salu_ops_per_wait;     /* 5 per-loop, 3 per-instruction, 3 per-engine (index, mask,
+                                    read), 0 barrier */
   int32_t n_waits;               /* waits emitted */
   int32_t n_sync_points;         /* barrier mode: loop statements + iteration ends in the tree;
                                     barrier-free: loops whose iteration ends carry a fallback barrier */
@@ -254,7 +281,8 @@ bfs_status bfs_plan_stats(const bfs_plan *plan, bfs_stats *out);
  * registers r_P (entries of the producer's parent loop) and rhat_S (entries of
  * the shared loop in its current trip): Eq. 5 in barrier-free mode, the static
  * ordinal (or 0) in barrier mode, 0 for a barrier-fallback dependency.  This
- * is the value the device computes.
+ * is the value the device computes.  BFS_E_UNSUPPORTED for a per-engine plan
+ * (its thresholds are snapshots of the walk, not a function of r_P, rhat_S).
  */
 bfs_status bfs_eval_threshold(const bfs_plan *plan, int32_t dep, uint32_t r_P, uint32_t rhat_S,
                               uint32_t *out);

@@ -33,6 +33,13 @@
  *     The semaphore threshold is the counter value right after the latest
  *     retirement among the counted producer instances (0 if none).
  *
+ *  5. The same requirement expressed on the per-engine semaphore of
+ *     Section 6.1: one counter per engine, incremented at the retirement of
+ *     every instruction of that engine (in-order retirement makes its value
+ *     the number of the engine's instructions retired so far).  The threshold
+ *     is that counter's value right after the latest counted producer
+ *     instance (0 if none).
+ *
  *  4. The barrier-based scheme of Section 3.4: all engines synchronize before
  *     every non-top loop statement and at the end of every iteration of a
  *     non-top loop, resetting one counter per engine.  A consumer instance
@@ -73,6 +80,7 @@ typedef struct {
   int64_t cnt_before;     /* value of that counter just before it issued */
   int64_t region;         /* barrier region id */
   int64_t bord;           /* ordinal on its engine within the barrier region */
+  int64_t ecnt_after;     /* per-engine counter (every instruction of the engine) after its retirement */
 } orc_inst;
 
 /* One consumer instance of one dependency. */
@@ -85,6 +93,7 @@ typedef struct {
   int64_t r_P, r_S, rhat_S; /* entry counts at the consumer's issue */
   int32_t order_ok;       /* program order already satisfies the requirement */
   int32_t pad;
+  int64_t eng_thr;        /* per-engine counter value that certifies them */
 } orc_rec;
 
 typedef struct {
@@ -96,6 +105,7 @@ typedef struct {
   int64_t rhat[ORC_MAX_LOOPS];  /* entries in the current trip */
   int64_t *cnt;                 /* [n_loops * n_engines] per-loop counters */
   int64_t bcnt[ORC_MAX_ENGINES];
+  int64_t ecnt[ORC_MAX_ENGINES];  /* per-engine counters */
   int64_t region;
   int64_t n_inst;
   int64_t cap;
@@ -195,9 +205,11 @@ static void exec_instr(orc_state *st, int32_t instr, int32_t parent) {
   }
   *c += 1;
   st->bcnt[e] += 1;
+  st->ecnt[e] += 1;
   if (st->inst) {
     st->inst[idx].cnt_after = *c;
     st->inst[idx].bord = st->bcnt[e];
+    st->inst[idx].ecnt_after = st->ecnt[e];
   }
 }
 
@@ -233,6 +245,7 @@ static void run_walk(orc_state *st) {
   memset(st->r, 0, sizeof st->r);
   memset(st->rhat, 0, sizeof st->rhat);
   memset(st->bcnt, 0, sizeof st->bcnt);
+  memset(st->ecnt, 0, sizeof st->ecnt);
   st->region = 0;
   st->n_inst = 0;
   st->r[0] = 1;                          /* the program is a loop entered once */
@@ -323,7 +336,7 @@ int orc_run(const orc_prog *P, const int32_t *trips, const int64_t *trip_off, in
       int64_t t[ORC_MAX_LOOPS];
       for (int32_t j = 0; j < depth; ++j) t[j] = rhat_snap[xi * L + path[j]];
       t[depth - 1] -= k;
-      int64_t count = 0, sem = 0, bthr = 0;
+      int64_t count = 0, sem = 0, bthr = 0, eng = 0;
       int64_t latest = -1;
       if (t[depth - 1] > 0) {
         for (int64_t yi = 0; yi < st.n_inst; ++yi) {
@@ -337,6 +350,7 @@ int orc_run(const orc_prog *P, const int32_t *trips, const int64_t *trip_off, in
           if (!le) continue;
           count += 1;
           if (inst[yi].cnt_after > sem) { sem = inst[yi].cnt_after; latest = yi; }
+          if (inst[yi].ecnt_after > eng) eng = inst[yi].ecnt_after;
         }
       }
       if (latest >= 0 && inst[latest].region == inst[xi].region) bthr = inst[latest].bord;
@@ -346,6 +360,7 @@ int orc_run(const orc_prog *P, const int32_t *trips, const int64_t *trip_off, in
         R->instance = instance;
         R->count_thr = count;
         R->sem_thr = sem;
+        R->eng_thr = eng;
         R->barrier_thr = bthr;
         R->r_P = r_snap[xi * L + parent[p]];
         R->r_S = r_snap[xi * L + S];

@@ -38,11 +38,12 @@ class _Prog(C.Structure):
 
 
 INST_DTYPE = np.dtype([("instr", np.int32), ("engine", np.int32), ("cnt_after", np.int64),
-                       ("cnt_before", np.int64), ("region", np.int64), ("bord", np.int64)])
+                       ("cnt_before", np.int64), ("region", np.int64), ("bord", np.int64),
+                       ("ecnt_after", np.int64)])
 REC_DTYPE = np.dtype([("dep", np.int32), ("instance", np.int32), ("count_thr", np.int64),
                       ("sem_thr", np.int64), ("barrier_thr", np.int64), ("r_P", np.int64),
                       ("r_S", np.int64), ("rhat_S", np.int64), ("order_ok", np.int32),
-                      ("pad", np.int32)])
+                      ("pad", np.int32), ("eng_thr", np.int64)])
 
 _lib = None
 
@@ -189,4 +190,5 @@ def linearized_records(prog, res, d):
         counted = [y for y in prod if rS[y] <= target] if target > 0 else []
         recs[j]["count_thr"] = len(counted)
         recs[j]["sem_thr"] = inst["cnt_after"][max(counted)] if counted else 0
+        recs[j]["eng_thr"] = inst["ecnt_after"][max(counted)] if counted else 0
     return recs

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libbfs.so")
 
 OK, E_INVALID, E_ORDER, E_NOT_ALLOCATABLE, E_RESOURCE, E_DEVICE, E_DEADLOCK, E_UNSUPPORTED = range(8)
 MODE_BARRIER_FREE, MODE_BARRIER = 0, 1
-ALLOC_PER_LOOP, ALLOC_PER_INSTR = 0, 1
+ALLOC_PER_LOOP, ALLOC_PER_INSTR, ALLOC_PER_ENGINE = 0, 1, 2
 PLAN_BARRIER_FALLBACK = 1
 KASE_FALLBACK = 4
 KERNELS = {"interp": 0, "stream3": 1, "gemm": 2, "attn": 3, "moe": 4, "rmsnorm": 5, "adamw": 6, "chain": 7}
@@ -48,7 +48,8 @@ class _Program(C.Structure):
 
 class Formula(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("dep", "kase", "loop_S", "loop_P", "k", "expr_sub", "N", "K",
-                                          "needs_mask", "counter", "prd_engine", "cns_engine", "forward")]
+                                          "needs_mask", "counter", "prd_engine", "cns_engine", "forward",
+                                          "snap_slots")]
 
 
 class StaticWait(C.Structure):

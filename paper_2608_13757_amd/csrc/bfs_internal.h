@@ -17,7 +17,10 @@ constexpr int kMaxWaves = 16;     // waves of one workgroup in the interpreter
 constexpr int kMaxSlots = 64;     // counter slots
 
 // Interpreter code words (one engine's projection of the statement tree).
-enum : int32_t { CODE_LOOP = 1, CODE_END = 2, CODE_INSTR = 3, CODE_HALT = 4 };
+// Per-engine allocation adds TRACK (a0 producer engine, a1 instructions of
+// that engine passed in program order) and SNAP (a0 dependency: record the
+// producer engine's running count after the producer's position).
+enum : int32_t { CODE_LOOP = 1, CODE_END = 2, CODE_INSTR = 3, CODE_HALT = 4, CODE_TRACK = 5, CODE_SNAP = 6 };
 
 // One wait as the device evaluates it.  Barrier-free: Eq. 5 on the consumer
 // engine's registers; barrier mode: a static ordinal on the producer engine's
@@ -35,6 +38,10 @@ struct DevWait {
   int32_t needs_mask;
   int32_t ordinal;      // barrier mode
   int32_t active;       // 0: no wait is needed (barrier mode, cross-region)
+  int32_t snap_slots;   // per-engine: snapshots kept (0: not per-engine)
+  int32_t snap_off;     // per-engine: first snapshot word in the consumer wave's area
+  int32_t linear;       // offset read over all trips of S (no mask)
+  int32_t pad;
 };
 
 // A wait packed into four words for kernels that carry their waits as
@@ -109,6 +116,10 @@ struct bfs_plan {
   std::vector<int32_t> instr_wait_off, instr_wait_list;
   // interpreter code (int32 x4 words), per engine
   std::vector<int32_t> code, code_off;
+  // per-engine allocation: first snapshot word of each dependency in its
+  // consumer engine's area, and the largest area (words)
+  std::vector<int32_t> snap_off;
+  int32_t snap_words = 0;
 
   std::mutex dev_mu;
   std::vector<bfs::DevImage> images;     // one per device used

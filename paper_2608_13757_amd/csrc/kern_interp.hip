@@ -45,6 +45,7 @@ struct InterpParams {
   int32_t ring_off[4];          // float offsets in the ring area
   int32_t acc_off;
   int32_t lds_state_off, lds_exec_off, lds_data_off;   // byte offsets in dynamic LDS
+  int32_t lds_snap_off, snap_words;   // per-engine allocation: running counts and snapshots per wave
 };
 
 __device__ __forceinline__ int slot_of(const int32_t *a, const uint32_t *r, const uint32_t *rhat) {
@@ -64,11 +65,16 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
   uint32_t *r = st, *rhat = st + bfs::kMaxLoops, *trip = st + 2 * bfs::kMaxLoops;
   uint32_t *execn = reinterpret_cast<uint32_t *>(lds + P.lds_exec_off) + wave * kMaxInstrsInterp;
   float *data = reinterpret_cast<float *>(lds + P.lds_data_off);
+  // per-engine allocation: words 0 .. kMaxEngines - 1 hold the running count
+  // of each producer engine's instructions up to this wave's position, then
+  // the dependencies' snapshots
+  uint32_t *snap = reinterpret_cast<uint32_t *>(lds + P.lds_snap_off) + wave * P.snap_words;
 
   // Zero counters, state and accumulators.
   for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
   for (int i = lane; i < 3 * bfs::kMaxLoops; i += 64) st[i] = 0;
   for (int i = lane; i < P.n_instrs; i += 64) execn[i] = 0;
+  for (int i = lane; i < P.snap_words; i += 64) snap[i] = 0;
   for (int i = threadIdx.x; i < (P.acc_off + 4 * P.tile); i += blockDim.x) data[i] = 0.f;
   __syncthreads();
 
@@ -138,6 +144,24 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
       __builtin_amdgcn_s_waitcnt(0);
       continue;
     }
+    if (kind == bfs::CODE_TRACK) {
+      if (lane == 0) snap[a0] += (uint32_t)a1;
+      __builtin_amdgcn_s_waitcnt(0);
+      pc += 1;
+      continue;
+    }
+    if (kind == bfs::CODE_SNAP) {
+      // the producer engine's running count right after the producer's
+      // position, kept for the iteration of S it belongs to
+      const bfs::DevWait W = P.waits[a0];
+      const uint32_t slots = (uint32_t)W.snap_slots;
+      const uint32_t idx = slots > 1 ? uniform(r[W.loop_S]) % slots : 0u;
+      const uint32_t v = uniform(snap[W.prd_engine]);
+      if (lane == 0) snap[W.snap_off + idx] = v;
+      __builtin_amdgcn_s_waitcnt(0);
+      pc += 1;
+      continue;
+    }
     // CODE_INSTR
     const int ins = a0;
     const uint32_t inst = uniform(execn[ins]);
@@ -146,6 +170,14 @@ __global__ void __launch_bounds__(512) interp_kernel(InterpParams P) {
       uint32_t thr;
       if (P.mode == BFS_MODE_BARRIER) {
         thr = W.active ? (uint32_t)W.ordinal : 0u;
+      } else if (W.snap_slots > 0) {
+        // per-engine: the snapshot of iteration r_S - k (or the latest one),
+        // under the mask of Eq. 5
+        const uint32_t slots = (uint32_t)W.snap_slots, k = (uint32_t)W.k;
+        const uint32_t rS = uniform(r[W.loop_S]), hS = uniform(rhat[W.loop_S]);
+        const bool owed = W.linear ? rS > k : (!W.needs_mask || hS > k);
+        const uint32_t idx = slots > 1 ? (rS - k) % slots : 0u;
+        thr = owed ? uniform(snap[W.snap_off + idx]) : 0u;
       } else {
         thr = eq5(uniform(r[W.loop_P]), uniform(rhat[W.loop_S]), W.k, W.expr_sub, W.N, W.K, W.needs_mask);
       }
@@ -268,7 +300,9 @@ bfs_status launch_interp(const bfs_plan *p, DevImage *img, const void *const *bu
   P.lds_state_off = counters_bytes;
   P.lds_exec_off = P.lds_state_off + p->n_engines * 3 * kMaxLoops * 4;
   P.lds_data_off = P.lds_exec_off + p->n_engines * kMaxInstrsInterp * 4;
-  const size_t lds_bytes = (size_t)P.lds_data_off + (size_t)(off + 4 * P.tile) * 4;
+  P.snap_words = p->mode == BFS_MODE_BARRIER_FREE && p->alloc == BFS_ALLOC_PER_ENGINE ? p->snap_words : 0;
+  P.lds_snap_off = P.lds_data_off + (off + 4 * P.tile) * 4;
+  const size_t lds_bytes = (size_t)P.lds_snap_off + (size_t)p->n_engines * P.snap_words * 4;
   if (lds_bytes > 160 * 1024) return fail(BFS_E_RESOURCE, "interpreter: LDS footprint over 160 KiB");
   hipError_t err = hipFuncSetAttribute((const void *)interp_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)lds_bytes);

@@ -158,6 +158,7 @@ bfs_status plan_build(bfs_plan &p) {
   p.static_waits.assign(D, bfs_static_wait{});
   std::map<std::pair<int32_t, int32_t>, int32_t> slot_of_loop_engine;  // per-loop allocation
   std::map<int32_t, int32_t> slot_of_instr;                            // per-instruction allocation
+  std::map<int32_t, int32_t> slot_of_engine;                           // per-engine allocation
   p.fallback_loops = 0;
   for (int32_t d = 0; d < D; ++d) {
     const int32_t a = p.deps[3 * d], c = p.deps[3 * d + 1], k = p.deps[3 * d + 2];
@@ -207,6 +208,15 @@ bfs_status plan_build(bfs_plan &p) {
       f.K = 0;
       f.counter = -1;
       if (S != 0) p.fallback_loops |= 1u << S;
+    } else if (p.alloc == BFS_ALLOC_PER_ENGINE) {
+      // one counter per producer engine; the consumer keeps snapshots of the
+      // producer engine's running count at the producer's position
+      f.N = 0;
+      f.K = 0;
+      f.snap_slots = P == S ? k + 1 : 1;
+      auto it = slot_of_engine.find(f.prd_engine);
+      if (it == slot_of_engine.end()) it = slot_of_engine.emplace(f.prd_engine, (int32_t)slot_of_engine.size()).first;
+      f.counter = it->second;
     } else if (p.alloc == BFS_ALLOC_PER_INSTR) {
       f.N = 1;
       f.K = 1;
@@ -262,6 +272,12 @@ bfs_status plan_build(bfs_plan &p) {
   } else if (p.alloc == BFS_ALLOC_PER_INSTR) {
     for (auto &kv : slot_of_instr) p.instr_update[kv.first] = kv.second;
     p.n_counters = (int32_t)slot_of_instr.size();
+  } else if (p.alloc == BFS_ALLOC_PER_ENGINE) {
+    for (int32_t i = 0; i < I; ++i) {
+      auto it = slot_of_engine.find(p.instr_engine[i]);
+      if (it != slot_of_engine.end()) p.instr_update[i] = it->second;
+    }
+    p.n_counters = (int32_t)slot_of_engine.size();
   } else {
     for (int32_t i = 0; i < I; ++i) {
       auto it = slot_of_loop_engine.find({p.instr_parent[i], p.instr_engine[i]});
@@ -283,6 +299,25 @@ bfs_status plan_build(bfs_plan &p) {
       }
   }
   p.instr_wait_off[I] = (int32_t)p.instr_wait_list.size();
+
+  // Per-engine allocation: each consumer engine's snapshot area holds one
+  // running count per engine (words 0 .. kMaxEngines - 1), then the
+  // snapshots of its dependencies in dependency order.
+  p.snap_off.assign(D, 0);
+  p.snap_words = 0;
+  const bool per_engine = p.mode == BFS_MODE_BARRIER_FREE && p.alloc == BFS_ALLOC_PER_ENGINE;
+  std::vector<std::vector<char>> tracks(E, std::vector<char>(kMaxEngines, 0));   // consumer -> producer engines
+  if (per_engine) {
+    std::vector<int32_t> used(E, kMaxEngines);
+    for (int32_t d = 0; d < D; ++d) {
+      const bfs_formula &f = p.formulas[d];
+      if (f.kase == 4) continue;
+      p.snap_off[d] = used[f.cns_engine];
+      used[f.cns_engine] += f.snap_slots;
+      tracks[f.cns_engine][f.prd_engine] = 1;
+    }
+    for (int32_t e = 0; e < E; ++e) p.snap_words = std::max(p.snap_words, used[e]);
+  }
 
   // Interpreter code: each engine's projection of the statement tree.
   p.code.clear();
@@ -311,8 +346,26 @@ bfs_status plan_build(bfs_plan &p) {
       int32_t kind = p.body_kind[f.it], id = p.body_id[f.it];
       ++f.it;
       if (kind == 0) {
-        for (int32_t j = p.block_off[id]; j < p.block_off[id + 1]; ++j)
-          if (p.instr_engine[p.block_instrs[j]] == e) emit(CODE_INSTR, p.block_instrs[j], 0);
+        // Per-engine: the counts of the tracked producer engines' instructions
+        // are added as the block is passed (once per execution of the block),
+        // flushed before every snapshot and at the block's end.
+        int32_t pend[kMaxEngines] = {0};
+        auto flush = [&](int32_t pe) {
+          if (pend[pe] > 0) emit(CODE_TRACK, pe, pend[pe]);
+          pend[pe] = 0;
+        };
+        for (int32_t j = p.block_off[id]; j < p.block_off[id + 1]; ++j) {
+          const int32_t ins = p.block_instrs[j], ie = p.instr_engine[ins];
+          if (ie == e) emit(CODE_INSTR, ins, 0);
+          if (!per_engine || !tracks[e][ie]) continue;
+          pend[ie] += 1;
+          for (int32_t d = 0; d < D; ++d)
+            if (p.deps[3 * d] == ins && p.formulas[d].kase != 4 && p.formulas[d].cns_engine == e) {
+              flush(ie);
+              emit(CODE_SNAP, d, 0);
+            }
+        }
+        for (int32_t pe = 0; pe < E; ++pe) flush(pe);
       } else {
         int32_t pc = emit(CODE_LOOP, id, -1);
         fr.push_back(Frame{id, p.body_off[id], pc});
@@ -341,8 +394,20 @@ bfs_status plan_build(bfs_plan &p) {
     }
     int32_t regs = 1;   // the wait register
     for (int32_t l = 0; l < L; ++l) regs += usedP[l] + usedS[l];
+    if (per_engine) {
+      // running counts of the tracked engines and the snapshots, most of any engine
+      int32_t extra = 0;
+      for (int32_t e = 0; e < E; ++e) {
+        int32_t x = 0;
+        for (int32_t pe = 0; pe < kMaxEngines; ++pe) x += tracks[e][pe];
+        for (int32_t d = 0; d < D; ++d)
+          if (p.formulas[d].kase != 4 && p.formulas[d].cns_engine == e) x += p.formulas[d].snap_slots;
+        extra = std::max(extra, x);
+      }
+      regs += extra;
+    }
     s.regs_per_engine = regs;
-    s.salu_ops_per_wait = p.alloc == BFS_ALLOC_PER_INSTR ? 3 : 5;
+    s.salu_ops_per_wait = p.alloc == BFS_ALLOC_PER_INSTR ? 3 : p.alloc == BFS_ALLOC_PER_ENGINE ? 3 : 5;
     s.n_sync_points = __builtin_popcount(p.fallback_loops);
     s.n_waits = 0;
     for (auto &f : p.formulas) s.n_waits += f.kase != 4;
@@ -369,7 +434,8 @@ bfs_status bfs_plan_create(const bfs_program *prog, bfs_mode mode, bfs_alloc all
   if (!prog || !out) return fail(BFS_E_INVALID, "null argument");
   if (flags & ~BFS_PLAN_BARRIER_FALLBACK) return fail(BFS_E_INVALID, "unknown plan flags");
   if (mode != BFS_MODE_BARRIER_FREE && mode != BFS_MODE_BARRIER) return fail(BFS_E_INVALID, "bad mode");
-  if (alloc != BFS_ALLOC_PER_LOOP && alloc != BFS_ALLOC_PER_INSTR) return fail(BFS_E_INVALID, "bad alloc");
+  if (alloc != BFS_ALLOC_PER_LOOP && alloc != BFS_ALLOC_PER_INSTR && alloc != BFS_ALLOC_PER_ENGINE)
+    return fail(BFS_E_INVALID, "bad alloc");
   if (prog->kernel < BFS_KERNEL_INTERP || prog->kernel > BFS_KERNEL_CHAIN) return fail(BFS_E_INVALID, "bad kernel");
   if (prog->n_loops < 1 || prog->n_blocks < 0 || prog->n_instrs < 0 || prog->n_deps < 0)
     return fail(BFS_E_INVALID, "negative sizes");
@@ -454,6 +520,9 @@ bfs_status bfs_eval_threshold(const bfs_plan *plan, int32_t dep, uint32_t r_P, u
     *out = w.same_region ? (uint32_t)w.ordinal : 0u;
   } else if (plan->formulas[dep].kase == 4) {
     *out = 0u;
+  } else if (plan->alloc == BFS_ALLOC_PER_ENGINE) {
+    return fail(BFS_E_UNSUPPORTED, "per-engine thresholds are snapshots taken during the walk, not a function "
+                                   "of r_P and rhat_S");
   } else {
     *out = eval_formula(plan->formulas[dep], r_P, rhat_S);
   }

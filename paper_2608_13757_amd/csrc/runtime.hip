@@ -44,6 +44,9 @@ std::vector<DevWait> device_waits(const bfs_plan *p) {
       x.K = f.K;
       x.needs_mask = f.needs_mask;
       x.active = f.kase != 4;
+      x.snap_slots = f.snap_slots;
+      x.snap_off = p->snap_off.empty() ? 0 : p->snap_off[d];
+      x.linear = f.kase == 6 ? 1 : 0;
     }
     w[d] = x;
   }
@@ -215,6 +218,8 @@ bfs_status run_prologue(const bfs_plan *plan, int32_t n_buffers, const void *con
   }
   if (plan->mode == BFS_MODE_BARRIER_FREE && plan->stats.n_fallback > 0 && plan->kernel != BFS_KERNEL_INTERP)
     return fail(BFS_E_UNSUPPORTED, "barrier-fallback dependencies run on the interpreter family only");
+  if (plan->mode == BFS_MODE_BARRIER_FREE && plan->alloc == BFS_ALLOC_PER_ENGINE && plan->kernel != BFS_KERNEL_INTERP)
+    return fail(BFS_E_UNSUPPORTED, "per-engine allocation runs on the interpreter family only");
   if (n_wg == 0) *skip = true;
   return BFS_OK;
 }

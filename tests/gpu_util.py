@@ -46,8 +46,10 @@ def compare_log_with_oracle(prog, plan, logs, recs_by_wg, mode, no_wait=()):
     and the observed counter was never below it.  mode "per_instr": a
     barrier-free plan with one counter per instruction, whose thresholds are
     the Eq. 1 counts.  Dependencies in ``no_wait`` (ordered by barriers)
-    must log nothing."""
-    key = {"barrier_free": "sem_thr", "barrier": "barrier_thr", "per_instr": "count_thr"}[mode]
+    must log nothing.  mode "per_engine": one counter per producer engine,
+    thresholds the per-engine counter values of the oracle."""
+    key = {"barrier_free": "sem_thr", "barrier": "barrier_thr", "per_instr": "count_thr",
+           "per_engine": "eng_thr"}[mode]
     n = 0
     for wg, recs in recs_by_wg.items():
         for d in range(len(prog.deps)):

@@ -12,8 +12,8 @@ import pytest
 torch = pytest.importorskip("torch")
 
 from oracle import core  # noqa: E402
-from paper_2608_13757_amd import (ALLOC_PER_INSTR, MODE_BARRIER, MODE_BARRIER_FREE, BfsError, Plan,  # noqa: E402
-                                  bfs)
+from paper_2608_13757_amd import (ALLOC_PER_ENGINE, ALLOC_PER_INSTR, MODE_BARRIER, MODE_BARRIER_FREE,  # noqa: E402
+                                  BfsError, Plan, bfs)
 from paper_2608_13757_amd.bfs import RUN_LOG_BATCHED, RUN_PER_INSTANCE  # noqa: E402
 from tests.gpu_util import (compare_batched_log_with_oracle, compare_log_with_oracle, dev, log_records,  # noqa: E402
                             trip_tensors)
@@ -144,6 +144,80 @@ def test_random_nests_interp_thresholds_per_instr():
         logs = log_records(plan, log.cpu().numpy().view(np.uint32), 1, cap)
         checked += compare_log_with_oracle(prog, plan, logs, {0: res.recs}, "per_instr")
     assert checked == expected and checked > 500
+
+
+# ---------------------------------------------------------------------------
+# per-engine allocation (Section 6.1): one counter per producer engine, the
+# thresholds equal to the oracle's per-engine counter values
+# ---------------------------------------------------------------------------
+def test_random_nests_interp_thresholds_per_engine():
+    checked = expected = 0
+    for seed in range(150):
+        prog, tt = random_nest(seed, max_trip=4 if seed % 2 else 3)
+        prog.deps = _allocatable(prog)
+        if not prog.deps:
+            continue
+        trips, off = tt.flat()
+        res = core.run(prog, trips, off[0], 0)
+        plan = Plan(prog, MODE_BARRIER_FREE, ALLOC_PER_ENGINE)
+        expected += len(res.recs)
+        t_trips, t_off = trip_tensors(tt)
+        base = torch.zeros(1, dtype=torch.int64, device="cuda")
+        x = torch.zeros(64, dtype=torch.float32, device="cuda")
+        out = torch.zeros(64, dtype=torch.float32, device="cuda")
+        cap = 256
+        log = torch.zeros(plan.debug_log_words(1, cap), dtype=torch.int32, device="cuda")
+        plan.run([base, x, out], t_trips, t_off, 1, debug_log=log, debug_capacity=cap)
+        plan.status()
+        logs = log_records(plan, log.cpu().numpy().view(np.uint32), 1, cap)
+        checked += compare_log_with_oracle(prog, plan, logs, {0: res.recs}, "per_engine")
+    assert checked == expected and checked > 500
+
+
+@pytest.mark.parametrize("case", ["chain", "stream_inplace", "stream_two_rings", "ring_linear"])
+def test_per_engine_workload_programs_interp(case):
+    """The chain, both stream layouts (with the inner reuse dependencies) and
+    the ring program with a linearized dependency, on the interpreter with
+    per-engine counters: every threshold equals the oracle's per-engine
+    counter value, and the values equal those of per-loop counters."""
+    from workloads import ring_workload
+    if case == "chain":
+        w = chain_workload(seed=1, kernel="interp", n_wg=2)
+        n_out = 2 * 256
+    elif case == "ring_linear":
+        w = ring_workload(seed=1, outer=8, n_wg=3, linear=True)
+        n_out = 3 * 256
+    else:
+        w = stream_workload(seed=2, n_wg=4, outer=6, inner_war=True,
+                            layout="inplace" if case == "stream_inplace" else "two_rings",
+                            n_gen=32 if case == "stream_inplace" else 8)
+        w.prog.kernel = "interp"
+        n_out = w.n_tiles * 64
+    trips, off = w.trips.flat()
+    recs = {}
+    for g in range(w.trips.n_wg):
+        res = core.run(w.prog, trips, off[g], g)
+        rr = res.recs.copy()
+        for d, lin in enumerate(w.prog.dep_linear or []):
+            if lin:
+                rr[rr["dep"] == d] = core.linearized_records(w.prog, res, d)
+        recs[g] = rr
+    _say(f"[per-engine] {case}")
+    plan = Plan(w.prog, MODE_BARRIER_FREE, ALLOC_PER_ENGINE)
+    out, logw = _run_tile_machine(w, plan, n_out, cap=2048)
+    logs = log_records(plan, logw, w.trips.n_wg, 2048)
+    assert compare_log_with_oracle(w.prog, plan, logs, recs, "per_engine") > 0
+    ref, _ = _run_tile_machine(w, Plan(w.prog), n_out)
+    assert np.array_equal(out.view(np.uint32), ref.view(np.uint32))
+
+
+def test_per_engine_refused_by_fused_families():
+    w = stream_workload(seed=0, n_wg=2, outer=3)
+    plan = Plan(w.prog, MODE_BARRIER_FREE, ALLOC_PER_ENGINE)
+    t = torch.zeros(4, dtype=torch.int32, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t, t, t], t, t, 1)
+    assert e.value.status == bfs.E_UNSUPPORTED
 
 
 @pytest.mark.parametrize("ring,n_wg,outer", [(2, 64, 9), (3, 5, 16), (8, 3, 12), (1, 2, 5)])

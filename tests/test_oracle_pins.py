@@ -229,6 +229,86 @@ def test_stream_inplace_trip_bounds():
     assert hazard.check(pw, core.run(pw, trips, off[0], 0), "barrier_free") == []
 
 
+def test_per_engine_counter_closed_forms():
+    """The per-engine counter column (Section 6.1: one counter per engine,
+    incremented by every instruction of the engine) against closed forms
+    computed from the trip tables alone.
+
+    Chain, engine 0 = {ACQ in A, LOAD in B}: right after the LOAD of B
+    iteration r_B it has retired r_A ACQs and r_B LOADs, so LOAD -> CONS
+    owes r_A + r_B.  Engine 1 = {CONS in B, STORE after A}: CONS -> LOAD
+    (k = 4) owes [rhat_B > 4] (r_B - 4) and CONS -> ACQ (k = 1) owes
+    [rhat_A > 1] r_B.  In-place stream, engine 2 = {STORE in I, MARK_O in O}:
+    MARK_O -> ACQ_O (k = 2) at O iteration o owes the STOREs of O iterations
+    1 .. o - 2 plus o - 2 markers; LOAD -> ADD owes r_O + r_I (one ACQ_O per
+    O iteration, one LOAD per I iteration)."""
+    w = chain_workload(seed=2)
+    trips, off = w.trips.flat()
+    res = core.run(w.prog, trips, off[0], 0)
+    A, B = w.prog.loop_id("A"), w.prog.loop_id("B")
+    names = {i: ins.name for i, ins in enumerate(w.prog.instrs)}
+    cons_at = {}
+    for d, (pp, cc, k) in enumerate(w.prog.deps):
+        idx = np.nonzero(res.inst["instr"] == cc)[0]
+        cons_at[(names[pp], names[cc])] = (d, idx)
+    d, idx = cons_at[("LOAD", "CONS")]
+    got = res.recs[res.recs["dep"] == d]["eng_thr"]
+    assert np.array_equal(got, res.r_snap[idx, A] + res.r_snap[idx, B])
+    d, idx = cons_at[("CONS", "LOAD")]
+    got = res.recs[res.recs["dep"] == d]["eng_thr"]
+    want = np.where(res.rhat_snap[idx, B] > 4, res.r_snap[idx, B] - 4, 0)
+    assert np.array_equal(got, want) and want.max() > 0
+    d, idx = cons_at[("CONS", "ACQ")]
+    got = res.recs[res.recs["dep"] == d]["eng_thr"]
+    want = np.where(res.rhat_snap[idx, A] > 1, res.r_snap[idx, B], 0)
+    assert np.array_equal(got, want) and want.max() > 0
+
+    s = stream_workload(seed=3, n_wg=2, outer=9, with_data=False)
+    trips, off = s.trips.flat()
+    res = core.run(s.prog, trips, off[1], 1)
+    per = s.trips.per_wg[1]
+    m_trips, i_trips = per[2], per[3]
+    stores_upto = np.concatenate([[0], np.cumsum([int(i_trips[int(m_trips[:o].sum()):int(m_trips[:o + 1].sum())].sum())
+                                                  for o in range(len(m_trips))])])
+    names = {i: ins.name for i, ins in enumerate(s.prog.instrs)}
+    O, I = s.prog.loop_id("O"), s.prog.loop_id("I")
+    for d, (pp, cc, k) in enumerate(s.prog.deps):
+        recs = res.recs[res.recs["dep"] == d]
+        idx = np.nonzero(res.inst["instr"] == cc)[0]
+        if (names[pp], names[cc]) == ("MARK_O", "ACQ_O"):
+            o = res.r_snap[idx, O]
+            want = np.where(o > 2, stores_upto[np.maximum(o - 2, 0)] + (o - 2), 0)
+        elif (names[pp], names[cc]) == ("LOAD", "ADD"):
+            want = res.r_snap[idx, O] + res.r_snap[idx, I]
+        else:                                            # ADD -> STORE: engine 1 is the ADD alone
+            want = res.r_snap[idx, I]
+        assert np.array_equal(recs["eng_thr"], want), names[pp] + "->" + names[cc]
+
+
+def test_per_engine_equals_per_loop_for_single_loop_engines():
+    """Where every instruction of the producer's engine sits directly in the
+    producer's loop, the per-engine and per-loop counters are the same
+    counter (random nests)."""
+    checked = 0
+    for seed in range(120):
+        prog, tt = random_nest(seed)
+        trips, off = tt.flat()
+        res = core.run(prog, trips, off[0], 0)
+        parent = {}
+        for l, items in enumerate(prog.body):
+            for kind, bid in items:
+                if kind == 0:
+                    for i in prog.blocks[bid]:
+                        parent[i] = l
+        for d, (pp, cc, k) in enumerate(prog.deps):
+            e = prog.instrs[pp].engine
+            if all(parent[i] == parent[pp] for i, ins in enumerate(prog.instrs) if ins.engine == e):
+                r = res.recs[res.recs["dep"] == d]
+                assert np.array_equal(r["eng_thr"], r["sem_thr"]), (seed, d)
+                checked += len(r)
+    assert checked > 200
+
+
 def test_hazard_catches_dropped_dependencies():
     w = chain_workload(seed=0)
     trips, off = w.trips.flat()

@@ -12,8 +12,8 @@ import numpy as np
 import pytest
 
 from oracle import core
-from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER, MODE_BARRIER_FREE,
-                                  BfsError, Plan, bfs)
+from paper_2608_13757_amd import (ALLOC_PER_ENGINE, ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER,
+                                  MODE_BARRIER_FREE, BfsError, Plan, bfs)
 from tests import fixtures
 from workloads import (OP_NOP, ProgramBuilder, TripTables, attn_program, attn_worklist, chain_workload,
                        draw_trips, gemm_program, gemm_trips, random_nest, stream_workload)
@@ -331,6 +331,31 @@ def test_resource_stats():
     # one counter per (loop, engine) pair that some dependency reads
     pairs = {(f["loop_P"], f["prd_engine"]) for f in pl.formulas()}
     assert st_l["n_counters"] == len(pairs)
+
+
+def test_per_engine_plans():
+    """Per-engine allocation (Section 6.1): one counter per producer engine
+    that every instruction of the engine increments; each dependency keeps
+    k + 1 snapshots when its producer sits directly in S, else one; host
+    evaluation is refused (the thresholds are snapshots of the walk)."""
+    s = stream_workload(seed=0, n_wg=1, outer=2, with_data=False, layout="two_rings", n_gen=8, inner_war=True)
+    pe, pl = Plan(s.prog, alloc=ALLOC_PER_ENGINE), Plan(s.prog)
+    fe, fl = pe.formulas(), pl.formulas()
+    prd_engines = {f["prd_engine"] for f in fe}
+    assert pe.stats()["n_counters"] == len(prd_engines) < pl.stats()["n_counters"]
+    for f, g in zip(fe, fl):
+        assert (f["kase"], f["loop_S"], f["loop_P"], f["k"]) == (g["kase"], g["loop_S"], g["loop_P"], g["k"])
+        assert f["snap_slots"] == (f["k"] + 1 if f["loop_P"] == f["loop_S"] else 1)
+        assert g["snap_slots"] == 0
+    slot = {f["prd_engine"]: f["counter"] for f in fe}
+    assert len(set(slot.values())) == len(slot)
+    assert pe.stats()["salu_ops_per_wait"] == 3
+    assert pe.stats()["regs_per_engine"] > pl.stats()["regs_per_engine"]
+    with pytest.raises(BfsError) as e:
+        pe.eval_threshold(0, 1, 1)
+    assert e.value.status == bfs.E_UNSUPPORTED
+    # barrier mode ignores the allocation
+    assert Plan(s.prog, MODE_BARRIER, ALLOC_PER_ENGINE).static_waits() == Plan(s.prog, MODE_BARRIER).static_waits()
 
 
 def test_abi_exports_every_header_symbol():
