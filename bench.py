@@ -148,6 +148,9 @@ def parse():
                          "drains the ring at every M-tile (MMA->ACQL, k = 1)")
     ap.add_argument("--k-unroll", type=int, default=0, choices=[0, 1, 2, 4, 8],
                     help="GEMM: K steps per copy of the loop bodies (static-trip unrolling)")
+    ap.add_argument("--k-unrolled", action="store_true",
+                    help="GEMM: the K-unrolled program (K loop removed, 128 steps in straight line, every K-phase "
+                         "wait a static immediate), the paper's K-unrolled tiled matmul")
     ap.add_argument("--alloc", default="per_loop", choices=["per_loop", "per_instr"],
                     help="counter allocation of the barrier-free plans (Eq. 5 per loop and engine, "
                          "or Eq. 3 one counter per producer instruction)")
@@ -302,7 +305,7 @@ def bench_gemm(a):
     import numpy as np
     import torch
     from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
-    from workloads import GEMM_BK, GEMM_RING, gemm_program, gemm_trips
+    from workloads import GEMM_BK, GEMM_RING, gemm_program, gemm_program_k_unrolled, gemm_trips, gemm_trips_k_unrolled
     from workloads.tensors import gemm_inputs
 
     m = n = k = 4096
@@ -320,13 +323,14 @@ def bench_gemm(a):
     A, Bt = dev(gi.a), dev(gi.bt)
     bias = torch.from_numpy(gi.bias).cuda()
     C = torch.empty(m * n, dtype=torch.int16, device="cuda")
-    tt = gemm_trips(m, n, k)
+    tt = gemm_trips_k_unrolled(m, n) if a.k_unrolled else gemm_trips(m, n, k)
+    prog = gemm_program_k_unrolled(m, n, k) if a.k_unrolled else gemm_program(m, n, k)
     t_np, o_np = tt.flat()
     trips, toff = torch.from_numpy(t_np).cuda(), torch.from_numpy(o_np).cuda()
     res, outs = {}, {}
     for name in a.modes.split(","):
         mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
-        plan = Plan(gemm_program(m, n, k), mode, alloc_of(a, mode))
+        plan = Plan(prog, mode, alloc_of(a, mode))
         C.fill_(-1)
         res[name] = time_mode(plan, [A, Bt, bias, C], trips, toff, tt.n_wg, a.steps, a.warmup,
                               k_unroll=a.k_unroll)
@@ -357,7 +361,8 @@ def bench_gemm(a):
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "GEMM + bias + GELU, A, B bf16 4096 x 4096 ~ N(0,1)/64, 256 x 256 tiles, "
                                f"K steps of {GEMM_BK} through a {GEMM_RING}-slot LDS ring", "m": m, "n": n, "k": k,
-                   "k_unroll": a.k_unroll or 1, "parallelism": "single GPU"},
+                   "k_unroll": a.k_unroll or 1, "k_unrolled_program": bool(a.k_unrolled),
+                   "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
@@ -365,7 +370,7 @@ def bench_gemm(a):
     }
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
-    out["paper_context"] = paper_context("gemm", res)
+    out["paper_context"] = paper_context("gemm_k_unrolled" if a.k_unrolled else "gemm", res)
     if cpu is not None:
         out["cpu_baseline"] = cpu
     emit(out, a, "gemm")

@@ -285,6 +285,24 @@ struct Sync {
     }
   }
 
+  // One wait whose threshold is a static immediate (straight-line code with
+  // no loop register, e.g. an unrolled loop): counter slot `slot` of a
+  // producer engine of `nw` waves; `seen` is the caller's monotone cache.
+  template <class OnBlock>
+  __device__ __forceinline__ void wait_fixed(uint32_t slot, uint32_t nw, uint32_t thr, uint32_t dep, uint32_t instance,
+                                             uint32_t &seen, OnBlock on_block) {
+    if (kInstr && (int)dep == C.fault_dep) thr += (uint32_t)C.fault_delta;
+    uint32_t obs = kMode == BFS_MODE_BARRIER ? 0u : seen;
+    if (!aborted && thr > 0 && (obs < thr || (kInstr && log))) {
+      obs = poll_geq(word(slot, 0), nw, thr, dep, instance, on_block);
+      seen = obs;
+    }
+    if (kInstr && log) {
+      on_block();
+      log_wait(log, C.dbg_cap, nlog, dep, instance, thr, thr > 0 ? obs : 0u);
+    }
+  }
+
   // Retirement: add 1 to this wave's word of the instruction's counter.
   // LDS executes one wave's DS instructions in issue order, so an add issued
   // after the instruction's LDS writes (its results) and LDS reads (its last

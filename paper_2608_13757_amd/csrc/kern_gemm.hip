@@ -57,6 +57,7 @@ constexpr int kTile = 256, kBK = 32;
 constexpr int kLoadW = 2, kMmaW = 8, kEpiW = 2, kWaves = 12;
 constexpr uint32_t kSlotBytes = 2 * kTile * kBK * 2;     // A + B of one K step
 constexpr uint32_t kESlotBytes = kMmaW * 32 * 32 * 2;     // 8 bf16 blocks
+constexpr int kMaxSteps = 128;                            // K steps of the K-unrolled program
 
 struct GemmParams {
   SyncCommon sc;
@@ -71,6 +72,11 @@ struct GemmParams {
   int32_t ring, e_ring;
   int32_t tiles_m, tiles_n;
   int32_t xcd_map;          // 1: group tiles per XCD
+  int32_t n_loops;          // 3 (top, K, C) or 2 (top, C: the K-unrolled program)
+  // K-unrolled program: counter slots of the top-level LOAD and MMA
+  // instructions, and the dependency id of each step's wait (debug log)
+  int32_t c_load, c_mma;
+  uint16_t dep_mma[kMaxSteps], dep_load[kMaxSteps];
 };
 
 __device__ __forceinline__ float gelu_erf(float x) {
@@ -91,7 +97,12 @@ __device__ __forceinline__ uint32_t swz(uint32_t row, uint32_t chunk) {
 // kUnroll: K steps per copy of the load and MFMA loop bodies (the trip of
 // loop K is static, so an unrolled body sees its thresholds as fixed offsets
 // of one value per copy); a remainder of trip_k % kUnroll steps runs singly.
-template <int kMode, bool kInstr, int kUnroll>
+// kSteps > 0: the K-unrolled program (no K loop; kSteps steps in straight
+// line at the top level): MMA of step s waits for s + 2 retirements of the
+// load engine's top-level counter (BIAS and LOADs 0 .. s), LOAD of step s
+// for s - ring + 1 of the MFMA engine's (MMAs 0 .. s - ring), both static
+// immediates that the launcher checks against the plan.
+template <int kMode, bool kInstr, int kUnroll, int kSteps>
 __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
@@ -119,15 +130,28 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
 
   Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), wave, wg);
   uint64_t k_end = 0;                      // statistics: end of the K loop
-  const int64_t *toff = P.trip_off + (int64_t)wg * 3;
-  uint32_t trip_k = (uint32_t)ldc(P.trips + ldc(toff + 1));
-  uint32_t trip_c = (uint32_t)ldc(P.trips + ldc(toff + 2));
+  constexpr bool kFlat = kSteps > 0;
+  constexpr uint32_t LC = kFlat ? 1u : 2u;          // loop id of C
+  const int64_t *toff = P.trip_off + (int64_t)wg * P.n_loops;
+  uint32_t trip_k = kFlat ? (uint32_t)kSteps : (uint32_t)ldc(P.trips + ldc(toff + 1));
+  uint32_t trip_c = (uint32_t)ldc(P.trips + ldc(toff + LC));
   if (trip_k > (uint32_t)(P.k / kBK) || trip_c > 8u) {
     report_input(P.sc.err, 2u, (uint32_t)wg, 0u, trip_k, trip_c, (uint32_t)wave);
     trip_k = min(trip_k, (uint32_t)(P.k / kBK));
     trip_c = min(trip_c, 8u);
   }
   Regs g;
+  // loop C's registers: r2, h2 below K, or r1, h1 without the K loop
+  auto c_iter = [&](uint32_t it) __attribute__((always_inline)) {
+    if (kFlat) {
+      g.r1 += 1;
+      g.h1 = it + 1;
+    } else {
+      g.r2 += 1;
+      g.h2 = it + 1;
+    }
+  };
+  auto c_r = [&]() __attribute__((always_inline)) { return kFlat ? g.r1 : g.r2; };
   const uint32_t ring_base = lds_addr(ring), ering_base = lds_addr(ering);
 
   if (wave < kLoadW) {
@@ -156,11 +180,12 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       __builtin_amdgcn_global_load_lds((const void *)(P.bias_v + n0 + 4 * lane), (BFS_LDS void *)bias_l, 16, 0, 0);
     wait_vm<0>();
     S.signal(P.bias.update, ew);
-    S.sync_point(S.word(0, ew));                            // before loop K
+    if (!kFlat) S.sync_point(S.word(0, ew));                // before loop K
     // per-lane source rows: lane l covers row 16 j + l / 4, logical chunk
     // (l % 4) ^ ((l / 16) % 4), so its 16 bytes land at the swizzled place.
     const uint32_t r_in = lane >> 2, chunk = (lane & 3u) ^ ((lane >> 4) & 3u);
-    S.enter(s_load, P.load, g, 1);
+    if (!kFlat) S.enter(s_load, P.load, g, 1);
+    uint32_t seen_mma = 0;
     // A wave-uniform base that advances one K step per iteration plus fixed
     // 32-bit per-lane byte offsets (one per 16-row group): the loads take the
     // scalar-base address form and need no vector address arithmetic, which
@@ -171,9 +196,15 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     for (int j = 0; j < 16; ++j) voff[j] = ((16u * j + r_in) * (uint32_t)P.k + 8u * chunk) * 2u;
     uint32_t slot = 0;
     auto load_step = [&](uint32_t it) __attribute__((always_inline)) {
-      g.r1 += 1;
-      g.h1 = it + 1;
-      S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
+      if (kFlat) {
+        if (it >= (uint32_t)P.ring)
+          S.wait_fixed((uint32_t)P.c_mma, kMmaW, it - (uint32_t)P.ring + 1u, P.dep_load[it], 0u, seen_mma,
+                       [&] { if (pending > 0) retire_one(); });
+      } else {
+        g.r1 += 1;
+        g.h1 = it + 1;
+        S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
+      }
       if (!S.aborted) {
         unsigned char *dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kSlotBytes / 2);
         const char *sb = sbase + (size_t)it * (kBK * 2);
@@ -187,24 +218,28 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       } else {
         S.signal(P.load.update, ew);
       }
-      if (kMode == BFS_MODE_BARRIER) {
+      if (kMode == BFS_MODE_BARRIER && !kFlat) {
         retire_all();
         S.sync_point(S.word(0, ew));                        // end of a K iteration
       }
       slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1;
     };
-    uint32_t it = 0;
-    for (; it + kUnroll <= trip_k; it += kUnroll) {
+    if constexpr (kFlat) {
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) load_step(it + u);
+      for (int st = 0; st < kSteps; ++st) load_step((uint32_t)st);
+    } else {
+      uint32_t it = 0;
+      for (; it + kUnroll <= trip_k; it += kUnroll) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) load_step(it + u);
+      }
+      for (; it < trip_k; ++it) load_step(it);
     }
-    for (; it < trip_k; ++it) load_step(it);
     retire_all();
     k_end = S.elapsed();
     S.sync_point(S.word(0, ew));                            // before loop C
     for (uint32_t it = 0; it < trip_c; ++it) {
-      g.r2 += 1;
-      g.h2 = it + 1;
+      c_iter(it);
       S.sync_point(S.word(0, ew));                          // end of a C iteration
     }
   } else if (wave < kLoadW + kMmaW) {
@@ -216,14 +251,21 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     for (int i = 0; i < 8; ++i) acc[i] = f32x16{};
     Site<1> s_mma;
     Site<3> s_spill;
-    S.sync_point(S.word(1, ew));                            // before loop K
-    S.enter(s_mma, P.mma, g, 1);
+    if (!kFlat) {
+      S.sync_point(S.word(1, ew));                          // before loop K
+      S.enter(s_mma, P.mma, g, 1);
+    }
+    uint32_t seen_load = 0;
     const uint32_t l32 = lane & 31u, lhi = lane >> 5;
     uint32_t slot = 0;
     auto mma_step = [&](uint32_t it) __attribute__((always_inline)) {
-      g.r1 += 1;
-      g.h1 = it + 1;
-      S.wait(s_mma, P.mma, g, it + 1, g.r1 - 1, [] {});
+      if (kFlat) {
+        S.wait_fixed((uint32_t)P.c_load, kLoadW, it + 2u, P.dep_mma[it], 0u, seen_load, [] {});
+      } else {
+        g.r1 += 1;
+        g.h1 = it + 1;
+        S.wait(s_mma, P.mma, g, it + 1, g.r1 - 1, [] {});
+      }
       const uint32_t a_base = ring_base + slot * kSlotBytes, b_base = a_base + kSlotBytes / 2;
       if (!S.aborted) {
         // Fragments are read one block ahead of the MFMAs that use them, so
@@ -262,26 +304,30 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       } else {
         S.signal(P.mma.update, ew);
       }
-      S.sync_point(S.word(1, ew));                          // end of a K iteration (barrier mode)
+      if (!kFlat) S.sync_point(S.word(1, ew));              // end of a K iteration (barrier mode)
       slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1;
     };
-    uint32_t it = 0;
-    for (; it + kUnroll <= trip_k; it += kUnroll) {
+    if constexpr (kFlat) {
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) mma_step(it + u);
+      for (int st = 0; st < kSteps; ++st) mma_step((uint32_t)st);
+    } else {
+      uint32_t it = 0;
+      for (; it + kUnroll <= trip_k; it += kUnroll) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) mma_step(it + u);
+      }
+      for (; it < trip_k; ++it) mma_step(it);
     }
-    for (; it < trip_k; ++it) mma_step(it);
     k_end = S.elapsed();
     S.sync_point(S.word(1, ew));                            // before loop C
-    S.enter(s_spill, P.spill, g, 2);
+    S.enter(s_spill, P.spill, g, LC);
     // The chunk loop is unrolled so that each chunk names its accumulator
     // block statically; trip_c <= 8 chunks run.
 #pragma unroll
     for (uint32_t it = 0; it < 8; ++it) {
       if (it >= trip_c) break;
-      g.r2 += 1;
-      g.h2 = it + 1;
-      S.wait(s_spill, P.spill, g, it + 1, g.r2 - 1, [] {});
+      c_iter(it);
+      S.wait(s_spill, P.spill, g, it + 1, c_r() - 1, [] {});
       if (!S.aborted) {
         const uint32_t b = it, bm = b >> 1, bn = b & 1u;
         const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
@@ -307,18 +353,19 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     // -------------------------------------------------------- epilogue engine
     const uint32_t ew = (uint32_t)(wave - kLoadW - kMmaW);
     Site<1> s_epi;
-    S.sync_point(S.word(2, ew));                            // before loop K
-    for (uint32_t it = 0; it < trip_k; ++it) {
-      g.r1 += 1;
-      g.h1 = it + 1;
-      S.sync_point(S.word(2, ew));                          // end of a K iteration
+    if (!kFlat) {
+      S.sync_point(S.word(2, ew));                          // before loop K
+      for (uint32_t it = 0; it < trip_k; ++it) {
+        g.r1 += 1;
+        g.h1 = it + 1;
+        S.sync_point(S.word(2, ew));                        // end of a K iteration
+      }
     }
     S.sync_point(S.word(2, ew));                            // before loop C
-    S.enter(s_epi, P.epi, g, 2);
+    S.enter(s_epi, P.epi, g, LC);
     for (uint32_t it = 0; it < trip_c; ++it) {
-      g.r2 += 1;
-      g.h2 = it + 1;
-      S.wait(s_epi, P.epi, g, it + 1, g.r2 - 1, [] {});
+      c_iter(it);
+      S.wait(s_epi, P.epi, g, it + 1, c_r() - 1, [] {});
       if (!S.aborted) {
         const uint32_t b = it, bm = b >> 1, bn = b & 1u;
         const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
@@ -352,25 +399,29 @@ namespace bfs {
 bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs, int32_t nbufs,
                        const int32_t *trips, const int64_t *trip_off, int32_t n_wg, void *stream, uint32_t *dbg,
                        int64_t dbg_cap, const bfs_run_opts &o) {
-  // structure: top{ BIAS(E0); K{ LOAD(E0) MMA(E1) }; C{ SPILL(E1) EPI(E2) } }
-  if (p->n_loops != 3 || p->loop_parent[1] != 0 || p->loop_parent[2] != 0)
-    return fail(BFS_E_UNSUPPORTED, "gemm: loops must be top -> K, top -> C");
+  // structure: top{ BIAS(E0); K{ LOAD(E0) MMA(E1) }; C{ SPILL(E1) EPI(E2) } }, or the K-unrolled
+  // top{ BIAS(E0); LOAD_0(E0) MMA_0(E1) ... LOAD_{S-1} MMA_{S-1}; C{ SPILL(E1) EPI(E2) } }
+  const bool flat = p->n_loops == 2;
+  const int LC = flat ? 1 : 2;
+  if (flat ? p->loop_parent[1] != 0 : (p->n_loops != 3 || p->loop_parent[1] != 0 || p->loop_parent[2] != 0))
+    return fail(BFS_E_UNSUPPORTED, "gemm: loops must be top -> K, top -> C (or top -> C with K unrolled)");
   if (p->n_engines != 3 || p->waves_per_engine[0] != kLoadW || p->waves_per_engine[1] != kMmaW ||
       p->waves_per_engine[2] != kEpiW)
     return fail(BFS_E_UNSUPPORTED, "gemm: engines of 2, 8 and 2 waves");
   int ins_bias = -1, ins_load = -1, ins_mma = -1, ins_spill = -1, ins_epi = -1;
+  std::vector<int> loads, mmas;   // K-unrolled: step s's instructions in listing order
   for (size_t i = 0; i < p->instr_engine.size(); ++i) {
     const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];
     if (op == 20 && e == 0 && par == 0 && ins_bias < 0) ins_bias = (int)i;
-    else if (op == 16 && e == 0 && par == 1 && ins_load < 0) ins_load = (int)i;
-    else if (op == 17 && e == 1 && par == 1 && ins_mma < 0) ins_mma = (int)i;
-    else if (op == 18 && e == 1 && par == 2 && ins_spill < 0) ins_spill = (int)i;
-    else if (op == 19 && e == 2 && par == 2 && ins_epi < 0) ins_epi = (int)i;
+    else if (op == 16 && e == 0 && par == (flat ? 0 : 1) && (flat || ins_load < 0)) loads.push_back((int)i), ins_load = (int)i;
+    else if (op == 17 && e == 1 && par == (flat ? 0 : 1) && (flat || ins_mma < 0)) mmas.push_back((int)i), ins_mma = (int)i;
+    else if (op == 18 && e == 1 && par == LC && ins_spill < 0) ins_spill = (int)i;
+    else if (op == 19 && e == 2 && par == LC && ins_epi < 0) ins_epi = (int)i;
     else return fail(BFS_E_UNSUPPORTED, "gemm: unexpected instruction " + std::to_string(i));
   }
   if (ins_bias < 0 || ins_load < 0 || ins_mma < 0 || ins_spill < 0 || ins_epi < 0)
     return fail(BFS_E_UNSUPPORTED, "gemm: needs BIAS, LOAD, MMA, SPILL and EPI");
-  const int32_t *la = &p->instr_args[8 * ins_load];
+  const int32_t *la = &p->instr_args[8 * loads[0]];
   const int M = la[0], N = la[1], K = la[2], ring = la[3];
   const int e_ring = p->instr_args[8 * ins_spill];
   if (M <= 0 || N <= 0 || K <= 0 || M % kTile || N % kTile || K % kBK)
@@ -378,18 +429,66 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
   if ((uint64_t)kTile * K * 2 > 0xffffffffull) return fail(BFS_E_UNSUPPORTED, "gemm: K too large for 32-bit load offsets");
   if (ring < 2 || ring > 4 || e_ring < 1 || e_ring > 2)
     return fail(BFS_E_UNSUPPORTED, "gemm: ring of 2..4 slots, epilogue ring of 1..2 slots");
-  // the epilogue ring lives in the K ring's memory: the program must order
-  // every spill after the whole K loop of every MFMA wave
-  if (!has_dep(p, ins_mma, ins_spill, 0) || (size_t)e_ring * kESlotBytes > (size_t)ring * kSlotBytes)
-    return fail(BFS_E_UNSUPPORTED, "gemm: needs the MMA -> SPILL dependency (epilogue ring reuses the K ring)");
   if ((M / kTile) * (N / kTile) != n_wg) return fail(BFS_E_INVALID, "gemm: n_wg must be (M / 256) * (N / 256)");
   if (nbufs < 4 || !bufs[0] || !bufs[1] || !bufs[2] || !bufs[3]) return fail(BFS_E_INVALID, "gemm: needs [A, Bt, bias, C]");
   if (!trips || !trip_off) return fail(BFS_E_INVALID, "gemm: needs trip tables");
   const std::vector<DevWait> dw = device_waits(p);
   GemmParams P{};
-  if (!fill_waits(p, dw, ins_bias, P.bias) || !fill_waits(p, dw, ins_load, P.load) ||
-      !fill_waits(p, dw, ins_mma, P.mma) || !fill_waits(p, dw, ins_spill, P.spill) || !fill_waits(p, dw, ins_epi, P.epi))
+  P.n_loops = p->n_loops;
+  const int steps = K / kBK;
+  if (flat) {
+    // the K-unrolled program: its K-phase waits are the static immediates
+    // the kernel is built with; check the plan gives exactly those
+    if ((int)loads.size() != steps || (int)mmas.size() != steps || (steps != 3 && steps != 8 && steps != 128))
+      return fail(BFS_E_UNSUPPORTED, "gemm: the K-unrolled kernel is built for 3, 8 or 128 steps, one LOAD and MMA each");
+    for (int st = 0; st < steps; ++st) {
+      const int32_t *a = &p->instr_args[8 * loads[st]];
+      if (a[0] != M || a[1] != N || a[2] != K || a[3] != ring || a[4] != st || p->instr_args[8 * mmas[st]] != st)
+        return fail(BFS_E_UNSUPPORTED, "gemm: K-unrolled steps out of order");
+    }
+    if (p->instr_update[ins_bias] != p->instr_update[loads[0]])
+      return fail(BFS_E_UNSUPPORTED, "gemm: BIAS and the LOADs must share the load engine's top-level counter");
+    P.c_load = p->instr_update[loads[0]];
+    P.c_mma = p->instr_update[mmas[0]];
+    for (int st = 0; st < steps; ++st) {
+      if (p->instr_update[loads[st]] != P.c_load || p->instr_update[mmas[st]] != P.c_mma)
+        return fail(BFS_E_UNSUPPORTED, "gemm: every step must update the engine's top-level counter");
+      auto check = [&](int ins, int want_prd, int want_slot, uint32_t want_thr, uint16_t &dep_out) -> bool {
+        int n = 0;
+        for (int wi = p->instr_wait_off[ins]; wi < p->instr_wait_off[ins + 1]; ++wi) {
+          const int d = p->instr_wait_list[wi];
+          uint32_t thr = 0;
+          if (bfs_eval_threshold(p, d, 1u, 1u, &thr) != BFS_OK) return false;
+          if (p->deps[3 * d] != want_prd || dw[d].counter != want_slot || thr != want_thr || !dw[d].active) return false;
+          dep_out = (uint16_t)d;
+          ++n;
+        }
+        return want_prd < 0 ? n == 0 : n == 1;
+      };
+      if (!check(mmas[st], loads[st], P.c_load, (uint32_t)st + 2u, P.dep_mma[st]))
+        return fail(BFS_E_UNSUPPORTED, "gemm: MMA " + std::to_string(st) + " must wait exactly for LOAD " +
+                                           std::to_string(st) + " (load counter " + std::to_string(st + 2) + ")");
+      const int prd = st >= ring ? mmas[st - ring] : -1;
+      if (!check(loads[st], prd, P.c_mma, st >= ring ? (uint32_t)(st - ring + 1) : 0u, P.dep_load[st]))
+        return fail(BFS_E_UNSUPPORTED, "gemm: LOAD " + std::to_string(st) + " must wait exactly for MMA " +
+                                           std::to_string(st - ring) + " (the ring)");
+    }
+    if (!has_dep(p, mmas[steps - 1], ins_spill, 0) || (size_t)e_ring * kESlotBytes > (size_t)ring * kSlotBytes)
+      return fail(BFS_E_UNSUPPORTED, "gemm: needs the last MMA -> SPILL dependency (epilogue ring reuses the K ring)");
+    ins_load = loads[0];
+    ins_mma = mmas[0];
+  } else {
+    // the epilogue ring lives in the K ring's memory: the program must order
+    // every spill after the whole K loop of every MFMA wave
+    if (!has_dep(p, ins_mma, ins_spill, 0) || (size_t)e_ring * kESlotBytes > (size_t)ring * kSlotBytes)
+      return fail(BFS_E_UNSUPPORTED, "gemm: needs the MMA -> SPILL dependency (epilogue ring reuses the K ring)");
+    if (!fill_waits(p, dw, ins_load, P.load) || !fill_waits(p, dw, ins_mma, P.mma))
+      return fail(BFS_E_RESOURCE, "gemm: at most 4 waits per instruction");
+  }
+  if (!fill_waits(p, dw, ins_bias, P.bias) || !fill_waits(p, dw, ins_spill, P.spill) || !fill_waits(p, dw, ins_epi, P.epi))
     return fail(BFS_E_RESOURCE, "gemm: at most 4 waits per instruction");
+  P.load.update = p->instr_update[ins_load];
+  P.mma.update = p->instr_update[ins_mma];
   if (!waits_fit({{&P.bias, 1}, {&P.load, 1}, {&P.mma, 1}, {&P.spill, 3}, {&P.epi, 1}}))
     return fail(BFS_E_RESOURCE, "gemm: more waits on an instruction than its engine loop takes");
   P.a = static_cast<const __bf16 *>(bufs[0]);
@@ -424,11 +523,16 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
   auto pick = [&](auto mode_tag, auto instr_tag) -> bfs_status {
     constexpr int kM = decltype(mode_tag)::value;
     constexpr bool kI = decltype(instr_tag)::value;
+    if (flat) {
+      if (steps == 3) return go(gemm_kernel<kM, kI, 1, 3>);
+      if (steps == 8) return go(gemm_kernel<kM, kI, 1, 8>);
+      return go(gemm_kernel<kM, kI, 1, 128>);
+    }
     switch (o.k_unroll) {
-      case 2: return go(gemm_kernel<kM, kI, 2>);
-      case 4: return go(gemm_kernel<kM, kI, 4>);
-      case 8: return go(gemm_kernel<kM, kI, 8>);
-      default: return go(gemm_kernel<kM, kI, 1>);
+      case 2: return go(gemm_kernel<kM, kI, 2, 0>);
+      case 4: return go(gemm_kernel<kM, kI, 4, 0>);
+      case 8: return go(gemm_kernel<kM, kI, 8, 0>);
+      default: return go(gemm_kernel<kM, kI, 1, 0>);
     }
   };
   using BF = std::integral_constant<int, BFS_MODE_BARRIER_FREE>;

@@ -15,7 +15,7 @@ from oracle import core, mathref  # noqa: E402
 from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER, MODE_BARRIER_FREE,  # noqa: E402
                                   BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
-from workloads import gemm_program, gemm_trips  # noqa: E402
+from workloads import gemm_program, gemm_program_k_unrolled, gemm_trips, gemm_trips_k_unrolled  # noqa: E402
 from workloads.tensors import bf16_to_f32, gemm_inputs  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -119,6 +119,54 @@ def test_gemm_k_unroll_thresholds(u):
             assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
             outs[name] = c.cpu().numpy()
         assert np.array_equal(outs["barrier_free"], outs["barrier"])
+
+
+@pytest.mark.parametrize("shape", [(512, 512, 256), (256, 768, 96), (512, 256, 4096)])
+def test_gemm_k_unrolled_program(shape):
+    """The K-unrolled program (K loop removed, the steps listed at the top
+    level, every K-phase wait a static immediate): outputs bit-identical to
+    the looped program's in both modes, every logged threshold equal to the
+    oracle's for every wave."""
+    m, n, k = shape
+    gi = gemm_inputs(seed=6, m=m, n=n, k=k)
+    a, bt = _bits_to_dev(gi.a), _bits_to_dev(gi.bt)
+    bias = torch.from_numpy(gi.bias).cuda()
+    prog = gemm_program_k_unrolled(m, n, k)
+    tt = gemm_trips_k_unrolled(m, n)
+    trips, toff = trip_tensors(tt)
+    t_np, off = tt.flat()
+    recs = {g: core.run(prog, t_np, off[g], g).recs for g in range(0, tt.n_wg, max(1, tt.n_wg // 3))}
+    _, _, _, ref, _ = run_gemm(gi, m, n, k, MODE_BARRIER_FREE)
+    for name, mode in MODES:
+        _say(f"[gemm-k-unrolled] {shape} mode={name}")
+        plan = Plan(prog, mode)
+        cap = 512
+        log = torch.zeros(plan.debug_log_words(tt.n_wg, cap), dtype=torch.int32, device="cuda")
+        c = torch.full((m * n,), -1, dtype=torch.int16, device="cuda")
+        plan.run([a, bt, bias, c], trips, toff, tt.n_wg, debug_log=log, debug_capacity=cap)
+        plan.status()
+        logs = log_records(plan, log.cpu().numpy().view(np.uint32), tt.n_wg, cap, per_wave=True)
+        assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
+        out = bf16_to_f32(c.cpu().numpy().view(np.uint16)).reshape(m, n)
+        assert np.array_equal(out.view(np.uint32), ref.view(np.uint32))
+        c.fill_(-1)
+        plan.run([a, bt, bias, c], trips, toff, tt.n_wg)
+        plan.status()
+        assert np.array_equal(bf16_to_f32(c.cpu().numpy().view(np.uint16)).reshape(m, n).view(np.uint32),
+                              ref.view(np.uint32))
+    if k <= 256:
+        check_close(ref, mathref.gemm_bias_gelu(gi.a, gi.bt, gi.bias))
+
+
+def test_gemm_k_unrolled_rejects_other_steps():
+    m, n, k = 256, 256, 64                     # 2 steps: no kernel built for it
+    plan = Plan(gemm_program_k_unrolled(m, n, k))
+    tt = gemm_trips_k_unrolled(m, n)
+    trips, toff = trip_tensors(tt)
+    t = torch.zeros(m * k, dtype=torch.int16, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t, t, torch.zeros(n, device="cuda"), t], trips, toff, tt.n_wg)
+    assert e.value.status == bfs.E_UNSUPPORTED
 
 
 def test_gemm_k_unroll_rejects_other_factors():

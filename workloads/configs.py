@@ -492,6 +492,48 @@ def gemm_program(m: int, n: int, k: int, ring: int = GEMM_RING, e_ring: int = 2,
     return b.build()
 
 
+GEMM_K_UNROLLED_STEPS = (3, 8, 128)   # K steps the K-unrolled kernel is built for
+
+
+def gemm_program_k_unrolled(m: int, n: int, k: int, ring: int = GEMM_RING, e_ring: int = 2) -> Program:
+    """The GEMM with its K loop removed (the K-unrolled variant of the
+    paper's tiled matmul): the K / 32 steps are listed one after another at
+    the top level, so every threshold of the K phase is a static ordinal:
+
+      E0: BIAS
+      E0: LOAD_0  E1: MMA_0  E0: LOAD_1  E1: MMA_1 ...  (step s in slot s % ring)
+      C{ E1: SPILL; E2: EPI }
+
+    LOAD_s->MMA_s and MMA_s->LOAD_{s+ring} at offset 0 (forward in the
+    straight line), BIAS->SPILL, MMA_last->SPILL (every MFMA wave has
+    retired its last step before the epilogue reuses the ring's memory;
+    retirement is in order), SPILL->EPI, EPI->SPILL as in gemm_program."""
+    steps = k // GEMM_BK
+    b = ProgramBuilder("gemm", n_engines=3, waves_per_engine=[2, 8, 2])
+    b.instr(0, OP_GEMM_BIAS, [m, n, k, 0, 0, 0, 0, 0], name="BIAS")
+    for st in range(steps):
+        b.instr(0, OP_GEMM_LOAD, [m, n, k, ring, st, 0, 0, 0], name=f"LOAD{st}")
+        b.instr(1, OP_GEMM_MMA, [st, 0, 0, 0, 0, 0, 0, 0], name=f"MMA{st}")
+    with b.loop("C"):
+        b.instr(1, OP_GEMM_SPILL, [e_ring, 0, 0, 0, 0, 0, 0, 0], name="SPILL")
+        b.instr(2, OP_GEMM_EPI, [0] * 8, name="EPI")
+    for st in range(steps):
+        b.dep(f"LOAD{st}", f"MMA{st}", 0)
+        if st + ring < steps:
+            b.dep(f"MMA{st}", f"LOAD{st + ring}", 0)
+    b.dep("BIAS", "SPILL", 0)
+    b.dep("SPILL", "EPI", 0)
+    b.dep("EPI", "SPILL", e_ring)
+    b.dep(f"MMA{steps - 1}", "SPILL", 0)
+    return b.build()
+
+
+def gemm_trips_k_unrolled(m: int, n: int) -> TripTables:
+    """The K-unrolled GEMM's trip tables: the epilogue loop's 8 chunks."""
+    n_wg = (m // GEMM_TILE) * (n // GEMM_TILE)
+    return TripTables([[np.array([1], np.int32), np.array([GEMM_CHUNKS], np.int32)] for _ in range(n_wg)])
+
+
 def gemm_trips(m: int, n: int, k: int, ring: int = GEMM_RING) -> TripTables:
     """Every workgroup runs the K loop once with K / 32 steps and the
     epilogue loop once with 8 chunks."""
