@@ -142,10 +142,7 @@ def parse():
                          "barrier_free_per_instance)")
     ap.add_argument("--algorithmic-bytes", action="store_true",
                     help="print the workload's algorithmic HBM bytes per step and exit (no GPU)")
-    ap.add_argument("--moe-ring", default="", choices=["", "linear", "acq"],
-                    help="MoE: protect the load ring across M-tiles with the linearized MMA->LOAD dependency "
-                         "(an extension of the paper's relation) or with the paper's acquire instruction that "
-                         "drains the ring at every M-tile (MMA->ACQL, k = 1)")
+
     ap.add_argument("--k-unroll", type=int, default=0, choices=[0, 1, 2, 4, 8],
                     help="GEMM: K steps per copy of the loop bodies (static-trip unrolling)")
     ap.add_argument("--k-unrolled", action="store_true",
@@ -175,14 +172,10 @@ def parse():
                          "(reference dispatch for HBM traffic counters)")
     a = ap.parse_args()
     if not a.modes:
-        a.modes = "barrier_free,barrier,barrier_free_per_instance" if a.workload == "stream" else "barrier_free,barrier"
+        a.modes = {"stream": "barrier_free,barrier,barrier_free_per_instance",
+                   "attn": "barrier_free,barrier_free_linearized,barrier",
+                   "moe": "barrier_free,barrier_free_linearized,barrier"}.get(a.workload, "barrier_free,barrier")
     return a
-
-
-def moe_linear(a):
-    """The MoE ring form: --moe-ring, else the benchmark default of workloads."""
-    from workloads.configs import MOE_LINEAR
-    return MOE_LINEAR if not a.moe_ring else a.moe_ring == "linear"
 
 
 def alloc_of(a, mode):
@@ -411,14 +404,20 @@ def bench_attn(a):
     t_np, o_np = wl.trips.flat()
     trips, toff = torch.from_numpy(t_np).cuda(), torch.from_numpy(o_np).cuda()
     res, outs = {}, {}
+    # barrier_free: the benchmark form (per-trip reuse dependencies and
+    # acquire instructions at each tile: the paper's relation only);
+    # barrier_free_linearized: the reuse read with the linearized offset
+    # across tiles (an extension)
     for name in a.modes.split(","):
-        mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
-        plan = Plan(attn_program(heads), mode, alloc_of(a, mode))
+        mode = MODE_BARRIER_FREE if name.startswith("barrier_free") else MODE_BARRIER
+        prog = attn_program(heads, linear=name == "barrier_free_linearized")
+        plan = Plan(prog, mode, alloc_of(a, mode))
         o.fill_(-1)
         res[name] = time_mode(plan, [work, q, k, v, o], trips, toff, wl.trips.n_wg, a.steps, a.warmup)
         outs[name] = o.clone()
-    if len(outs) == 2 and not torch.equal(outs["barrier_free"], outs["barrier"]):
-        raise SystemExit("attn: the two modes disagree")
+    for name in outs:
+        if not torch.equal(outs[name], next(iter(outs.values()))):
+            raise SystemExit(f"attn: {name} disagrees with the other modes")
     lens = ai.lengths.astype(np.float64)
     flop = 4.0 * 128 * heads * float(np.sum(lens * lens))
     bf = res.get("barrier_free", next(iter(res.values())))
@@ -433,7 +432,8 @@ def bench_attn(a):
                                "KV blocks of 64, 128-query tiles", "batch": 32, "heads": heads,
                    "head_dim": 128, "tokens": int(lens.sum()), "n_wg": wl.trips.n_wg,
                    "rings": {"k": ATTN_NK, "v": ATTN_NV, "s_p": ATTN_SP},
-                   "ring_across_tiles": "linearized reuse dependencies (extension)",
+                   "ring_across_tiles": "barrier_free: acquires at each tile (the paper's relation); "
+                                        "barrier_free_linearized: linearized reuse dependencies (extension)",
                    "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -441,6 +441,8 @@ def bench_attn(a):
     }
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
+    if "barrier" in res and "barrier_free_linearized" in res:
+        out["speedup_vs_barrier_linearized"] = res["barrier"]["ms_mean"] / res["barrier_free_linearized"]["ms_mean"]
     out["paper_context"] = paper_context("attn", res)
     if cpu is not None:
         out["cpu_baseline"] = cpu
@@ -493,9 +495,12 @@ def bench_moe(a):
         launches[ph] = (bufs, torch.from_numpy(t_np).cuda(), torch.from_numpy(o_np).cuda(), wl.trips.n_wg)
     stream = torch.cuda.current_stream()
     res, outs = {}, {}
+    # barrier_free: the paper's relation (ACQL drains the ring at every
+    # M-tile); barrier_free_linearized: MMA->LOAD read with the linearized
+    # offset across M-tiles (an extension)
     for name in a.modes.split(","):
-        mode = MODE_BARRIER_FREE if name == "barrier_free" else MODE_BARRIER
-        plans = {ph: Plan(moe_program(ph, H, F, linear=moe_linear(a)), mode, alloc_of(a, mode))
+        mode = MODE_BARRIER_FREE if name.startswith("barrier_free") else MODE_BARRIER
+        plans = {ph: Plan(moe_program(ph, H, F, linear=name == "barrier_free_linearized"), mode, alloc_of(a, mode))
                  for ph in (1, 2)}
         h.fill_(-1)
         y.fill_(-1)
@@ -526,8 +531,10 @@ def bench_moe(a):
         res[name] = {"ms_mean": (sum(p1) + sum(p2)) / a.steps, "phase1_ms": sum(p1) / a.steps,
                      "phase2_ms": sum(p2) / a.steps}
         outs[name] = (h.clone(), y.clone())
-    if len(outs) == 2 and not all(torch.equal(u, v) for u, v in zip(outs["barrier_free"], outs["barrier"])):
-        raise SystemExit("moe: the two modes disagree")
+    first = next(iter(outs.values()))
+    for name, o in outs.items():
+        if not all(torch.equal(u, v) for u, v in zip(o, first)):
+            raise SystemExit(f"moe: {name} disagrees with the other modes")
     c = moe.counts.astype(np.float64)
     flop = float(6.0 * c.sum() * H * F)
     # per-expert roofline: every expert's weights and token rows cross HBM once
@@ -544,8 +551,9 @@ def bench_moe(a):
         "config": {"workload": "MoE grouped GEMM, 32768 tokens top-1 to 64 experts (Zipf 1.1 counts), hidden 4096, "
                                "ffn 1408, SiLU-gated, bf16 weights N(0,0.02); gate/up launch + down launch",
                    "tokens": T, "experts": len(c), "hidden": H, "ffn": F,
-                   "ring_across_m_tiles": "linearized MMA->LOAD (extension)" if moe_linear(a)
-                   else "ACQL drain (paper's relation)", "m_tiles_per_workgroup_run": MOE_MCHUNK,
+                   "ring_across_m_tiles": "barrier_free: ACQL drain (paper's relation); "
+                                          "barrier_free_linearized: linearized MMA->LOAD (extension)",
+                   "m_tiles_per_workgroup_run": MOE_MCHUNK,
                    "ring_slots": MOE_RING, "n_wg": [launches[1][3], launches[2][3]], "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
         "phase_us": {kk: [v["phase1_ms"] * 1e3, v["phase2_ms"] * 1e3] for kk, v in res.items()},
@@ -555,6 +563,8 @@ def bench_moe(a):
     }
     if "barrier" in res and "barrier_free" in res:
         out["speedup_vs_barrier"] = res["barrier"]["ms_mean"] / res["barrier_free"]["ms_mean"]
+    if "barrier" in res and "barrier_free_linearized" in res:
+        out["speedup_vs_barrier_linearized"] = res["barrier"]["ms_mean"] / res["barrier_free_linearized"]["ms_mean"]
     out["paper_context"] = paper_context("moe", res)
     if cpu is not None:
         out["cpu_baseline"] = cpu

@@ -80,6 +80,7 @@ constexpr int kMaxPend = 3;                      // load groups in flight per lo
 struct AttnParams {
   SyncCommon sc;
   InstrWaits loadk, loadv, qk, sm, pread, pv, norm;
+  InstrWaits acqk, acqv, acqs;   // acquire form: the drains at each tile (n = 0 in the linearized form)
   const int32_t *work;
   const __bf16 *q, *k, *v;
   __bf16 *o;
@@ -168,6 +169,7 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
   };
   Regs g;
   Site<2> site;
+  Site<1> s_acq;                            // acquire form: the engine's wait at each tile
   uint64_t mark = 0;
 
   if (eng == 0 || eng == 4) {
@@ -207,14 +209,22 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
       voff[j] = (row * (uint32_t)row_stride + 8u * chunk) * 2u;
     }
     // ring slots follow r_KV over all tiles: a tile's loads go on where the
-    // previous tile's stopped, ordered by the linearized ring dependency
+    // previous tile's stopped, ordered by the linearized ring dependency, or
+    // (acquire form) after ACQK / ACQV drained the previous tile's reads
+    const InstrWaits &acq = is_v ? P.acqv : P.acqk;
     uint32_t slot = 0;
     S.sync_point(own);                                       // before loop T
+    S.enter(s_acq, acq, g, 1);
     for (uint32_t t = 0; t < trip_t; ++t) {
       g.r1 += 1;
       g.h1 = t + 1;
       const Tile x = tile(t);
       const __bf16 *base = (is_v ? P.v : P.k) + (size_t)x.head * kD;
+      S.wait(s_acq, acq, g, t + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });   // ACQK / ACQV
+      if (acq.update >= 0) {
+        retire_all();
+        S.signal(acq.update, 0);
+      }
       S.sync_point(own);                                     // before loop KV
       S.enter(site, iw, g, 2);
       for (uint32_t it = 0; it < x.trip; ++it, slot = (slot + 1 == depth) ? 0u : slot + 1) {
@@ -261,11 +271,16 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
     // ---------------------------------------------------------- QK^T engine
     const uint32_t qr = 64u * ew;
     S.sync_point(own);                                       // before loop T
+    S.enter(s_acq, P.acqs, g, 1);
     uint32_t kslot = 0;
     for (uint32_t t = 0; t < trip_t; ++t) {
       g.r1 += 1;
       g.h1 = t + 1;
       const Tile x = tile(t);
+      // acquire form: the previous tile's S/P slots are released (its PREADs
+      // have read them) before this tile's first QK writes one
+      S.wait(s_acq, P.acqs, g, t + 1, g.r1 - 1, [] {});   // ACQS
+      S.signal(P.acqs.update, ew);
       // the tile's 64 query rows of this wave, held in registers for its KV
       // loop
       bf16x8 qf[2][8];
@@ -520,11 +535,14 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   if (p->n_engines != 5) return fail(BFS_E_UNSUPPORTED, "attn: five engines");
   for (int e = 0; e < 5; ++e)
     if (p->waves_per_engine[e] != want_w[e]) return fail(BFS_E_UNSUPPORTED, "attn: engines of 1, 2, 4, 4, 1 waves");
-  int lk = -1, lv = -1, qk = -1, sm = -1, pr = -1, pv = -1, nm = -1;
+  int lk = -1, lv = -1, qk = -1, sm = -1, pr = -1, pv = -1, nm = -1, ak = -1, av = -1, as = -1;
   for (size_t i = 0; i < p->instr_engine.size(); ++i) {
     const int op = p->instr_opcode[i], e = p->instr_engine[i], par = p->instr_parent[i];
     const int32_t *a = &p->instr_args[8 * i];
-    if (op == 32 && e == 0 && par == 2 && a[0] == 0 && lk < 0) lk = (int)i;
+    if (op == 0 && par == 1 && e == 0 && ak < 0 && lk < 0) ak = (int)i;         // acquire form: ACQK
+    else if (op == 0 && par == 1 && e == 4 && av < 0 && lv < 0) av = (int)i;    // ACQV
+    else if (op == 0 && par == 1 && e == 1 && as < 0 && qk < 0) as = (int)i;    // ACQS
+    else if (op == 32 && e == 0 && par == 2 && a[0] == 0 && lk < 0) lk = (int)i;
     else if (op == 32 && e == 4 && par == 2 && a[0] == 1 && lv < 0) lv = (int)i;
     else if (op == 33 && e == 1 && par == 2 && qk < 0) qk = (int)i;
     else if (op == 34 && e == 2 && par == 2 && sm < 0) sm = (int)i;
@@ -541,19 +559,29 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   if (heads <= 0 || p->instr_args[8 * lv + 2] != heads) return fail(BFS_E_INVALID, "attn: heads must match");
   const size_t lds = kCntBytes + (size_t)(nk + nv) * kKVSlot + 2 * kSPSlot + 4 * kBQ * 4;
   if (nk < 2 || nv < 2 || lds > 160 * 1024) return fail(BFS_E_UNSUPPORTED, "attn: ring depths >= 2 within 160 KiB of LDS");
-  // the kernel's buffers are only race-free under these dependencies; the
+  // The kernel's buffers are only race-free under these dependencies.  The
   // rings and S/P slots are indexed by r_KV over all tiles, so their reuse
-  // dependencies must be read with the linearized offset
-  auto linear_dep = [&](int prd, int cns, int k) {
+  // across tiles is ordered either by reading the reuse dependencies with
+  // the linearized offset (extension), or, with the paper's relation, by
+  // acquire instructions at each tile on the K loader, the V loader and the
+  // QK engine whose C3 dependencies (offset 1 at T) drain the previous
+  // tile's QK, PV and PREAD.
+  auto dep_form = [&](int prd, int cns, int k, int linear) {
     for (size_t d = 0; d < p->deps.size() / 3; ++d)
-      if (p->deps[3 * d] == prd && p->deps[3 * d + 1] == cns && p->deps[3 * d + 2] == k && p->dep_linear[d])
+      if (p->deps[3 * d] == prd && p->deps[3 * d + 1] == cns && p->deps[3 * d + 2] == k &&
+          (p->dep_linear.empty() ? 0 : p->dep_linear[d]) == linear)
         return true;
     return false;
   };
-  if (!has_dep(p, lk, qk, 0) || !has_dep(p, lv, pv, 0) || !has_dep(p, qk, sm, 0) || !has_dep(p, sm, pr, 0) ||
-      !linear_dep(qk, lk, nk) || !linear_dep(pv, lv, nv) || !linear_dep(pr, qk, 2) || !has_dep(p, sm, nm, 0) ||
-      !has_dep(p, nm, sm, 2))
-    return fail(BFS_E_UNSUPPORTED, "attn: missing a ring, S/P or row-sum dependency");
+  const bool acq_form = ak >= 0 && av >= 0 && as >= 0;
+  if ((ak >= 0 || av >= 0 || as >= 0) && !acq_form)
+    return fail(BFS_E_UNSUPPORTED, "attn: the acquire form needs ACQK, ACQV and ACQS");
+  const int lin = acq_form ? 0 : 1;
+  bool ok = has_dep(p, lk, qk, 0) && has_dep(p, lv, pv, 0) && has_dep(p, qk, sm, 0) && has_dep(p, sm, pr, 0) &&
+            dep_form(qk, lk, nk, lin) && dep_form(pv, lv, nv, lin) && dep_form(pr, qk, 2, lin) &&
+            has_dep(p, sm, nm, 0) && has_dep(p, nm, sm, 2);
+  if (acq_form) ok = ok && dep_form(qk, ak, 1, 0) && dep_form(pv, av, 1, 0) && dep_form(pr, as, 1, 0);
+  if (!ok) return fail(BFS_E_UNSUPPORTED, "attn: missing a ring, S/P or row-sum dependency");
   if (nbufs < 5) return fail(BFS_E_INVALID, "attn: needs [work, Q, K, V, O]");
   for (int i = 0; i < 5; ++i)
     if (!bufs[i]) return fail(BFS_E_INVALID, "attn: null buffer");
@@ -565,7 +593,11 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
       !fill_waits(p, dw, sm, P.sm) || !fill_waits(p, dw, pr, P.pread) || !fill_waits(p, dw, pv, P.pv) ||
       !fill_waits(p, dw, nm, P.norm))
     return fail(BFS_E_RESOURCE, "attn: at most 4 waits per instruction");
-  if (!waits_fit({{&P.loadk, 2}, {&P.loadv, 2}, {&P.qk, 2}, {&P.sm, 2}, {&P.pread, 2}, {&P.pv, 2}, {&P.norm, 1}}))
+  P.acqk.update = P.acqv.update = P.acqs.update = -1;
+  if (acq_form && (!fill_waits(p, dw, ak, P.acqk) || !fill_waits(p, dw, av, P.acqv) || !fill_waits(p, dw, as, P.acqs)))
+    return fail(BFS_E_RESOURCE, "attn: at most 4 waits per instruction");
+  if (!waits_fit({{&P.loadk, 2}, {&P.loadv, 2}, {&P.qk, 2}, {&P.sm, 2}, {&P.pread, 2}, {&P.pv, 2}, {&P.norm, 1},
+                  {&P.acqk, 1}, {&P.acqv, 1}, {&P.acqs, 1}}))
     return fail(BFS_E_RESOURCE, "attn: more waits on an instruction than its engine loop takes");
   P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
   P.work = static_cast<const int32_t *>(bufs[0]);

@@ -17,7 +17,7 @@ from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER,
                                   BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import attn_program, attn_worklist  # noqa: E402
-from workloads.configs import ATTN_NK, ATTN_NV, ATTN_WG  # noqa: E402
+from workloads.configs import ATTN_LINEAR, ATTN_NK, ATTN_NV, ATTN_WG  # noqa: E402
 from workloads.tensors import attn_inputs, bf16_to_f32  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -42,8 +42,8 @@ def _dev16(bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
 
 
-def run_attn(ai, heads, mode, cap=0, nk=ATTN_NK, nv=ATTN_NV, alloc=ALLOC_PER_LOOP, n_wg=ATTN_WG):
-    prog = attn_program(heads, nk=nk, nv=nv)
+def run_attn(ai, heads, mode, cap=0, nk=ATTN_NK, nv=ATTN_NV, alloc=ALLOC_PER_LOOP, n_wg=ATTN_WG, linear=ATTN_LINEAR):
+    prog = attn_program(heads, nk=nk, nv=nv, linear=linear)
     plan = Plan(prog, mode, alloc)
     wl = attn_worklist(ai.lengths, heads, n_wg=n_wg)
     trips, toff = trip_tensors(wl.trips)
@@ -92,9 +92,9 @@ SMALL = [1, 64, 100, 129, 300]
 
 @pytest.mark.parametrize("rings,n_wg", [((3, 2), 3), ((2, 2), 3), ((2, 3), 3), ((3, 2), 64)])
 def test_attn_small_parity_and_thresholds(rings, n_wg):
-    """Three workgroups run all 16 tiles (several tiles each, so the rings,
-    S/P slots and row sums cross tile boundaries); 64 workgroups leave most
-    with one tile or none."""
+    """The linearized form: three workgroups run all 16 tiles (several tiles
+    each, so the rings, S/P slots and row sums cross tile boundaries); 64
+    workgroups leave most with one tile or none."""
     nk, nv = rings
     heads = 2
     ai = attn_inputs(seed=1, heads=heads, lengths=SMALL)
@@ -102,13 +102,38 @@ def test_attn_small_parity_and_thresholds(rings, n_wg):
     outs = {}
     for name, mode in MODES:
         _say(f"[attn-small] rings={rings} n_wg={n_wg} mode={name}")
-        prog, plan, wl, out, logw = run_attn(ai, heads, mode, cap=256, nk=nk, nv=nv, n_wg=n_wg)
+        prog, plan, wl, out, logw = run_attn(ai, heads, mode, cap=256, nk=nk, nv=nv, n_wg=n_wg, linear=True)
         check_close(out, ref)
         recs = oracle_recs(prog, wl)
         logs = log_records(plan, logw, wl.trips.n_wg, 256, per_wave=True)
         assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
         outs[name] = out
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+@pytest.mark.parametrize("rings,n_wg", [((2, 3), 3), ((3, 2), 3), ((2, 2), 64)])
+def test_attn_acquire_form_parity_and_thresholds(rings, n_wg):
+    """The paper's relation only: per-trip reuse dependencies and acquire
+    instructions at each tile (C3 drains of the previous tile's QK, PV and
+    PREAD).  Values against the oracle, every wave's thresholds equal to the
+    brute force of Eq. 1, both modes bit-identical, and equal to the
+    linearized form's output."""
+    nk, nv = rings
+    heads = 2
+    ai = attn_inputs(seed=5, heads=heads, lengths=SMALL)
+    ref = mathref.attention(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[attn-acq] rings={rings} n_wg={n_wg} mode={name}")
+        prog, plan, wl, out, logw = run_attn(ai, heads, mode, cap=256, nk=nk, nv=nv, n_wg=n_wg, linear=False)
+        check_close(out, ref)
+        recs = oracle_recs(prog, wl)
+        logs = log_records(plan, logw, wl.trips.n_wg, 256, per_wave=True)
+        assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+    _, _, _, lin, _ = run_attn(ai, heads, MODE_BARRIER_FREE, nk=nk, nv=nv, n_wg=n_wg, linear=True)
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), lin.view(np.uint32))
 
 
 def test_attn_per_instr():
@@ -157,17 +182,19 @@ def full_attn():
     return heads, ai, items, ref
 
 
-@pytest.mark.parametrize("rings", [(ATTN_NK, ATTN_NV), (3, 2)], ids=["bench", "k3v2"])
-def test_attn_full_size_sampled(full_attn, rings):
+@pytest.mark.parametrize("rings,linear", [((ATTN_NK, ATTN_NV), ATTN_LINEAR), ((ATTN_NK, ATTN_NV), not ATTN_LINEAR),
+                                         ((3, 2), ATTN_LINEAR)], ids=["bench", "bench_other_form", "k3v2"])
+def test_attn_full_size_sampled(full_attn, rings, linear):
     """The benchmark shape and launch (256 persistent workgroups, the
-    benchmark's K and V ring depths first, then the other layout), checked
-    on sampled rows one by one; both modes bit-identical."""
+    benchmark's K and V ring depths and its acquire form; then the
+    linearized form and the other ring layout), checked on sampled rows one
+    by one; both modes bit-identical."""
     heads, ai, items, ref = full_attn
     nk, nv = rings
     outs = {}
     for name, mode in MODES:
-        _say(f"[attn-full] rings={rings} mode={name}")
-        _, _, wl, out, _ = run_attn(ai, heads, mode, nk=nk, nv=nv)
+        _say(f"[attn-full] rings={rings} linear={linear} mode={name}")
+        _, _, wl, out, _ = run_attn(ai, heads, mode, nk=nk, nv=nv, linear=linear)
         assert wl.trips.n_wg == ATTN_WG
         got = np.array([out[ai.cu_seqlens[b] + i, h] for b, h, i in items])
         check_close(got, ref)
@@ -179,9 +206,19 @@ def test_attn_rejects_paper_relation_for_ring_reuse():
     """The kernel indexes the rings and S/P slots by r_KV over all tiles:
     a program whose reuse dependencies use the paper's per-trip relation
     would let a tile's first loads overwrite slots the previous tile still
-    reads, so the launcher refuses it."""
-    prog = attn_program(2)
+    reads unless acquires drain them, so the launcher refuses it without
+    the acquires (and refuses the acquire form with a drain missing)."""
+    prog = attn_program(2, linear=True)
     prog.dep_linear = [0] * len(prog.deps)
+    plan = Plan(prog)
+    t = torch.zeros(16, dtype=torch.int32, device="cuda")
+    with pytest.raises(BfsError) as e:
+        plan.run([t, t, t, t, t], t, t, 1)
+    assert e.value.status == bfs.E_UNSUPPORTED
+    prog = attn_program(2, linear=False)
+    keep = [i for i, d in enumerate(prog.deps) if prog.instrs[d[1]].name != "ACQV"]
+    prog.deps = [prog.deps[i] for i in keep]
+    prog.dep_linear = [prog.dep_linear[i] for i in keep]
     plan = Plan(prog)
     t = torch.zeros(16, dtype=torch.int32, device="cuda")
     with pytest.raises(BfsError) as e:

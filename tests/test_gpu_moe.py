@@ -213,11 +213,13 @@ def full_moe():
     return r, tokens, ref_y, rows, ref_h
 
 
-@pytest.mark.parametrize("mchunk,linear", [(MOE_MCHUNK, MOE_LINEAR), (8, False)], ids=["bench", "m8_acq"])
+@pytest.mark.parametrize("mchunk,linear", [(MOE_MCHUNK, MOE_LINEAR), (MOE_MCHUNK, not MOE_LINEAR), (8, MOE_LINEAR)],
+                         ids=["bench", "bench_other_form", "m8"])
 def test_moe_full_size_sampled(full_moe, mchunk, linear):
     """The benchmark shape and launch (runs of at most four M-tiles, the
-    linearized ring, as timed), then runs of eight with the paper's ACQL
-    drain; sampled y tokens and h rows one by one; both modes bit-identical."""
+    paper's ACQL drain, as timed), then the linearized ring, then runs of
+    eight; sampled y tokens and h rows one by one; both modes
+    bit-identical."""
     r, tokens, ref_y, rows, ref_h = full_moe
     r.set_mchunk(mchunk)
     outs = {}

@@ -247,13 +247,19 @@ def test_fused_family_formulas():
     fg = {(g.instrs[p].name, g.instrs[c].name): f for (p, c, k), f in zip(g.deps, Plan(g).formulas())}
     assert fg[("MMA", "LOAD")]["kase"] == 1 and fg[("MMA", "LOAD")]["k"] == 4 and not fg[("MMA", "LOAD")]["forward"]
     assert fg[("MMA", "SPILL")]["kase"] == 2 and fg[("BIAS", "SPILL")]["kase"] == 1
-    a = attn_program(16, nk=3, nv=2)
-    fa = {(a.instrs[p].name, a.instrs[c].name): f for (p, c, k), f in zip(a.deps, Plan(a).formulas())}
-    assert fa[("QK", "LOADK")]["k"] == 3 and fa[("PV", "LOADV")]["k"] == 2 and fa[("PREAD", "QK")]["k"] == 2
-    assert all(fa[x]["kase"] == 1 for x in [("LOADK", "QK"), ("QK", "SM"), ("SM", "PREAD"), ("LOADV", "PV")])
-    assert all(fa[x]["kase"] == 6 for x in [("QK", "LOADK"), ("PV", "LOADV"), ("PREAD", "QK")])
-    assert fa[("SM", "NORM")]["kase"] == 2
-    assert fa[("NORM", "SM")]["kase"] == 1 and fa[("NORM", "SM")]["loop_S"] == a.loop_id("T")
+    for linear in (True, False):
+        a = attn_program(16, nk=3, nv=2, linear=linear)
+        fa = {(a.instrs[p].name, a.instrs[c].name): f for (p, c, k), f in zip(a.deps, Plan(a).formulas())}
+        assert fa[("QK", "LOADK")]["k"] == 3 and fa[("PV", "LOADV")]["k"] == 2 and fa[("PREAD", "QK")]["k"] == 2
+        assert all(fa[x]["kase"] == 1 for x in [("LOADK", "QK"), ("QK", "SM"), ("SM", "PREAD"), ("LOADV", "PV")])
+        reuse = [("QK", "LOADK"), ("PV", "LOADV"), ("PREAD", "QK")]
+        assert all(fa[x]["kase"] == (6 if linear else 1) for x in reuse)
+        if not linear:
+            # the acquires drain the previous tile: C3 at T, offset 1
+            for x in [("QK", "ACQK"), ("PV", "ACQV"), ("PREAD", "ACQS")]:
+                assert fa[x]["kase"] == 3 and fa[x]["k"] == 1 and fa[x]["loop_S"] == a.loop_id("T")
+        assert fa[("SM", "NORM")]["kase"] == 2
+        assert fa[("NORM", "SM")]["kase"] == 1 and fa[("NORM", "SM")]["loop_S"] == a.loop_id("T")
     # the work list covers every (sequence, head, query tile) once; tile j of
     # workgroup w sits at row w + j * n_wg, on w's XCD (w % 8) with every
     # tile of its (sequence, head)

@@ -552,9 +552,11 @@ ATTN_D = 128        # head dimension
 ATTN_SP = 2         # S/P buffer slots
 ATTN_NK = 2         # K ring slots of the benchmark layout
 ATTN_NV = 3         # V ring slots of the benchmark layout (2 + 3 measured 2 % faster than 3 + 2)
+ATTN_LINEAR = False # benchmark form: the paper's relation with acquires at each tile (True: linearized reuse)
 
 
-def attn_program(heads: int, dim: int = ATTN_D, nk: int = ATTN_NK, nv: int = ATTN_NV) -> Program:
+def attn_program(heads: int, dim: int = ATTN_D, nk: int = ATTN_NK, nv: int = ATTN_NV,
+                 linear: bool = ATTN_LINEAR) -> Program:
     """A fixed set of workgroups, each running a run-time list of (sequence,
     head, 128-query tile) work items:
 
@@ -576,9 +578,19 @@ def attn_program(heads: int, dim: int = ATTN_D, nk: int = ATTN_NK, nv: int = ATT
     end of the previous tile.  SM->NORM (k=0, C2) delivers a tile's final
     row sums; they are double-buffered by tile, and NORM->SM (k=2, C1 at T)
     keeps a tile's softmax from overwriting a buffer before NORM of the tile
-    before last has read it."""
+    before last has read it.
+
+    ``linear=False`` uses the paper's relation only: the three reuse
+    dependencies are read per trip of KV, and acquire instructions at each
+    tile (ACQK on E0, ACQV on E4, ACQS on E1, before the KV loop) with
+    QK->ACQK, PV->ACQV, PREAD->ACQS (k=1, C3 at T) drain the previous tile's
+    reads of the rings and S/P slots before the next tile refills them."""
     b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 4, 4, 1])
     with b.loop("T"):
+        if not linear:
+            b.instr(0, OP_NOP, [0] * 8, name="ACQK")
+            b.instr(4, OP_NOP, [0] * 8, name="ACQV")
+            b.instr(1, OP_NOP, [0] * 8, name="ACQS")
         with b.loop("KV"):
             b.instr(0, OP_ATTN_LOAD, [0, nk, heads, dim, 0, 0, 0, 0], name="LOADK")
             b.instr(4, OP_ATTN_LOAD, [1, nv, heads, dim, 0, 0, 0, 0], name="LOADV")
@@ -591,9 +603,13 @@ def attn_program(heads: int, dim: int = ATTN_D, nk: int = ATTN_NK, nv: int = ATT
     b.dep("LOADV", "PV", 0)
     b.dep("QK", "SM", 0)
     b.dep("SM", "PREAD", 0)
-    b.dep("QK", "LOADK", nk, linear=True)
-    b.dep("PV", "LOADV", nv, linear=True)
-    b.dep("PREAD", "QK", ATTN_SP, linear=True)
+    b.dep("QK", "LOADK", nk, linear=linear)
+    b.dep("PV", "LOADV", nv, linear=linear)
+    b.dep("PREAD", "QK", ATTN_SP, linear=linear)
+    if not linear:
+        b.dep("QK", "ACQK", 1)
+        b.dep("PV", "ACQV", 1)
+        b.dep("PREAD", "ACQS", 1)
     b.dep("SM", "NORM", 0)
     b.dep("NORM", "SM", 2)
     return b.build()
@@ -667,12 +683,12 @@ MOE_BN = {1: 128, 2: 256}    # output columns per workgroup: h columns (phase 1)
 MOE_CHUNKS = {1: 2, 2: 4}    # epilogue chunks per M-tile
 MOE_RING = 5
 MOE_MCHUNK = 4               # at most this many M-tiles per workgroup
-MOE_LINEAR = True            # benchmark ring form: the linearized MMA->LOAD dependency (extension);
-                             # False selects the paper's ACQL drain at every M-tile
+MOE_LINEAR = False           # benchmark ring form: the paper's ACQL drain at every M-tile;
+                             # True selects the linearized MMA->LOAD dependency (extension)
 
 
 def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring: int = 2,
-                linear: bool = False) -> Program:
+                linear: bool = MOE_LINEAR) -> Program:
     """One workgroup per (expert, N-tile, run of M-tiles); phase 1 computes
     h = SiLU(x W_gate) * (x W_up) for 128 h columns, phase 2 y = h W_down for
     256 y columns:
