@@ -164,6 +164,10 @@ def parse():
     ap.add_argument("--adam-chunk", type=int, default=1024, help="adamw: parameters per chunk (256, 512, 1024)")
     ap.add_argument("--adam-waves", type=int, default=2, help="adamw: vector-engine waves")
     ap.add_argument("--adam-ring", type=int, default=2, help="adamw: ring slots")
+    ap.add_argument("--moe-bm", type=int, default=0, choices=[0, 128, 256],
+                    help="moe: token rows per M-tile (0: the library default)")
+    ap.add_argument("--moe-mchunk", type=int, default=0,
+                    help="moe: at most this many M-tiles per workgroup (0: the default for the tile height)")
     ap.add_argument("--rms-wg", type=int, default=768, help="rmsnorm: workgroups (3 per CU)")
     ap.add_argument("--rms-waves", type=int, default=4, help="rmsnorm: vector-engine waves sharing each row")
     ap.add_argument("--rms-ring", default="2,2", help="rmsnorm: x-ring and q-ring slots")
@@ -457,11 +461,13 @@ def bench_moe(a):
     import torch
     from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
     from workloads import moe_program, moe_worklist
-    from workloads.configs import MOE_MCHUNK, MOE_RING
+    from workloads.configs import MOE_BM, MOE_MCHUNKS, MOE_RINGS
     from workloads.tensors import moe_inputs, moe_weights_all
 
     moe = moe_inputs(seed=a.seed)
     H, F = moe.hidden, moe.ffn
+    bm = a.moe_bm or MOE_BM
+    mchunk = a.moe_mchunk or MOE_MCHUNKS[bm]
     cpu = None
     if not a.no_cpu_baseline:
         from oracle import mathref
@@ -488,7 +494,7 @@ def bench_moe(a):
     y = torch.empty((T, H), dtype=torch.int16, device="cuda")
     launches = {}
     for ph in (1, 2):
-        wl = moe_worklist(moe.counts, ph, H, F)
+        wl = moe_worklist(moe.counts, ph, H, F, bm=bm, mchunk=mchunk)
         t_np, o_np = wl.trips.flat()
         work = torch.from_numpy(wl.work.reshape(-1)).cuda()
         bufs = [work, perm, eoff, x, wg, wu, h] if ph == 1 else [work, perm, eoff, h, wd, y]
@@ -500,7 +506,8 @@ def bench_moe(a):
     # offset across M-tiles (an extension)
     for name in a.modes.split(","):
         mode = MODE_BARRIER_FREE if name.startswith("barrier_free") else MODE_BARRIER
-        plans = {ph: Plan(moe_program(ph, H, F, linear=name == "barrier_free_linearized"), mode, alloc_of(a, mode))
+        plans = {ph: Plan(moe_program(ph, H, F, linear=name == "barrier_free_linearized", bm=bm), mode,
+                          alloc_of(a, mode))
                  for ph in (1, 2)}
         h.fill_(-1)
         y.fill_(-1)
@@ -553,8 +560,8 @@ def bench_moe(a):
                    "tokens": T, "experts": len(c), "hidden": H, "ffn": F,
                    "ring_across_m_tiles": "barrier_free: ACQL drain (paper's relation); "
                                           "barrier_free_linearized: linearized MMA->LOAD (extension)",
-                   "m_tiles_per_workgroup_run": MOE_MCHUNK,
-                   "ring_slots": MOE_RING, "n_wg": [launches[1][3], launches[2][3]], "parallelism": "single GPU"},
+                   "m_tile_rows": bm, "m_tiles_per_workgroup_run": mchunk,
+                   "ring_slots": MOE_RINGS[bm][0], "epilogue_slots": MOE_RINGS[bm][1], "n_wg": [launches[1][3], launches[2][3]], "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
         "phase_us": {kk: [v["phase1_ms"] * 1e3, v["phase2_ms"] * 1e3] for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",

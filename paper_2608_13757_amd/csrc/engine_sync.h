@@ -285,6 +285,30 @@ struct Sync {
     }
   }
 
+  // The waits of a site whose waits are all affine (the host checked that
+  // each producer and shared loop is the consumer's innermost loop): the
+  // threshold is base + N * t under the mask t > k, evaluated without the
+  // per-kind dispatch of wait().  Barrier mode and instrumented builds take
+  // wait().
+  template <int kN, class OnBlock>
+  __device__ __forceinline__ void wait_affine(Site<kN> &s, const InstrWaits &iw, const Regs &g, uint32_t t,
+                                              uint32_t instance, OnBlock on_block) {
+    if constexpr (kMode == BFS_MODE_BARRIER || kInstr) {
+      wait(s, iw, g, t, instance, on_block);
+    } else {
+#pragma unroll
+      for (int j = 0; j < kN; ++j) {
+        if ((uint32_t)j < s.n) {
+          const int32_t v = s.base[j] + (int32_t)((s.mk[j] >> 16) * t);
+          const uint32_t thr = (t > (s.mk[j] & 0xffffu) && v > 0) ? (uint32_t)v : 0u;
+          if (!aborted && thr > s.seen[j])
+            s.seen[j] = poll_geq(s.meta[j] & 0xffffu, (s.meta[j] >> 16) & 0xfu, thr, iw.w[j].w.w3 & 0xffffu,
+                                 instance, on_block);
+        }
+      }
+    }
+  }
+
   // One wait whose threshold is a static immediate (straight-line code with
   // no loop register, e.g. an unrolled loop): counter slot `slot` of a
   // producer engine of `nw` waves; `seen` is the caller's monotone cache.
@@ -380,6 +404,14 @@ inline bool has_dep(const bfs_plan *p, int prd, int cns, int k) {
   for (size_t d = 0; d < p->deps.size() / 3; ++d)
     if (p->deps[3 * d] == prd && p->deps[3 * d + 1] == cns && p->deps[3 * d + 2] == k) return true;
   return false;
+}
+
+// Host: every wait of the instruction is affine in its innermost loop's
+// iteration (Sync::wait_affine may serve it).
+inline bool all_affine(const bfsdev::InstrWaits &iw) {
+  for (int j = 0; j < iw.n; ++j)
+    if (iw.w[j].kind != bfsdev::kWaitAffine) return false;
+  return true;
 }
 
 // Host: every instruction's wait count fits its kernel call site.

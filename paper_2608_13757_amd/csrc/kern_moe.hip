@@ -1,5 +1,6 @@
 // MoE grouped GEMM with top-1 routing, two launches per layer, three engines
-// per workgroup, one workgroup per (expert, N-tile, run of 128-token M-tiles):
+// per workgroup, one workgroup per (expert, N-tile, run of M-tiles of BM token
+// rows, BM = 128 or 256):
 //
 //   phase 1  h[rows of expert e][n0 .. n0 + 127] = SiLU(x W_gate) * (x W_up),
 //            token rows gathered from x through the expert-grouped
@@ -7,11 +8,11 @@
 //   phase 2  y[token][n0 .. n0 + 255] = h W_down, rows scattered back to
 //            their tokens.
 //
-//   E0 (2 waves, load)      ACQL at each M-tile; LOAD: the step's 128 token
+//   E0 (2 waves, load)      ACQL at each M-tile; LOAD: the step's BM token
 //                           rows (wave 0) and 256 weight rows (wave 1), 32
 //                           wide in K, into a ring slot with direct-to-LDS
 //                           loads.
-//   E1 (8 waves, MFMA)      MMA: a 64-row sub-tile per wave, fp32
+//   E1 (8 waves, MFMA)      MMA: a BM / 2-row sub-tile per wave, fp32
 //                           accumulators (phase 1: gate and up for 32 h
 //                           columns, so SiLU(g) * u needs no exchange;
 //                           phase 2: 64 y columns); ACQE at each M-tile;
@@ -20,8 +21,8 @@
 //   E2 (2 waves, epilogue)  EPI: 16-byte row segments of the chunk to HBM.
 //
 // The M loop runs the workgroup's M-tiles, a count derived from the routing
-// and known only at run time; K runs K / 32 steps, C 2 (phase 1) or 4
-// (phase 2) chunks per M-tile.  Dependencies: LOAD->MMA (k = 0), MMA->LOAD
+// and known only at run time; K runs K / 32 steps, C BM / 64 (phase 1) or
+// BM / 32 (phase 2) chunks per M-tile.  Dependencies: LOAD->MMA (k = 0), MMA->LOAD
 // (k = ring), MMA->ACQL (k = 1, C3: an M-tile's loads start after the
 // previous tile's MFMAs released the ring), SPILL->EPI (k = 0), EPI->SPILL
 // (k = epilogue slots), EPI->ACQE (k = 1, C3).  In place of MMA->ACQL the
@@ -32,12 +33,13 @@
 // MFMAs; ACQL then waits for nothing.  Token rows past the expert's
 // count are loaded from a clamped row and never stored.
 //
-// LDS (bytes): counters 2048 | ring slots of 24 KiB (token rows 128 x 64 B,
-// then weight rows 256 x 64 B; 16-byte chunk c of row r at c ^ ((r / 4) % 4))
+// LDS (bytes): counters 2048 | ring slots of BM x 64 + 16 KiB (token rows
+// BM x 64 B, then weight rows 256 x 64 B; 16-byte chunk c of row r at
+// c ^ ((r / 4) % 4))
 // | epilogue slots of 16 KiB (8 blocks of 32 x 32 bf16, row-major).
 //
 // Family contract (BFS_KERNEL_MOE): loops top -> M -> {K, C}; ACQL (E0, NOP)
-// at M before K; LOAD (E0, opcode 48, args [phase, K, N, ring]) and MMA (E1,
+// at M before K; LOAD (E0, opcode 48, args [phase, K, N, ring, BM (0: 128)]) and MMA (E1,
 // 49) in K; ACQE (E1, NOP) at M between K and C; SPILL (E1, 51, args
 // [epilogue ring]) and EPI (E2, 50) in C; waves 2, 8, 2.  Phase 1: K = hidden
 // (multiple of 32), N = ffn (multiple of 128); phase 2: K = ffn (multiple of
@@ -48,6 +50,7 @@
 // [experts][ffn][hidden], [6] h bf16 [tokens][ffn]; phase 2: [3] h, [4]
 // W_down bf16 [experts][hidden][ffn], [5] y bf16 [tokens][hidden].
 #include <string>
+#include <type_traits>
 
 #include "engine_sync.h"
 
@@ -55,10 +58,12 @@ using namespace bfsdev;
 
 namespace {
 
-constexpr int kBM = 128, kBK = 32;
+constexpr int kBK = 32;
 constexpr int kLoadW = 2, kMmaW = 8, kEpiW = 2, kWaves = 12;
-constexpr uint32_t kASlot = kBM * kBK * 2;          // 8 KiB of token rows
-constexpr uint32_t kSlotBytes = kASlot + 256 * kBK * 2;
+// ring slot: the token rows of one K step (8 KiB for M-tiles of 128 rows,
+// 16 KiB for 256), then 256 weight rows (16 KiB)
+constexpr uint32_t a_slot_bytes(int bm) { return (uint32_t)bm * kBK * 2; }
+constexpr uint32_t slot_bytes(int bm) { return a_slot_bytes(bm) + 256 * kBK * 2; }
 constexpr uint32_t kESlotBytes = kMmaW * 32 * 32 * 2;
 
 struct MoeParams {
@@ -82,8 +87,14 @@ __device__ __forceinline__ uint32_t swz(uint32_t row, uint32_t chunk) {
 
 __device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
-template <int kPhase, int kMode, bool kInstr>
+// kBM: token rows per M-tile.  128: each MFMA wave holds a 64-row sub-tile
+// (two row blocks); 256: a 128-row sub-tile (four row blocks), twice the MFMA
+// work per K step and per synchronization, half the weight re-reads.
+template <int kPhase, int kMode, bool kInstr, int kBM>
 __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
+  constexpr uint32_t kASlot = a_slot_bytes(kBM), kSlotBytes = slot_bytes(kBM);
+  constexpr int kRB = kBM / 64;                     // 32-row blocks per MFMA wave
+  constexpr uint32_t kChunks = kPhase == 1 ? (uint32_t)kRB : 2u * kRB;
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
   const uint32_t ring = lds_addr(lds) + kCntBytes;
@@ -102,20 +113,21 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
   const int64_t *toff = P.trip_off + (int64_t)wg * 4;
   uint32_t trip_m = (uint32_t)ldc(P.trips + ldc(toff + 1));
   const int64_t k_off = ldc(toff + 2), c_off = ldc(toff + 3);
-  const uint32_t ksteps = (uint32_t)(P.kdim / kBK), chunks = kPhase == 1 ? 2u : 4u;
+  const uint32_t ksteps = (uint32_t)(P.kdim / kBK), chunks = kChunks;
   const uint32_t max_m = (uint32_t)max(0, (e_cnt + kBM - 1) / kBM - mt0);
   if (trip_m > max_m) {
     report_input(P.sc.err, 1u, (uint32_t)wg, 1u, trip_m, max_m, (uint32_t)wave);
     trip_m = max_m;
   }
   Regs g;
-  Site<2> sa, sb, sc;               // one per wait site of the engine
+  Site<1> sa, sb, sc;               // one per wait site of the engine (each has one wait)
   uint64_t mark = 0;
 
   if (wave < kLoadW) {
     // ------------------------------------------------------------ load engine
     const uint32_t ew = (uint32_t)wave;
-    const int per_group = wave == 0 ? 8 : 16;                 // loads per step
+    constexpr int kALoads = kBM / 16;                          // token-row loads per step (16 rows each)
+    const int per_group = wave == 0 ? kALoads : 16;           // loads per step
     int pending = 0;
     auto retire_one = [&]() {
       if (pending == 3) {
@@ -161,7 +173,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
       uint32_t voff[16];
       if (wave == 0) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < kALoads; ++j) {
           const int32_t r = min(m0 + 16 * j + (int32_t)r_in, e_cnt - 1);
           const int32_t row = kPhase == 1 ? P.perm[e_lo + r] : e_lo + r;
           const uint64_t off = ((uint64_t)(uint32_t)row * (uint32_t)P.kdim + 8u * chunk) * 2u;
@@ -172,7 +184,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
           voff[j] = (uint32_t)off;
         }
 #pragma unroll
-        for (int j = 8; j < 16; ++j) voff[j] = 0u;
+        for (int j = kALoads; j < 16; ++j) voff[j] = 0u;
         wait_vm<0>();
       } else {
 #pragma unroll
@@ -188,14 +200,14 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
       for (uint32_t it = 0; it < ksteps; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
         g.r2 += 1;
         g.h2 = it + 1;
-        S.wait(sb, P.load, g, it + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
+        S.wait_affine(sb, P.load, g, it + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
         if (!S.aborted) {
           const uint32_t dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kASlot);
           const size_t kb = (size_t)it * (kBK * 2);
           if (wave == 0) {
             const char *sb = reinterpret_cast<const char *>(P.a) + kb;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
+            for (int j = 0; j < kALoads; ++j) {
               asm volatile("" : "+v"(voff[j]));   // keep the offset a 32-bit value at its use
               __builtin_amdgcn_global_load_lds((const void *)(sb + voff[j]), (BFS_LDS void *)(uintptr_t)(dst + 1024u * j),
                                                16, 0, 0);
@@ -235,46 +247,91 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
     // ------------------------------------------------------------ MFMA engine
     const uint32_t ew = (uint32_t)(wave - kLoadW);
     const uint32_t wm = ew >> 2, wn = ew & 3u;
-    const uint32_t arow = wm * 64u + l32;
+    const uint32_t arow = wm * (uint32_t)(kBM / 2) + l32;
     // weight rows of the two column blocks of this wave
     const uint32_t brow0 = kPhase == 1 ? 32u * wn + l32 : 64u * wn + l32;
     const uint32_t brow1 = kPhase == 1 ? 128u + 32u * wn + l32 : 64u * wn + 32u + l32;
+    // swizzled byte offsets of this lane's 16-byte chunk in k-half 0 and 1;
+    // row blocks 32 rows apart are 2048 bytes apart with the same swizzle,
+    // and brow1 lies b_step bytes after brow0 (a multiple of 16 rows)
+    const uint32_t a_off[2] = {swz(arow, lhi), swz(arow, 2u + lhi)};
+    const uint32_t b_off[2] = {swz(brow0, lhi), swz(brow0, 2u + lhi)};
+    constexpr uint32_t b_step = kPhase == 1 ? 128u * 64u : 32u * 64u;
+    auto rd_at = [](uint32_t addr, uint32_t imm) {
+      return __builtin_bit_cast(bf16x8, *(const BFS_LDS u32x4 *)(uintptr_t)(addr + imm));
+    };
     S.sync_point(S.word(1, ew));                                  // before loop M
     S.enter(sb, P.acqe, g, 1);
     for (uint32_t mi = 0; mi < trip_m; ++mi) {
       g.r1 += 1;
       g.h1 = mi + 1;
-      f32x16 acc[4];                 // [b * 2 + rb]: b = weight block (gate / up, or column block)
+      f32x16 acc[2 * kRB];           // [b * kRB + rb]: b = weight block (gate / up, or column block), rb = row block
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[i] = f32x16{};
+      for (int i = 0; i < 2 * kRB; ++i) acc[i] = f32x16{};
       S.sync_point(S.word(1, ew));                                // before loop K
       S.enter(sa, P.mma, g, 2);
       uint32_t slot = g.r2 % (uint32_t)P.ring;
       for (uint32_t it = 0; it < ksteps; ++it, slot = (slot + 1 == (uint32_t)P.ring) ? 0u : slot + 1) {
         g.r2 += 1;
         g.h2 = it + 1;
-        S.wait(sa, P.mma, g, it + 1, g.r2 - 1, [] {});
+        S.wait_affine(sa, P.mma, g, it + 1, g.r2 - 1, [] {});
         if (!S.aborted) {
           const uint32_t a_base = ring + slot * kSlotBytes, b_base = a_base + kASlot;
           auto rd = [&](uint32_t base, uint32_t row, uint32_t c) {
             return __builtin_bit_cast(bf16x8, *(const BFS_LDS u32x4 *)(uintptr_t)(base + swz(row, c)));
           };
-          bf16x8 a0 = rd(a_base, arow, lhi), a1 = rd(a_base, arow + 32u, lhi);
-          bf16x8 b0 = rd(b_base, brow0, lhi), b1 = rd(b_base, brow1, lhi);
-          const bf16x8 a0n = rd(a_base, arow, 2u + lhi), a1n = rd(a_base, arow + 32u, 2u + lhi);
-          const bf16x8 b0n = rd(b_base, brow0, 2u + lhi), b1n = rd(b_base, brow1, 2u + lhi);
-          // MMA retires from the slot once its fragments are read: LDS
-          // executes this wave's reads before the signal that follows them,
-          // and the MFMAs below use registers only
-          S.signal(P.mma.update, ew);
-          acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a0, acc[0], 0, 0, 0);
-          acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a1, acc[1], 0, 0, 0);
-          acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a0, acc[2], 0, 0, 0);
-          acc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a1, acc[3], 0, 0, 0);
-          acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0n, a0n, acc[0], 0, 0, 0);
-          acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0n, a1n, acc[1], 0, 0, 0);
-          acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a0n, acc[2], 0, 0, 0);
-          acc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a1n, acc[3], 0, 0, 0);
+          if constexpr (kBM == 128) {
+            bf16x8 a0 = rd(a_base, arow, lhi), a1 = rd(a_base, arow + 32u, lhi);
+            bf16x8 b0 = rd(b_base, brow0, lhi), b1 = rd(b_base, brow1, lhi);
+            const bf16x8 a0n = rd(a_base, arow, 2u + lhi), a1n = rd(a_base, arow + 32u, 2u + lhi);
+            const bf16x8 b0n = rd(b_base, brow0, 2u + lhi), b1n = rd(b_base, brow1, 2u + lhi);
+            // MMA retires from the slot once its fragments are read: LDS
+            // executes this wave's reads before the signal that follows them,
+            // and the MFMAs below use registers only
+            S.signal(P.mma.update, ew);
+            acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a0, acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a1, acc[1], 0, 0, 0);
+            acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a0, acc[2], 0, 0, 0);
+            acc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a1, acc[3], 0, 0, 0);
+            acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0n, a0n, acc[0], 0, 0, 0);
+            acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0n, a1n, acc[1], 0, 0, 0);
+            acc[2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a0n, acc[2], 0, 0, 0);
+            acc[3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1n, a1n, acc[3], 0, 0, 0);
+          } else {
+            // four row blocks, fragments of one k-half (4 A, 2 B) in
+            // registers: each A fragment is refilled with the next k-half's
+            // as soon as its two MFMAs are issued, the B pair after the last
+            // row block, so the second k-half's LDS reads run under the
+            // first k-half's MFMAs; the scheduling barriers keep the compiler
+            // from hoisting the refills (which would need a second set of
+            // registers) or sinking them behind waits
+            const uint32_t a_lo = a_base + a_off[0], a_hi = a_base + a_off[1];
+            const uint32_t b_lo = b_base + b_off[0], b_hi = b_base + b_off[1];
+            bf16x8 fa[kRB], fb0, fb1;
+            fb0 = rd_at(b_lo, 0u);
+            fb1 = rd_at(b_lo, b_step);
+#pragma unroll
+            for (int rb = 0; rb < kRB; ++rb) fa[rb] = rd_at(a_lo, 2048u * rb);
+#pragma unroll
+            for (int hk = 0; hk < 2; ++hk) {
+#pragma unroll
+              for (int rb = 0; rb < kRB; ++rb) {
+                acc[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb0, fa[rb], acc[rb], 0, 0, 0);
+                acc[kRB + rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb1, fa[rb], acc[kRB + rb], 0, 0, 0);
+                if (hk == 0) {
+                  fa[rb] = rd_at(a_hi, 2048u * rb);
+                  if (rb == kRB - 1) {
+                    fb0 = rd_at(b_hi, 0u);
+                    fb1 = rd_at(b_hi, b_step);
+                  }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+              }
+              // every fragment read of the step is issued: MMA retires from
+              // the slot (LDS executes the reads before the signal)
+              if (hk == 0) S.signal(P.mma.update, ew);
+            }
+          }
         } else {
           S.signal(P.mma.update, ew);
         }
@@ -286,11 +343,10 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
       S.sync_point(S.word(1, ew));                                // before loop C
       S.enter(sc, P.spill, g, 3);
 #pragma unroll
-      for (uint32_t c = 0; c < 4; ++c) {
-        if (c >= chunks) break;
+      for (uint32_t c = 0; c < kChunks; ++c) {
         g.r3 += 1;
         g.h3 = c + 1;
-        S.wait(sc, P.spill, g, c + 1, g.r3 - 1, [] {});
+        S.wait_affine(sc, P.spill, g, c + 1, g.r3 - 1, [] {});
         if (!S.aborted) {
           const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
           const uint32_t blk = ering + eslot * kESlotBytes + ew * 2048u;
@@ -299,8 +355,8 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
             float v[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              if (kPhase == 1) v[e] = silu(acc[c][4 * j + e]) * acc[2 + c][4 * j + e];   // chunk = row block
-              else v[e] = acc[(c & 1u) * 2 + (c >> 1)][4 * j + e];                        // chunk = rb * 2 + cb
+              if (kPhase == 1) v[e] = silu(acc[c][4 * j + e]) * acc[kRB + c][4 * j + e];   // chunk = row block
+              else v[e] = acc[(c & 1u) * kRB + (c >> 1)][4 * j + e];                      // chunk = rb * 2 + cb
             }
             const u32x2 q = {__builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{v[0], v[1]}, bf16x2)),
                              __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{v[2], v[3]}, bf16x2))};
@@ -321,13 +377,13 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
       g.h1 = mi + 1;
       const int32_t m0 = (mt0 + (int32_t)mi) * kBM;
       // this wave stores the blocks of MFMA waves 4 ew .. 4 ew + 3 (rows
-      // 64 ew ..), lane rows 16 h + lane / 4 of each 32-row block
-      int32_t tok[2][2];
+      // kBM / 2 * ew ..), lane rows 16 h + lane / 4 of each 32-row block
+      int32_t tok[kRB][2];
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
+      for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int32_t r = m0 + 64 * (int32_t)ew + 32 * rb + 16 * h + (int32_t)(lane >> 2);
+          const int32_t r = m0 + (kBM / 2) * (int32_t)ew + 32 * rb + 16 * h + (int32_t)(lane >> 2);
           tok[rb][h] = r < e_cnt ? (kPhase == 1 ? e_lo + r : P.perm[e_lo + r]) : -1;
         }
       S.sync_point(S.word(2, ew));                                // before loop K
@@ -341,7 +397,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
       for (uint32_t c = 0; c < chunks; ++c) {
         g.r3 += 1;
         g.h3 = c + 1;
-        S.wait(sa, P.epi, g, c + 1, g.r3 - 1, [] {});
+        S.wait_affine(sa, P.epi, g, c + 1, g.r3 - 1, [] {});
         if (!S.aborted) {
           const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
           const uint32_t rb = kPhase == 1 ? c : (c >> 1), cb = kPhase == 1 ? 0u : (c & 1u);
@@ -353,7 +409,9 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
             for (int h = 0; h < 2; ++h) {
               const uint32_t row = 16u * h + (lane >> 2), cc = lane & 3u;
               const u32x4 d = *(const BFS_LDS u32x4 *)(uintptr_t)(blk + row * 64u + cc * 16u);
-              const int32_t t = rb == 0 ? tok[0][h] : tok[1][h];
+              int32_t t = tok[0][h];                        // tok[rb][h] without dynamic indexing
+#pragma unroll
+              for (int i = 1; i < kRB; ++i) t = rb == (uint32_t)i ? tok[i][h] : t;
               const uint32_t col = kPhase == 1 ? (n0 + 32u * q + 8u * cc) : (n0 + 64u * q + 32u * cb + 8u * cc);
               if (t >= 0) {
                 u32x4 *dst = reinterpret_cast<u32x4 *>(P.out + (size_t)t * P.ndim + col);
@@ -400,13 +458,15 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   if (acql < 0 || load < 0 || mma < 0 || acqe < 0 || spill < 0 || epi < 0)
     return fail(BFS_E_UNSUPPORTED, "moe: needs ACQL, LOAD, MMA, ACQE, SPILL and EPI");
   const int32_t *la = &p->instr_args[8 * load];
-  const int phase = la[0], K = la[1], N = la[2], ring = la[3];
+  const int phase = la[0], K = la[1], N = la[2], ring = la[3], bm = la[4] == 0 ? 128 : la[4];
   const int e_ring = p->instr_args[8 * spill];
+  if (bm != 128 && bm != 256) return fail(BFS_E_UNSUPPORTED, "moe: M-tiles of 128 or 256 token rows");
   if (phase != 1 && phase != 2) return fail(BFS_E_UNSUPPORTED, "moe: phase 1 or 2");
   if (K <= 0 || K % kBK || N <= 0 || N % (phase == 1 ? 128 : 256))
     return fail(BFS_E_UNSUPPORTED, "moe: K a multiple of 32, N a multiple of 128 (phase 1) or 256 (phase 2)");
   if (ring < 2 || ring > 5 || e_ring < 1 || e_ring > 2) return fail(BFS_E_UNSUPPORTED, "moe: ring 2..5, epilogue 1..2");
-  if (kCntBytes + (size_t)ring * kSlotBytes + (size_t)e_ring * kESlotBytes > 160 * 1024)
+  const size_t lds = kCntBytes + (size_t)ring * slot_bytes(bm) + (size_t)e_ring * kESlotBytes;
+  if (lds > 160 * 1024)
     return fail(BFS_E_RESOURCE, "moe: ring and epilogue slots exceed 160 KiB of LDS");
   if ((uint64_t)N * K * 2 > 0xffffffffull) return fail(BFS_E_UNSUPPORTED, "moe: one expert's matrix must stay below 4 GiB");
   // the ring is protected across M-tiles either by MMA->ACQL (k = 1) or by
@@ -428,8 +488,11 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   if (!fill_waits(p, dw, acql, P.acql) || !fill_waits(p, dw, load, P.load) || !fill_waits(p, dw, mma, P.mma) ||
       !fill_waits(p, dw, acqe, P.acqe) || !fill_waits(p, dw, spill, P.spill) || !fill_waits(p, dw, epi, P.epi))
     return fail(BFS_E_RESOURCE, "moe: at most 4 waits per instruction");
-  if (!waits_fit({{&P.acql, 2}, {&P.load, 2}, {&P.mma, 2}, {&P.acqe, 2}, {&P.spill, 2}, {&P.epi, 2}}))
+  if (!waits_fit({{&P.acql, 1}, {&P.load, 1}, {&P.mma, 1}, {&P.acqe, 1}, {&P.spill, 1}, {&P.epi, 1}}))
     return fail(BFS_E_RESOURCE, "moe: more waits on an instruction than its engine loop takes");
+  if (p->mode == BFS_MODE_BARRIER_FREE &&
+      (!all_affine(P.load) || !all_affine(P.mma) || !all_affine(P.spill) || !all_affine(P.epi)))
+    return fail(BFS_E_UNSUPPORTED, "moe: K- and C-loop waits must have their producer in the same loop");
   P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
   P.work = static_cast<const int32_t *>(bufs[0]);
   P.perm = static_cast<const int32_t *>(bufs[1]);
@@ -444,7 +507,6 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   P.ndim = N;
   P.ring = ring;
   P.e_ring = e_ring;
-  const size_t lds = kCntBytes + (size_t)ring * kSlotBytes + (size_t)e_ring * kESlotBytes;
   const bool instr = dbg || o.dev_stats || o.fault_dep >= 0;
   hipStream_t s = (hipStream_t)stream;
   auto go = [&](auto kern) -> bfs_status {
@@ -456,12 +518,19 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
     return BFS_OK;
   };
   const bool bar = p->mode == BFS_MODE_BARRIER;
-  if (phase == 1) {
-    if (bar) return instr ? go(moe_kernel<1, BFS_MODE_BARRIER, true>) : go(moe_kernel<1, BFS_MODE_BARRIER, false>);
-    return instr ? go(moe_kernel<1, BFS_MODE_BARRIER_FREE, true>) : go(moe_kernel<1, BFS_MODE_BARRIER_FREE, false>);
-  }
-  if (bar) return instr ? go(moe_kernel<2, BFS_MODE_BARRIER, true>) : go(moe_kernel<2, BFS_MODE_BARRIER, false>);
-  return instr ? go(moe_kernel<2, BFS_MODE_BARRIER_FREE, true>) : go(moe_kernel<2, BFS_MODE_BARRIER_FREE, false>);
+  auto pick = [&](auto ph, auto bmc) -> bfs_status {
+    constexpr int kP = decltype(ph)::value, kB = decltype(bmc)::value;
+    if (bar)
+      return instr ? go(moe_kernel<kP, BFS_MODE_BARRIER, true, kB>) : go(moe_kernel<kP, BFS_MODE_BARRIER, false, kB>);
+    return instr ? go(moe_kernel<kP, BFS_MODE_BARRIER_FREE, true, kB>)
+                 : go(moe_kernel<kP, BFS_MODE_BARRIER_FREE, false, kB>);
+  };
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using B128 = std::integral_constant<int, 128>;
+  using B256 = std::integral_constant<int, 256>;
+  if (phase == 1) return bm == 128 ? pick(I1{}, B128{}) : pick(I1{}, B256{});
+  return bm == 128 ? pick(I2{}, B128{}) : pick(I2{}, B256{});
 }
 
 }  // namespace bfs

@@ -18,7 +18,7 @@ from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER,
                                   BfsError, Plan, bfs)
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import moe_program, moe_worklist  # noqa: E402
-from workloads.configs import MOE_LINEAR, MOE_MCHUNK  # noqa: E402
+from workloads.configs import MOE_BM, MOE_LINEAR, MOE_MCHUNKS  # noqa: E402
 from workloads.tensors import bf16_to_f32, moe_inputs, moe_weights_all  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -45,7 +45,7 @@ def _dev16(bits):
 class MoeRun:
     """Device copies of one MoE problem and the two launches."""
 
-    def __init__(self, moe, mchunk=MOE_MCHUNK):
+    def __init__(self, moe, mchunk=None, bm=MOE_BM):
         self.moe = moe
         wg, wu, wd = moe_weights_all(moe)
         self.wg, self.wu, self.wd = _dev16(wg), _dev16(wu), _dev16(wd)
@@ -55,12 +55,13 @@ class MoeRun:
         T = len(moe.assign)
         self.h = torch.full((T, moe.ffn), -1, dtype=torch.int16, device="cuda")
         self.y = torch.full((T, moe.hidden), -1, dtype=torch.int16, device="cuda")
-        self.set_mchunk(mchunk)
+        self.set_mchunk(mchunk, bm)
 
-    def set_mchunk(self, mchunk):
-        """Work lists with runs of at most ``mchunk`` M-tiles per workgroup."""
-        self.mchunk = mchunk
-        self.wl = {ph: moe_worklist(self.moe.counts, ph, self.moe.hidden, self.moe.ffn, mchunk=mchunk)
+    def set_mchunk(self, mchunk=None, bm=MOE_BM):
+        """Work lists of ``bm``-token M-tiles with runs of at most ``mchunk``
+        M-tiles per workgroup (the default for that tile height if None)."""
+        self.mchunk, self.bm = (MOE_MCHUNKS[bm] if mchunk is None else mchunk), bm
+        self.wl = {ph: moe_worklist(self.moe.counts, ph, self.moe.hidden, self.moe.ffn, mchunk=self.mchunk, bm=bm)
                    for ph in (1, 2)}
         self.dev_wl = {}
         for ph, wl in self.wl.items():
@@ -76,7 +77,7 @@ class MoeRun:
     def run(self, mode, cap=0, alloc=ALLOC_PER_LOOP, linear=False):
         logs = {}
         for ph in (1, 2):
-            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn, linear=linear), mode, alloc)
+            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn, linear=linear, bm=self.bm), mode, alloc)
             work, trips, toff, n_wg = self.dev_wl[ph]
             log = None
             if cap:
@@ -102,24 +103,26 @@ def check_close(got, ref):
 # an empty expert, a one-token expert, ragged tiles, runs of M-tiles split
 # over workgroups (mchunk 2)
 SMALL_COUNTS = [300, 0, 129, 1, 530]
+BMS = [128, 256]
 
 
-def test_moe_small_parity_and_thresholds():
+@pytest.mark.parametrize("bm", BMS)
+def test_moe_small_parity_and_thresholds(bm):
     moe = moe_inputs(seed=1, hidden=256, ffn=256, counts=SMALL_COUNTS)
-    r = MoeRun(moe, mchunk=2)
+    r = MoeRun(moe, mchunk=2, bm=bm)
     T = len(moe.assign)
     ref_y = mathref.moe_tokens(moe, range(T))
     grouped = moe.perm                                  # h rows are in expert-grouped order
     ref_h = mathref.moe_hidden(moe, grouped)
     outs = {}
     for name, mode in MODES:
-        _say(f"[moe-small] mode={name}")
+        _say(f"[moe-small] bm={bm} mode={name}")
         h, y, logs = r.run(mode, cap=64)
         check_close(h, ref_h)
         check_close(y, ref_y)
         for ph in (1, 2):
             plan, logw = logs[ph]
-            prog = moe_program(ph, moe.hidden, moe.ffn)
+            prog = moe_program(ph, moe.hidden, moe.ffn, bm=bm)
             wl = r.wl[ph]
             trips, off = wl.trips.flat()
             recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
@@ -129,21 +132,22 @@ def test_moe_small_parity_and_thresholds():
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
 
 
-def test_moe_linear_ring_parity_and_thresholds():
+@pytest.mark.parametrize("bm", BMS)
+def test_moe_linear_ring_parity_and_thresholds(bm):
     """MMA->LOAD read with the linearized offset (an extension) in place of
     the M-tile drain: outputs equal the oracle's and, bit for bit, the
     drained program's in both modes; every logged barrier-free threshold
     equals the brute force of the linearized relation (the paper's for the
     other dependencies), across M-tile boundaries (runs of 3 M-tiles)."""
     moe = moe_inputs(seed=2, hidden=256, ffn=256, counts=SMALL_COUNTS)
-    r = MoeRun(moe, mchunk=3)
+    r = MoeRun(moe, mchunk=3, bm=bm)
     T = len(moe.assign)
     ref_y = mathref.moe_tokens(moe, range(T))
     ref_h = mathref.moe_hidden(moe, moe.perm)
     _say("[moe-linear] drained program")
     h0, y0, _ = r.run(MODE_BARRIER_FREE)
     for name, mode in MODES:
-        _say(f"[moe-linear] mode={name}")
+        _say(f"[moe-linear] bm={bm} mode={name}")
         h, y, logs = r.run(mode, cap=64, linear=True)
         check_close(h, ref_h)
         check_close(y, ref_y)
@@ -153,7 +157,7 @@ def test_moe_linear_ring_parity_and_thresholds():
             continue
         for ph in (1, 2):
             plan, logw = logs[ph]
-            prog = moe_program(ph, moe.hidden, moe.ffn, linear=True)
+            prog = moe_program(ph, moe.hidden, moe.ffn, linear=True, bm=bm)
             d_lin = [i for i, x in enumerate(prog.dep_linear) if x]
             wl = r.wl[ph]
             trips, off = wl.trips.flat()
@@ -168,17 +172,18 @@ def test_moe_linear_ring_parity_and_thresholds():
             assert compare_wave_logs_with_oracle(prog, plan, lg, recs, name) > 0
 
 
-def test_moe_per_instr():
+@pytest.mark.parametrize("bm", BMS)
+def test_moe_per_instr(bm):
     """One counter per producer instruction (Eq. 3): thresholds equal the
     Eq. 1 counts for every wave, values as with per-loop counters."""
     moe = moe_inputs(seed=3, hidden=256, ffn=256, counts=SMALL_COUNTS)
-    r = MoeRun(moe, mchunk=2)
-    _say("[moe-per-instr]")
+    r = MoeRun(moe, mchunk=2, bm=bm)
+    _say(f"[moe-per-instr] bm={bm}")
     h, y, logs = r.run(MODE_BARRIER_FREE, cap=64, alloc=ALLOC_PER_INSTR)
     check_close(y, mathref.moe_tokens(moe, range(len(moe.assign))))
     for ph in (1, 2):
         plan, logw = logs[ph]
-        prog = moe_program(ph, moe.hidden, moe.ffn)
+        prog = moe_program(ph, moe.hidden, moe.ffn, bm=bm)
         wl = r.wl[ph]
         trips, off = wl.trips.flat()
         recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
@@ -205,26 +210,32 @@ def full_moe():
         group = moe.perm[lo:hi]
         tokens += [int(group[0]), int(group[-1])] + [int(t) for t in rng.choice(group, 6)]
         # h rows are in expert-grouped order: the first and last row of the
-        # expert, the first row of its last (ragged) M-tile, and random ones
-        rows += [lo, hi - 1, lo + (hi - 1 - lo) // 128 * 128] + [int(i) for i in rng.integers(lo, hi, 4)]
+        # expert, the first row of its last (ragged) M-tile at both tile
+        # heights, and random ones
+        rows += [lo, hi - 1, lo + (hi - 1 - lo) // 128 * 128, lo + (hi - 1 - lo) // 256 * 256]
+        rows += [int(i) for i in rng.integers(lo, hi, 4)]
     weights = {}
     ref_y = mathref.moe_tokens(moe, tokens, weights)
     ref_h = mathref.moe_hidden(moe, [int(moe.perm[i]) for i in rows], weights)
     return r, tokens, ref_y, rows, ref_h
 
 
-@pytest.mark.parametrize("mchunk,linear", [(MOE_MCHUNK, MOE_LINEAR), (MOE_MCHUNK, not MOE_LINEAR), (8, MOE_LINEAR)],
-                         ids=["bench", "bench_other_form", "m8"])
-def test_moe_full_size_sampled(full_moe, mchunk, linear):
-    """The benchmark shape and launch (runs of at most four M-tiles, the
-    paper's ACQL drain, as timed), then the linearized ring, then runs of
-    eight; sampled y tokens and h rows one by one; both modes
-    bit-identical."""
+OTHER_BM = 256 if MOE_BM == 128 else 128
+
+
+@pytest.mark.parametrize("mchunk,linear,bm", [(None, MOE_LINEAR, MOE_BM), (None, not MOE_LINEAR, MOE_BM),
+                                              (8, MOE_LINEAR, MOE_BM), (None, MOE_LINEAR, OTHER_BM)],
+                         ids=["bench", "bench_other_form", "m8", "other_bm"])
+def test_moe_full_size_sampled(full_moe, mchunk, linear, bm):
+    """The benchmark shape and launch (the default M-tile height and runs,
+    the paper's ACQL drain, as timed), then the linearized ring, runs of
+    eight M-tiles, and the other M-tile height; sampled y tokens and h rows
+    one by one; both modes bit-identical."""
     r, tokens, ref_y, rows, ref_h = full_moe
-    r.set_mchunk(mchunk)
+    r.set_mchunk(mchunk, bm)
     outs = {}
     for name, mode in MODES:
-        _say(f"[moe-full] mchunk={mchunk} linear={linear} mode={name}")
+        _say(f"[moe-full] bm={bm} mchunk={r.mchunk} linear={linear} mode={name}")
         r.h.fill_(-1)
         r.y.fill_(-1)
         h, y, _ = r.run(mode, linear=linear)

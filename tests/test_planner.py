@@ -219,24 +219,27 @@ def test_moe_linear_ring_thresholds():
 
 def test_moe_worklist_covers_every_tile_once():
     """Every (expert, output tile, M-tile) of both phases appears in exactly
-    one work item, runs hold at most MOE_MCHUNK M-tiles, trips match."""
-    from workloads import MOE_BM, MOE_BN, moe_worklist
-    from workloads.configs import MOE_MCHUNK
+    one work item, runs hold at most the default run length of M-tiles,
+    trips match; both M-tile heights."""
+    from workloads import MOE_BN, moe_worklist
+    from workloads.configs import MOE_MCHUNKS, moe_chunks
     from workloads.tensors import zipf_counts
-    for counts in (zipf_counts(32768, 64), np.array([300, 0, 129, 1, 530])):
-        for ph, (hidden, ffn) in ((1, (4096, 1408)), (2, (4096, 1408)), (1, (256, 256)), (2, (256, 256))):
-            wl = moe_worklist(counts, ph, hidden, ffn)
-            n_dim = ffn if ph == 1 else hidden
-            seen = set()
-            for (e, n0, mt0, n_mt), tr in zip(wl.work.tolist(), wl.trips.per_wg):
-                assert int(tr[1][0]) == n_mt and len(tr[2]) == n_mt and n_mt <= MOE_MCHUNK
-                for m in range(mt0, mt0 + n_mt):
-                    key = (e, n0, m)
-                    assert key not in seen
-                    seen.add(key)
-            want = {(e, n0, m) for e in range(len(counts)) for n0 in range(0, n_dim, MOE_BN[ph])
-                    for m in range(-(-int(counts[e]) // MOE_BM))}
-            assert seen == want
+    for bm in (128, 256):
+        for counts in (zipf_counts(32768, 64), np.array([300, 0, 129, 1, 530])):
+            for ph, (hidden, ffn) in ((1, (4096, 1408)), (2, (4096, 1408)), (1, (256, 256)), (2, (256, 256))):
+                wl = moe_worklist(counts, ph, hidden, ffn, bm=bm)
+                n_dim = ffn if ph == 1 else hidden
+                seen = set()
+                for (e, n0, mt0, n_mt), tr in zip(wl.work.tolist(), wl.trips.per_wg):
+                    assert int(tr[1][0]) == n_mt and len(tr[2]) == n_mt and n_mt <= MOE_MCHUNKS[bm]
+                    assert all(int(c) == moe_chunks(ph, bm) for c in tr[3])
+                    for m in range(mt0, mt0 + n_mt):
+                        key = (e, n0, m)
+                        assert key not in seen
+                        seen.add(key)
+                want = {(e, n0, m) for e in range(len(counts)) for n0 in range(0, n_dim, MOE_BN[ph])
+                        for m in range(-(-int(counts[e]) // bm))}
+                assert seen == want
 
 
 def test_fused_family_formulas():

@@ -677,18 +677,28 @@ def attn_worklist(lengths, heads: int, xcds: int = 8, n_wg: int = ATTN_WG) -> At
 # cfg5: MoE grouped GEMM, two phases with load / MFMA / epilogue engines and a
 # runtime M-tile loop per workgroup
 # ---------------------------------------------------------------------------
-MOE_BM = 128                 # token rows per M-tile
+MOE_BM = 256                 # token rows per M-tile (128 or 256)
 MOE_BK = 32                  # K step per ring slot
 MOE_BN = {1: 128, 2: 256}    # output columns per workgroup: h columns (phase 1), y columns (phase 2)
-MOE_CHUNKS = {1: 2, 2: 4}    # epilogue chunks per M-tile
-MOE_RING = 5
-MOE_MCHUNK = 4               # at most this many M-tiles per workgroup
+# (ring slots, epilogue slots) per M-tile height: a ring slot holds BM x 64 B
+# of token rows and 16 KiB of weight rows; with the 2 KiB of counters and
+# 16 KiB epilogue slots they stay within 160 KiB of LDS
+MOE_RINGS = {128: (5, 2), 256: (4, 1)}
+MOE_MCHUNKS = {128: 4, 256: 4}   # at most this many M-tiles per workgroup
+
+
+def moe_chunks(phase: int, bm: int = MOE_BM) -> int:
+    """Epilogue chunks per M-tile: one 32-row block of each MFMA wave's
+    BM / 2-row sub-tile (phase 1), times its two 32-column blocks (phase 2)."""
+    return bm // 64 * (1 if phase == 1 else 2)
+
+
 MOE_LINEAR = False           # benchmark ring form: the paper's ACQL drain at every M-tile;
                              # True selects the linearized MMA->LOAD dependency (extension)
 
 
-def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring: int = 2,
-                linear: bool = MOE_LINEAR) -> Program:
+def moe_program(phase: int, hidden: int, ffn: int, ring: int = None, e_ring: int = None,
+                linear: bool = MOE_LINEAR, bm: int = MOE_BM) -> Program:
     """One workgroup per (expert, N-tile, run of M-tiles); phase 1 computes
     h = SiLU(x W_gate) * (x W_up) for 128 h columns, phase 2 y = h W_down for
     256 y columns:
@@ -698,8 +708,10 @@ def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring:
          E1: ACQE
          C{ E1: SPILL one accumulator block per MFMA wave -> ering[(rhat_C - 1) % e_ring]; E2: EPI store } }
 
-    The M loop's trip count is the number of 128-token tiles of the
-    workgroup's expert it covers, known only at run time.  LOAD->MMA (k=0)
+    The M loop's trip count is the number of ``bm``-token tiles (128 or
+    256) of the workgroup's expert it covers, known only at run time;
+    ``ring`` and ``e_ring`` default to the largest that fit in LDS for that
+    tile height.  LOAD->MMA (k=0)
     and MMA->LOAD (k=ring) protect the ring inside an M-tile, MMA->ACQL (k=1,
     C3) across M-tiles (the next tile's loads reuse the slots); SPILL->EPI
     (k=0) and EPI->SPILL (k=e_ring) protect the epilogue ring inside an
@@ -711,11 +723,13 @@ def moe_program(phase: int, hidden: int, ffn: int, ring: int = MOE_RING, e_ring:
     ring across M-tiles by itself, so MMA->ACQL is dropped and the next
     tile's loads may start while the MFMAs of the previous tile run."""
     k_dim, n_dim = (hidden, ffn) if phase == 1 else (ffn, hidden)
+    ring = MOE_RINGS[bm][0] if ring is None else ring
+    e_ring = MOE_RINGS[bm][1] if e_ring is None else e_ring
     b = ProgramBuilder("moe", n_engines=3, waves_per_engine=[2, 8, 2])
     with b.loop("M"):
         b.instr(0, OP_NOP, [0] * 8, name="ACQL")
         with b.loop("K"):
-            b.instr(0, OP_MOE_LOAD, [phase, k_dim, n_dim, ring, 0, 0, 0, 0], name="LOAD")
+            b.instr(0, OP_MOE_LOAD, [phase, k_dim, n_dim, ring, bm, 0, 0, 0], name="LOAD")
             b.instr(1, OP_MOE_MMA, [0] * 8, name="MMA")
         b.instr(1, OP_NOP, [0] * 8, name="ACQE")
         with b.loop("C"):
@@ -737,7 +751,8 @@ class MoeWork:
     trips: TripTables     # per workgroup: [[1], [n_mt], [K / 32] * n_mt, [chunks] * n_mt]
 
 
-def moe_worklist(counts, phase: int, hidden: int, ffn: int, mchunk: int = MOE_MCHUNK, xcds: int = 8) -> MoeWork:
+def moe_worklist(counts, phase: int, hidden: int, ffn: int, mchunk: int = None, xcds: int = 8,
+                 bm: int = MOE_BM) -> MoeWork:
     """Work items (expert, N-tile, run of at most ``mchunk`` M-tiles) in launch
     order.
 
@@ -750,11 +765,12 @@ def moe_worklist(counts, phase: int, hidden: int, ffn: int, mchunk: int = MOE_MC
     N-tiles on the same XCD.  Workgroup w runs on XCD w % xcds; shorter XCD
     lists are padded with empty items (no M-tiles)."""
     k_dim, n_dim = (hidden, ffn) if phase == 1 else (ffn, hidden)
+    mchunk = MOE_MCHUNKS[bm] if mchunk is None else mchunk
     bn = MOE_BN[phase]
     n_tiles = n_dim // bn
     counts = np.asarray(counts, dtype=np.int64)
     order = sorted(range(len(counts)), key=lambda e: (-int(counts[e]), e))
-    mtiles = {e: -(-int(counts[e]) // MOE_BM) for e in order}
+    mtiles = {e: -(-int(counts[e]) // bm) for e in order}
     share = sum(mtiles.values()) * n_tiles / xcds
     load = [0] * xcds
     lists = [[] for _ in range(xcds)]
@@ -784,7 +800,7 @@ def moe_worklist(counts, phase: int, hidden: int, ffn: int, mchunk: int = MOE_MC
         for x in range(xcds):
             items.append(lists[x][i] if i < len(lists[x]) else (0, 0, 0, 0))
     work = np.array(items, dtype=np.int32).reshape(-1, 4)
-    ksteps, chunks = k_dim // MOE_BK, MOE_CHUNKS[phase]
+    ksteps, chunks = k_dim // MOE_BK, moe_chunks(phase, bm)
     trips = TripTables([[np.array([1], np.int32), np.array([n_mt], np.int32),
                          np.full(n_mt, ksteps, np.int32), np.full(n_mt, chunks, np.int32)]
                         for _, _, _, n_mt in work])
