@@ -203,7 +203,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       } else {
         g.r1 += 1;
         g.h1 = it + 1;
-        S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
+        S.wait_affine(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
       }
       if (!S.aborted) {
         unsigned char *dst = ring + slot * kSlotBytes + (wave == 0 ? 0u : kSlotBytes / 2);
@@ -257,50 +257,68 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     }
     uint32_t seen_load = 0;
     const uint32_t l32 = lane & 31u, lhi = lane >> 5;
+    // Swizzled byte offset of this lane's 16-byte chunk in k-half 0 of its
+    // first A row; k-half 1 is the same offset XOR 32 (chunk lhi ^ 2).  Row
+    // blocks 32 rows apart lie 2048 bytes apart with the same swizzle, and
+    // the lane's B row (wn * 64 + l32) has the A row's swizzle too, so its
+    // offset is the A offset plus a wave-uniform distance: one per-lane
+    // register serves every fragment address.
+    const uint32_t arow = wm * 128u + l32;
+    const uint32_t a_off0 = swz(arow, lhi);
+    const uint32_t b_dist = kSlotBytes / 2 + (wn * 64u - wm * 128u) * 64u;   // B slot half + row distance
     uint32_t slot = 0;
+    // Fragments of one k-half (4 A row blocks, 2 B column blocks) live in
+    // registers.  mma_half issues the 8 MFMAs of the fragments held and, when
+    // it refills, replaces each A fragment with k-half h of ring slot sl as
+    // soon as its two MFMAs are issued and the B pair after the last row
+    // block, so the next k-half's LDS reads run under these MFMAs; the
+    // scheduling barriers keep the compiler from hoisting the refills (a
+    // second register set) or sinking them.
+    auto rd_at = [](uint32_t addr, uint32_t imm) {
+      return __builtin_bit_cast(bf16x8, *(const BFS_LDS u32x4 *)(uintptr_t)(addr + imm));
+    };
+    bf16x8 fa[4], fb0, fb1;
+    auto read_half = [&](uint32_t sl, int h) __attribute__((always_inline)) {
+      const uint32_t a_addr = (a_off0 ^ (32u * h)) + ring_base + sl * kSlotBytes;
+      fb0 = rd_at(a_addr + b_dist, 0u);
+      fb1 = rd_at(a_addr + b_dist, 2048u);
+#pragma unroll
+      for (int bm = 0; bm < 4; ++bm) fa[bm] = rd_at(a_addr, 2048u * bm);
+    };
+    auto mma_half = [&](auto refill, uint32_t sl, int h) __attribute__((always_inline)) {
+#pragma unroll
+      for (int bm = 0; bm < 4; ++bm) {
+        acc[bm * 2 + 0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb0, fa[bm], acc[bm * 2 + 0], 0, 0, 0);
+        acc[bm * 2 + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb1, fa[bm], acc[bm * 2 + 1], 0, 0, 0);
+        if constexpr (decltype(refill)::value) {
+          const uint32_t a_addr = (a_off0 ^ (32u * h)) + ring_base + sl * kSlotBytes;
+          fa[bm] = rd_at(a_addr, 2048u * bm);
+          if (bm == 3) {
+            fb0 = rd_at(a_addr + b_dist, 0u);
+            fb1 = rd_at(a_addr + b_dist, 2048u);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    using Refill = std::true_type;
+    using NoRefill = std::false_type;
     auto mma_step = [&](uint32_t it) __attribute__((always_inline)) {
       if (kFlat) {
         S.wait_fixed((uint32_t)P.c_load, kLoadW, it + 2u, P.dep_mma[it], 0u, seen_load, [] {});
       } else {
         g.r1 += 1;
         g.h1 = it + 1;
-        S.wait(s_mma, P.mma, g, it + 1, g.r1 - 1, [] {});
+        S.wait_affine(s_mma, P.mma, g, it + 1, g.r1 - 1, [] {});
       }
-      const uint32_t a_base = ring_base + slot * kSlotBytes, b_base = a_base + kSlotBytes / 2;
       if (!S.aborted) {
-        // Fragments are read one block ahead of the MFMAs that use them, so
-        // each LDS read overlaps the previous block's MFMAs.
-        auto rd = [&](uint32_t base, uint32_t row, uint32_t c) {
-          return __builtin_bit_cast(bf16x8, *(const BFS_LDS u32x4 *)(uintptr_t)(base + swz(row, c)));
-        };
-        const uint32_t arow = wm * 128u + l32, brow = wn * 64u + l32;
-        bf16x8 b0 = rd(b_base, brow, lhi), b1 = rd(b_base, brow + 32u, lhi);
-        bf16x8 a_cur = rd(a_base, arow, lhi);
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const uint32_t c = 2u * s + lhi;
-          bf16x8 nb0 = b0, nb1 = b1;
-#pragma unroll
-          for (int bm = 0; bm < 4; ++bm) {
-            bf16x8 a_next = a_cur;
-            if (bm < 3) {
-              a_next = rd(a_base, arow + 32u * (bm + 1), c);
-              // the step's last fragment read is issued: MMA retires from
-              // the slot (LDS executes this wave's reads before the signal
-              // that follows them; the remaining MFMAs use registers only)
-              if (s == 1 && bm == 2) S.signal(P.mma.update, ew);
-            } else if (s == 0) {
-              nb0 = rd(b_base, brow, c + 2u);
-              nb1 = rd(b_base, brow + 32u, c + 2u);
-              a_next = rd(a_base, arow, c + 2u);
-            }
-            acc[bm * 2 + 0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b0, a_cur, acc[bm * 2 + 0], 0, 0, 0);
-            acc[bm * 2 + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b1, a_cur, acc[bm * 2 + 1], 0, 0, 0);
-            a_cur = a_next;
-          }
-          b0 = nb0;
-          b1 = nb1;
-        }
+        read_half(slot, 0);
+        mma_half(Refill{}, slot, 1);
+        // every fragment read of the step is issued: MMA retires from the
+        // slot (LDS executes this wave's reads before the signal that
+        // follows them; the remaining MFMAs use registers only)
+        S.signal(P.mma.update, ew);
+        mma_half(NoRefill{}, slot, 0);
       } else {
         S.signal(P.mma.update, ew);
       }
@@ -365,7 +383,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
     S.enter(s_epi, P.epi, g, LC);
     for (uint32_t it = 0; it < trip_c; ++it) {
       c_iter(it);
-      S.wait(s_epi, P.epi, g, it + 1, c_r() - 1, [] {});
+      S.wait_affine(s_epi, P.epi, g, it + 1, c_r() - 1, [] {});
       if (!S.aborted) {
         const uint32_t b = it, bm = b >> 1, bn = b & 1u;
         const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
@@ -491,6 +509,8 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
   P.mma.update = p->instr_update[ins_mma];
   if (!waits_fit({{&P.bias, 1}, {&P.load, 1}, {&P.mma, 1}, {&P.spill, 3}, {&P.epi, 1}}))
     return fail(BFS_E_RESOURCE, "gemm: more waits on an instruction than its engine loop takes");
+  if (p->mode == BFS_MODE_BARRIER_FREE && ((!flat && (!all_affine(P.load) || !all_affine(P.mma))) || !all_affine(P.epi)))
+    return fail(BFS_E_UNSUPPORTED, "gemm: K- and C-loop waits must have their producer in the same loop");
   P.a = static_cast<const __bf16 *>(bufs[0]);
   P.bt = static_cast<const __bf16 *>(bufs[1]);
   P.bias_v = static_cast<const float *>(bufs[2]);
