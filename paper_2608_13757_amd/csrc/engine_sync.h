@@ -234,7 +234,7 @@ struct Sync {
         const bool aff = kind == (uint32_t)kWaitAffine, cst = kind == (uint32_t)kWaitConst;
         const int32_t b_cst = cst ? (int32_t)threshold_plain(w, g) : 0;
         base = aff ? b_aff : (cst ? b_cst : base);
-        mk = aff ? mk_aff : mk;
+        mk = aff ? mk_aff : (cst ? 0u : mk);        // a constant: slope 0, no mask
       }
       const uint32_t meta = word(w.w0 & 0xffu, 0) | ((uint32_t)iw.w[j].n_prd_waves << 16) | (kind << 20);
       s.base[j] = on ? base : s.base[j];
@@ -285,11 +285,11 @@ struct Sync {
     }
   }
 
-  // The waits of a site whose waits are all affine (the host checked that
-  // each producer and shared loop is the consumer's innermost loop): the
-  // threshold is base + N * t under the mask t > k, evaluated without the
-  // per-kind dispatch of wait().  Barrier mode and instrumented builds take
-  // wait().
+  // The waits of a site none of whose waits is dynamic (checked on the
+  // host): an affine threshold is base + N * t under the mask t > k, a
+  // constant one the same with slope 0 and no mask (as enter() stores it),
+  // so every wait is evaluated without the per-kind dispatch of wait().
+  // Barrier mode and instrumented builds take wait().
   template <int kN, class OnBlock>
   __device__ __forceinline__ void wait_affine(Site<kN> &s, const InstrWaits &iw, const Regs &g, uint32_t t,
                                               uint32_t instance, OnBlock on_block) {
@@ -406,11 +406,12 @@ inline bool has_dep(const bfs_plan *p, int prd, int cns, int k) {
   return false;
 }
 
-// Host: every wait of the instruction is affine in its innermost loop's
-// iteration (Sync::wait_affine may serve it).
-inline bool all_affine(const bfsdev::InstrWaits &iw) {
+// Host: no wait of the instruction is dynamic (each is affine in its
+// innermost loop's iteration or constant during its trip), so
+// Sync::wait_affine may serve it.
+inline bool no_dynamic(const bfsdev::InstrWaits &iw) {
   for (int j = 0; j < iw.n; ++j)
-    if (iw.w[j].kind != bfsdev::kWaitAffine) return false;
+    if (iw.w[j].kind == bfsdev::kWaitDynamic) return false;
   return true;
 }
 

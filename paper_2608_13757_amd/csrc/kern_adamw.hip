@@ -98,7 +98,7 @@ __global__ void __launch_bounds__(64 * 6) adamw_kernel(AdamParams P) {
     for (uint32_t it = 0; it < trip; ++it) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
+      S.wait_affine(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
       if (!S.aborted) {
         const int64_t e0 = (c0 + it) * (int64_t)CH;     // first parameter of the chunk
         unsigned char *dst = ring + slot * P.slot_bytes;
@@ -138,7 +138,7 @@ __global__ void __launch_bounds__(64 * 6) adamw_kernel(AdamParams P) {
     for (uint32_t it = 0; it < trip; ++it) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.wait(s_upd, P.upd, g, it + 1, g.r1 - 1, [] {});
+      S.wait_affine(s_upd, P.upd, g, it + 1, g.r1 - 1, [] {});
       if (!S.aborted) {
         const uint32_t base = lds_addr(ring) + slot * P.slot_bytes + 16u * lane;
         for (uint32_t b = ew; b < blocks; b += W) {
@@ -174,7 +174,7 @@ __global__ void __launch_bounds__(64 * 6) adamw_kernel(AdamParams P) {
     for (uint32_t it = 0; it < trip; ++it) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.wait(s_store, P.store, g, it + 1, g.r1 - 1, [] {});
+      S.wait_affine(s_store, P.store, g, it + 1, g.r1 - 1, [] {});
       if (!S.aborted) {
         const int64_t e0 = (c0 + it) * (int64_t)CH;
         const uint32_t base = lds_addr(ring) + slot * P.slot_bytes + 16u * lane;
@@ -242,6 +242,8 @@ bfs_status launch_adamw(const bfs_plan *p, DevImage *img, const void *const *buf
     return fail(BFS_E_RESOURCE, "adamw: at most 4 waits per instruction");
   if (!waits_fit({{&P.load, 1}, {&P.upd, 1}, {&P.store, 1}}))
     return fail(BFS_E_RESOURCE, "adamw: more waits on an instruction than its engine loop takes");
+  if (p->mode == BFS_MODE_BARRIER_FREE && (!no_dynamic(P.load) || !no_dynamic(P.upd) || !no_dynamic(P.store)))
+    return fail(BFS_E_UNSUPPORTED, "adamw: a chunk-loop wait depends on a loop register other than the chunk loop's");
   P.chunk_base = static_cast<const int64_t *>(bufs[0]);
   P.p = static_cast<float *>(const_cast<void *>(bufs[1]));
   P.g = static_cast<const float *>(bufs[2]);

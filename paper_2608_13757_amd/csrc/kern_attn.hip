@@ -230,7 +230,7 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
       for (uint32_t it = 0; it < x.trip; ++it, slot = (slot + 1 == depth) ? 0u : slot + 1) {
         g.r2 += 1;
         g.h2 = it + 1;
-        S.wait(site, iw, g, it + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
+        S.wait_affine(site, iw, g, it + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
         if (!S.aborted) {
           const uint32_t dst = ring + slot * kKVSlot;
           const int32_t key0 = (int32_t)it * kBKV;
@@ -297,7 +297,7 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
       for (uint32_t it = 0; it < x.trip; ++it, kslot = (kslot + 1 == (uint32_t)P.nk) ? 0u : kslot + 1) {
         g.r2 += 1;
         g.h2 = it + 1;
-        S.wait(site, P.qk, g, it + 1, g.r2 - 1, [] {});
+        S.wait_affine(site, P.qk, g, it + 1, g.r2 - 1, [] {});
         if (!S.aborted) {
           const uint32_t kb_base = kring + kslot * kKVSlot;
           const uint32_t sp = spbuf + ((g.r2 - 1) & 1u) * kSPSlot;
@@ -360,7 +360,7 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
       for (uint32_t it = 0; it < x.trip; ++it) {
         g.r2 += 1;
         g.h2 = it + 1;
-        S.wait(site, P.sm, g, it + 1, g.r2 - 1, [] {});
+        S.wait_affine(site, P.sm, g, it + 1, g.r2 - 1, [] {});
         if (!S.aborted) {
           const uint32_t par = (g.r2 - 1) & 1u;
           const uint32_t sp = spbuf + par * kSPSlot;
@@ -446,7 +446,7 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
         g.h2 = it + 1;
         // PREAD: P and alpha of the step into registers, then the S/P slot
         // is released (LDS executes this wave's reads before its signal)
-        S.wait(s_pr, P.pread, g, it + 1, g.r2 - 1, [] {});
+        S.wait_affine(s_pr, P.pread, g, it + 1, g.r2 - 1, [] {});
         bf16x8 pf[4];
         float a = 1.0f;
         if (!S.aborted) {
@@ -457,7 +457,7 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
           a = *(const BFS_LDS float *)(uintptr_t)(alpha_l + (par * kBQ + qr + l32) * 4u);
         }
         S.signal(P.pread.update, (uint32_t)ew);
-        S.wait(site, P.pv, g, it + 1, g.r2 - 1, [] {});
+        S.wait_affine(site, P.pv, g, it + 1, g.r2 - 1, [] {});
         if (!S.aborted) {
           const uint32_t vb = vring + vslot * kKVSlot;
           auto vfrag = [&](int ks, int db) {
@@ -599,6 +599,10 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   if (!waits_fit({{&P.loadk, 2}, {&P.loadv, 2}, {&P.qk, 2}, {&P.sm, 2}, {&P.pread, 2}, {&P.pv, 2}, {&P.norm, 1},
                   {&P.acqk, 1}, {&P.acqv, 1}, {&P.acqs, 1}}))
     return fail(BFS_E_RESOURCE, "attn: more waits on an instruction than its engine loop takes");
+  if (p->mode == BFS_MODE_BARRIER_FREE &&
+      (!no_dynamic(P.loadk) || !no_dynamic(P.loadv) || !no_dynamic(P.qk) || !no_dynamic(P.sm) ||
+       !no_dynamic(P.pread) || !no_dynamic(P.pv)))
+    return fail(BFS_E_UNSUPPORTED, "attn: a KV-loop wait depends on a loop register other than the KV loop's");
   P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
   P.work = static_cast<const int32_t *>(bufs[0]);
   P.q = static_cast<const __bf16 *>(bufs[1]);

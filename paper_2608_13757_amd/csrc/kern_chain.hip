@@ -105,7 +105,7 @@ __global__ void __launch_bounds__(128) chain_kernel(ChainParams P) {
       for (uint32_t ib = 0; ib < trip_b; ++ib) {
         g.r2 += 1;
         g.h2 = ib + 1;
-        S.wait(s_load, P.load, g, ib + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
+        S.wait_affine(s_load, P.load, g, ib + 1, g.r2 - 1, [&] { if (pending > 0) retire_one(); });
         if (!S.aborted) {
           __builtin_amdgcn_global_load_lds((const void *)(src + (int64_t)(g.r2 - 1) * kTileFloats),
                                            (BFS_LDS void *)(ring + slot * kTileBytes), 16, 0, 0);
@@ -145,7 +145,7 @@ __global__ void __launch_bounds__(128) chain_kernel(ChainParams P) {
       for (uint32_t ib = 0; ib < trip_b; ++ib) {
         g.r2 += 1;
         g.h2 = ib + 1;
-        S.wait(s_cons, P.cons, g, ib + 1, g.r2 - 1, [] {});
+        S.wait_affine(s_cons, P.cons, g, ib + 1, g.r2 - 1, [] {});
         if (!S.aborted) {
           const f32x4 v = *(const BFS_LDS f32x4 *)(uintptr_t)(lds_addr(ring) + slot * kTileBytes + 16u * lane);
 #pragma unroll
@@ -224,6 +224,8 @@ bfs_status launch_chain(const bfs_plan *p, DevImage *img, const void *const *buf
     return fail(BFS_E_RESOURCE, "chain: at most 4 waits per instruction");
   if (!waits_fit({{&P.acq, 1}, {&P.load, 1}, {&P.cons, 1}, {&P.store, 1}}))
     return fail(BFS_E_RESOURCE, "chain: more waits on an instruction than its engine loop takes");
+  if (p->mode == BFS_MODE_BARRIER_FREE && (!no_dynamic(P.load) || !no_dynamic(P.cons)))
+    return fail(BFS_E_UNSUPPORTED, "chain: a B-loop wait depends on a loop register other than the B loop's");
   P.trips = trips;
   P.trip_off = trip_off;
   P.base = static_cast<const int64_t *>(bufs[0]);

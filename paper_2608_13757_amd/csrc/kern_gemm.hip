@@ -509,8 +509,8 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
   P.mma.update = p->instr_update[ins_mma];
   if (!waits_fit({{&P.bias, 1}, {&P.load, 1}, {&P.mma, 1}, {&P.spill, 3}, {&P.epi, 1}}))
     return fail(BFS_E_RESOURCE, "gemm: more waits on an instruction than its engine loop takes");
-  if (p->mode == BFS_MODE_BARRIER_FREE && ((!flat && (!all_affine(P.load) || !all_affine(P.mma))) || !all_affine(P.epi)))
-    return fail(BFS_E_UNSUPPORTED, "gemm: K- and C-loop waits must have their producer in the same loop");
+  if (p->mode == BFS_MODE_BARRIER_FREE && ((!flat && (!no_dynamic(P.load) || !no_dynamic(P.mma))) || !no_dynamic(P.epi)))
+    return fail(BFS_E_UNSUPPORTED, "gemm: a K- or C-loop wait depends on a loop register other than its own loop's");
   P.a = static_cast<const __bf16 *>(bufs[0]);
   P.bt = static_cast<const __bf16 *>(bufs[1]);
   P.bias_v = static_cast<const float *>(bufs[2]);

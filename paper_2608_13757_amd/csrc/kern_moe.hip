@@ -491,8 +491,8 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   if (!waits_fit({{&P.acql, 1}, {&P.load, 1}, {&P.mma, 1}, {&P.acqe, 1}, {&P.spill, 1}, {&P.epi, 1}}))
     return fail(BFS_E_RESOURCE, "moe: more waits on an instruction than its engine loop takes");
   if (p->mode == BFS_MODE_BARRIER_FREE &&
-      (!all_affine(P.load) || !all_affine(P.mma) || !all_affine(P.spill) || !all_affine(P.epi)))
-    return fail(BFS_E_UNSUPPORTED, "moe: K- and C-loop waits must have their producer in the same loop");
+      (!no_dynamic(P.load) || !no_dynamic(P.mma) || !no_dynamic(P.spill) || !no_dynamic(P.epi)))
+    return fail(BFS_E_UNSUPPORTED, "moe: a K- or C-loop wait depends on a loop register other than its own loop's");
   P.sc = sync_common(img, dbg, dbg_cap, o, kWaves);
   P.work = static_cast<const int32_t *>(bufs[0]);
   P.perm = static_cast<const int32_t *>(bufs[1]);

@@ -143,7 +143,7 @@ __global__ void __launch_bounds__(64 * (kMaxVecWaves + 2)) rms_kernel(RmsParams 
     for (uint32_t it = 0; it < trip; ++it) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.wait(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
+      S.wait_affine(s_load, P.load, g, it + 1, g.r1 - 1, [&] { if (pending > 0) retire_one(); });
       if (!S.aborted) {
         const char *src = reinterpret_cast<const char *>(P.x + (size_t)(row0 + it) * H);
         unsigned char *dst = xring + slot * P.x_slot;
@@ -186,7 +186,7 @@ __global__ void __launch_bounds__(64 * (kMaxVecWaves + 2)) rms_kernel(RmsParams 
     for (uint32_t it = 0; it < trip; ++it) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.wait(s_norm, P.norm, g, it + 1, g.r1 - 1, [] {});
+      S.wait_affine(s_norm, P.norm, g, it + 1, g.r1 - 1, [] {});
       const uint32_t xa = lds_addr(xring) + xs * P.x_slot + 2u * col0;
       float ss = 0.f, mg = 0.f;
       if (!S.aborted) {
@@ -270,7 +270,7 @@ __global__ void __launch_bounds__(64 * (kMaxVecWaves + 2)) rms_kernel(RmsParams 
     for (uint32_t it = 0; it < trip; ++it) {
       g.r1 += 1;
       g.h1 = it + 1;
-      S.wait(s_store, P.store, g, it + 1, g.r1 - 1, [] {});
+      S.wait_affine(s_store, P.store, g, it + 1, g.r1 - 1, [] {});
       if (!S.aborted) {
         const int64_t row = row0 + it;
         const uint32_t qa = lds_addr(qring) + qs * P.q_slot;
@@ -337,6 +337,8 @@ bfs_status launch_rms(const bfs_plan *p, DevImage *img, const void *const *bufs,
     return fail(BFS_E_RESOURCE, "rmsnorm: at most 4 waits per instruction");
   if (!waits_fit({{&P.load, 1}, {&P.norm, 2}, {&P.store, 1}}))
     return fail(BFS_E_RESOURCE, "rmsnorm: more waits on an instruction than its engine loop takes");
+  if (p->mode == BFS_MODE_BARRIER_FREE && (!no_dynamic(P.load) || !no_dynamic(P.norm) || !no_dynamic(P.store)))
+    return fail(BFS_E_UNSUPPORTED, "rmsnorm: a row-loop wait depends on a loop register other than the row loop's");
   P.row_base = static_cast<const int64_t *>(bufs[0]);
   P.x = static_cast<const __bf16 *>(bufs[1]);
   P.gamma = static_cast<const __bf16 *>(bufs[2]);
