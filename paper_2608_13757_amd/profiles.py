@@ -12,7 +12,8 @@ Turns rocprofv3 output into the short records kept under ``profiles/``:
 * ``sq``: shader-sequencer counters of the uninstrumented dispatches of both
   modes from ``--pmc`` runs (at most 8 SQ counters per run): wave cycles,
   cycles spent waiting, instruction mix, MFMA busy cycles and MFMA work, per
-  dispatch, with the wait and issue shares of the wave cycles.
+  dispatch, with the wait and issue shares of the wave cycles and, from
+  ``GRBM_GUI_ACTIVE``, the shader clock and the MFMA and LDS busy shares.
 
 Usage (from the repository root, after the rocprofv3 runs)::
 
@@ -37,12 +38,12 @@ PROFILES = os.path.join(ROOT, "profiles")
 # its barrier-free, uninstrumented dispatch in rocprofv3 output
 KERNELS = {
     "stream3": (["kern_stream3.hip", "device_sync.h", "bfs_internal.h"], ["stream3_kernel<0, false"]),
-    "gemm": (["kern_gemm.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["gemm_kernel<0, false, 1>"]),
+    "gemm": (["kern_gemm.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["gemm_kernel<0, false, 1, 0>"]),
     "attn": (["kern_attn.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["attn_kernel<0, false>"]),
     "rms": (["kern_rms.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["rms_kernel<0, false, 4>"]),
     "adamw": (["kern_adamw.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["adamw_kernel<0, false>"]),
     "moe": (["kern_moe.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"],
-            ["moe_kernel<1, 0, false>", "moe_kernel<2, 0, false>"]),
+            ["moe_kernel<1, 0, false, 256>", "moe_kernel<2, 0, false, 256>"]),
 }
 COPY_NAMES = ("__amd_rocclr_copyBuffer",)   # the runtime's device-to-device copy
 
@@ -172,12 +173,29 @@ SQ_DERIVED = [
 ]
 
 
+N_XCD, N_CU, N_SIMD = 8, 256, 1024     # MI355X: XCDs, compute units, SIMDs
+
+
+def _mean_duration_s(rows, match):
+    """Mean duration (s) of the dispatches whose kernel name contains
+    ``match``, from the start and end timestamps (ns) of their rows."""
+    spans = {}
+    for r in rows:
+        if match in r["Kernel_Name"] and r.get("Start_Timestamp") and r.get("End_Timestamp"):
+            key = r.get("Dispatch_Id") or r.get("Correlation_Id")
+            spans[key] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+    return sum(spans.values()) / len(spans) if spans else None
+
+
 def sq(args):
     """Per-dispatch means of every SQ counter of the runs, for each
-    uninstrumented kernel instantiation of the family."""
+    uninstrumented kernel instantiation of the family, with the shader clock
+    (GRBM_GUI_ACTIVE per XCD over the dispatch's duration) and the MFMA and
+    LDS busy shares of the clock cycles when those counters are present."""
     stem = {"stream3": "stream3_kernel<", "gemm": "gemm_kernel<", "attn": "attn_kernel<",
             "moe": "moe_kernel<", "rms": "rms_kernel<", "adamw": "adamw_kernel<"}[args.kernel]
     table = {}          # kernel -> counter -> (mean, dispatches)
+    clock = {}          # kernel -> (GRBM_GUI_ACTIVE per XCD, mean dispatch duration)
     for d in args.dir:
         rows = _counter_rows(d)
         names = sorted({r["Kernel_Name"] for r in rows if stem in r["Kernel_Name"]})
@@ -188,6 +206,8 @@ def sq(args):
                 continue
             for c in counters:
                 table.setdefault(short, {})[c] = _per_dispatch(rows, c, n)
+            if "GRBM_GUI_ACTIVE" in counters:
+                clock[short] = (table[short]["GRBM_GUI_ACTIVE"][0] / N_XCD, _mean_duration_s(rows, n))
     kernels = sorted(table)
     counters = sorted({c for k in kernels for c in table[k]})
     lines = [f"# {args.kernel} kernel: SQ counters, barrier-free vs barrier ({args.workload})", "",
@@ -196,8 +216,11 @@ def sq(args):
         lines += ["```", c, "```", ""]
     lines += ["Per-dispatch means over the timed and warm-up launches (counter values summed over the "
               "hardware instances).  Template arguments: <mode, instrumented, ...> (mode 0 = barrier-free, "
-              "1 = barrier); MoE: <phase, mode, instrumented>.  Cycle counters are in the hardware's "
-              "units (quad cycles); only their ratios are used.", "",
+              "1 = barrier); MoE: <phase, mode, instrumented, M-tile rows>.  SQ_WAVE_CYCLES, SQ_BUSY_CYCLES, "
+              "SQ_WAIT_ANY and SQ_ACTIVE_INST_ANY are in quad cycles (only their ratios are used); "
+              "SQ_VALU_MFMA_BUSY_CYCLES counts shader-clock cycles per SIMD, SQ_LDS_IDX_ACTIVE per compute "
+              "unit, and GRBM_GUI_ACTIVE per XCD.  The profiler serializes dispatches, so the clock row "
+              "divides GRBM_GUI_ACTIVE per XCD by the dispatch's own duration.", "",
               "| Counter | " + " | ".join(f"`{k}`" for k in kernels) + " |",
               "|---|" + "---|" * len(kernels)]
     for c in counters:
@@ -214,6 +237,18 @@ def sq(args):
             else:
                 vals.append(f"{t[num][0] / t[den][0]:.3f}")
         lines.append(f"| *{label}* | " + " | ".join(vals) + " |")
+    if clock:
+        def busy(counter, units):
+            return [f"{table[k][counter][0] / (clock[k][0] * units):.3f}" if k in clock and counter in table[k]
+                    else "" for k in kernels]
+        # launches of a few microseconds are dominated by the time the GPU
+        # stays active around the dispatch: no clock estimate for them
+        lines.append("| *shader clock (GHz)* | " + " | ".join(
+            f"{clock[k][0] / clock[k][1] / 1e9:.2f}" if k in clock and clock[k][1] and clock[k][1] > 50e-6 else ""
+            for k in kernels) + " |")
+        lines.append("| *MFMA busy share of SIMD cycles* | " + " | ".join(busy("SQ_VALU_MFMA_BUSY_CYCLES", N_SIMD))
+                     + " |")
+        lines.append("| *LDS busy share of CU cycles* | " + " | ".join(busy("SQ_LDS_IDX_ACTIVE", N_CU)) + " |")
     out = os.path.join(PROFILES, f"{args.kernel}_sq.md")
     with open(out, "w") as fh:
         fh.write("\n".join(lines) + "\n")
