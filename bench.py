@@ -796,7 +796,7 @@ def bench_chain(a):
     launch), both modes; ops/s = 2 engine operations per inner iteration /
     latency."""
     import torch
-    from paper_2608_13757_amd import MODE_BARRIER, MODE_BARRIER_FREE, Plan
+    from paper_2608_13757_amd import ALLOC_PER_ENGINE, MODE_BARRIER, MODE_BARRIER_FREE, Plan
     from workloads import chain_workload
 
     seeds = (0, 1, 2)
@@ -835,10 +835,21 @@ def bench_chain(a):
                 r[name]["in_kernel_us"] = float(stats.view(-1, 8)[:, 0].max().item()) * 0.01   # 100 MHz ticks
             if len(outs) == 2 and not torch.equal(outs["barrier_free"], outs["barrier"]):
                 raise SystemExit(f"chain ({kern}) seed {sd}: the two modes disagree")
+            if kern == "interp" and "barrier_free" in outs:
+                # per-engine counters (Section 6.1), which the interpreter runs
+                plan = Plan(w.prog, MODE_BARRIER_FREE, ALLOC_PER_ENGINE)
+                out.fill_(float("nan"))
+                r["barrier_free_per_engine"] = time_mode(plan, [base, x, out], trips, toff, 1, a.steps, a.warmup)
+                if not torch.equal(out, outs["barrier_free"]):
+                    raise SystemExit(f"chain (interp) seed {sd}: per-engine counters disagree with per-loop")
+                stats = torch.zeros(plan.n_waves * 8, dtype=torch.int64, device="cuda")
+                plan.run([base, x, out], trips, toff, 1, stats=stats)
+                plan.status()
+                r["barrier_free_per_engine"]["in_kernel_us"] = float(stats.view(-1, 8)[:, 0].max().item()) * 0.01
             per_seed[sd] = {"inner_iterations": w.n_tiles,
                             "latency_us": {k: v["ms_mean"] * 1e3 for k, v in r.items()},
                             "in_kernel_us": {k: v["in_kernel_us"] for k, v in r.items()}}
-            if len(r) == 2:
+            if "barrier" in r and "barrier_free" in r:
                 per_seed[sd]["speedup_vs_barrier"] = r["barrier"]["ms_mean"] / r["barrier_free"]["ms_mean"]
                 per_seed[sd]["in_kernel_speedup_vs_barrier"] = (r["barrier"]["in_kernel_us"] /
                                                                 r["barrier_free"]["in_kernel_us"])

@@ -560,7 +560,8 @@ def attn_program(heads: int, dim: int = ATTN_D, nk: int = ATTN_NK, nv: int = ATT
     """A fixed set of workgroups, each running a run-time list of (sequence,
     head, 128-query tile) work items:
 
-      T{ KV{ E0: LOADK K block -> kring[(r_KV - 1) % nk]
+      T{ E0: ACQK  E4: ACQV  E1: ACQS
+         KV{ E0: LOADK K block -> kring[(r_KV - 1) % nk]
              E4: LOADV V block -> vring[(r_KV - 1) % nv]
              E1: QK    S = Q K^T -> sp[(r_KV - 1) % 2]
              E2: SM    online softmax: P over S in place, alpha, running sum l
@@ -572,19 +573,19 @@ def attn_program(heads: int, dim: int = ATTN_D, nk: int = ATTN_NK, nv: int = ATT
     the tile's sequence length L; both known only at run time.  LOADK->QK,
     LOADV->PV, QK->SM, SM->PREAD (k=0) carry the data forward.  The rings
     and S/P slots are indexed by r_KV, which counts KV iterations over all
-    tiles, so their reuse dependencies QK->LOADK (k=nk), PV->LOADV (k=nv)
-    and PREAD->QK (k=2) are read with the linearized offset (an extension of
-    the paper's relation): the next tile's loads and QK steps overlap the
-    end of the previous tile.  SM->NORM (k=0, C2) delivers a tile's final
-    row sums; they are double-buffered by tile, and NORM->SM (k=2, C1 at T)
-    keeps a tile's softmax from overwriting a buffer before NORM of the tile
-    before last has read it.
+    tiles.  Their reuse dependencies QK->LOADK (k=nk), PV->LOADV (k=nv) and
+    PREAD->QK (k=2) are read per trip of KV (the paper's relation), and the
+    acquire instructions at each tile with QK->ACQK, PV->ACQV, PREAD->ACQS
+    (k=1, C3 at T) drain the previous tile's reads of the rings and S/P
+    slots before the next tile refills them.  SM->NORM (k=0, C2) delivers a
+    tile's final row sums; they are double-buffered by tile, and NORM->SM
+    (k=2, C1 at T) keeps a tile's softmax from overwriting a buffer before
+    NORM of the tile before last has read it.
 
-    ``linear=False`` uses the paper's relation only: the three reuse
-    dependencies are read per trip of KV, and acquire instructions at each
-    tile (ACQK on E0, ACQV on E4, ACQS on E1, before the KV loop) with
-    QK->ACQK, PV->ACQV, PREAD->ACQS (k=1, C3 at T) drain the previous tile's
-    reads of the rings and S/P slots before the next tile refills them."""
+    ``linear=True`` reads the three reuse dependencies with the linearized
+    offset instead (an extension of the paper's relation) and drops the
+    acquire instructions: the next tile's loads and QK steps overlap the end
+    of the previous tile."""
     b = ProgramBuilder("attn", n_engines=5, waves_per_engine=[1, 2, 4, 4, 1])
     with b.loop("T"):
         if not linear:
