@@ -291,7 +291,14 @@ bfs_status bfs_eval_threshold(const bfs_plan *plan, int32_t dep, uint32_t r_P, u
 void bfs_plan_destroy(bfs_plan *plan);
 
 /*
- * Enqueue one execution of the planned program on stream (asynchronous).
+ * Enqueue one execution of the planned program on stream (asynchronous): the
+ * engines run the program with the synchronization the plan emitted, the
+ * counter waits with Eq. 5's thresholds on the engines' loop registers
+ * (Section 5.1, entries and per-trip entries per loop; Section 5.5, one
+ * counter per loop and producer engine, or Eq. 3 per instruction, or the
+ * per-engine counters of Section 6.1) in barrier-free mode, the all-engine
+ * barriers and static ordinals of Section 3.4 in barrier mode; each
+ * instruction's counter is incremented when it retires.
  *
  *   dev_buffers  family-specific device pointers, n_buffers of them
  *                (interp / stream3: [0] int64 per-workgroup tile base,
