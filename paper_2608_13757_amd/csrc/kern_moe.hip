@@ -18,7 +18,9 @@
 //                           phase 2: 64 y columns); ACQE at each M-tile;
 //                           SPILL: one 32 x 32 block per chunk, packed to
 //                           bf16 into an epilogue slot.
-//   E2 (2 waves, epilogue)  EPI: 16-byte row segments of the chunk to HBM.
+//   E2 (2 waves, epilogue)  EPI: the chunk's 16-byte row segments into
+//                           registers, then to HBM (retiring from a single
+//                           epilogue slot before the stores).
 //
 // The M loop runs the workgroup's M-tiles, a count derived from the routing
 // and known only at run time; K runs K / 32 steps, C BM / 64 (phase 1) or
@@ -401,27 +403,62 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
         if (!S.aborted) {
           const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
           const uint32_t rb = kPhase == 1 ? c : (c >> 1), cb = kPhase == 1 ? 0u : (c & 1u);
+          auto seg = [&](int q, int h) {            // row segment h of MFMA wave ew * 4 + q's block
+            const uint32_t blk = ering + eslot * kESlotBytes + (ew * 4u + q) * 2048u;
+            const uint32_t row = 16u * h + (lane >> 2), cc = lane & 3u;
+            return *(const BFS_LDS u32x4 *)(uintptr_t)(blk + row * 64u + cc * 16u);
+          };
+          // the chunk's token of each lane row, tok[rb][h], selected without
+          // dynamic indexing (and before the lambdas, which must not take
+          // the array's address)
+          int32_t trow0 = tok[0][0], trow1 = tok[0][1];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const uint32_t v = ew * 4u + q;                 // MFMA wave whose block this is
-            const uint32_t blk = ering + eslot * kESlotBytes + v * 2048u;
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              const uint32_t row = 16u * h + (lane >> 2), cc = lane & 3u;
-              const u32x4 d = *(const BFS_LDS u32x4 *)(uintptr_t)(blk + row * 64u + cc * 16u);
-              int32_t t = tok[0][h];                        // tok[rb][h] without dynamic indexing
-#pragma unroll
-              for (int i = 1; i < kRB; ++i) t = rb == (uint32_t)i ? tok[i][h] : t;
-              const uint32_t col = kPhase == 1 ? (n0 + 32u * q + 8u * cc) : (n0 + 64u * q + 32u * cb + 8u * cc);
-              if (t >= 0) {
-                u32x4 *dst = reinterpret_cast<u32x4 *>(P.out + (size_t)t * P.ndim + col);
-                if (kPhase == 1) *dst = d;
-                else __builtin_nontemporal_store(d, dst);
-              }
-            }
+          for (int i = 1; i < kRB; ++i) {
+            trow0 = rb == (uint32_t)i ? tok[i][0] : trow0;
+            trow1 = rb == (uint32_t)i ? tok[i][1] : trow1;
           }
+          auto store = [&](int q, int h, const u32x4 &d) {
+            const uint32_t cc = lane & 3u;
+            const int32_t t = h == 0 ? trow0 : trow1;
+            const uint32_t col = kPhase == 1 ? (n0 + 32u * q + 8u * cc) : (n0 + 64u * q + 32u * cb + 8u * cc);
+            if (t >= 0) {
+              u32x4 *dst = reinterpret_cast<u32x4 *>(P.out + (size_t)t * P.ndim + col);
+              if (kPhase == 1) *dst = d;
+              else __builtin_nontemporal_store(d, dst);
+            }
+          };
+          // With one epilogue slot (256-row M-tiles) the chunk's segments go
+          // into registers first and EPI retires from the slot once these
+          // reads are issued
+          // (LDS executes the wave's reads before the signal that follows
+          // them), so the next chunk's spill does not wait behind this
+          // chunk's global stores.  With two slots the spill of chunk c + 2
+          // already overlaps these stores; there each segment is stored as
+          // it arrives and EPI retires after the stores (reading everything
+          // first measured slower at 128-row tiles).
+          bool early = false;
+          if constexpr (kBM == 256) early = P.e_ring == 1;
+          if (early) {
+            u32x4 d[4][2];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+              for (int h = 0; h < 2; ++h) d[q][h] = seg(q, h);
+            S.signal(P.epi.update, ew);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+              for (int h = 0; h < 2; ++h) store(q, h, d[q][h]);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+              for (int h = 0; h < 2; ++h) store(q, h, seg(q, h));
+            S.signal(P.epi.update, ew);
+          }
+        } else {
+          S.signal(P.epi.update, ew);
         }
-        S.signal(P.epi.update, ew);
         S.sync_point(S.word(2, ew));                              // end of a C iteration
       }
       S.sync_point(S.word(2, ew));                                // end of an M iteration
