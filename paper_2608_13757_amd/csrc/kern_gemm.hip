@@ -24,10 +24,11 @@
 // LDS (bytes): counters 2048 | K ring slots of 32 KiB (A 256 x 32 bf16, then
 // B 256 x 32 bf16; each row 64 B in four 16-byte chunks stored at chunk
 // c ^ ((row / 4) % 4), which makes the MFMA fragment reads conflict-free) |
-// bias 1 KiB.  The epilogue slots (16 KiB each: 8 blocks of 32 x 32 bf16,
-// row-major) reuse the memory of the K ring once the K loop is over; the
-// program's MMA->SPILL dependency orders every spill after the last K step
-// of every MFMA wave.
+// bias 1 KiB.  The epilogue slots (1, 2, 4 or 8 of 16 KiB each: 8 blocks of
+// 32 x 32 bf16, row-major; chunk c in slot c % slots) reuse the memory of
+// the K ring once the K loop is over; the program's MMA->SPILL dependency
+// orders every spill after the last K step of every MFMA wave.  With four
+// or eight slots the spills of a tile rarely or never wait for the stores.
 //
 // MFMA operand order: the first operand is the B^T fragment and the second
 // the A fragment, so lane l of a 32 x 32 block holds output row (l % 32) and
@@ -348,7 +349,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       S.wait(s_spill, P.spill, g, it + 1, c_r() - 1, [] {});
       if (!S.aborted) {
         const uint32_t b = it, bm = b >> 1, bn = b & 1u;
-        const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
+        const uint32_t eslot = it & (uint32_t)(P.e_ring - 1);   // e_ring is a power of two
         const uint32_t blk = ering_base + eslot * kESlotBytes + ew * 2048u;
         const f32x16 v = acc[it];
 #pragma unroll
@@ -386,7 +387,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
       S.wait_affine(s_epi, P.epi, g, it + 1, c_r() - 1, [] {});
       if (!S.aborted) {
         const uint32_t b = it, bm = b >> 1, bn = b & 1u;
-        const uint32_t eslot = P.e_ring == 2 ? (it & 1u) : 0u;
+        const uint32_t eslot = it & (uint32_t)(P.e_ring - 1);   // e_ring is a power of two
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const uint32_t v = ew * 4u + q;              // MFMA wave whose block this is
@@ -445,8 +446,8 @@ bfs_status launch_gemm(const bfs_plan *p, DevImage *img, const void *const *bufs
   if (M <= 0 || N <= 0 || K <= 0 || M % kTile || N % kTile || K % kBK)
     return fail(BFS_E_UNSUPPORTED, "gemm: M and N must be multiples of 256, K a multiple of 32");
   if ((uint64_t)kTile * K * 2 > 0xffffffffull) return fail(BFS_E_UNSUPPORTED, "gemm: K too large for 32-bit load offsets");
-  if (ring < 2 || ring > 4 || e_ring < 1 || e_ring > 2)
-    return fail(BFS_E_UNSUPPORTED, "gemm: ring of 2..4 slots, epilogue ring of 1..2 slots");
+  if (ring < 2 || ring > 4 || e_ring < 1 || e_ring > 8 || (e_ring & (e_ring - 1)))
+    return fail(BFS_E_UNSUPPORTED, "gemm: ring of 2..4 slots, epilogue ring of 1, 2, 4 or 8 slots");
   if ((M / kTile) * (N / kTile) != n_wg) return fail(BFS_E_INVALID, "gemm: n_wg must be (M / 256) * (N / 256)");
   if (nbufs < 4 || !bufs[0] || !bufs[1] || !bufs[2] || !bufs[3]) return fail(BFS_E_INVALID, "gemm: needs [A, Bt, bias, C]");
   if (!trips || !trip_off) return fail(BFS_E_INVALID, "gemm: needs trip tables");
