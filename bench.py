@@ -129,7 +129,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--n-wg", type=int, default=1024)
     ap.add_argument("--outer", type=int, default=256)
@@ -561,7 +561,9 @@ def bench_moe(a):
                    "ring_across_m_tiles": "barrier_free: ACQL drain (paper's relation); "
                                           "barrier_free_linearized: linearized MMA->LOAD (extension)",
                    "m_tile_rows": bm, "m_tiles_per_workgroup_run": mchunk,
-                   "ring_slots": MOE_RINGS[bm][0], "epilogue_slots": MOE_RINGS[bm][1], "n_wg": [launches[1][3], launches[2][3]], "parallelism": "single GPU"},
+                   "ring_slots": [MOE_RINGS[bm, 1][0], MOE_RINGS[bm, 2][0]],
+                   "epilogue_slots": [MOE_RINGS[bm, 1][1], MOE_RINGS[bm, 2][1]],
+                   "epilogue_slots_note": "0: each chunk of an M-tile in its own 16 KiB of the ring", "n_wg": [launches[1][3], launches[2][3]], "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
         "phase_us": {kk: [v["phase1_ms"] * 1e3, v["phase2_ms"] * 1e3] for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -19,31 +19,40 @@
 //                           SPILL: one 32 x 32 block per chunk, packed to
 //                           bf16 into an epilogue slot.
 //   E2 (2 waves, epilogue)  EPI: the chunk's 16-byte row segments into
-//                           registers, then to HBM (retiring from a single
-//                           epilogue slot before the stores).
+//                           registers, then to HBM (at 256-row tiles with at
+//                           most one epilogue slot, retiring before the
+//                           stores).
 //
 // The M loop runs the workgroup's M-tiles, a count derived from the routing
 // and known only at run time; K runs K / 32 steps, C BM / 64 (phase 1) or
-// BM / 32 (phase 2) chunks per M-tile.  Dependencies: LOAD->MMA (k = 0), MMA->LOAD
-// (k = ring), MMA->ACQL (k = 1, C3: an M-tile's loads start after the
-// previous tile's MFMAs released the ring), SPILL->EPI (k = 0), EPI->SPILL
-// (k = epilogue slots), EPI->ACQE (k = 1, C3).  In place of MMA->ACQL the
-// program may read MMA->LOAD with the linearized offset (an extension of
-// the paper's relation: k counts K steps over all M-tiles of the
-// workgroup), which orders exactly the reuse of ring slot (r_K - 1) % ring
-// across M-tiles, so the next tile's loads overlap the previous tile's
-// MFMAs; ACQL then waits for nothing.  Token rows past the expert's
-// count are loaded from a clamped row and never stored.
+// BM / 32 (phase 2) chunks per M-tile.  Dependencies: LOAD->MMA (k = 0),
+// MMA->LOAD (k = ring), SPILL->EPI (k = 0), EPI->ACQE (k = 1, C3), and one of
+// two epilogue layouts:
+//   * epilogue slots after the ring: EPI->SPILL (k = epilogue slots) and
+//     MMA->ACQL (k = 1, C3: an M-tile's loads start after the previous
+//     tile's MFMAs released the ring);
+//   * epilogue in the ring (epilogue ring 0): every chunk of an M-tile has
+//     its own 16 KiB of the ring, MMA->SPILL (k = 0, C2: the spills start
+//     after the tile's last MFMAs read the ring) and EPI->ACQL (k = 1, C3:
+//     the next tile's loads start after the epilogue read its chunks), so
+//     the MFMA engine spills a whole M-tile without waiting for the stores.
+// In place of MMA->ACQL the program may read MMA->LOAD with the linearized
+// offset (an extension of the paper's relation: k counts K steps over all
+// M-tiles of the workgroup), which orders exactly the reuse of ring slot
+// (r_K - 1) % ring across M-tiles, so the next tile's loads overlap the
+// previous tile's MFMAs.  Token rows past the expert's count are loaded from
+// a clamped row and never stored.
 //
 // LDS (bytes): counters 2048 | ring slots of BM x 64 + 16 KiB (token rows
 // BM x 64 B, then weight rows 256 x 64 B; 16-byte chunk c of row r at
 // c ^ ((r / 4) % 4))
-// | epilogue slots of 16 KiB (8 blocks of 32 x 32 bf16, row-major).
+// | epilogue slots of 16 KiB (8 blocks of 32 x 32 bf16, row-major), unless
+// the epilogue lives in the ring.
 //
 // Family contract (BFS_KERNEL_MOE): loops top -> M -> {K, C}; ACQL (E0, NOP)
 // at M before K; LOAD (E0, opcode 48, args [phase, K, N, ring, BM (0: 128)]) and MMA (E1,
 // 49) in K; ACQE (E1, NOP) at M between K and C; SPILL (E1, 51, args
-// [epilogue ring]) and EPI (E2, 50) in C; waves 2, 8, 2.  Phase 1: K = hidden
+// [epilogue slots, 0: in the ring]) and EPI (E2, 50) in C; waves 2, 8, 2.  Phase 1: K = hidden
 // (multiple of 32), N = ffn (multiple of 128); phase 2: K = ffn (multiple of
 // 32), N = hidden (multiple of 256).  Buffers: [0] work list int32 [n_wg][4]
 // = (expert, first output column, first M-tile, M-tiles), [1] perm int32
@@ -100,7 +109,9 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint32_t *cnt = reinterpret_cast<uint32_t *>(lds);
   const uint32_t ring = lds_addr(lds) + kCntBytes;
-  const uint32_t ering = ring + (uint32_t)P.ring * kSlotBytes;
+  // epilogue slots: after the ring, or (e_ring 0) the ring's own memory,
+  // one 16 KiB slot per chunk, free once the M-tile's K loop is over
+  const uint32_t ering = P.e_ring == 0 ? ring : ring + (uint32_t)P.ring * kSlotBytes;
   for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
   __syncthreads();
 
@@ -350,7 +361,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
         g.h3 = c + 1;
         S.wait_affine(sc, P.spill, g, c + 1, g.r3 - 1, [] {});
         if (!S.aborted) {
-          const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
+          const uint32_t eslot = P.e_ring == 0 ? c : (P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u);
           const uint32_t blk = ering + eslot * kESlotBytes + ew * 2048u;
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
@@ -401,7 +412,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
         g.h3 = c + 1;
         S.wait_affine(sa, P.epi, g, c + 1, g.r3 - 1, [] {});
         if (!S.aborted) {
-          const uint32_t eslot = P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u;
+          const uint32_t eslot = P.e_ring == 0 ? c : (P.e_ring == 2 ? ((g.r3 - 1) & 1u) : 0u);
           const uint32_t rb = kPhase == 1 ? c : (c >> 1), cb = kPhase == 1 ? 0u : (c & 1u);
           auto seg = [&](int q, int h) {            // row segment h of MFMA wave ew * 4 + q's block
             const uint32_t blk = ering + eslot * kESlotBytes + (ew * 4u + q) * 2048u;
@@ -437,7 +448,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
           // it arrives and EPI retires after the stores (reading everything
           // first measured slower at 128-row tiles).
           bool early = false;
-          if constexpr (kBM == 256) early = P.e_ring == 1;
+          if constexpr (kBM == 256) early = P.e_ring <= 1;
           if (early) {
             u32x4 d[4][2];
 #pragma unroll
@@ -501,19 +512,31 @@ bfs_status launch_moe(const bfs_plan *p, DevImage *img, const void *const *bufs,
   if (phase != 1 && phase != 2) return fail(BFS_E_UNSUPPORTED, "moe: phase 1 or 2");
   if (K <= 0 || K % kBK || N <= 0 || N % (phase == 1 ? 128 : 256))
     return fail(BFS_E_UNSUPPORTED, "moe: K a multiple of 32, N a multiple of 128 (phase 1) or 256 (phase 2)");
-  if (ring < 2 || ring > 5 || e_ring < 1 || e_ring > 2) return fail(BFS_E_UNSUPPORTED, "moe: ring 2..5, epilogue 1..2");
+  if (ring < 2 || ring > 5 || e_ring < 0 || e_ring > 2)
+    return fail(BFS_E_UNSUPPORTED, "moe: ring 2..5, epilogue 1..2 slots or 0 (in the ring)");
+  const int chunks = phase == 1 ? bm / 64 : bm / 32;
+  if (e_ring == 0 && (size_t)chunks * kESlotBytes > (size_t)ring * slot_bytes(bm))
+    return fail(BFS_E_UNSUPPORTED, "moe: the M-tile's chunks do not fit in the ring");
   const size_t lds = kCntBytes + (size_t)ring * slot_bytes(bm) + (size_t)e_ring * kESlotBytes;
   if (lds > 160 * 1024)
     return fail(BFS_E_RESOURCE, "moe: ring and epilogue slots exceed 160 KiB of LDS");
   if ((uint64_t)N * K * 2 > 0xffffffffull) return fail(BFS_E_UNSUPPORTED, "moe: one expert's matrix must stay below 4 GiB");
-  // the ring is protected across M-tiles either by MMA->ACQL (k = 1) or by
-  // reading MMA->LOAD with the linearized offset (slots are indexed by r_K)
+  // the ring is protected across M-tiles by MMA->ACQL (k = 1), or by reading
+  // MMA->LOAD with the linearized offset (slots are indexed by r_K); with
+  // the epilogue in the ring (e_ring 0) the spills wait for the M-tile's
+  // last MFMAs (MMA->SPILL, k = 0) and the next M-tile's loads for the
+  // epilogue's reads (EPI->ACQL, k = 1), which also orders them after the
+  // MFMAs; the epilogue slots are otherwise reused by EPI->SPILL (k =
+  // e_ring) within an M-tile
   bool ring_linear = false;
   for (size_t d = 0; d < p->deps.size() / 3; ++d)
     if (p->deps[3 * d] == mma && p->deps[3 * d + 1] == load && p->deps[3 * d + 2] == ring && p->dep_linear[d])
       ring_linear = true;
-  if (!has_dep(p, load, mma, 0) || !has_dep(p, mma, load, ring) || !(ring_linear || has_dep(p, mma, acql, 1)) ||
-      !has_dep(p, spill, epi, 0) || !has_dep(p, epi, spill, e_ring) || !has_dep(p, epi, acqe, 1))
+  const bool epi_ok = e_ring == 0 ? (has_dep(p, mma, spill, 0) && has_dep(p, epi, acql, 1))
+                                  : has_dep(p, epi, spill, e_ring);
+  const bool across = ring_linear || has_dep(p, mma, acql, 1) || (e_ring == 0 && has_dep(p, epi, acql, 1));
+  if (!has_dep(p, load, mma, 0) || !has_dep(p, mma, load, ring) || !across || !epi_ok ||
+      !has_dep(p, spill, epi, 0) || !has_dep(p, epi, acqe, 1))
     return fail(BFS_E_UNSUPPORTED, "moe: missing a ring or M-tile dependency");
   const int need = phase == 1 ? 7 : 6;
   if (nbufs < need) return fail(BFS_E_INVALID, "moe: too few buffers");
