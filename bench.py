@@ -128,8 +128,8 @@ def oracle_rate(fn, chunks, units, budget_s=8.0, max_cores=16):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--n-wg", type=int, default=1024)
     ap.add_argument("--outer", type=int, default=256)

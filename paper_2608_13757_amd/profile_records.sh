@@ -2,7 +2,7 @@
 # Writes profiles/<kernel>_traffic.json and profiles/<kernel>_kernel_trace.md
 # from the rocprofv3 output of these runs under one output root R (repository
 # root, TMPDIR=/tmp):
-#   rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 20 --warmup 20 --modes barrier_free,barrier --no-cpu-baseline
+#   rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 50 --warmup 50 --modes barrier_free,barrier --no-cpu-baseline
 #   rocprofv3 --pmc FETCH_SIZE --output-format csv -d $R/pf_$wl -o f -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024
 #   rocprofv3 --pmc WRITE_SIZE --output-format csv -d $R/pw_$wl -o w -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free --no-cpu-baseline --copy-calibration-mib 1024
 #   rocprofv3 --pmc $SQ1 --output-format csv -d $R/ps1_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free,barrier --no-cpu-baseline
@@ -37,6 +37,6 @@ for wl in ${WLS:-stream gemm attn moe rmsnorm adamw}; do
       --command "WLS=$wl bash paper_2608_13757_amd/profile_records.sh $R"
   fi
   python -m paper_2608_13757_amd.profiles trace --kernel $k --stats-dir $R/pt_$wl --workload "$wk" \
-    --command "rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 20 --warmup 20 --modes barrier_free,barrier --no-cpu-baseline" \
+    --command "rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 50 --warmup 50 --modes barrier_free,barrier --no-cpu-baseline" \
     --command "WLS=$wl bash paper_2608_13757_amd/profile_records.sh $R"
 done
