@@ -39,8 +39,8 @@ def _bits_to_dev(bits):
     return torch.from_numpy(bits.view(np.int16)).cuda()
 
 
-def run_gemm(gi, m, n, k, mode, cap=0, alloc=ALLOC_PER_LOOP):
-    prog = gemm_program(m, n, k)
+def run_gemm(gi, m, n, k, mode, cap=0, alloc=ALLOC_PER_LOOP, e_ring=None):
+    prog = gemm_program(m, n, k) if e_ring is None else gemm_program(m, n, k, e_ring=e_ring)
     plan = Plan(prog, mode, alloc)
     tt = gemm_trips(m, n, k)
     trips, toff = trip_tensors(tt)
@@ -213,6 +213,34 @@ def test_gemm_small_parity_and_thresholds(shape):
         assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
         outs[name] = out
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+def test_gemm_epilogue_rings():
+    """Epilogue rings of 1, 2, 4 and 8 slots in the idle K ring (EPI->SPILL
+    at offset = slots): every logged threshold equals the oracle's in both
+    modes, outputs bit-identical across ring sizes and modes; sizes that are
+    not a power of two, or larger than 8, are refused."""
+    m, n, k = 512, 512, 256
+    gi = gemm_inputs(seed=4, m=m, n=n, k=k)
+    ref = mathref.gemm_bias_gelu(gi.a, gi.bt, gi.bias)
+    outs = {}
+    for e_ring in (1, 2, 4, 8):
+        for name, mode in MODES:
+            _say(f"[gemm-epilogue] e_ring={e_ring} mode={name}")
+            prog, plan, tt, out, logw = run_gemm(gi, m, n, k, mode, cap=512, e_ring=e_ring)
+            check_close(out, ref)
+            trips, off = tt.flat()
+            recs = {g: core.run(prog, trips, off[g], g).recs for g in range(tt.n_wg)}
+            logs = log_records(plan, logw, tt.n_wg, 512, per_wave=True)
+            assert compare_wave_logs_with_oracle(prog, plan, logs, recs, name) > 0
+            outs[(e_ring, name)] = out
+    first = next(iter(outs.values()))
+    for key, out in outs.items():
+        assert np.array_equal(out.view(np.uint32), first.view(np.uint32)), key
+    for bad in (3, 16):
+        with pytest.raises(BfsError) as e:
+            run_gemm(gi, m, n, k, MODE_BARRIER_FREE, e_ring=bad)
+        assert e.value.status == bfs.E_UNSUPPORTED
 
 
 def test_gemm_special_cases():

@@ -74,10 +74,11 @@ class MoeRun:
             return [work, self.perm, self.eoff, self.x, self.wg, self.wu, self.h]
         return [work, self.perm, self.eoff, self.h, self.wd, self.y]
 
-    def run(self, mode, cap=0, alloc=ALLOC_PER_LOOP, linear=False):
+    def run(self, mode, cap=0, alloc=ALLOC_PER_LOOP, linear=False, ring=None, e_ring=None):
         logs = {}
         for ph in (1, 2):
-            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn, linear=linear, bm=self.bm), mode, alloc)
+            plan = Plan(moe_program(ph, self.moe.hidden, self.moe.ffn, linear=linear, bm=self.bm, ring=ring,
+                                    e_ring=e_ring), mode, alloc)
             work, trips, toff, n_wg = self.dev_wl[ph]
             log = None
             if cap:
@@ -191,6 +192,40 @@ def test_moe_per_instr(bm):
         assert compare_wave_logs_with_oracle(prog, plan, lg, recs, "per_instr") > 0
     _, y2, _ = r.run(MODE_BARRIER_FREE)
     assert np.array_equal(y.view(np.uint32), y2.view(np.uint32))
+
+
+@pytest.mark.parametrize("bm,layouts", [(128, [(5, 0), (5, 1), (5, 2)]), (256, [(4, 0), (4, 1), (3, 2)])])
+def test_moe_epilogue_layouts(bm, layouts):
+    """Both epilogue layouts in both phases: (ring, epilogue slots) with the
+    chunks in the K ring (0: MMA->SPILL and EPI->ACQL) or in 1 or 2 slots
+    after it (EPI->SPILL and MMA->ACQL); outputs equal the oracle's and,
+    bit for bit, each other in both modes, and every logged threshold equals
+    the oracle's.  A layout beyond 160 KiB of LDS is refused."""
+    moe = moe_inputs(seed=4, hidden=256, ffn=256, counts=SMALL_COUNTS)
+    r = MoeRun(moe, mchunk=2, bm=bm)
+    ref_y = mathref.moe_tokens(moe, range(len(moe.assign)))
+    first = None
+    for ring, e_ring in layouts:
+        for name, mode in MODES:
+            _say(f"[moe-epilogue] bm={bm} ring={ring} e_ring={e_ring} mode={name}")
+            h, y, logs = r.run(mode, cap=64, ring=ring, e_ring=e_ring)
+            check_close(y, ref_y)
+            for ph in (1, 2):
+                plan, logw = logs[ph]
+                prog = moe_program(ph, moe.hidden, moe.ffn, bm=bm, ring=ring, e_ring=e_ring)
+                wl = r.wl[ph]
+                trips, off = wl.trips.flat()
+                recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
+                lg = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
+                assert compare_wave_logs_with_oracle(prog, plan, lg, recs, name) > 0
+            if first is None:
+                first = (h, y)
+            assert np.array_equal(h.view(np.uint32), first[0].view(np.uint32))
+            assert np.array_equal(y.view(np.uint32), first[1].view(np.uint32))
+    if bm == 256:
+        with pytest.raises(BfsError) as e:
+            r.run(MODE_BARRIER_FREE, ring=4, e_ring=2)
+        assert e.value.status == bfs.E_RESOURCE
 
 
 @pytest.fixture(scope="module")
