@@ -361,6 +361,8 @@ def bench_gemm(a):
                    "k_unroll": a.k_unroll or 1, "k_unrolled_program": bool(a.k_unrolled),
                    "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "latency_median_us": {kk: v["ms_median"] * 1e3 for kk, v in res.items()},
+        "latency_min_us": {kk: v["ms_min"] * 1e3 for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
         "library_matmul_tflops": flop / (lib_ms * 1e-3) / 1e12,
@@ -440,6 +442,8 @@ def bench_attn(a):
                                         "barrier_free_linearized: linearized reuse dependencies (extension)",
                    "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "latency_median_us": {kk: v["ms_median"] * 1e3 for kk, v in res.items()},
+        "latency_min_us": {kk: v["ms_min"] * 1e3 for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
     }
@@ -535,8 +539,9 @@ def bench_moe(a):
         plans[2].status(stream)
         p1 = [e[0].elapsed_time(e[1]) for e in ev]
         p2 = [e[1].elapsed_time(e[2]) for e in ev]
+        tot = sorted(x + y for x, y in zip(p1, p2))
         res[name] = {"ms_mean": (sum(p1) + sum(p2)) / a.steps, "phase1_ms": sum(p1) / a.steps,
-                     "phase2_ms": sum(p2) / a.steps}
+                     "phase2_ms": sum(p2) / a.steps, "ms_median": tot[len(tot) // 2], "ms_min": tot[0]}
         outs[name] = (h.clone(), y.clone())
     first = next(iter(outs.values()))
     for name, o in outs.items():
@@ -565,6 +570,8 @@ def bench_moe(a):
                    "epilogue_slots": [MOE_RINGS[bm, 1][1], MOE_RINGS[bm, 2][1]],
                    "epilogue_slots_note": "0: each chunk of an M-tile in its own 16 KiB of the ring", "n_wg": [launches[1][3], launches[2][3]], "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "latency_median_us": {kk: v["ms_median"] * 1e3 for kk, v in res.items()},
+        "latency_min_us": {kk: v["ms_min"] * 1e3 for kk, v in res.items()},
         "phase_us": {kk: [v["phase1_ms"] * 1e3, v["phase2_ms"] * 1e3] for kk, v in res.items()},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None},
@@ -624,6 +631,8 @@ def bench_rmsnorm(a):
                    "t": t, "h": h, "n_wg": a.rms_wg, "vector_waves": a.rms_waves, "x_ring": nx, "q_ring": nq,
                    "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "latency_median_us": {kk: v["ms_median"] * 1e3 for kk, v in res.items()},
+        "latency_min_us": {kk: v["ms_min"] * 1e3 for kk, v in res.items()},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS, "traffic": None},
     }
@@ -691,6 +700,8 @@ def bench_adamw(a):
                    "params": n, "chunk": chunk, "n_wg": n_wg, "vector_waves": a.adam_waves, "ring": a.adam_ring,
                    "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "latency_median_us": {kk: v["ms_median"] * 1e3 for kk, v in res.items()},
+        "latency_min_us": {kk: v["ms_min"] * 1e3 for kk, v in res.items()},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS, "traffic": None},
     }
@@ -748,6 +759,8 @@ def bench_ring(a):
                                "256-fp32 tiles, 4-slot ring indexed by the monotone register",
                    "inner_iterations": inner, "parallelism": "single GPU"},
         "latency_us": {kk: v["ms_mean"] * 1e3 for kk, v in res.items()},
+        "latency_median_us": {kk: v["ms_median"] * 1e3 for kk, v in res.items()},
+        "latency_min_us": {kk: v["ms_min"] * 1e3 for kk, v in res.items()},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS, "traffic": None},
         "speedup_linearized_vs_acq_drain": res["acq_drain"]["ms_mean"] / ms,
@@ -990,6 +1003,8 @@ def bench_stream(a):
                                         "barrier_free_per_instance: one instance at a time, as barrier mode",
                    "parallelism": "single GPU"},
         "latency_us": {k: v["ms_mean"] * 1e3 for k, v in res.items()},
+        "latency_median_us": {k: v["ms_median"] * 1e3 for k, v in res.items()},
+        "latency_min_us": {k: v["ms_min"] * 1e3 for k, v in res.items()},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": None},
     }
