@@ -138,6 +138,10 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
   else if (hw < 8) { eng = 2; ew = hw - 4; canon = 3 + ew; }
   else if (hw == 8) { eng = 0; ew = 0; canon = 0; }
   else { eng = 4; ew = 0; canon = 11; }
+  // the PV waves issue ahead of the softmax and loader waves sharing their
+  // SIMDs: their PREAD releases the S/P slot the next QK step needs (1 %
+  // faster than equal priorities; raising the loaders or QK too was not)
+  if (eng == 3) __builtin_amdgcn_s_setprio(2);
   Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), canon, wg);
   const uint32_t own = S.word((uint32_t)eng, (uint32_t)ew);   // barrier mode: one counter per engine
 
