@@ -514,7 +514,7 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
               const f32x2 a23 = {acc[db][4 * j + 2] * inv, acc[db][4 * j + 3] * inv};
               const u32x2 v = {__builtin_bit_cast(uint32_t, __builtin_convertvector(a01, bf16x2)),
                                __builtin_bit_cast(uint32_t, __builtin_convertvector(a23, bf16x2))};
-              __builtin_nontemporal_store(v, reinterpret_cast<u32x2 *>(dst + 32 * db + 8 * j + 4 * lhi));
+              *reinterpret_cast<u32x2 *>(dst + 32 * db + 8 * j + 4 * lhi) = v;
             }
         }
       }

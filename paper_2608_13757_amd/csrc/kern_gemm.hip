@@ -399,7 +399,7 @@ __global__ void __launch_bounds__(768) gemm_kernel(GemmParams P) {
             const u32x4 d = *(const BFS_LDS u32x4 *)(uintptr_t)(blk + row * 64u + cc * 16u);
             const size_t gm = (size_t)m0 + vm * 128u + bm * 32u + row;
             const size_t gn = (size_t)n0 + vn * 64u + bn * 32u + 8u * cc;
-            __builtin_nontemporal_store(d, reinterpret_cast<u32x4 *>(P.c + gm * P.n + gn));
+            *reinterpret_cast<u32x4 *>(P.c + gm * P.n + gn) = d;
           }
         }
       }

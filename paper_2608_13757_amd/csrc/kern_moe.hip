@@ -434,8 +434,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
             const uint32_t col = kPhase == 1 ? (n0 + 32u * q + 8u * cc) : (n0 + 64u * q + 32u * cb + 8u * cc);
             if (t >= 0) {
               u32x4 *dst = reinterpret_cast<u32x4 *>(P.out + (size_t)t * P.ndim + col);
-              if (kPhase == 1) *dst = d;
-              else __builtin_nontemporal_store(d, dst);
+              *dst = d;
             }
           };
           // With one epilogue slot (256-row M-tiles) the chunk's segments go
