@@ -40,7 +40,10 @@
 // of row r at c ^ 4 (r mod 4), the layout the transposing fragment reads need
 // to be conflict-free) | 2 S/P slots of 32 KiB (S fp32 [128][64]: 16-byte
 // chunk c of row r at c ^ (r mod 16); P bf16 overwrites it with 8 chunks per
-// row at the same permutation) | alpha [2][128] fp32 | l [2][128] fp32.
+// row at the same permutation) | alpha [2][128] fp32 | l [2][128] fp32 |
+// the workgroup's tile descriptors, staged at the start in what is left of
+// the 160 KiB (up to 1024 tiles, 16 bytes plus a 4-byte KV trip each; later
+// tiles read their descriptors from memory).
 //
 // MFMA v_mfma_f32_32x32x16_bf16: lane l supplies row l % 32 of the first
 // operand and column l % 32 of the second, k = 8 (l / 32) .. + 7, and holds
@@ -87,6 +90,7 @@ struct AttnParams {
   const int32_t *trips;
   const int64_t *trip_off;
   int32_t heads, nk, nv;
+  int32_t desc_cap;          // tile descriptors staged in LDS at most
   float scale_log2;          // log2(e) / sqrt(128)
 };
 
@@ -122,12 +126,26 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
   const uint32_t spbuf = vring + (uint32_t)P.nv * kKVSlot;
   const uint32_t alpha_l = spbuf + 2u * kSPSlot;
   const uint32_t lsum_l = alpha_l + 2u * kBQ * 4u;
+  // the workgroup's tile descriptors (first token, length, first query row,
+  // head) and KV trips, staged in LDS once so that a tile's start reads LDS
+  // rather than memory
+  const uint32_t desc_l = lsum_l + 2u * kBQ * 4u;
+  const uint32_t dtrip_l = desc_l + 16u * (uint32_t)P.desc_cap;
+  const int wg = blockIdx.x;
+  const int64_t *toff = P.trip_off + (int64_t)wg * 3;
+  const uint32_t trip_t = (uint32_t)ldc(P.trips + ldc(toff + 1));
+  const int64_t kv_off = ldc(toff + 2);
+  const uint32_t n_staged = min(trip_t, (uint32_t)P.desc_cap);
   for (int i = threadIdx.x; i < bfs::kMaxSlots * bfs::kMaxWavesPerEngine; i += blockDim.x) cnt[i] = 0;
+  for (uint32_t t = threadIdx.x; t < n_staged; t += blockDim.x) {
+    const int64_t row = (int64_t)wg + (int64_t)t * gridDim.x;
+    *(BFS_LDS u32x4 *)(uintptr_t)(desc_l + 16u * t) = *reinterpret_cast<const u32x4 *>(P.work + 4 * row);
+    *(BFS_LDS int32_t *)(uintptr_t)(dtrip_l + 4u * t) = P.trips[kv_off + t];
+  }
   __syncthreads();
 
   const int hw = wave_id();
   const uint32_t lane = lane_id(), l32 = lane & 31u, lhi = lane >> 5;
-  const int wg = blockIdx.x;
   // hardware wave -> (engine, wave within the engine), hardware wave w on
   // SIMD w % 4: the two QK waves on SIMDs 0 and 1, the four PV waves two
   // each on SIMDs 2 and 3 (equal MFMA work per SIMD), one softmax wave per
@@ -145,9 +163,6 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
   Sync<kMode, kInstr> S(P.sc, lds_addr(cnt), canon, wg);
   const uint32_t own = S.word((uint32_t)eng, (uint32_t)ew);   // barrier mode: one counter per engine
 
-  const int64_t *toff = P.trip_off + (int64_t)wg * 3;
-  const uint32_t trip_t = (uint32_t)ldc(P.trips + ldc(toff + 1));
-  const int64_t kv_off = ldc(toff + 2);
   const size_t row_stride = (size_t)P.heads * kD;     // elements between tokens
   // tile t of this workgroup: row wg + t * n_wg of the work list, its KV
   // trip from the trip table (a trip beyond the sequence is reported and
@@ -157,13 +172,22 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
     uint32_t trip;
   };
   auto tile = [&](uint32_t t) {
-    const int64_t row = (int64_t)wg + (int64_t)t * gridDim.x;
     Tile x;
-    x.s0 = ldc(P.work + 4 * row + 0);
-    x.L = ldc(P.work + 4 * row + 1);
-    x.q0 = ldc(P.work + 4 * row + 2);
-    x.head = ldc(P.work + 4 * row + 3);
-    x.trip = (uint32_t)ldc(P.trips + kv_off + t);
+    if (t < n_staged) {
+      const u32x4 d = *(const BFS_LDS u32x4 *)(uintptr_t)(desc_l + 16u * t);
+      x.s0 = __builtin_amdgcn_readfirstlane((int32_t)d.x);
+      x.L = __builtin_amdgcn_readfirstlane((int32_t)d.y);
+      x.q0 = __builtin_amdgcn_readfirstlane((int32_t)d.z);
+      x.head = __builtin_amdgcn_readfirstlane((int32_t)d.w);
+      x.trip = (uint32_t)__builtin_amdgcn_readfirstlane(*(const BFS_LDS int32_t *)(uintptr_t)(dtrip_l + 4u * t));
+    } else {
+      const int64_t row = (int64_t)wg + (int64_t)t * gridDim.x;
+      x.s0 = ldc(P.work + 4 * row + 0);
+      x.L = ldc(P.work + 4 * row + 1);
+      x.q0 = ldc(P.work + 4 * row + 2);
+      x.head = ldc(P.work + 4 * row + 3);
+      x.trip = (uint32_t)ldc(P.trips + kv_off + t);
+    }
     const uint32_t max_trip = x.L > 0 ? (uint32_t)((x.L + kBKV - 1) / kBKV) : 0u;
     if (x.trip > max_trip) {
       report_input(P.sc.err, 1u, (uint32_t)wg, t, x.trip, max_trip, (uint32_t)hw);
@@ -281,12 +305,8 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
       g.r1 += 1;
       g.h1 = t + 1;
       const Tile x = tile(t);
-      // acquire form: the previous tile's S/P slots are released (its PREADs
-      // have read them) before this tile's first QK writes one
-      S.wait(s_acq, P.acqs, g, t + 1, g.r1 - 1, [] {});   // ACQS
-      S.signal(P.acqs.update, ew);
       // the tile's 64 query rows of this wave, held in registers for its KV
-      // loop
+      // loop; loaded before the acquire so that their latency overlaps it
       bf16x8 qf[2][8];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
@@ -296,6 +316,10 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
         for (int s = 0; s < 8; ++s)
           qf[qb][s] = x.L > 0 ? __builtin_bit_cast(bf16x8, *(const u32x4 *)(src + 16 * s)) : bf16x8{};
       }
+      // acquire form: the previous tile's S/P slots are released (its PREADs
+      // have read them) before this tile's first QK writes one
+      S.wait(s_acq, P.acqs, g, t + 1, g.r1 - 1, [] {});   // ACQS
+      S.signal(P.acqs.update, ew);
       S.sync_point(own);                                     // before loop KV
       S.enter(site, P.qk, g, 2);
       for (uint32_t it = 0; it < x.trip; ++it, kslot = (kslot + 1 == (uint32_t)P.nk) ? 0u : kslot + 1) {
@@ -561,8 +585,13 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   const int heads = p->instr_args[8 * lk + 2], dim = p->instr_args[8 * lk + 3];
   if (dim != kD || p->instr_args[8 * lv + 3] != kD) return fail(BFS_E_UNSUPPORTED, "attn: head dimension 128");
   if (heads <= 0 || p->instr_args[8 * lv + 2] != heads) return fail(BFS_E_INVALID, "attn: heads must match");
-  const size_t lds = kCntBytes + (size_t)(nk + nv) * kKVSlot + 2 * kSPSlot + 4 * kBQ * 4;
-  if (nk < 2 || nv < 2 || lds > 160 * 1024) return fail(BFS_E_UNSUPPORTED, "attn: ring depths >= 2 within 160 KiB of LDS");
+  const size_t lds_base = kCntBytes + (size_t)(nk + nv) * kKVSlot + 2 * kSPSlot + 4 * kBQ * 4;
+  if (nk < 2 || nv < 2 || lds_base > 160 * 1024)
+    return fail(BFS_E_UNSUPPORTED, "attn: ring depths >= 2 within 160 KiB of LDS");
+  // the rest of the LDS (up to 1024 tiles) stages tile descriptors: 16 bytes
+  // and a 4-byte KV trip per tile; tiles beyond it read memory
+  const int32_t desc_cap = (int32_t)std::min<size_t>(1024, (160 * 1024 - lds_base) / 20);
+  const size_t lds = lds_base + (size_t)desc_cap * 20;
   // The kernel's buffers are only race-free under these dependencies.  The
   // rings and S/P slots are indexed by r_KV over all tiles, so their reuse
   // across tiles is ordered either by reading the reuse dependencies with
@@ -618,6 +647,7 @@ bfs_status launch_attn(const bfs_plan *p, DevImage *img, const void *const *bufs
   P.heads = heads;
   P.nk = nk;
   P.nv = nv;
+  P.desc_cap = desc_cap;
   P.scale_log2 = 1.4426950408889634f / 11.313708498984761f;   // log2(e) / sqrt(128)
   const bool instr = dbg || o.dev_stats || o.fault_dep >= 0;
   hipStream_t s = (hipStream_t)stream;

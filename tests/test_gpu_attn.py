@@ -136,6 +136,25 @@ def test_attn_acquire_form_parity_and_thresholds(rings, n_wg):
     assert np.array_equal(outs["barrier_free"].view(np.uint32), lin.view(np.uint32))
 
 
+def test_attn_tiles_beyond_staged_descriptors():
+    """One workgroup runs 700 tiles (700 sequences of 1 to 128 keys, one
+    head): the kernel stages the first tile descriptors in the LDS left over
+    by the rings (614 of them at the benchmark's rings) and reads the rest
+    from memory.  Values against the oracle, both modes bit-identical."""
+    heads = 1
+    lengths = np.random.default_rng(7).integers(1, 129, 700)
+    ai = attn_inputs(seed=7, heads=heads, lengths=lengths)
+    ref = mathref.attention(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[attn-many-tiles] mode={name}")
+        _, _, wl, out, _ = run_attn(ai, heads, mode, n_wg=1)
+        assert len(wl.trips.per_wg[0][2]) == 700
+        check_close(out, ref)
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
 def test_attn_per_instr():
     """One counter per producer instruction (Eq. 3): thresholds equal the
     Eq. 1 counts for every wave, values as with per-loop counters."""
