@@ -625,9 +625,9 @@ class AttnWork:
 
 
 ATTN_WG = 256                # workgroups: one per compute unit (the LDS allows one per CU)
-ATTN_TILE_COST = 14          # fixed cost of a tile in KV steps, for balancing (measured: about 20 us
-                             # per tile of fill and drain against 1.4 us per KV step with one tile
-                             # per workgroup)
+ATTN_TILE_COST = 5           # fixed cost of a tile in KV steps, for balancing (measured on uniform
+                             # lengths: about 6.3 us per tile against 1.27 us per KV step; 0, 5, 9
+                             # and 14 time the same within 2 %)
 
 
 def attn_worklist(lengths, heads: int, xcds: int = 8, n_wg: int = ATTN_WG) -> AttnWork:
