@@ -8,9 +8,10 @@
 #   rocprofv3 --pmc $SQ1 --output-format csv -d $R/ps1_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free,barrier --no-cpu-baseline
 #   rocprofv3 --pmc $SQ2 --output-format csv -d $R/ps2_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free,barrier --no-cpu-baseline
 # (SQ1, SQ2 below; the SQ records are written when those runs exist)
-# for wl in stream gemm attn moe rmsnorm adamw.  The algorithmic bytes per
-# step come from bench.py --algorithmic-bytes (the same count the benchmark
-# divides by).
+# for wl in stream gemm attn moe rmsnorm adamw, and the trace run alone for
+# chain (one workgroup, latency-bound: no traffic or SQ record).  The
+# algorithmic bytes per step come from bench.py --algorithmic-bytes (the same
+# count the benchmark divides by).
 set -e
 R=${1:?usage: profile_records.sh <rocprofv3 output root>}
 SQ1="SQ_WAVES SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY SQ_INSTS_SALU SQ_INSTS_LDS"
@@ -23,7 +24,9 @@ for wl in ${WLS:-stream gemm attn moe rmsnorm adamw}; do
     adamw) k=adamw; wk="AdamW step, 2^20 fp32 parameters, 512 workgroups of 2 chunks of 1024, 2 vector waves, 2-slot ring, seed 0";;
     rmsnorm) k=rms; wk="RMSNorm + FP8 E4M3 quantization, 32768 x 8192 bf16, 768 workgroups, 4 vector waves, rings 2 + 2, seed 0";;
     moe) k=moe; wk="MoE grouped GEMM, 32768 tokens, 64 Zipf(1.1) experts, hidden 4096, ffn 1408, M-tiles of 256 tokens, seed 0 (both launches)";;
+    chain) k=chain; wk="two-engine chain, 1 workgroup, loop A of 16 iterations, inner trips U[1,8], 4-slot ring, seeds 0, 1, 2, on its own kernel and on the interpreter";;
   esac
+  if [ $wl != chain ]; then
   ab=$(python bench.py --workload $wl --algorithmic-bytes)
   python -m paper_2608_13757_amd.profiles traffic --kernel $k --fetch-dir $R/pf_$wl --write-dir $R/pw_$wl --copy-mib 1024 \
     --algorithmic-bytes $ab --workload "$wk" \
@@ -35,6 +38,7 @@ for wl in ${WLS:-stream gemm attn moe rmsnorm adamw}; do
       --command "rocprofv3 --pmc $SQ1 --output-format csv -d $R/ps1_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free,barrier --no-cpu-baseline" \
       --command "rocprofv3 --pmc $SQ2 --output-format csv -d $R/ps2_$wl -o s -- python -u bench.py --workload $wl --steps 2 --warmup 1 --modes barrier_free,barrier --no-cpu-baseline" \
       --command "WLS=$wl bash paper_2608_13757_amd/profile_records.sh $R"
+  fi
   fi
   python -m paper_2608_13757_amd.profiles trace --kernel $k --stats-dir $R/pt_$wl --workload "$wk" \
     --command "rocprofv3 --kernel-trace --stats --output-format csv -d $R/pt_$wl -o t -- python -u bench.py --workload $wl --steps 50 --warmup 50 --modes barrier_free,barrier --no-cpu-baseline" \

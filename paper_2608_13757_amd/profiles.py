@@ -44,6 +44,7 @@ KERNELS = {
     "adamw": (["kern_adamw.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["adamw_kernel<0, false>"]),
     "moe": (["kern_moe.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"],
             ["moe_kernel<1, 0, false, 256>", "moe_kernel<2, 0, false, 256>"]),
+    "chain": (["kern_chain.hip", "engine_sync.h", "device_sync.h", "bfs_internal.h"], ["chain_kernel<0, false>"]),
 }
 COPY_NAMES = ("__amd_rocclr_copyBuffer",)   # the runtime's device-to-device copy
 
@@ -147,9 +148,11 @@ def trace(args):
     for c in args.command:
         lines += ["```", c, "```", ""]
     lines += ["Template arguments: <mode, instrumented> (mode 0 = barrier-free, 1 = barrier); "
-              "MoE: <phase, mode, instrumented>.", "",
+              "MoE: <phase, mode, instrumented>.  `interp_kernel` is the generic interpreter "
+              "(mode and instrumentation are run-time arguments there).", "",
               "| Kernel | Calls | Average ns | Min ns | Max ns |", "|---|---|---|---|---|"]
-    stems = ("stream3_kernel<", "gemm_kernel<", "attn_kernel<", "moe_kernel<", "rms_kernel<", "adamw_kernel<")
+    stems = ("stream3_kernel<", "gemm_kernel<", "attn_kernel<", "moe_kernel<", "rms_kernel<", "adamw_kernel<",
+             "chain_kernel<", "interp_kernel")
     for r in rows:
         name = r["Name"]
         if not any(t in name for t in stems):
@@ -193,7 +196,8 @@ def sq(args):
     (GRBM_GUI_ACTIVE per XCD over the dispatch's duration) and the MFMA and
     LDS busy shares of the clock cycles when those counters are present."""
     stem = {"stream3": "stream3_kernel<", "gemm": "gemm_kernel<", "attn": "attn_kernel<",
-            "moe": "moe_kernel<", "rms": "rms_kernel<", "adamw": "adamw_kernel<"}[args.kernel]
+            "moe": "moe_kernel<", "rms": "rms_kernel<", "adamw": "adamw_kernel<",
+            "chain": "chain_kernel<"}[args.kernel]
     table = {}          # kernel -> counter -> (mean, dispatches)
     clock = {}          # kernel -> (GRBM_GUI_ACTIVE per XCD, mean dispatch duration)
     for d in args.dir:
