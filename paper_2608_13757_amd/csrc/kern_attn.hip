@@ -23,13 +23,18 @@
 // program's; Eq. 5 on the engines' loop registers): LOADK->QK, LOADV->PV,
 // QK->SM, SM->PREAD (k = 0); QK->LOADK (k = K ring depth), PV->LOADV (k = V
 // ring depth), PREAD->QK (k = 2: the S/P slot and its alpha row are free
-// once PREAD holds them in registers, before the MFMAs of PV), these three
-// read with the linearized offset (an extension of the paper's relation:
-// ring slots and S/P slots follow r_KV over all tiles, so the next tile's
-// loads and QK steps overlap the end of the previous tile); SM->NORM (k = 0,
-// C2: the tile's final row sums); NORM->SM (k = 2 at T: the row sums are
-// double-buffered by tile, and a tile's softmax overwrites a buffer only
-// after NORM of the tile before last has read it).
+// once PREAD holds them in registers, before the MFMAs of PV).  Ring slots
+// and S/P slots follow r_KV over all tiles, and their reuse across tiles is
+// ordered in one of two forms: the paper's relation, with these three read
+// per trip of KV and acquire instructions at each tile (ACQK on E0, ACQV on
+// E4, ACQS on E1; QK->ACQK, PV->ACQV, PREAD->ACQS at k = 1, C3 at T) that
+// drain the previous tile's reads before the next tile refills; or these
+// three read with the linearized offset (an extension of the paper's
+// relation), so the next tile's loads and QK steps overlap the end of the
+// previous tile.  SM->NORM (k = 0, C2: the tile's final row sums); NORM->SM
+// (k = 2 at T: the row sums are double-buffered by tile, and a tile's
+// softmax overwrites a buffer only after NORM of the tile before last has
+// read it).
 //
 // Query rows of the tile beyond the sequence are computed on a clamped copy
 // of the last row and never stored; keys beyond the sequence in the last
@@ -59,7 +64,8 @@
 // in T, KV holding LOADK (E0, opcode 32, args [0, K ring depth, heads,
 // 128]), LOADV (E4, opcode 32, args [1, V ring depth, heads, 128]), QK (E1,
 // 33), SM (E2, 34), PREAD (E3, 37), PV (E3, 35); NORM (E3, 36) in T after
-// KV; waves per engine 1, 2, 4, 4, 1; the dependencies listed above.
+// KV; in the paper's form ACQK (E0), ACQV (E4) and ACQS (E1), no-ops in T
+// before KV; waves per engine 1, 2, 4, 4, 1; the dependencies listed above.
 // Buffers: [0] work list int32 [rows][4] = (first token of the sequence,
 // length L, first query row of the tile, head), tile t of workgroup w at
 // row w + t * n_wg (the caller provides every row its trip tables reach),
