@@ -18,7 +18,7 @@ from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER,
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import attn_program, attn_worklist  # noqa: E402
 from workloads.configs import ATTN_LINEAR, ATTN_NK, ATTN_NV, ATTN_WG  # noqa: E402
-from workloads.tensors import attn_inputs, bf16_to_f32  # noqa: E402
+from workloads.tensors import attn_inputs, bf16_to_f32, to_bf16_bits  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -180,6 +180,32 @@ def test_attn_special_cases():
     _, _, _, out, _ = run_attn(ai, heads, MODE_BARRIER_FREE)
     check_close(out[0], bf16_to_f32(ai.v[0]))
     check_close(out[1:], np.broadcast_to(bf16_to_f32(const), out[1:].shape))
+
+
+def test_attn_peaked_and_flat_softmax():
+    """Large and vanishing logits.  Q scaled by 16 (an exact power of two in
+    bf16): scores with a standard deviation near 180 make the softmax nearly
+    one-hot and move the running maximum by large steps between KV blocks,
+    so the rescale factor underflows to 0 for some rows.  A sequence with
+    Q = 0 weights its keys equally: every block after the first keeps the
+    running maximum (a rescale by exactly 1, which the kernel skips) and O
+    is the mean of V.  Values against the oracle, both modes bit-identical."""
+    heads = 2
+    ai = attn_inputs(seed=9, heads=heads, lengths=[300, 1000, 129, 700])
+    q = bf16_to_f32(ai.q) * 16.0
+    s3 = int(ai.cu_seqlens[3])
+    q[s3:] = 0.0
+    ai.q = to_bf16_bits(q)
+    ref = np.asarray(mathref.attention(ai.q, ai.k, ai.v, ai.cu_seqlens, SCALE), np.float64)
+    mean_v = bf16_to_f32(ai.v[s3:]).astype(np.float64).mean(axis=0)
+    assert np.allclose(ref[s3:], mean_v[None], rtol=1e-9, atol=1e-12)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[attn-peaked-flat] mode={name}")
+        _, _, _, out, _ = run_attn(ai, heads, mode, n_wg=8)
+        check_close(out, ref)
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
 
 
 @pytest.fixture(scope="module")
