@@ -258,6 +258,30 @@ def test_gemm_special_cases():
     check_close(out, np.broadcast_to(mathref.gelu(gi.bias.astype(np.float64)), (m, n)))
 
 
+def test_gemm_gelu_range():
+    """A = 0, so every row of C is GELU(bias) as the epilogue evaluates it:
+    bias values from -64 to 64 (one per column) cover GELU's saturated tails
+    and its curved middle.  Each element is within the bf16 output rounding
+    (2^-8 relative) plus the erf approximation's error (1.5e-7 absolute in
+    erf, and the fp32 cancellation in 1 + erf at negative arguments, both
+    scaled by |x| / 2) of the exact-erf oracle; both modes bit-identical."""
+    m, n, k = 256, 512, 64
+    gi = gemm_inputs(seed=3, m=m, n=n, k=k)
+    gi.a = np.zeros_like(gi.a)
+    gi.bias = np.linspace(-64.0, 64.0, n).astype(np.float32)
+    x = gi.bias.astype(np.float64)
+    ref = mathref.gelu(x)
+    bound = 2.0 ** -8 * np.abs(ref) + 2e-7 * np.abs(x)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[gemm-gelu-range] mode={name}")
+        _, _, _, out, _ = run_gemm(gi, m, n, k, mode)
+        err = np.abs(out.astype(np.float64) - ref[None, :])
+        assert (err <= bound[None, :]).all(), (err / np.maximum(bound, 1e-300)).max()
+        outs[name] = out
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
 def test_gemm_full_size_sampled():
     """The benchmark shape 4096^3, checked on sampled elements one by one."""
     m = n = k = 4096
