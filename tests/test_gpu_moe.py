@@ -19,7 +19,7 @@ from paper_2608_13757_amd import (ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER,
 from tests.gpu_util import compare_wave_logs_with_oracle, log_records, trip_tensors  # noqa: E402
 from workloads import moe_program, moe_worklist  # noqa: E402
 from workloads.configs import MOE_BM, MOE_LINEAR, MOE_MCHUNKS  # noqa: E402
-from workloads.tensors import bf16_to_f32, moe_inputs, moe_weights_all  # noqa: E402
+from workloads.tensors import bf16_to_f32, moe_inputs, moe_weights_all, to_bf16_bits  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -129,6 +129,29 @@ def test_moe_small_parity_and_thresholds(bm):
             recs = {g: core.run(prog, trips, off[g], g).recs for g in range(wl.trips.n_wg)}
             lg = log_records(plan, logw, wl.trips.n_wg, 64, per_wave=True)
             assert compare_wave_logs_with_oracle(prog, plan, lg, recs, name) > 0
+        outs[name] = y
+    assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
+
+
+@pytest.mark.parametrize("bm", BMS)
+def test_moe_large_gate_values(bm):
+    """x scaled by 256 (exact in bf16): gate and up pre-activations with a
+    standard deviation near 80 reach SiLU's tails, where exp(-g) overflows to
+    infinity for the most negative gates (SiLU(g) = -0) and SiLU(g) = g for
+    the positive ones.  h and y against the oracle, both modes
+    bit-identical."""
+    moe = moe_inputs(seed=4, hidden=256, ffn=256, counts=SMALL_COUNTS)
+    moe.x = to_bf16_bits(bf16_to_f32(moe.x) * 256.0)
+    r = MoeRun(moe, mchunk=2, bm=bm)
+    T = len(moe.assign)
+    ref_y = mathref.moe_tokens(moe, range(T))
+    ref_h = mathref.moe_hidden(moe, moe.perm)
+    outs = {}
+    for name, mode in MODES:
+        _say(f"[moe-large] bm={bm} mode={name}")
+        h, y, _ = r.run(mode)
+        check_close(h, ref_h)
+        check_close(y, ref_y)
         outs[name] = y
     assert np.array_equal(outs["barrier_free"].view(np.uint32), outs["barrier"].view(np.uint32))
 
