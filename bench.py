@@ -915,8 +915,8 @@ def bf16_bits_as_f32(bits):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {a.gpus}); the hot path is intra-workgroup "
-              "synchronization and is not sharded across GPUs in this build.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {a.gpus}); the hot path is synchronization "
+              "inside one workgroup and is not sharded across GPUs.", file=sys.stderr)
         sys.exit(2)
     if a.algorithmic_bytes:
         print(int(algorithmic_bytes(a)))
