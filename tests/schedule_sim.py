@@ -77,7 +77,7 @@ class Model:
     their datapath accesses.  ``threshold_delta`` maps a dependency to an
     amount added to the implementation's threshold, ``drop_updates`` lists
     (instruction, counter) increments the implementation omits: planted
-    mistakes for the tests of this checker."""
+    mistakes for the tests of this simulator."""
 
     def __init__(self, prog, plan, trips, trip_off_wg, wg=0, per_instr=False, threshold_delta=None,
                  drop_updates=(), barrier_loops=None):
