@@ -16,7 +16,7 @@ from paper_2608_13757_amd import (ALLOC_PER_ENGINE, ALLOC_PER_INSTR, ALLOC_PER_L
                                   MODE_BARRIER_FREE, BfsError, Plan, bfs)
 from tests import fixtures
 from workloads import (OP_NOP, ProgramBuilder, TripTables, attn_program, attn_worklist, chain_workload,
-                       draw_trips, gemm_program, gemm_trips, random_nest, stream_workload)
+                       draw_trips, gemm_program, gemm_trips, random_nest, stream_program, stream_workload)
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -374,3 +374,79 @@ def test_abi_exports_every_header_symbol():
     L = bfs.lib()
     for n in names:
         assert hasattr(L, n), n
+
+
+def _mutate(f, rng):
+    """A copy of flat program ``f`` with random contents: every array keeps
+    the length its counts and offsets imply (the caller's side of the C
+    ABI's contract), every entry may be out of range."""
+    g = copy.deepcopy(f)
+    n_loops, n_instrs = len(g["loop_parent"]), len(g["instr_engine"])
+    n_body, n_blk = len(g["body_kind"]), len(g["block_off"]) - 1
+    bad = lambda lo, hi: int(rng.integers(lo, hi + 1))
+    for _ in range(int(rng.integers(1, 5))):
+        what = int(rng.integers(0, 14))
+        if what == 0 and n_loops:
+            g["loop_parent"][bad(0, n_loops - 1)] = bad(-3, n_loops + 2)
+        elif what == 1 and n_loops:
+            g["loop_is_cond"][bad(0, n_loops - 1)] = bad(-1, 3)
+        elif what == 2 and n_loops > 1:
+            g["body_off"][bad(1, n_loops - 1)] = bad(-2, n_body + 2)
+        elif what == 3 and n_body:
+            g["body_kind"][bad(0, n_body - 1)] = bad(-2, 3)
+        elif what == 4 and n_body:
+            g["body_id"][bad(0, n_body - 1)] = bad(-3, max(n_loops, n_blk) + 3)
+        elif what == 5 and n_blk > 1:
+            g["block_off"][bad(1, n_blk - 1)] = bad(-2, len(g["block_instrs"]) + 2)
+        elif what == 6 and g["block_instrs"]:
+            g["block_instrs"][bad(0, len(g["block_instrs"]) - 1)] = bad(-3, n_instrs + 3)
+        elif what == 7 and n_instrs:
+            g["instr_engine"][bad(0, n_instrs - 1)] = bad(-2, 10)
+        elif what == 8 and n_instrs:
+            g["instr_opcode"][bad(0, n_instrs - 1)] = bad(-2, 64)
+        elif what == 9 and n_instrs:
+            g["instr_args"][bad(0, n_instrs - 1)][bad(0, 7)] = bad(-5, 300)
+        elif what == 10 and g["deps"]:
+            d = list(g["deps"][bad(0, len(g["deps"]) - 1)])
+            d[bad(0, 2)] = bad(-3, n_instrs + 3) if rng.random() < 0.7 else bad(-5, 40)
+            g["deps"][bad(0, len(g["deps"]) - 1)] = tuple(d)
+        elif what == 11:
+            g["n_engines"] = bad(-1, 10)
+        elif what == 12:
+            g["waves_per_engine"][bad(0, 7)] = bad(-2, 12)
+        elif what == 13:
+            g["dep_linear"] = [bad(-1, 2) for _ in g["deps"]]
+    return g
+
+
+def test_planner_rejects_malformed_programs():
+    """Random malformed programs through the C ABI: every call returns OK or
+    an error status (never crashes), and every accepted plan answers its
+    query calls.  Run under a sanitizer build of the planner, this also
+    checks memory safety of the validation."""
+    rng = np.random.default_rng(2024)
+    bases = [random_nest(seed=s)[0].flat() for s in range(40)]
+    bases += [gemm_program(512, 512, 256).flat(), attn_program(2).flat(), stream_program().flat()]
+    valid = {getattr(bfs, n) for n in dir(bfs) if n.startswith("E_")} | {0}
+    accepted = rejected = 0
+    for i in range(600):
+        g = _mutate(bases[i % len(bases)], rng)
+        mode = int(rng.choice([MODE_BARRIER_FREE, MODE_BARRIER, 5]))
+        alloc = int(rng.choice([ALLOC_PER_LOOP, ALLOC_PER_INSTR, ALLOC_PER_ENGINE, 7]))
+        try:
+            plan = Plan(g, mode, alloc)
+        except BfsError as e:
+            assert e.status in valid and e.status != 0
+            rejected += 1
+            continue
+        accepted += 1
+        plan.formulas()
+        plan.stats()
+        if mode == MODE_BARRIER:
+            plan.static_waits()
+        for d in range(len(g["deps"]) + 2):
+            try:
+                plan.eval_threshold(d, int(rng.integers(0, 9)), int(rng.integers(0, 9)))
+            except BfsError as e:
+                assert e.status in valid and e.status != 0
+    assert rejected > 100 and accepted > 10
