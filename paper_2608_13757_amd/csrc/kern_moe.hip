@@ -163,6 +163,21 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
     // lane l covers rows 16 j + l / 4 and the 16-byte chunk that belongs at
     // position l % 4 of its row
     const uint32_t r_in = lane >> 2, chunk = (lane & 3u) ^ ((lane >> 4) & 3u);
+    // phase 1: the token ids of an M-tile's rows (gathered through perm)
+    // are loaded during the previous M-tile, so a tile's first row loads
+    // need not wait for them.  These loads are older than the ring loads
+    // issued after them, so the counted vmcnt waits below only wait longer
+    // for them, never shorter.
+    int32_t prow[kALoads];
+    auto load_rows = [&](uint32_t mi) __attribute__((always_inline)) {
+      const int32_t m0 = (mt0 + (int32_t)mi) * kBM;
+#pragma unroll
+      for (int j = 0; j < kALoads; ++j) {
+        const int32_t r = min(m0 + 16 * j + (int32_t)r_in, e_cnt - 1);
+        prow[j] = kPhase == 1 ? P.perm[e_lo + r] : e_lo + r;
+      }
+    };
+    if (wave == 0 && trip_m > 0) load_rows(0);
     S.sync_point(S.word(0, ew));                                  // before loop M
     S.enter(sa, P.acql, g, 1);
     for (uint32_t mi = 0; mi < trip_m; ++mi) {
@@ -187,8 +202,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
       if (wave == 0) {
 #pragma unroll
         for (int j = 0; j < kALoads; ++j) {
-          const int32_t r = min(m0 + 16 * j + (int32_t)r_in, e_cnt - 1);
-          const int32_t row = kPhase == 1 ? P.perm[e_lo + r] : e_lo + r;
+          const int32_t row = prow[j];
           const uint64_t off = ((uint64_t)(uint32_t)row * (uint32_t)P.kdim + 8u * chunk) * 2u;
           if (__ballot((off >> 32) != 0) != 0ull) {
             report_input(P.sc.err, 3u, (uint32_t)wg, mi, (uint32_t)row, 0u, (uint32_t)wave);
@@ -198,7 +212,7 @@ __global__ void __launch_bounds__(768) moe_kernel(MoeParams P) {
         }
 #pragma unroll
         for (int j = kALoads; j < 16; ++j) voff[j] = 0u;
-        wait_vm<0>();
+        if (mi + 1 < trip_m) load_rows(mi + 1);
       } else {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
