@@ -687,9 +687,12 @@ MOE_BN = {1: 128, 2: 256}    # output columns per workgroup: h columns (phase 1)
 # counters and 16 KiB epilogue slots they stay within 160 KiB of LDS.
 # Epilogue slots 0: each chunk of an M-tile in its own 16 KiB of the ring,
 # after the tile's K loop (four 32 KiB slots hold phase 2's eight chunks of
-# a 256-row tile).  At 256 rows, in one process: phase 1 (4 chunks) 1.0 %
-# faster with one epilogue slot, phase 2 (8 chunks) 2 % faster in the ring.
-MOE_RINGS = {(128, 1): (5, 2), (128, 2): (5, 2), (256, 1): (4, 1), (256, 2): (4, 0)}
+# a 256-row tile).  At 256 rows, in one process: phase 1 (4 chunks) 1-1.7 %
+# faster in the ring than with one epilogue slot (1001 against 1011-1018 us;
+# the other way round before the output stores were plain and the gather
+# indices prefetched), phase 2 (8 chunks) 2-3 % faster in the ring than with
+# three ring slots and one or two epilogue slots.
+MOE_RINGS = {(128, 1): (5, 2), (128, 2): (5, 2), (256, 1): (4, 0), (256, 2): (4, 0)}
 MOE_MCHUNKS = {128: 4, 256: 4}   # at most this many M-tiles per workgroup
 
 
