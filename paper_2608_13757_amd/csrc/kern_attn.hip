@@ -534,19 +534,41 @@ __global__ void __launch_bounds__(768) attn_kernel(AttnParams P) {
         const int32_t row = x.q0 + (int32_t)rloc;
         const float lr = *(const BFS_LDS float *)(uintptr_t)(lsum_l + (((g.r1 - 1) & 1u) * kBQ + rloc) * 4u);
         const float inv = 1.0f / lr;
-        if (row < x.L) {
-          __bf16 *dst = P.o + (size_t)(x.s0 + row) * row_stride + (size_t)x.head * kD;
+        // lane l holds columns 8 j + 4 (l / 32) .. + 3 of each 32-column
+        // block db: lanes l and l + 32 exchange halves (v_permlane32_swap) so
+        // that the low lane holds the 8 columns of j = 0, 2 and the high lane
+        // those of j = 1, 3, and each stores 16-byte row segments
+        __bf16 *dst = P.o + (size_t)(x.s0 + max(min(row, x.L - 1), 0)) * row_stride + (size_t)x.head * kD;
 #pragma unroll
-          for (int db = 0; db < 4; ++db)
+        for (int db = 0; db < 4; ++db)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+          for (int jp = 0; jp < 2; ++jp) {
+            uint32_t q[2][2];   // [j - 2 jp][dword]: this lane's 4 columns of j = 2 jp, 2 jp + 1
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj) {
+              const int j = 2 * jp + jj;
               const f32x2 a01 = {acc[db][4 * j] * inv, acc[db][4 * j + 1] * inv};
               const f32x2 a23 = {acc[db][4 * j + 2] * inv, acc[db][4 * j + 3] * inv};
-              const u32x2 v = {__builtin_bit_cast(uint32_t, __builtin_convertvector(a01, bf16x2)),
-                               __builtin_bit_cast(uint32_t, __builtin_convertvector(a23, bf16x2))};
-              *reinterpret_cast<u32x2 *>(dst + 32 * db + 8 * j + 4 * lhi) = v;
+              q[jj][0] = __builtin_bit_cast(uint32_t, __builtin_convertvector(a01, bf16x2));
+              q[jj][1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(a23, bf16x2));
             }
-        }
+            // low lane: keep j = 2 jp, receive the high lane's half of it;
+            // high lane: keep j = 2 jp + 1, receive the low lane's half of it
+            u32x4 v;
+#pragma unroll
+            for (int d = 0; d < 2; ++d) {
+              // r[0]: a lane below 32 keeps its q[0][d], a lane above gets
+              // q[1][d] of lane - 32; r[1]: a lane below 32 gets q[0][d] of
+              // lane + 32, a lane above keeps its q[1][d]
+              const auto r = __builtin_amdgcn_permlane32_swap(q[0][d], q[1][d], false, false);
+              const uint32_t mine = lhi == 0 ? q[0][d] : q[1][d];
+              const uint32_t other = lhi == 0 ? (uint32_t)r[1] : (uint32_t)r[0];
+              v[d] = lhi == 0 ? mine : other;
+              v[2 + d] = lhi == 0 ? other : mine;
+            }
+            const int j = 2 * jp + (int)lhi;
+            if (row < x.L) *reinterpret_cast<u32x4 *>(dst + 32 * db + 8 * j) = v;
+          }
       }
       S.signal(P.norm.update, (uint32_t)ew);
       S.sync_point(own);                                     // end of a T iteration
