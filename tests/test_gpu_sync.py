@@ -12,7 +12,7 @@ import pytest
 torch = pytest.importorskip("torch")
 
 from oracle import core  # noqa: E402
-from paper_2608_13757_amd import (ALLOC_PER_ENGINE, ALLOC_PER_INSTR, MODE_BARRIER, MODE_BARRIER_FREE,  # noqa: E402
+from paper_2608_13757_amd import (ALLOC_PER_ENGINE, ALLOC_PER_INSTR, ALLOC_PER_LOOP, MODE_BARRIER, MODE_BARRIER_FREE,  # noqa: E402
                                   BfsError, Plan, bfs)
 from paper_2608_13757_amd.bfs import RUN_LOG_BATCHED, RUN_PER_INSTANCE  # noqa: E402
 from tests.gpu_util import (compare_batched_log_with_oracle, compare_log_with_oracle, dev, log_records,  # noqa: E402
@@ -491,3 +491,53 @@ def test_stream_program_shape_is_checked():
     with pytest.raises(BfsError) as e:
         plan.run([t, t, t], t, t, 1)
     assert e.value.status == bfs.E_UNSUPPORTED
+
+
+def test_random_nests_deeper_all_allocations():
+    """Deeper and wider random nests than the tests above (depth up to 4,
+    trips up to 5 including empty conditionals, up to 10 dependencies with
+    offsets up to 4, 2 to 4 engines), each under the per-loop,
+    per-instruction and per-engine allocations barrier-free and per-loop in
+    barrier mode: every logged threshold equals the oracle's."""
+    checked = expected = 0
+    base = torch.zeros(1, dtype=torch.int64, device="cuda")
+    x = torch.zeros(64, dtype=torch.float32, device="cuda")
+    out = torch.zeros(64, dtype=torch.float32, device="cuda")
+    cap = 1024
+    for seed in range(5000, 6000):
+        rng = np.random.default_rng(seed)
+        kw = dict(max_depth=int(rng.integers(2, 5)), max_trip=int(rng.integers(1, 6)),
+                  n_deps=int(rng.integers(4, 11)), max_k=int(rng.integers(0, 5)), n_engines=int(rng.integers(2, 5)))
+        prog0, tt = random_nest(seed, **kw)
+        trips, off = tt.flat()
+        t_trips, t_off = trip_tensors(tt)
+        for alloc, key in ((ALLOC_PER_LOOP, "barrier_free"), (ALLOC_PER_INSTR, "per_instr"),
+                           (ALLOC_PER_ENGINE, "per_engine")):
+            prog = copy.deepcopy(prog0)
+            ok = []
+            for d in prog.deps:
+                q = copy.deepcopy(prog)
+                q.deps = [d]
+                try:
+                    Plan(q, MODE_BARRIER_FREE, alloc)
+                    ok.append(d)
+                except BfsError:
+                    pass
+            prog.deps = ok
+            if not prog.deps:
+                continue
+            res = core.run(prog, trips, off[0], 0)
+            modes = [(key, MODE_BARRIER_FREE)] + ([("barrier", MODE_BARRIER)] if alloc == ALLOC_PER_LOOP else [])
+            for name, mode in modes:
+                plan = Plan(prog, mode, alloc if mode == MODE_BARRIER_FREE else ALLOC_PER_LOOP)
+                if mode == MODE_BARRIER_FREE:
+                    expected += len(res.recs)
+                else:
+                    same = [w["same_region"] for w in plan.static_waits()]
+                    expected += sum(1 for r in res.recs if same[int(r["dep"])])
+                log = torch.zeros(plan.debug_log_words(1, cap), dtype=torch.int32, device="cuda")
+                plan.run([base, x, out], t_trips, t_off, 1, debug_log=log, debug_capacity=cap)
+                plan.status()
+                logs = log_records(plan, log.cpu().numpy().view(np.uint32), 1, cap)
+                checked += compare_log_with_oracle(prog, plan, logs, {0: res.recs}, name)
+    assert checked == expected and checked > 10000
