@@ -19,6 +19,7 @@ from tests.gpu_util import (compare_batched_log_with_oracle, compare_log_with_or
                             trip_tensors)
 from workloads import (chain_workload, random_nest, stream_fixed_trips, stream_program,  # noqa: E402
                        stream_workload, tile_bases)
+from workloads.configs import TripTables, draw_trips  # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -496,19 +497,25 @@ def test_stream_program_shape_is_checked():
 def test_random_nests_deeper_all_allocations():
     """Deeper and wider random nests than the tests above (depth up to 4,
     trips up to 5 including empty conditionals, up to 10 dependencies with
-    offsets up to 4, 2 to 4 engines), each under the per-loop,
-    per-instruction and per-engine allocations barrier-free and per-loop in
-    barrier mode: every logged threshold equals the oracle's."""
+    offsets up to 4, 2 to 4 engines), three workgroups with trip tables of
+    their own, each program under the per-loop, per-instruction and
+    per-engine allocations barrier-free and per-loop in barrier mode: every
+    logged threshold of every workgroup equals the oracle's."""
+    n_wg = 3
     checked = expected = 0
-    base = torch.zeros(1, dtype=torch.int64, device="cuda")
+    base = torch.zeros(n_wg, dtype=torch.int64, device="cuda")
     x = torch.zeros(64, dtype=torch.float32, device="cuda")
-    out = torch.zeros(64, dtype=torch.float32, device="cuda")
+    out = torch.zeros(64 * n_wg, dtype=torch.float32, device="cuda")
     cap = 1024
     for seed in range(5000, 6000):
         rng = np.random.default_rng(seed)
         kw = dict(max_depth=int(rng.integers(2, 5)), max_trip=int(rng.integers(1, 6)),
                   n_deps=int(rng.integers(4, 11)), max_k=int(rng.integers(0, 5)), n_engines=int(rng.integers(2, 5)))
-        prog0, tt = random_nest(seed, **kw)
+        prog0, tt1 = random_nest(seed, **kw)
+
+        def draw(l, n):
+            return rng.integers(0, (1 if prog0.loop_is_cond[l] else kw["max_trip"]) + 1, size=n)
+        tt = TripTables([tt1.per_wg[0]] + [draw_trips(prog0, draw) for _ in range(n_wg - 1)])
         trips, off = tt.flat()
         t_trips, t_off = trip_tensors(tt)
         for alloc, key in ((ALLOC_PER_LOOP, "barrier_free"), (ALLOC_PER_INSTR, "per_instr"),
@@ -526,18 +533,16 @@ def test_random_nests_deeper_all_allocations():
             prog.deps = ok
             if not prog.deps:
                 continue
-            res = core.run(prog, trips, off[0], 0)
+            recs = {g: core.run(prog, trips, off[g], g).recs for g in range(n_wg)}
             modes = [(key, MODE_BARRIER_FREE)] + ([("barrier", MODE_BARRIER)] if alloc == ALLOC_PER_LOOP else [])
             for name, mode in modes:
                 plan = Plan(prog, mode, alloc if mode == MODE_BARRIER_FREE else ALLOC_PER_LOOP)
-                if mode == MODE_BARRIER_FREE:
-                    expected += len(res.recs)
-                else:
-                    same = [w["same_region"] for w in plan.static_waits()]
-                    expected += sum(1 for r in res.recs if same[int(r["dep"])])
-                log = torch.zeros(plan.debug_log_words(1, cap), dtype=torch.int32, device="cuda")
-                plan.run([base, x, out], t_trips, t_off, 1, debug_log=log, debug_capacity=cap)
+                same = [w["same_region"] for w in plan.static_waits()] if mode == MODE_BARRIER else None
+                for g in range(n_wg):
+                    expected += len(recs[g]) if same is None else sum(1 for r in recs[g] if same[int(r["dep"])])
+                log = torch.zeros(plan.debug_log_words(n_wg, cap), dtype=torch.int32, device="cuda")
+                plan.run([base, x, out], t_trips, t_off, n_wg, debug_log=log, debug_capacity=cap)
                 plan.status()
-                logs = log_records(plan, log.cpu().numpy().view(np.uint32), 1, cap)
-                checked += compare_log_with_oracle(prog, plan, logs, {0: res.recs}, name)
-    assert checked == expected and checked > 10000
+                logs = log_records(plan, log.cpu().numpy().view(np.uint32), n_wg, cap)
+                checked += compare_log_with_oracle(prog, plan, logs, recs, name)
+    assert checked == expected and checked > 30000
