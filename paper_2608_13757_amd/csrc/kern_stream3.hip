@@ -344,6 +344,12 @@ __device__ __forceinline__ InnerWait make_inner(const bfs::PackedWait w, uint32_
   return iw;
 }
 
+// The 32-bit word at a byte offset from base, read through the scalar cache
+// with the offset in a scalar register (no 64-bit address arithmetic).
+__device__ __forceinline__ uint32_t ldc_at(const int32_t *base, uint32_t byte_off) {
+  return (uint32_t)ldc(reinterpret_cast<const int32_t *>(reinterpret_cast<const char *>(base) + byte_off));
+}
+
 // kk of a mask on rhat of O or M, at the statement of loop I.
 __device__ __forceinline__ void enter_inner(InnerWait &iw, uint32_t h1, uint32_t h2) {
   if (iw.kk_lvl != 0u) iw.kk = ((iw.kk_lvl == 1u ? h1 : h2) > iw.k) ? 0u : 0xffffffffu;
@@ -438,8 +444,8 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
         // Two M iterations whose trips each fit one batch: one wait, one
         // LDS round trip and one counter add for both.
         const uint32_t ta = tq0, tb = tq1;
-        tq0 = (uint32_t)ldc(trip_i_of + min(m + 2u, trip_m - 1u));
-        tq1 = (uint32_t)ldc(trip_i_of + min(m + 3u, trip_m - 1u));
+        tq0 = ldc_at(trip_i_of, 4u * min(m + 2u, trip_m - 1u));
+        tq1 = ldc_at(trip_i_of, 4u * min(m + 3u, trip_m - 1u));
         E.r2 += 2;
         E.h2 = m + 2;
         const uint32_t sa = soff0;
@@ -490,10 +496,12 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
           // lanes read slots of the same generations that no engine uses in
           // these M iterations, and their values are dropped
           const uint32_t base = kRole == ROLE_ADD ? xl4 : yl4;
-          f32x4 va = {0.f, 0.f, 0.f, 0.f}, vb = {0.f, 0.f, 0.f, 0.f};
+          // (lanes beyond the longer trip leave va and vb undefined: they
+          // store and write nothing)
+          f32x4 va, vb;
           if (lane < 16u * kmax)
             asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3\n\ts_waitcnt lgkmcnt(0)"
-                         : "+v"(va), "+v"(vb) : "v"(base + sa), "v"(base + sb) : "memory");
+                         : "=&v"(va), "=&v"(vb) : "v"(base + sa), "v"(base + sb) : "memory");
           asm volatile("" ::"s"(tq0), "s"(tq1));   // arrived by now (see the single batch)
           if (kRole == ROLE_ADD) {
             if (lane < 16u * ta) {
@@ -526,7 +534,7 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
       E.sync_point();                                     // before loop I
       const uint32_t trip_i = tq0;
       tq0 = tq1;
-      tq1 = (uint32_t)ldc(trip_i_of + min(m + 2u, trip_m - 1u));
+      tq1 = ldc_at(trip_i_of, 4u * min(m + 2u, trip_m - 1u));
       if (kShort) {
         // Batches of up to kBatchMax instances within one generation of
         // slots: the tiles of consecutive r_I are adjacent in HBM and their
@@ -571,9 +579,9 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
             asm volatile("" ::"s"(tq1));
             E.issued_batch(k);   // batch loads land in issue order
           } else if (kRole == ROLE_ADD) {
-            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            f32x4 v;   // undefined in the idle lanes, which write nothing
             if (act)
-              asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "+v"(v) : "v"(xl4 + boff) : "memory");
+              asm volatile("ds_read_b128 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(xl4 + boff) : "memory");
             asm volatile("" ::"s"(tq1));   // arrived by now (see the load engine)
             if (act) {
               v = v + addc;
