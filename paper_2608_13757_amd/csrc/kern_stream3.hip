@@ -124,9 +124,9 @@ struct Engine {
   uint32_t *log = nullptr;
   uint32_t nlog = 0;
   int pending = 0;                        // load engine: loads issued, not yet retired
-  // Load engine batches: lane (b % 64) of bq holds the tile count of batch b;
-  // nb batches issued so far; btiles tiles in batches not yet retired.
-  uint32_t bq = 0, nb = 0, btiles = 0;
+  // Load engine batches: the tile counts of the last kBatchQ batches issued,
+  // oldest first, in scalar registers (0 once retired).
+  uint32_t q0 = 0, q1 = 0, q2 = 0;
   // Retirement add with every lane active: lane 0 adds to the inner
   // instruction's counter (or to its own scratch word when the instruction
   // has no consumer), the other lanes add 0 to this wave's private scratch
@@ -138,7 +138,9 @@ struct Engine {
       : P(p), C(c), cnt_base(cb), wave(w), wg(g) {}
 
   __device__ __forceinline__ void add_own(uint32_t n) {
-    const uint32_t v = n == 1u ? one_v : (lane_id() == 0 ? n : 0u);
+    // (a constant 1 uses the value prepared at the start; any other count
+    // is selected into lane 0 here)
+    const uint32_t v = (__builtin_constant_p(n) && n == 1u) ? one_v : (lane_id() == 0 ? n : 0u);
     asm volatile("ds_add_u32 %0, %1" ::"v"(own_vaddr), "v"(v) : "memory");
   }
   __device__ __forceinline__ void add_one(uint32_t addr) {
@@ -175,23 +177,25 @@ struct Engine {
   }
   // Load engine: retire every outstanding batch load.
   __device__ __forceinline__ void flush_batches() {
-    if (kRole == ROLE_LOAD && btiles != 0u) {
-      wait_vm<0>();
-      add_own(btiles);
-      btiles = 0;
-      bq = 0;   // the retired batches' entries read as 0 from now on
+    if (kRole == ROLE_LOAD) {
+      const uint32_t held = q0 + q1 + q2;
+      if (held != 0u) {
+        wait_vm<0>();
+        add_own(held);
+        q0 = q1 = q2 = 0;
+      }
     }
   }
   // Load engine: batch b of k tiles was issued; the batch issued kBatchQ
   // batches earlier retires (entries of batches already flushed are 0).
   __device__ __forceinline__ void issued_batch(uint32_t k) {
-    bq = lane_id() == (nb & 63u) ? k : bq;
-    const uint32_t t = (uint32_t)__builtin_amdgcn_readlane((int)bq, (int)((nb - kBatchQ) & 63u));
-    nb += 1;
-    btiles += k;
+    static_assert(kBatchQ == 3, "three batch counts held");
+    const uint32_t t = q0;
+    q0 = q1;
+    q1 = q2;
+    q2 = k;
     wait_vm<kBatchQ>();
     add_own(t);
-    btiles -= t;
   }
   // Retire everything held.
   __device__ __forceinline__ void retire_all() {
@@ -399,7 +403,8 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
   const int64_t *toff = P.trip_off + (int64_t)wg * 4;
   const int64_t tbase = ldc(P.base + wg);
   // per-lane addresses of the rings and of this workgroup's tiles
-  const uint32_t xl = lds_addr(ring_x) + 4u * lane, yl = lds_addr(ring_y) + 4u * lane;
+  const uint32_t xlds = lds_addr(ring_x);                 // LDS byte address of the ring loaded into
+  const uint32_t xl = xlds + 4u * lane, yl = lds_addr(ring_y) + 4u * lane;
   const float *xg = P.x + tbase * 64 + lane;
   float *yg = P.y + tbase * 64 + lane;
   // batches: lane l moves bytes [16 l, 16 l + 16) of a block of tiles
@@ -485,11 +490,11 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
         const uint32_t kmax = max(ta, tb);
         if (kRole == ROLE_LOAD) {
           if (lane < 16u * ta)
-            __builtin_amdgcn_global_load_lds((const void *)(xb + tile_a), (BFS_LDS void *)(ring_x + sa / 4u), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void *)(xb + tile_a), (BFS_LDS void *)(uintptr_t)(xlds + sa), 16, 0, 0);
           asm volatile("" ::"s"(tq0), "s"(tq1));   // arrived by now (see the single batch)
           E.issued_batch(ta);
           if (lane < 16u * tb)
-            __builtin_amdgcn_global_load_lds((const void *)(xb + tile_b), (BFS_LDS void *)(ring_x + sb / 4u), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void *)(xb + tile_b), (BFS_LDS void *)(uintptr_t)(xlds + sb), 16, 0, 0);
           E.issued_batch(tb);
         } else {
           // both blocks read with the lanes of the longer trip: the extra
@@ -571,7 +576,7 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
           const bool act = lane < 16u * k;
           if (kRole == ROLE_LOAD) {
             if (act)
-              __builtin_amdgcn_global_load_lds((const void *)(xb + tile), (BFS_LDS void *)(ring_x + boff / 4u), 16, 0,
+              __builtin_amdgcn_global_load_lds((const void *)(xb + tile), (BFS_LDS void *)(uintptr_t)(xlds + boff), 16, 0,
                                                0);
             // the next trip has arrived by now; taking it here keeps its
             // wait ahead of the counter add, which then never holds up the
