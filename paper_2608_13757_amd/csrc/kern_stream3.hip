@@ -491,10 +491,12 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
         if (kRole == ROLE_LOAD) {
           if (lane < 16u * ta)
             __builtin_amdgcn_global_load_lds((const void *)(xb + tile_a), (BFS_LDS void *)(uintptr_t)(xlds + sa), 16, 0, 0);
-          asm volatile("" ::"s"(tq0), "s"(tq1));   // arrived by now (see the single batch)
           E.issued_batch(ta);
           if (lane < 16u * tb)
             __builtin_amdgcn_global_load_lds((const void *)(xb + tile_b), (BFS_LDS void *)(uintptr_t)(xlds + sb), 16, 0, 0);
+          // the trips have had the first batch to arrive; taking them before
+          // the second counter add keeps that add out of the wait
+          asm volatile("" ::"s"(tq0), "s"(tq1));
           E.issued_batch(tb);
         } else {
           // both blocks read with the lanes of the longer trip: the extra
@@ -528,6 +530,7 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
         soff0 = sb + gen_bytes;
         if (soff0 == ring_bytes) soff0 = 0;
         m += 2;
+        asm volatile("" ::"s"(tq0), "s"(tq1));   // taken already (see the end of the loop body)
         continue;
       }
       E.r2 += 1;
@@ -713,6 +716,10 @@ __device__ __forceinline__ void run_engine(kconst<Stream3Params> &P, uint32_t cn
       E.nops(C.m_post, C.n_m_post, E.r2 - 1);
       E.sync_point();                                     // end of an iteration of M
       m += 1;
+      // Every path has taken the fetched trips by now (a no-op where it
+      // already waited for them), so none is still in flight where the
+      // paths meet and the next fetch into the same registers need not wait.
+      asm volatile("" ::"s"(tq0), "s"(tq1));
     }
     E.nops(C.o_post, C.n_o_post, E.r1 - 1);
     E.sync_point();                                       // end of an iteration of O
