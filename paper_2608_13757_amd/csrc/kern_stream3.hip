@@ -50,8 +50,8 @@ constexpr int kMaxWaitsPerEngine = 16;
 constexpr int kMaxInnerWaits = 2;
 // Batch loads the load engine keeps in flight beyond the one just issued:
 // more hides more HBM latency but delays every completion signal by as many
-// batches (measured best at 2 to 3, 3 with M iterations in pairs).
-constexpr uint32_t kBatchQ = 3;
+// batches (measured best at 4; 2, 3, 5 and 6 slower).
+constexpr uint32_t kBatchQ = 4;
 
 struct InstrSync {
   int16_t first;     // index of its first wait in the engine's wait list
@@ -126,7 +126,7 @@ struct Engine {
   int pending = 0;                        // load engine: loads issued, not yet retired
   // Load engine batches: the tile counts of the last kBatchQ batches issued,
   // oldest first, in scalar registers (0 once retired).
-  uint32_t q0 = 0, q1 = 0, q2 = 0;
+  uint32_t q[kBatchQ] = {};
   // Retirement add with every lane active: lane 0 adds to the inner
   // instruction's counter (or to its own scratch word when the instruction
   // has no consumer), the other lanes add 0 to this wave's private scratch
@@ -178,22 +178,24 @@ struct Engine {
   // Load engine: retire every outstanding batch load.
   __device__ __forceinline__ void flush_batches() {
     if (kRole == ROLE_LOAD) {
-      const uint32_t held = q0 + q1 + q2;
+      uint32_t held = 0;
+#pragma unroll
+      for (int i = 0; i < (int)kBatchQ; ++i) held += q[i];
       if (held != 0u) {
         wait_vm<0>();
         add_own(held);
-        q0 = q1 = q2 = 0;
+#pragma unroll
+        for (int i = 0; i < (int)kBatchQ; ++i) q[i] = 0;
       }
     }
   }
   // Load engine: batch b of k tiles was issued; the batch issued kBatchQ
   // batches earlier retires (entries of batches already flushed are 0).
   __device__ __forceinline__ void issued_batch(uint32_t k) {
-    static_assert(kBatchQ == 3, "three batch counts held");
-    const uint32_t t = q0;
-    q0 = q1;
-    q1 = q2;
-    q2 = k;
+    const uint32_t t = q[0];
+#pragma unroll
+    for (int i = 0; i + 1 < (int)kBatchQ; ++i) q[i] = q[i + 1];
+    q[kBatchQ - 1] = k;
     wait_vm<kBatchQ>();
     add_own(t);
   }
