@@ -439,6 +439,41 @@ def test_stream_uninstrumented_values(layout, per_gen, inner_war):
         assert torch.equal(y, ref)
 
 
+@pytest.mark.parametrize("n_gen,mid_max", [(2, 1), (4, 2), (6, 3)])
+def test_stream_tight_ring_values(n_gen, mid_max):
+    """The in-place ring at its fewest generations for the M trips (twice the
+    largest): the load engine waits for the store engine two O iterations
+    back at nearly every O iteration, so it retires the batches it holds
+    before blocking, and M-iteration pairs wrap around the ring (six
+    generations, trips up to three: a pair can straddle the wrap).  Outputs
+    equal x + 1 in both modes and with the batched waits logged, every
+    threshold equals the oracle's."""
+    w = stream_workload(seed=11, n_wg=32, outer=64, mid_max=mid_max, n_gen=n_gen)
+    trips, toff = trip_tensors(w.trips)
+    base, x = dev(w.base), dev(w.x)
+    ref = torch.from_numpy(w.x.reshape(-1)).cuda() + 1.0
+    for name, mode in MODES:
+        _say(f"[stream-tight] n_gen={n_gen} mid_max={mid_max} mode={name}")
+        y = torch.full((w.n_tiles * 64,), float("nan"), dtype=torch.float32, device="cuda")
+        plan = Plan(w.prog, mode)
+        plan.run([base, x, y], trips, toff, w.trips.n_wg)
+        plan.status()
+        assert torch.equal(y, ref)
+    plan = Plan(w.prog, MODE_BARRIER_FREE)
+    cap = 4096
+    sample = [0, 17, 31]
+    log = torch.zeros(plan.debug_log_words(w.trips.n_wg, cap), dtype=torch.int32, device="cuda")
+    y = torch.full((w.n_tiles * 64,), float("nan"), dtype=torch.float32, device="cuda")
+    plan.run([base, x, y], trips, toff, w.trips.n_wg, debug_log=log, debug_capacity=cap, flags=RUN_LOG_BATCHED)
+    plan.status()
+    assert torch.equal(y, ref)
+    t_all, o_all = w.trips.flat()
+    logs = log_records(plan, log.cpu().numpy().view(np.uint32), w.trips.n_wg, cap)
+    recs = {g: core.run(w.prog, t_all, o_all[g], g).recs for g in sample}
+    logs = {k: v for k, v in logs.items() if k[0] in sample}
+    assert compare_batched_log_with_oracle(w.prog, logs, recs) > 0
+
+
 def test_stream_uninstrumented_watchdog_ends():
     """A one-poll watchdog on the uninstrumented kernel: every engine that
     gives up finishes its trips without waiting, so the launch ends, with the
