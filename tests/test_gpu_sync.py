@@ -439,21 +439,22 @@ def test_stream_uninstrumented_values(layout, per_gen, inner_war):
         assert torch.equal(y, ref)
 
 
-@pytest.mark.parametrize("n_gen,mid_max", [(2, 1), (4, 2), (6, 3)])
-def test_stream_tight_ring_values(n_gen, mid_max):
+@pytest.mark.parametrize("n_gen,mid_max,per_gen", [(2, 1, 4), (4, 2, 4), (6, 3, 4), (6, 3, 2)])
+def test_stream_tight_ring_values(n_gen, mid_max, per_gen):
     """The in-place ring at its fewest generations for the M trips (twice the
     largest): the load engine waits for the store engine two O iterations
     back at nearly every O iteration, so it retires the batches it holds
     before blocking, and M-iteration pairs wrap around the ring (six
-    generations, trips up to three: a pair can straddle the wrap).  Outputs
+    generations, trips up to three: a pair can straddle the wrap), also with
+    two slots per generation (batches and pairs of at most two).  Outputs
     equal x + 1 in both modes and with the batched waits logged, every
     threshold equals the oracle's."""
-    w = stream_workload(seed=11, n_wg=32, outer=64, mid_max=mid_max, n_gen=n_gen)
+    w = stream_workload(seed=11, n_wg=32, outer=64, mid_max=mid_max, inner_max=per_gen, n_gen=n_gen)
     trips, toff = trip_tensors(w.trips)
     base, x = dev(w.base), dev(w.x)
     ref = torch.from_numpy(w.x.reshape(-1)).cuda() + 1.0
     for name, mode in MODES:
-        _say(f"[stream-tight] n_gen={n_gen} mid_max={mid_max} mode={name}")
+        _say(f"[stream-tight] n_gen={n_gen} mid_max={mid_max} per_gen={per_gen} mode={name}")
         y = torch.full((w.n_tiles * 64,), float("nan"), dtype=torch.float32, device="cuda")
         plan = Plan(w.prog, mode)
         plan.run([base, x, y], trips, toff, w.trips.n_wg)
